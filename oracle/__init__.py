@@ -1,0 +1,19 @@
+"""CPU oracle for attention forward and backward (f64) -- TEST INFRASTRUCTURE.
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg may
+import this package.  The product library never touches it; it shares no code
+with the HIP path.  The arithmetic lives in ``attn_oracle.c`` (plain C99,
+double precision, no FMA contraction); this module only builds that file and
+marshals numpy arrays to it.
+
+Every function follows the textbook definition of exact attention, which the
+paper's tiled forward, dQ and fused dK+dV kernels (Sec. 3.3, Sec. 7.3)
+compute up to floating-point ordering.
+"""
+from .oracle import (  # noqa: F401
+    build_oracle,
+    oracle_forward,
+    oracle_backward,
+    oracle_head_matrices,
+    ORACLE_SRC,
+)

@@ -1,0 +1,142 @@
+"""ctypes front end of the C attention oracle (TEST INFRASTRUCTURE ONLY).
+
+Inputs are converted to float64 copies of the exact stored values (f32, or
+bf16 widened to f32 first); outputs are float64.  The C library is compiled
+from ``attn_oracle.c`` next to this file with gcc.
+"""
+import ctypes
+import os
+import subprocess
+import threading
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+ORACLE_SRC = os.path.join(_HERE, "attn_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "liboracle.so")
+_lock = threading.Lock()
+_lib = None
+
+CFLAGS = ["-O2", "-std=c99", "-ffp-contract=off", "-fno-fast-math", "-fopenmp",
+          "-fPIC", "-shared", "-Wall", "-Wextra"]
+
+
+def build_oracle(src=ORACLE_SRC, out=_LIB_PATH):
+    """Compile the oracle with gcc; returns the path of the shared object."""
+    tmp = out + ".tmp%d" % os.getpid()
+    subprocess.run(["gcc", *CFLAGS, src, "-o", tmp, "-lm"], check=True)
+    os.replace(tmp, out)
+    return out
+
+
+def _bind(lib):
+    dp = ctypes.POINTER(ctypes.c_double)
+    ip = ctypes.POINTER(ctypes.c_int)
+    up = ctypes.POINTER(ctypes.c_ubyte)
+    ci, cd = ctypes.c_int, ctypes.c_double
+    lib.oracle_attn_fwd.argtypes = [dp, dp, dp, ip, ci, ci, ci, ci, ci, cd, up, dp, dp]
+    lib.oracle_attn_fwd.restype = ci
+    lib.oracle_attn_bwd.argtypes = [dp, dp, dp, dp, ip, ci, ci, ci, ci, ci, cd, up,
+                                    dp, dp, dp, dp]
+    lib.oracle_attn_bwd.restype = ci
+    lib.oracle_head_matrices.argtypes = [dp, dp, dp, dp, ip, ci, ci, ci, ci, ci, cd,
+                                         ci, ci, dp, dp, dp]
+    lib.oracle_head_matrices.restype = ci
+    return lib
+
+
+def load_oracle(path=None):
+    """Load (building first if absent) the oracle library."""
+    global _lib
+    with _lock:
+        if path is not None:
+            return _bind(ctypes.CDLL(path))
+        if _lib is None:
+            if not os.path.exists(_LIB_PATH) or (
+                    os.path.getmtime(_LIB_PATH) < os.path.getmtime(ORACLE_SRC)):
+                build_oracle()
+            _lib = _bind(ctypes.CDLL(_LIB_PATH))
+        return _lib
+
+
+def _f64(x):
+    return np.ascontiguousarray(np.asarray(x, dtype=np.float64))
+
+
+def _ptr(a, ctype=ctypes.c_double):
+    return a.ctypes.data_as(ctypes.POINTER(ctype))
+
+
+def _prep(Q, K, V, key_len, heads):
+    Q, K, V = _f64(Q), _f64(K), _f64(V)
+    if Q.ndim != 4 or K.shape != Q.shape or V.shape != Q.shape:
+        raise ValueError("Q, K, V must share one [B,H,L,d] shape")
+    B, H, L, d = Q.shape
+    kl = None
+    if key_len is not None:
+        kl = np.ascontiguousarray(np.asarray(key_len, dtype=np.int32))
+        if kl.shape != (B,):
+            raise ValueError("key_len must have shape [B]")
+    mask = None
+    if heads is not None:
+        mask = np.zeros(B * H, dtype=np.uint8)
+        for b, h in heads:
+            mask[b * H + h] = 1
+    return Q, K, V, kl, mask, (B, H, L, d)
+
+
+def oracle_forward(Q, K, V, causal, scale, key_len=None, heads=None, lib=None):
+    """O [B,H,L,d] and LSE [B,H,L] (natural log) in float64.
+
+    heads: optional iterable of (b, h) to compute; other heads are NaN.
+    """
+    lib = lib or load_oracle()
+    Q, K, V, kl, mask, (B, H, L, d) = _prep(Q, K, V, key_len, heads)
+    O = np.full((B, H, L, d), np.nan)
+    LSE = np.full((B, H, L), np.nan)
+    rc = lib.oracle_attn_fwd(_ptr(Q), _ptr(K), _ptr(V),
+                             None if kl is None else _ptr(kl, ctypes.c_int),
+                             B, H, L, d, int(bool(causal)), float(scale),
+                             None if mask is None else _ptr(mask, ctypes.c_ubyte),
+                             _ptr(O), _ptr(LSE))
+    if rc != 0:
+        raise RuntimeError("oracle_attn_fwd failed")
+    return O, LSE
+
+
+def oracle_backward(Q, K, V, dO, causal, scale, key_len=None, heads=None, lib=None):
+    """dQ, dK, dV [B,H,L,d] and D [B,H,L] in float64 (recomputing O and LSE)."""
+    lib = lib or load_oracle()
+    Q, K, V, kl, mask, (B, H, L, d) = _prep(Q, K, V, key_len, heads)
+    dO = _f64(dO)
+    if dO.shape != Q.shape:
+        raise ValueError("dO must have the shape of Q")
+    dQ = np.full((B, H, L, d), np.nan)
+    dK = np.full((B, H, L, d), np.nan)
+    dV = np.full((B, H, L, d), np.nan)
+    D = np.full((B, H, L), np.nan)
+    rc = lib.oracle_attn_bwd(_ptr(Q), _ptr(K), _ptr(V), _ptr(dO),
+                             None if kl is None else _ptr(kl, ctypes.c_int),
+                             B, H, L, d, int(bool(causal)), float(scale),
+                             None if mask is None else _ptr(mask, ctypes.c_ubyte),
+                             _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(D))
+    if rc != 0:
+        raise RuntimeError("oracle_attn_bwd failed")
+    return dQ, dK, dV, D
+
+
+def oracle_head_matrices(Q, K, V, dO, causal, scale, b, h, key_len=None, lib=None):
+    """P, dS [L,L] and Dalt [L] (= sum_j P_ij dP_ij) of head (b, h)."""
+    lib = lib or load_oracle()
+    Q, K, V, kl, _, (B, H, L, d) = _prep(Q, K, V, key_len, None)
+    dO = _f64(dO)
+    P = np.empty((L, L))
+    dS = np.empty((L, L))
+    Dalt = np.empty(L)
+    rc = lib.oracle_head_matrices(_ptr(Q), _ptr(K), _ptr(V), _ptr(dO),
+                                  None if kl is None else _ptr(kl, ctypes.c_int),
+                                  B, H, L, d, int(bool(causal)), float(scale),
+                                  int(b), int(h), _ptr(P), _ptr(dS), _ptr(Dalt))
+    if rc != 0:
+        raise RuntimeError("oracle_head_matrices failed")
+    return P, dS, Dalt

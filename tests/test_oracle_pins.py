@@ -1,0 +1,331 @@
+"""Pins of the CPU oracle against facts fixed by the mathematics of exact
+attention, independent of the oracle's own code: closed forms, library
+routines (scipy softmax/logsumexp, torch autograd in f64), central finite
+differences, brute force with the explicit softmax Jacobian, and invariants.
+
+The paper prints no attention tensors or worked example, so every pin here is
+self-made; tests/test_oracle_mutants.py checks that each plausible planted
+mistake in the oracle fails at least one of these pins.
+"""
+import math
+
+import numpy as np
+import pytest
+import scipy.special
+
+from oracle import oracle_forward, oracle_backward, oracle_head_matrices
+
+RNG = np.random.default_rng(12345)
+
+
+def normwise(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    den = np.max(np.abs(b))
+    num = np.max(np.abs(a - b))
+    return num / den if den > 0 else num
+
+
+def rand(*shape, std=1.0):
+    return RNG.standard_normal(shape) * std
+
+
+def allowed_mask(L, causal, n):
+    i = np.arange(L)[:, None]
+    j = np.arange(L)[None, :]
+    m = j < n
+    if causal:
+        m = m & (j <= i)
+    return np.broadcast_to(m, (L, L))
+
+
+# ---------------------------------------------------------------- forward --
+
+def test_fwd_single_key_returns_value():
+    Q, K, V = rand(2, 3, 1, 5), rand(2, 3, 1, 5), rand(2, 3, 1, 5)
+    for causal in (False, True):
+        O, LSE = oracle_forward(Q, K, V, causal, 0.7)
+        assert np.array_equal(O, V)
+        assert np.allclose(LSE, 0.7 * np.sum(Q * K, axis=-1), rtol=0, atol=1e-15)
+
+
+def test_fwd_zero_scale_gives_prefix_means():
+    B, H, L, d = 2, 2, 9, 3
+    Q, K, V = rand(B, H, L, d), rand(B, H, L, d), rand(B, H, L, d)
+    # causal: row i averages V_0..V_i
+    O, LSE = oracle_forward(Q, K, V, True, 0.0)
+    counts = np.arange(1, L + 1)
+    expect = np.cumsum(V, axis=2) / counts[None, None, :, None]
+    assert normwise(O, expect) < 1e-14
+    assert np.allclose(LSE, np.log(counts)[None, None, :], rtol=0, atol=1e-14)
+    # padded, non-causal: every row averages the first n keys
+    kl = np.array([4, 9], dtype=np.int32)
+    O, LSE = oracle_forward(Q, K, V, False, 0.0, key_len=kl)
+    for b in range(B):
+        n = kl[b]
+        mean = V[b, :, :n, :].mean(axis=1, keepdims=True)
+        assert normwise(O[b], np.broadcast_to(mean, O[b].shape)) < 1e-14
+        assert np.allclose(LSE[b], math.log(n), rtol=0, atol=1e-14)
+
+
+def test_fwd_two_keys_is_logistic():
+    # Two keys: P_i0 = 1 / (1 + exp(s_i1 - s_i0)); LSE = log(e^s0 + e^s1)
+    B, H, L, d = 1, 1, 2, 1
+    Q, K, V = rand(B, H, L, d), rand(B, H, L, d), rand(B, H, L, d)
+    scale = 1.3
+    O, LSE = oracle_forward(Q, K, V, False, scale)
+    for i in range(2):
+        s0 = scale * Q[0, 0, i, 0] * K[0, 0, 0, 0]
+        s1 = scale * Q[0, 0, i, 0] * K[0, 0, 1, 0]
+        p0 = 1.0 / (1.0 + math.exp(s1 - s0))
+        assert abs(O[0, 0, i, 0] - (p0 * V[0, 0, 0, 0] + (1 - p0) * V[0, 0, 1, 0])) < 1e-15
+        hi, lo = max(s0, s1), min(s0, s1)
+        assert abs(LSE[0, 0, i] - (hi + math.log1p(math.exp(lo - hi)))) < 1e-15
+    # causal: row 0 sees only key 0
+    O, LSE = oracle_forward(Q, K, V, True, scale)
+    assert O[0, 0, 0, 0] == V[0, 0, 0, 0]
+    assert abs(LSE[0, 0, 0] - scale * Q[0, 0, 0, 0] * K[0, 0, 0, 0]) < 1e-15
+
+
+def test_fwd_large_scale_is_hard_argmax():
+    B, H, L, d = 1, 2, 12, 4
+    Q, K, V = rand(B, H, L, d), rand(B, H, L, d), rand(B, H, L, d)
+    S = np.einsum("bhid,bhjd->bhij", Q, K)
+    srt = np.sort(S, axis=-1)
+    scale = 80.0 / np.min(srt[..., -1] - srt[..., -2])   # winners clear by e^-80
+    O, _ = oracle_forward(Q, K, V, False, scale)
+    idx = np.argmax(S, axis=-1)
+    expect = np.take_along_axis(V, idx[..., None], axis=2)
+    assert normwise(O, expect) < 1e-12
+
+
+def test_fwd_causal_first_row_is_first_value():
+    Q, K, V = rand(2, 2, 7, 8), rand(2, 2, 7, 8), rand(2, 2, 7, 8)
+    O, LSE = oracle_forward(Q, K, V, True, 0.35)
+    assert np.array_equal(O[:, :, 0, :], V[:, :, 0, :])
+    assert np.allclose(LSE[:, :, 0], 0.35 * np.sum(Q[:, :, 0] * K[:, :, 0], -1),
+                       rtol=0, atol=1e-15)
+
+
+@pytest.mark.parametrize("causal,padded", [(False, False), (True, False), (False, True),
+                                           (True, True)])
+def test_fwd_matches_scipy_softmax(causal, padded):
+    B, H, L, d = 3, 2, 23, 6
+    Q, K, V = rand(B, H, L, d), rand(B, H, L, d), rand(B, H, L, d)
+    kl = np.array([23, 1, 11], dtype=np.int32) if padded else None
+    scale = 1 / math.sqrt(d)
+    O, LSE = oracle_forward(Q, K, V, causal, scale, key_len=kl)
+    for b in range(B):
+        n = L if kl is None else kl[b]
+        m = allowed_mask(L, causal, n)
+        S = scale * np.matmul(Q[b], np.swapaxes(K[b], -1, -2))
+        S = np.where(m, S, -np.inf)
+        P = scipy.special.softmax(S, axis=-1)
+        assert normwise(O[b], np.matmul(P, V[b])) < 1e-13
+        assert normwise(LSE[b], scipy.special.logsumexp(S, axis=-1)) < 1e-14
+
+
+def test_fwd_row_shift_invariance():
+    # A constant added to every score of a row leaves O unchanged and shifts
+    # LSE by that constant.  K has a last column of ones, so adding a to the
+    # last element of Q_i adds scale*a to every S_ij.
+    B, H, L, d = 1, 1, 10, 5
+    Q, K, V = rand(B, H, L, d), rand(B, H, L, d), rand(B, H, L, d)
+    K[..., -1] = 1.0
+    scale = 0.8
+    O1, L1 = oracle_forward(Q, K, V, True, scale)
+    shift = rand(L)
+    Q2 = Q.copy()
+    Q2[0, 0, :, -1] += shift
+    O2, L2 = oracle_forward(Q2, K, V, True, scale)
+    assert normwise(O2, O1) < 1e-14
+    assert np.allclose(L2[0, 0] - L1[0, 0], scale * shift, rtol=0, atol=1e-13)
+
+
+def test_fwd_key_permutation_and_value_linearity():
+    B, H, L, d = 2, 2, 13, 4
+    Q, K, V = rand(B, H, L, d), rand(B, H, L, d), rand(B, H, L, d)
+    perm = RNG.permutation(L)
+    O1, L1 = oracle_forward(Q, K, V, False, 0.6)
+    O2, L2 = oracle_forward(Q, K[:, :, perm], V[:, :, perm], False, 0.6)
+    assert normwise(O2, O1) < 1e-14 and normwise(L2, L1) < 1e-14
+    qp = RNG.permutation(L)
+    O3, _ = oracle_forward(Q[:, :, qp], K, V, False, 0.6)
+    assert normwise(O3, O1[:, :, qp]) < 1e-14
+    V2 = rand(B, H, L, d)
+    Oa, _ = oracle_forward(Q, K, V + 2.5 * V2, True, 0.6)
+    Ob, _ = oracle_forward(Q, K, V, True, 0.6)
+    Oc, _ = oracle_forward(Q, K, V2, True, 0.6)
+    assert normwise(Oa, Ob + 2.5 * Oc) < 1e-13
+
+
+def test_fwd_invariants_from_matrices():
+    B, H, L, d = 2, 2, 17, 4
+    Q, K, V, dO = (rand(B, H, L, d) for _ in range(4))
+    kl = np.array([17, 6], dtype=np.int32)
+    scale = 0.9
+    for causal in (False, True):
+        _, LSE = oracle_forward(Q, K, V, causal, scale, key_len=kl)
+        for b in range(B):
+            for h in range(H):
+                P, dS, Dalt = oracle_head_matrices(Q, K, V, dO, causal, scale, b, h, key_len=kl)
+                m = allowed_mask(L, causal, kl[b])
+                assert np.all(P[~m] == 0.0) and np.all(dS[~m] == 0.0)
+                assert np.max(np.abs(P.sum(axis=1) - 1.0)) < 1e-14
+                assert np.all(P >= 0)
+                S = scale * Q[b, h] @ K[b, h].T
+                S = np.where(m, S, -np.inf)
+                smax = S.max(axis=1)
+                nall = m.sum(axis=1)
+                assert np.all(LSE[b, h] >= smax - 1e-14)
+                assert np.all(LSE[b, h] <= smax + np.log(nall) + 1e-14)
+
+
+def test_fwd_fully_masked_rows():
+    B, H, L, d = 2, 1, 6, 3
+    Q, K, V = rand(B, H, L, d), rand(B, H, L, d), rand(B, H, L, d)
+    kl = np.array([0, 6], dtype=np.int32)
+    for causal in (False, True):
+        O, LSE = oracle_forward(Q, K, V, causal, 0.5, key_len=kl)
+        assert np.all(O[0] == 0.0)
+        assert np.all(LSE[0] == -np.inf)
+        assert np.all(np.isfinite(O[1])) and np.all(np.isfinite(LSE[1]))
+
+
+def test_fwd_head_selection_leaves_others_untouched():
+    Q, K, V = rand(2, 3, 5, 4), rand(2, 3, 5, 4), rand(2, 3, 5, 4)
+    O, LSE = oracle_forward(Q, K, V, True, 0.5, heads=[(1, 2)])
+    Ofull, _ = oracle_forward(Q, K, V, True, 0.5)
+    assert np.array_equal(O[1, 2], Ofull[1, 2])
+    assert np.all(np.isnan(O[0])) and np.all(np.isnan(LSE[1, :2]))
+
+
+# --------------------------------------------------------------- backward --
+
+def _loss(Q, K, V, dO, causal, scale, kl):
+    O, _ = oracle_forward(Q, K, V, causal, scale, key_len=kl)
+    return float(np.sum(dO * O))
+
+
+FD_CASES = [(L, d, causal, padded)
+            for L in (1, 2, 3, 5, 8) for d in (1, 2, 4)
+            for causal, padded in ((False, False), (True, False), (False, True))]
+
+
+@pytest.mark.parametrize("L,d,causal,padded", FD_CASES)
+def test_bwd_central_finite_differences(L, d, causal, padded):
+    B, H = 1, 2
+    Q, K, V, dO = (rand(B, H, L, d) for _ in range(4))
+    kl = np.array([max(1, (L + 1) // 2)], dtype=np.int32) if padded else None
+    scale = 0.77
+    dQ, dK, dV, _ = oracle_backward(Q, K, V, dO, causal, scale, key_len=kl)
+    h = 1e-5
+    for X, G in ((Q, dQ), (K, dK), (V, dV)):
+        num = np.zeros_like(X)
+        it = np.nditer(X, flags=["multi_index"])
+        for _ in it:
+            idx = it.multi_index
+            old = X[idx]
+            X[idx] = old + h
+            fp = _loss(Q, K, V, dO, causal, scale, kl)
+            X[idx] = old - h
+            fm = _loss(Q, K, V, dO, causal, scale, kl)
+            X[idx] = old
+            num[idx] = (fp - fm) / (2 * h)
+        assert np.max(np.abs(num - G)) <= 1e-7 * max(1.0, np.max(np.abs(G)))
+
+
+def _torch_reference(Q, K, V, dO, causal, scale, kl):
+    import torch
+    B, H, L, d = Q.shape
+    q, k, v = (torch.tensor(x, dtype=torch.float64, requires_grad=True) for x in (Q, K, V))
+    S = scale * torch.matmul(q, k.transpose(-1, -2))
+    mask = torch.ones(B, 1, L, L, dtype=torch.bool)
+    if causal:
+        mask &= torch.ones(L, L, dtype=torch.bool).tril()
+    if kl is not None:
+        for b in range(B):
+            mask[b, :, :, int(kl[b]):] = False
+    S = S.masked_fill(~mask, float("-inf"))
+    lse = torch.logsumexp(S, dim=-1)
+    O = torch.matmul(torch.softmax(S, dim=-1), v)
+    O.backward(torch.tensor(dO, dtype=torch.float64))
+    return (O.detach().numpy(), lse.detach().numpy(),
+            q.grad.numpy(), k.grad.numpy(), v.grad.numpy())
+
+
+@pytest.mark.parametrize("causal,padded,L,d", [(True, False, 37, 8), (False, False, 20, 16),
+                                               (False, True, 33, 8), (True, True, 16, 4)])
+def test_fwd_bwd_match_torch_autograd_f64(causal, padded, L, d):
+    B, H = 2, 3
+    Q, K, V, dO = (rand(B, H, L, d) for _ in range(4))
+    kl = np.array([L, max(1, L // 3)], dtype=np.int32) if padded else None
+    scale = 1 / math.sqrt(d)
+    O, LSE = oracle_forward(Q, K, V, causal, scale, key_len=kl)
+    dQ, dK, dV, _ = oracle_backward(Q, K, V, dO, causal, scale, key_len=kl)
+    tO, tL, tdQ, tdK, tdV = _torch_reference(Q, K, V, dO, causal, scale, kl)
+    assert normwise(O, tO) < 1e-13
+    assert normwise(LSE, tL) < 1e-13
+    assert normwise(dQ, tdQ) < 1e-12
+    assert normwise(dK, tdK) < 1e-12
+    assert normwise(dV, tdV) < 1e-12
+
+
+def test_bwd_explicit_softmax_jacobian():
+    B, H, L, d = 2, 2, 19, 5
+    Q, K, V, dO = (rand(B, H, L, d) for _ in range(4))
+    kl = np.array([19, 7], dtype=np.int32)
+    scale = 0.45
+    for causal in (False, True):
+        dQ, dK, dV, _ = oracle_backward(Q, K, V, dO, causal, scale, key_len=kl)
+        for b in range(B):
+            m = allowed_mask(L, causal, kl[b])
+            for h in range(H):
+                S = np.where(m, scale * Q[b, h] @ K[b, h].T, -np.inf)
+                P = scipy.special.softmax(S, axis=-1)
+                dP = dO[b, h] @ V[b, h].T
+                dS = np.stack([(np.diag(P[i]) - np.outer(P[i], P[i])) @ dP[i]
+                               for i in range(L)])
+                assert normwise(dQ[b, h], scale * dS @ K[b, h]) < 1e-12
+                assert normwise(dK[b, h], scale * dS.T @ Q[b, h]) < 1e-12
+                assert normwise(dV[b, h], P.T @ dO[b, h]) < 1e-12
+
+
+def test_bwd_invariants():
+    B, H, L, d = 2, 2, 21, 6
+    Q, K, V, dO = (rand(B, H, L, d) for _ in range(4))
+    kl = np.array([21, 9], dtype=np.int32)
+    scale = 0.6
+    for causal in (False, True):
+        dQ, dK, dV, D = oracle_backward(Q, K, V, dO, causal, scale, key_len=kl)
+        # a common shift of every key changes each score row by a constant
+        assert np.max(np.abs(dK.sum(axis=2))) < 1e-12 * max(1, np.max(np.abs(dK)))
+        # every row's probabilities sum to one
+        assert normwise(dV.sum(axis=2), dO.sum(axis=2)) < 1e-12
+        # padded keys get exactly zero gradient
+        assert np.all(dK[1, :, 9:] == 0.0) and np.all(dV[1, :, 9:] == 0.0)
+        for b in range(B):
+            for h in range(H):
+                P, dS, Dalt = oracle_head_matrices(Q, K, V, dO, causal, scale, b, h,
+                                                   key_len=kl)
+                assert np.max(np.abs(dS.sum(axis=1))) < 1e-13 * max(1, np.abs(dS).max())
+                assert normwise(D[b, h], Dalt) < 1e-13
+
+
+def test_bwd_single_key_special_case():
+    Q, K, V, dO = (rand(2, 2, 1, 4) for _ in range(4))
+    dQ, dK, dV, _ = oracle_backward(Q, K, V, dO, True, 0.5)
+    assert np.array_equal(dV, dO)
+    assert np.max(np.abs(dQ)) < 1e-15 and np.max(np.abs(dK)) < 1e-15
+
+
+def test_bwd_linear_in_upstream_gradient_and_masked_batch():
+    B, H, L, d = 2, 2, 11, 4
+    Q, K, V, dO = (rand(B, H, L, d) for _ in range(4))
+    kl = np.array([0, 11], dtype=np.int32)
+    g1 = oracle_backward(Q, K, V, dO, True, 0.5, key_len=kl)
+    g2 = oracle_backward(Q, K, V, 2 * dO, True, 0.5, key_len=kl)
+    for a, b in zip(g1[:3], g2[:3]):
+        assert np.array_equal(2 * a, b)
+    for g in g1[:3]:
+        assert np.all(g[0] == 0.0)
