@@ -1,0 +1,254 @@
+"""Throughput of attention forward + backward on one MI355X.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload 3]
+
+One step is the whole hot path on one batch: mg_attn_fwd (O, LSE) followed
+by mg_attn_bwd (D = rowsum(dO o O), the dK/dV kernel, the dQ kernel), with
+every input resident in HBM before the timed region.  The timed region is
+exactly `steps` steps, bracketed by device synchronization.  FLOPs are
+credited only for what exact attention must compute on unmasked (i, j)
+pairs: 4d per pair forward (Q K^T and P V) and 10d per pair backward (the
+score recompute, dP, dV, dK and dQ products).
+
+Rank 0 prints one JSON line.  Besides the contract fields it carries
+`roofline` for the dominant kernel (its algorithmic FLOPs per launch over its
+average duration, timed with HIP events on the launch stream inside the timed
+region), `cpu_baseline` (the f64 oracle on the host's cores, same workload),
+and `parity` (the timed run's outputs against the oracle).
+"""
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "attention fwd+bwd TFLOP/s (strict f32) at B8 H8 L1024 d64; % MFMA peak"
+PEAK_TFLOPS = {"strict_f32": 157.3, "fast_bf16": 2516.6}   # MI355X dense MFMA
+HBM_PEAK_GBS = 8000.0
+KERNEL_SOURCES = {"strict_f32": "paper_2608_01563_amd/csrc/attn_f32.hip",
+                  "fast_bf16": "paper_2608_01563_amd/csrc/attn_bf16.hip"}
+COUNTER_FILE = "profiles/hbm_traffic_{kernel}.json"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=3,
+                    help="workload id (3 = causal B8 H8 L1024 d64 strict f32)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-repeats", type=int, default=3)
+    ap.add_argument("--no-kernel-events", action="store_true",
+                    help="do not bracket kernels with events (no roofline)")
+    return ap.parse_args()
+
+
+def sha256_of(path):
+    with open(os.path.join(ROOT, path), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def kernel_work(name, w, pairs, rows):
+    """Algorithmic work of one launch of kernel `name`: (amount, unit, bound)."""
+    d, es = w.d, (4 if w.contract == "strict_f32" else 2)
+    if name.startswith("attn_fwd"):
+        return 4.0 * d * pairs, "flop", "mfma"
+    if name.startswith("attn_dkdv"):
+        return 8.0 * d * pairs, "flop", "mfma"        # S recompute, dV, dP, dK
+    if name.startswith("attn_dq"):
+        return 2.0 * d * pairs, "flop", "mfma"        # the dQ product itself
+    if name.startswith("attn_rowdot"):
+        n = w.B * w.H * w.L * d
+        return 2.0 * n * es + 4.0 * rows, "byte", "hbm"
+    raise KeyError(name)
+
+
+def traffic_for(kernel, contract):
+    """HBM bytes per launch from committed counter runs, or None if absent or
+    taken on a different kernel source."""
+    path = os.path.join(ROOT, COUNTER_FILE.format(kernel=kernel))
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_sha256") != sha256_of(KERNEL_SOURCES[contract]):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py: this build runs on one GPU only; --gpus %d is not supported "
+              "(B*H heads shard across GPUs with no exchange, see the design notes)"
+              % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2608_01563_amd as mg
+    from workloads import WORKLOADS, workload_inputs, unmasked_pairs
+
+    w = WORKLOADS[args.workload]
+    x = workload_inputs(args.workload)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def dev_tensor(name):
+        if w.contract == "fast_bf16":
+            return torch.from_numpy(x.bits[name].view(np.int16).copy()).to(dev).view(
+                torch.bfloat16)
+        return torch.from_numpy(getattr(x, name).copy()).to(dev)
+
+    Q, K, V, dO = (dev_tensor(n) for n in ("Q", "K", "V", "dO"))
+    kl = None if x.key_len is None else torch.from_numpy(x.key_len.copy()).to(dev)
+    O = torch.empty_like(Q)
+    LSE = torch.empty(Q.shape[:3], dtype=torch.float32, device=dev)
+    dQ, dK, dV = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
+    ws = torch.empty(mg.mg_attn_bwd_workspace_bytes(w.B, w.H, w.L, w.d, w.causal, w.contract),
+                     dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        mg.mg_attn_fwd(Q, K, V, O, LSE, kl, causal=w.causal, scale=w.scale,
+                       contract=w.contract, stream=stream)
+        mg.mg_attn_bwd(Q, K, V, O, LSE, dO, dQ, dK, dV, kl, causal=w.causal, scale=w.scale,
+                       contract=w.contract, workspace=ws, stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    use_events = not args.no_kernel_events
+    if use_events:
+        mg.mg_profile_reset()
+        mg.mg_profile_enable(True)
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    stops = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        starts[k].record(stream)
+        step()
+        stops[k].record(stream)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kernels = {}
+    if use_events:
+        mg.mg_profile_enable(False)
+        kernels = mg.mg_profile_collect()
+    samples = sorted(a.elapsed_time(b) for a, b in zip(starts, stops))
+
+    pairs = unmasked_pairs(w.B, w.H, w.L, w.causal, x.key_len)
+    rows = w.B * w.H * w.L
+    flops = 14.0 * w.d * pairs
+    ms_per_step = elapsed * 1e3 / args.steps
+    value = flops / (ms_per_step * 1e-3) / 1e12
+
+    out = {
+        "metric": METRIC if args.workload == 3 else
+        "attention fwd+bwd TFLOP/s (%s) at %s" % (w.contract, w.name),
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if w.contract == "strict_f32" else "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "L": w.L, "d": w.d,
+                   "causal": w.causal, "key_padding": w.padded, "contract": w.contract,
+                   "unmasked_pairs": pairs, "credited_gflop_per_step": flops / 1e9},
+        "step_ms": {"median": round(float(np.median(samples)), 4),
+                    "q1": round(float(np.percentile(samples, 25)), 4),
+                    "q3": round(float(np.percentile(samples, 75)), 4),
+                    "min": round(samples[0], 4), "max": round(samples[-1], 4)},
+        "pct_of_mfma_peak": round(100.0 * value / PEAK_TFLOPS[w.contract], 2),
+    }
+
+    if kernels:
+        per = {}
+        for name, (n, total) in kernels.items():
+            avg = total / n
+            amount, unit, bound = kernel_work(name, w, pairs, rows)
+            rate = amount / (avg * 1e-3) / (1e12 if unit == "flop" else 1e9)
+            per[name] = {"launches": n, "avg_ms": round(avg, 5), "bound": bound,
+                         "achieved": round(rate, 3),
+                         "unit": "TFLOP/s" if unit == "flop" else "GB/s"}
+        out["kernels"] = per
+        dom = max(kernels, key=lambda k: kernels[k][1])
+        n, total = kernels[dom]
+        amount, unit, bound = kernel_work(dom, w, pairs, rows)
+        avg_s = total / n * 1e-3
+        if unit == "flop":
+            ach, peak, u = amount / avg_s / 1e12, PEAK_TFLOPS[w.contract], "TFLOP/s"
+        else:
+            ach, peak, u = amount / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
+        out["roofline"] = {"kernel": dom, "bound": bound, "achieved": round(ach, 3),
+                           "peak": peak, "unit": u, "frac": round(ach / peak, 4),
+                           "traffic": traffic_for(dom, w.contract),
+                           "algorithmic_per_launch": amount}
+        out["bwd_credited_tflops"] = round(
+            10.0 * w.d * pairs / (sum(kernels[k][1] / kernels[k][0] for k in kernels
+                                      if not k.startswith("attn_fwd")) * 1e-3) / 1e12, 3)
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"], out["parity"] = cpu_baseline(args, w, x, pairs,
+                                                          (O, LSE, dQ, dK, dV))
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(args, w, x, pairs, gpu_outputs):
+    """Time the f64 oracle on this host over the whole workload (or a head
+    sample for the largest one), and compare the timed run's outputs to it."""
+    import numpy as np
+    from oracle import oracle_forward, oracle_backward, oracle_num_threads
+    B, H = w.B, w.H
+    heads = None
+    if B * H * w.L * w.L * w.d > 2 ** 33:          # keep the CPU leg to seconds
+        heads = [(b, h) for b in range(B) for h in range(H)][:: max(1, (B * H) // 4)][:4]
+    times = []
+    for _ in range(max(1, args.cpu_repeats)):
+        t0 = time.perf_counter()
+        O, LSE = oracle_forward(x.Q, x.K, x.V, w.causal, w.scale, key_len=x.key_len, heads=heads)
+        dQ, dK, dV, _ = oracle_backward(x.Q, x.K, x.V, x.dO, w.causal, w.scale,
+                                        key_len=x.key_len, heads=heads)
+        times.append(time.perf_counter() - t0)
+    t = float(np.median(times))
+    frac = 1.0 if heads is None else len(heads) / float(B * H)
+    value = 14.0 * w.d * pairs * frac / t / 1e12
+    sample = ("whole workload (%d heads), fwd+bwd, median of %d runs, %.2f s each"
+              % (B * H, len(times), t)) if heads is None else (
+        "%d of %d heads, fwd+bwd, median of %d runs, %.2f s each"
+        % (len(heads), B * H, len(times), t))
+    base = {"value": round(value, 6), "unit": "TFLOP/s", "cores": oracle_num_threads(),
+            "kind": "oracle", "sample": sample}
+    ref = {"O": O, "LSE": LSE, "dQ": dQ, "dK": dK, "dV": dV}
+    parity = {}
+    for name, tens in zip(("O", "LSE", "dQ", "dK", "dV"), gpu_outputs):
+        g = tens.detach().float().cpu().numpy().astype(np.float64)
+        r = ref[name]
+        if heads is not None:
+            g = np.stack([g[b, h] for b, h in heads])
+            r = np.stack([r[b, h] for b, h in heads])
+        fin = np.isfinite(r)
+        den = np.max(np.abs(r[fin])) if fin.any() else 1.0
+        parity[name] = float(np.max(np.abs(g[fin] - r[fin])) / den) if fin.any() else 0.0
+    parity["tolerance"] = 1e-4 if w.contract == "strict_f32" else 2e-2
+    parity["pass"] = all(v <= parity["tolerance"] for k, v in parity.items()
+                         if k in ("O", "LSE", "dQ", "dK", "dV"))
+    return base, parity
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,142 @@
+/*
+ * mg_attn.h -- C ABI of the MI355X (gfx950) attention library.
+ *
+ * Multi-head scaled-dot-product attention, forward and backward, as the
+ * paper's tiled attention forward kernel, fused dK+dV kernel and dQ kernel
+ * (Sec. 3.3 "Kernel archetypes and specialization"; Sec. 7.3, where the
+ * backward pair is the largest measured cost of the Whisper training step).
+ * The operation is exact attention:
+ *
+ *   allowed(i,j) = (!causal || j <= i) && j < key_len[b]
+ *   S = scale * Q K^T,  P = softmax over allowed j (masked P is exactly 0)
+ *   O = P V,  LSE_i = ln sum_j exp(S_ij)      (natural log)
+ *   D_i = sum_k dO_ik O_ik,  dP = dO V^T,  dS = P o (dP - D)
+ *   dQ = scale * dS K,  dK = scale * dS^T Q,  dV = P^T dO
+ *
+ * Arithmetic contracts (Sec. 4.2 "Arithmetic contracts", Table of arithmetic
+ * permissions):
+ *   MG_CONTRACT_STRICT_F32  every tensor f32; products on f32 matrix cores
+ *                           with f32 accumulation (the paper's --strict mode).
+ *   MG_CONTRACT_FAST_BF16   Q,K,V,O,dO,dQ,dK,dV are bf16; products run on
+ *                           bf16 matrix cores with f32 accumulation, P and dS
+ *                           are rounded to bf16 (nearest even) as operands;
+ *                           outputs are rounded to bf16 (nearest even).  The
+ *                           paper's reduced-input mode uses f16 and keeps the
+ *                           backward f32; this contract uses bf16 (f32
+ *                           exponent range) for both passes.
+ *   LSE and the workspace are always f32.
+ *
+ * Layout: Q, K, V, O, dO, dQ, dK, dV are contiguous [B][H][L][d] with d
+ * fastest; LSE is [B][H][L].  key_len is an int32 device array [B] or NULL
+ * (no padding); its values are clamped to [0, L] on the device.  A row with
+ * no allowed key (key_len[b] == 0) yields O = 0, LSE = -inf and zero
+ * gradients.  Causal masking is top-left aligned (equal query/key length).
+ *
+ * Ownership: the caller owns every buffer, including the backward workspace.
+ * The library allocates no device memory, keeps no per-call state and is
+ * reentrant.  All pointers except key_len must be device pointers, 16-byte
+ * aligned.  Outputs must not alias inputs (not checked; undefined results).
+ *
+ * Asynchrony: every call enqueues kernels on `stream` and returns without
+ * synchronizing.  Results are valid once the stream reaches that point.
+ *
+ * Errors: argument errors are detected on the host before anything is
+ * enqueued; the call then returns a non-MG_OK status and enqueues nothing.
+ * Launch failures return MG_ERR_HIP.  mg_last_error_detail() gives a
+ * message for the last failing call on the calling thread.
+ */
+#ifndef MG_ATTN_H
+#define MG_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    MG_CONTRACT_STRICT_F32 = 0,
+    MG_CONTRACT_FAST_BF16 = 1
+} mg_contract_t;
+
+typedef enum {
+    MG_OK = 0,
+    MG_ERR_INVALID_ARGUMENT = 1, /* null pointer, size < 1, non-finite scale,
+                                    bad contract, B*H*L*d > 2^31-1         */
+    MG_ERR_UNSUPPORTED = 2,      /* head dimension d not in {32, 64, 128}   */
+    MG_ERR_MISALIGNED = 3,       /* a tensor pointer not 16-byte aligned    */
+    MG_ERR_WORKSPACE = 4,        /* backward workspace missing or too small */
+    MG_ERR_HIP = 5               /* a HIP runtime call or launch failed     */
+} mg_status_t;
+
+/*
+ * Forward pass: O and LSE from Q, K, V (the paper's tiled attention forward,
+ * Sec. 3.3).  Inputs Q, K, V [B][H][L][d]; outputs O [B][H][L][d] and LSE
+ * [B][H][L] (f32, natural log, saved for the backward pass).  Element type of
+ * Q, K, V, O follows `contract`.  `scale` multiplies Q K^T (typically
+ * 1/sqrt(d)); it must be finite.
+ */
+mg_status_t mg_attn_fwd(const void *Q, const void *K, const void *V,
+                        void *O, float *LSE,
+                        const int32_t *key_len,
+                        int B, int H, int L, int d, int causal, float scale,
+                        mg_contract_t contract, hipStream_t stream);
+
+/*
+ * Bytes of device workspace that mg_attn_bwd needs for these arguments
+ * (f32 D = rowsum(dO o O), one per query row, rounded up to 256 bytes).
+ * Returns 0 when the arguments are invalid.
+ */
+size_t mg_attn_bwd_workspace_bytes(int B, int H, int L, int d, int causal,
+                                   mg_contract_t contract);
+
+/*
+ * Backward pass: dQ, dK, dV from Q, K, V, the forward outputs O and LSE, and
+ * the upstream gradient dO (the paper's attention derivative node, Sec. 3.1,
+ * lowered to a fused dK+dV kernel and a separate dQ kernel, Sec. 3.3 and
+ * Sec. 8).  P is recomputed from Q, K and the saved LSE; nothing of size
+ * L x L is stored.  `workspace` is caller-owned device memory of at least
+ * mg_attn_bwd_workspace_bytes(...) bytes; its contents on entry are ignored
+ * and on return are unspecified.  dK and dV rows of masked (padded) keys are
+ * written as exact zeros.  Deterministic: no atomics, bitwise identical
+ * results for identical inputs.
+ */
+mg_status_t mg_attn_bwd(const void *Q, const void *K, const void *V,
+                        const void *O, const float *LSE, const void *dO,
+                        void *dQ, void *dK, void *dV,
+                        const int32_t *key_len,
+                        int B, int H, int L, int d, int causal, float scale,
+                        mg_contract_t contract,
+                        void *workspace, size_t workspace_bytes,
+                        hipStream_t stream);
+
+/* Static, human-readable name of a status code. */
+const char *mg_status_string(mg_status_t status);
+
+/* Message describing the last failing call on the calling thread ("" if the
+ * last call succeeded).  Valid until the next call on that thread. */
+const char *mg_last_error_detail(void);
+
+/*
+ * Kernel timing for measurement tools (not needed for computation).  While
+ * enabled, every kernel the library launches is bracketed by a pair of HIP
+ * events recorded on the launch stream.  mg_profile_collect waits for the
+ * recorded events, adds each kernel's durations to per-kernel totals, and
+ * copies up to `max_entries` totals (name, launches, total milliseconds)
+ * into the caller's arrays; it returns the number of distinct kernels
+ * (which may exceed max_entries) or -1 on a HIP error.  mg_profile_reset
+ * clears the totals.  Enabling and collecting are process-wide and
+ * serialized by a mutex; events are created lazily and reused.
+ */
+mg_status_t mg_profile_enable(int enable);
+int mg_profile_collect(const char **names, int64_t *launches, double *total_ms,
+                       int max_entries);
+void mg_profile_reset(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MG_ATTN_H */

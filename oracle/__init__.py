@@ -15,5 +15,6 @@ from .oracle import (  # noqa: F401
     oracle_forward,
     oracle_backward,
     oracle_head_matrices,
+    oracle_num_threads,
     ORACLE_SRC,
 )

@@ -48,6 +48,9 @@
  */
 #include <math.h>
 #include <stddef.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 #include <stdlib.h>
 #include <string.h>
 
@@ -233,4 +236,14 @@ int oracle_head_matrices(const double *Q, const double *K, const double *V,
     }
     free(S); free(O); free(LSE);
     return 0;
+}
+
+/* Number of threads the parallel loops above use (1 without OpenMP). */
+int oracle_num_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
 }

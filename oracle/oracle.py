@@ -42,6 +42,8 @@ def _bind(lib):
     lib.oracle_head_matrices.argtypes = [dp, dp, dp, dp, ip, ci, ci, ci, ci, ci, cd,
                                          ci, ci, dp, dp, dp]
     lib.oracle_head_matrices.restype = ci
+    lib.oracle_num_threads.argtypes = []
+    lib.oracle_num_threads.restype = ci
     return lib
 
 
@@ -123,6 +125,11 @@ def oracle_backward(Q, K, V, dO, causal, scale, key_len=None, heads=None, lib=No
     if rc != 0:
         raise RuntimeError("oracle_attn_bwd failed")
     return dQ, dK, dV, D
+
+
+def oracle_num_threads(lib=None):
+    """Threads the oracle's parallel loops use."""
+    return int((lib or load_oracle()).oracle_num_threads())
 
 
 def oracle_head_matrices(Q, K, V, dO, causal, scale, b, h, key_len=None, lib=None):

@@ -1,0 +1,225 @@
+"""ctypes binding of libmgattn.so: argument marshalling only.
+
+Every function here checks the torch tensors it is given (device, dtype,
+shape, contiguity), passes their device pointers and the current HIP stream
+to the C entry point of the same name, and raises MgError on a non-MG_OK
+status.  No arithmetic of the attention path happens here; if the library is
+missing, load_library() raises instead of falling back to anything.
+"""
+import ctypes
+import os
+import threading
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmgattn.so")
+HEADER_PATH = os.path.join(os.path.dirname(HERE), "include", "mg_attn.h")
+
+STRICT_F32 = 0
+FAST_BF16 = 1
+CONTRACTS = {"strict_f32": STRICT_F32, "fast_bf16": FAST_BF16}
+
+MG_OK = 0
+STATUS_NAMES = {0: "MG_OK", 1: "MG_ERR_INVALID_ARGUMENT", 2: "MG_ERR_UNSUPPORTED",
+                3: "MG_ERR_MISALIGNED", 4: "MG_ERR_WORKSPACE", 5: "MG_ERR_HIP"}
+
+_lock = threading.Lock()
+_lib = None
+
+
+class MgError(RuntimeError):
+    def __init__(self, status, detail):
+        self.status = status
+        self.detail = detail
+        super().__init__("%s: %s" % (STATUS_NAMES.get(status, status), detail))
+
+
+def _declare(lib):
+    vp, c_int, c_float, c_size = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    lib.mg_attn_fwd.argtypes = [vp, vp, vp, vp, vp, vp, c_int, c_int, c_int, c_int, c_int,
+                                c_float, c_int, vp]
+    lib.mg_attn_fwd.restype = c_int
+    lib.mg_attn_bwd_workspace_bytes.argtypes = [c_int, c_int, c_int, c_int, c_int, c_int]
+    lib.mg_attn_bwd_workspace_bytes.restype = c_size
+    lib.mg_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, c_int, c_int, c_int,
+                                c_int, c_int, c_float, c_int, vp, c_size, vp]
+    lib.mg_attn_bwd.restype = c_int
+    lib.mg_status_string.argtypes = [c_int]
+    lib.mg_status_string.restype = ctypes.c_char_p
+    lib.mg_last_error_detail.argtypes = []
+    lib.mg_last_error_detail.restype = ctypes.c_char_p
+    lib.mg_profile_enable.argtypes = [c_int]
+    lib.mg_profile_enable.restype = c_int
+    lib.mg_profile_collect.argtypes = [ctypes.POINTER(ctypes.c_char_p),
+                                       ctypes.POINTER(ctypes.c_int64),
+                                       ctypes.POINTER(ctypes.c_double), c_int]
+    lib.mg_profile_collect.restype = c_int
+    lib.mg_profile_reset.argtypes = []
+    lib.mg_profile_reset.restype = None
+    return lib
+
+
+def load_library(path=LIB_PATH):
+    """Load libmgattn.so (after torch, so both share one HIP runtime)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            import torch  # noqa: F401  (brings in the HIP runtime the library binds to)
+            if not os.path.exists(path):
+                raise RuntimeError(
+                    "libmgattn.so is not built (%s); run `python -m "
+                    "paper_2608_01563_amd.build` or __graft_entry__.build()" % path)
+            _lib = _declare(ctypes.CDLL(path))
+        return _lib
+
+
+def _check(status):
+    if status != MG_OK:
+        raise MgError(status, load_library().mg_last_error_detail().decode())
+
+
+def _contract_id(contract):
+    if isinstance(contract, str):
+        return CONTRACTS[contract]
+    return int(contract)
+
+
+def _stream_handle(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _check_tensors(contract, ref, named):
+    import torch
+    want = torch.float32 if contract == STRICT_F32 else torch.bfloat16
+    for name, t in named:
+        if not t.is_cuda:
+            raise ValueError("%s must be a GPU tensor" % name)
+        if t.dtype != want:
+            raise ValueError("%s has dtype %s, contract needs %s" % (name, t.dtype, want))
+        if tuple(t.shape) != tuple(ref.shape):
+            raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape),
+                                                               tuple(ref.shape)))
+        if not t.is_contiguous():
+            raise ValueError("%s must be contiguous" % name)
+
+
+def _check_lse(LSE, shape):
+    import torch
+    if not LSE.is_cuda or LSE.dtype != torch.float32 or tuple(LSE.shape) != tuple(shape[:3]) \
+            or not LSE.is_contiguous():
+        raise ValueError("LSE must be a contiguous float32 GPU tensor of shape %s"
+                         % (tuple(shape[:3]),))
+
+
+def _check_key_len(key_len, B):
+    import torch
+    if key_len is None:
+        return
+    if not key_len.is_cuda or key_len.dtype != torch.int32 or tuple(key_len.shape) != (B,) \
+            or not key_len.is_contiguous():
+        raise ValueError("key_len must be a contiguous int32 GPU tensor of shape [%d]" % B)
+
+
+def mg_attn_fwd(Q, K, V, O, LSE, key_len=None, *, causal, scale, contract=STRICT_F32,
+                stream=None):
+    """Forward pass into caller-provided O [B,H,L,d] and LSE [B,H,L]."""
+    lib = load_library()
+    c = _contract_id(contract)
+    if Q.dim() != 4:
+        raise ValueError("Q must be [B,H,L,d]")
+    B, H, L, d = Q.shape
+    _check_tensors(c, Q, (("Q", Q), ("K", K), ("V", V), ("O", O)))
+    _check_lse(LSE, Q.shape)
+    _check_key_len(key_len, B)
+    _check(lib.mg_attn_fwd(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(LSE), _ptr(key_len),
+                           B, H, L, d, int(bool(causal)), float(scale), c,
+                           _stream_handle(stream)))
+
+
+def mg_attn_bwd_workspace_bytes(B, H, L, d, causal, contract=STRICT_F32):
+    return int(load_library().mg_attn_bwd_workspace_bytes(B, H, L, d, int(bool(causal)),
+                                                          _contract_id(contract)))
+
+
+def mg_attn_bwd(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len=None, *, causal, scale,
+                contract=STRICT_F32, workspace=None, stream=None):
+    """Backward pass into caller-provided dQ, dK, dV.  `workspace` is a GPU
+    tensor of at least mg_attn_bwd_workspace_bytes(...) bytes; when None, one
+    is allocated here with torch (the library itself never allocates)."""
+    import torch
+    lib = load_library()
+    c = _contract_id(contract)
+    if Q.dim() != 4:
+        raise ValueError("Q must be [B,H,L,d]")
+    B, H, L, d = Q.shape
+    _check_tensors(c, Q, (("Q", Q), ("K", K), ("V", V), ("O", O), ("dO", dO), ("dQ", dQ),
+                          ("dK", dK), ("dV", dV)))
+    _check_lse(LSE, Q.shape)
+    _check_key_len(key_len, B)
+    need = mg_attn_bwd_workspace_bytes(B, H, L, d, causal, c)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=Q.device)
+    nbytes = workspace.numel() * workspace.element_size()
+    _check(lib.mg_attn_bwd(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(LSE), _ptr(dO), _ptr(dQ),
+                           _ptr(dK), _ptr(dV), _ptr(key_len), B, H, L, d, int(bool(causal)),
+                           float(scale), c, _ptr(workspace), nbytes, _stream_handle(stream)))
+
+
+def mg_status_string(status):
+    return load_library().mg_status_string(int(status)).decode()
+
+
+def mg_last_error_detail():
+    return load_library().mg_last_error_detail().decode()
+
+
+def mg_profile_enable(enable=True):
+    _check(load_library().mg_profile_enable(int(bool(enable))))
+
+
+def mg_profile_reset():
+    load_library().mg_profile_reset()
+
+
+def mg_profile_collect(max_entries=32):
+    """{kernel name: (launches, total_ms)} accumulated since the last reset."""
+    lib = load_library()
+    names = (ctypes.c_char_p * max_entries)()
+    launches = (ctypes.c_int64 * max_entries)()
+    total = (ctypes.c_double * max_entries)()
+    n = lib.mg_profile_collect(names, launches, total, max_entries)
+    if n < 0:
+        raise MgError(5, lib.mg_last_error_detail().decode())
+    return {names[i].decode(): (int(launches[i]), float(total[i]))
+            for i in range(min(n, max_entries))}
+
+
+# ------------------------------------------------------------ conveniences --
+def attention_forward(Q, K, V, *, causal, scale, key_len=None, contract=None, stream=None):
+    """Allocate O and LSE with torch and run mg_attn_fwd; returns (O, LSE)."""
+    import torch
+    c = _contract_id(contract) if contract is not None else (
+        FAST_BF16 if Q.dtype == torch.bfloat16 else STRICT_F32)
+    O = torch.empty_like(Q)
+    LSE = torch.empty(Q.shape[:3], dtype=torch.float32, device=Q.device)
+    mg_attn_fwd(Q, K, V, O, LSE, key_len, causal=causal, scale=scale, contract=c,
+                stream=stream)
+    return O, LSE
+
+
+def attention_backward(Q, K, V, O, LSE, dO, *, causal, scale, key_len=None, contract=None,
+                       workspace=None, stream=None):
+    """Allocate dQ, dK, dV with torch and run mg_attn_bwd; returns (dQ, dK, dV)."""
+    import torch
+    c = _contract_id(contract) if contract is not None else (
+        FAST_BF16 if Q.dtype == torch.bfloat16 else STRICT_F32)
+    dQ, dK, dV = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
+    mg_attn_bwd(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len, causal=causal, scale=scale,
+                contract=c, workspace=workspace, stream=stream)
+    return dQ, dK, dV

@@ -1,0 +1,527 @@
+// attn_f32.hip -- strict-f32 attention kernels for gfx950 (f32 MFMA).
+//
+// The paper's attention archetype is three kernels: a tiled forward, a dQ
+// kernel and a fused dK+dV kernel (Sec. 3.3; Sec. 8 makes the fused dK+dV
+// kernel a compiler invariant; Sec. 7.3 profiles the backward pair).  Here:
+//
+//   attn_fwd_f32      query tile stationary, streams K/V tiles, online
+//                     softmax in base 2, writes O and LSE (natural log).
+//   attn_rowdot_f32   D_i = sum_k dO_ik O_ik (HBM-bound row reduction).
+//   attn_dkdv_f32     key tile stationary: recomputes P from LSE, then
+//                     dV += P^T dO, dP = dO V^T, dS = P(dP - D), dK += dS^T Q.
+//   attn_dq_f32       query tile stationary: recomputes P and dS, then
+//                     dQ += dS K.  Separate from dK/dV, so no atomics and
+//                     bitwise-reproducible results.
+//
+// Every product runs on v_mfma_f32_16x16x4_f32 (f32 inputs, f32 accumulate),
+// which is what the strict contract permits (Sec. 4.2).  Each wave owns 16
+// rows of the stationary tile (one per lane column l%16); the other operand
+// is staged through LDS and shared by the four waves of a workgroup.
+//
+// Workgroup order: the 1-D grid is numbered rank-major over heads
+// (id = rank * B*H + head) with rank 0 the tile that has the most work under
+// a causal mask, so the longest tiles start first; with B*H a multiple of 8
+// every tile of a head lands on the same XCD (workgroups are dealt to the
+// eight XCDs round-robin), so a head's K/V or Q/dO stay in one L2.
+#include "device_common.h"
+#include "launch.h"
+#include "tiles_f32.h"
+
+namespace mg {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kStatRows = 16 * kWaves;   // stationary rows per workgroup
+constexpr int kStream = 64;              // streamed rows per step
+
+// ---------------------------------------------------------------- forward --
+template <int D>
+__global__ __launch_bounds__(kThreads) void attn_fwd_f32(
+    const float *__restrict__ Q, const float *__restrict__ K, const float *__restrict__ V,
+    float *__restrict__ O, float *__restrict__ LSE, const int32_t *__restrict__ key_len,
+    int H, int L, int causal, float scale_log2, int n_qtiles, int BH) {
+    constexpr int DQ = D / 4;    // contraction values per lane in one S chain
+    constexpr int NC = D / 16;   // 16-column blocks of the head dimension
+    using Stager = F32TileStager<kStream, D, kThreads>;
+    constexpr int LD = Stager::kLd;
+    __shared__ __attribute__((aligned(16))) float Ks[kStream][LD];
+    __shared__ __attribute__((aligned(16))) float Vs[kStream][LD];
+
+    const int rank = blockIdx.x / BH;
+    const int head = blockIdx.x - rank * BH;
+    const int qt = causal ? (n_qtiles - 1 - rank) : rank;
+    const int b = head / H;
+    const float *Qh = Q + (size_t)head * L * D;
+    const float *Kh = K + (size_t)head * L * D;
+    const float *Vh = V + (size_t)head * L * D;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int il = lane & 15;
+    const int g = lane >> 4;
+    const int q0 = qt * kStatRows;
+    const int qi = q0 + 16 * (tid >> 6) + il;
+
+    const int klen = key_limit(key_len, b, L);
+    const int kend = causal ? min(klen, q0 + kStatRows) : klen;
+    const int ntiles = (kend + kStream - 1) / kStream;
+
+    // B operand of S^T = K Q^T: lane holds Q[qi][g*DQ + s].
+    float qreg[DQ];
+#pragma unroll
+    for (int s4 = 0; s4 < DQ / 4; ++s4) {
+        f32x4 v = (qi < L) ? *reinterpret_cast<const f32x4 *>(Qh + (size_t)qi * D + g * DQ + 4 * s4)
+                           : zero4();
+#pragma unroll
+        for (int e = 0; e < 4; ++e) qreg[4 * s4 + e] = v[e];
+    }
+
+    float m_run = -INFINITY;   // running max of this lane's row, base-2 units
+    float l_run = 0.f;         // this lane's share of the row sum
+    f32x4 oacc[NC];            // O^T[16c + 4g + r][qi]
+#pragma unroll
+    for (int c = 0; c < NC; ++c) oacc[c] = zero4();
+
+    Stager kst, vst;
+    if (ntiles > 0) {
+        kst.load(Kh, 0, L, tid);
+        vst.load(Vh, 0, L, tid);
+    }
+    for (int kt = 0; kt < ntiles; ++kt) {
+        __syncthreads();
+        kst.store(Ks, tid);
+        vst.store(Vs, tid);
+        __syncthreads();
+        if (kt + 1 < ntiles) {
+            kst.load(Kh, (kt + 1) * kStream, L, tid);
+            vst.load(Vh, (kt + 1) * kStream, L, tid);
+        }
+
+        // S^T[16jb + 4g + r][qi] = sum_k K[j][k] Q[qi][k]
+        f32x4 sacc[4];
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb) sacc[jb] = zero4();
+#pragma unroll
+        for (int s4 = 0; s4 < DQ / 4; ++s4) {
+            f32x4 a[4];
+#pragma unroll
+            for (int jb = 0; jb < 4; ++jb)
+                a[jb] = *reinterpret_cast<const f32x4 *>(&Ks[16 * jb + il][g * DQ + 4 * s4]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int jb = 0; jb < 4; ++jb)
+                    sacc[jb] = mfma16x16x4(a[jb][e], qreg[4 * s4 + e], sacc[jb]);
+        }
+
+        // Mask, scale to base 2, and update the running max and sum.
+        const int j0 = kt * kStream + 4 * g;
+        float mx = -INFINITY;
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int j = j0 + 16 * jb + r;
+                const bool ok = (j < klen) && (!causal || j <= qi);
+                const float t = ok ? sacc[jb][r] * scale_log2 : -INFINITY;
+                sacc[jb][r] = t;
+                mx = fmaxf(mx, t);
+            }
+        mx = max_over_groups(mx);
+        const float m_new = fmaxf(m_run, mx);
+        const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+        const float alpha = exp2_fast(m_run - m_use);
+        float psum = 0.f;
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const float p = exp2_fast(sacc[jb][r] - m_use);
+                sacc[jb][r] = p;
+                psum += p;
+            }
+        l_run = l_run * alpha + psum;
+        m_run = m_new;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) oacc[c] *= alpha;
+
+        // O^T[16c + 4g + r][qi] += sum_j V[j][16c + il'] P^T[j][qi]
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int c = 0; c < NC; ++c)
+                    oacc[c] = mfma16x16x4(Vs[16 * jb + 4 * g + r][16 * c + il], sacc[jb][r],
+                                          oacc[c]);
+    }
+
+    const float l = sum_over_groups(l_run);
+    if (qi < L) {
+        const float inv = (l > 0.f) ? 1.f / l : 0.f;
+        float *orow = O + ((size_t)head * L + qi) * D;
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+            *reinterpret_cast<f32x4 *>(orow + 16 * c + 4 * g) = oacc[c] * inv;
+        if (g == 0)
+            LSE[(size_t)head * L + qi] = (l > 0.f) ? (m_run + log2f(l)) * kLn2 : -INFINITY;
+    }
+}
+
+// ------------------------------------------------- backward: D = rowsum(dO o O)
+template <int D>
+__global__ __launch_bounds__(256) void attn_rowdot_f32(const float *__restrict__ O,
+                                                       const float *__restrict__ dO,
+                                                       float *__restrict__ Dws, int rows) {
+    constexpr int TPR = D / 4;   // threads per row, one 16-byte chunk each
+    const int row = blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
+    const int c4 = threadIdx.x % TPR;
+    float v = 0.f;
+    if (row < rows) {
+        const f32x4 o = *reinterpret_cast<const f32x4 *>(O + (size_t)row * D + 4 * c4);
+        const f32x4 go = *reinterpret_cast<const f32x4 *>(dO + (size_t)row * D + 4 * c4);
+        v = o[0] * go[0] + o[1] * go[1] + o[2] * go[2] + o[3] * go[3];
+    }
+#pragma unroll
+    for (int m = TPR / 2; m >= 1; m >>= 1) v += xor_lanes(v, m);
+    if (row < rows && c4 == 0) Dws[row] = v;
+}
+
+// ------------------------------------------------------- backward: dK, dV
+// Key tile of 64 keys stationary (16 per wave, one per lane column); query
+// tiles of NIB*16 rows stream through LDS.
+template <int D, int NIB>
+__global__ __launch_bounds__(kThreads) void attn_dkdv_f32(
+    const float *__restrict__ Q, const float *__restrict__ K, const float *__restrict__ V,
+    const float *__restrict__ dO, const float *__restrict__ LSE, const float *__restrict__ Dws,
+    float *__restrict__ dK, float *__restrict__ dV, const int32_t *__restrict__ key_len, int H,
+    int L, int causal, float scale, float scale_log2, int BH) {
+    constexpr int DQ = D / 4;
+    constexpr int NC = D / 16;
+    constexpr int BR = 16 * NIB;
+    using Stager = F32TileStager<BR, D, kThreads>;
+    constexpr int LD = Stager::kLd;
+    __shared__ __attribute__((aligned(16))) float Qs[BR][LD];
+    __shared__ __attribute__((aligned(16))) float dOs[BR][LD];
+    __shared__ __attribute__((aligned(16))) float lse2s[BR];
+    __shared__ __attribute__((aligned(16))) float Ds[BR];
+
+    const int rank = blockIdx.x / BH;
+    const int head = blockIdx.x - rank * BH;
+    const int kt = rank;   // low key tiles see the most queries under a causal mask
+    const int b = head / H;
+    const size_t hoff = (size_t)head * L * D;
+    const float *Qh = Q + hoff;
+    const float *dOh = dO + hoff;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int il = lane & 15;
+    const int g = lane >> 4;
+    const int k0 = kt * kStatRows;
+    const int kj = k0 + 16 * (tid >> 6) + il;   // this lane's key
+
+    const int klen = key_limit(key_len, b, L);
+    const int nq = (L + BR - 1) / BR;
+    const int qstart = causal ? (k0 / BR) : 0;
+    const int qstop = (k0 < klen) ? nq : qstart;   // a fully padded key tile does no work
+
+    // B operands of S = Q K^T and dP = dO V^T: lane holds K[kj][g*DQ + s].
+    float kreg[DQ], vreg[DQ];
+#pragma unroll
+    for (int s4 = 0; s4 < DQ / 4; ++s4) {
+        const size_t off = hoff + (size_t)kj * D + g * DQ + 4 * s4;
+        const f32x4 kv = (kj < L) ? *reinterpret_cast<const f32x4 *>(K + off) : zero4();
+        const f32x4 vv = (kj < L) ? *reinterpret_cast<const f32x4 *>(V + off) : zero4();
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            kreg[4 * s4 + e] = kv[e];
+            vreg[4 * s4 + e] = vv[e];
+        }
+    }
+
+    f32x4 dkacc[NC], dvacc[NC];   // dK^T[16c + 4g + r][kj], dV^T likewise
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        dkacc[c] = zero4();
+        dvacc[c] = zero4();
+    }
+
+    Stager qst, ost;
+    float lse_pre = 0.f, d_pre = 0.f;
+    auto load_rows = [&](int qt) {
+        qst.load(Qh, qt * BR, L, tid);
+        ost.load(dOh, qt * BR, L, tid);
+        if (tid < BR) {
+            const int row = qt * BR + tid;
+            lse_pre = (row < L) ? LSE[(size_t)head * L + row] * kLog2e : 0.f;
+            d_pre = (row < L) ? Dws[(size_t)head * L + row] : 0.f;
+        }
+    };
+    if (qstart < qstop) load_rows(qstart);
+
+    for (int qt = qstart; qt < qstop; ++qt) {
+        __syncthreads();
+        qst.store(Qs, tid);
+        ost.store(dOs, tid);
+        if (tid < BR) {
+            lse2s[tid] = lse_pre;
+            Ds[tid] = d_pre;
+        }
+        __syncthreads();
+        if (qt + 1 < qstop) load_rows(qt + 1);
+
+        // S[16ib + 4g + r][kj] and dP[..][kj]
+        f32x4 sacc[NIB], pacc[NIB];
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib) {
+            sacc[ib] = zero4();
+            pacc[ib] = zero4();
+        }
+#pragma unroll
+        for (int s4 = 0; s4 < DQ / 4; ++s4) {
+            f32x4 aq[NIB], ao[NIB];
+#pragma unroll
+            for (int ib = 0; ib < NIB; ++ib) {
+                aq[ib] = *reinterpret_cast<const f32x4 *>(&Qs[16 * ib + il][g * DQ + 4 * s4]);
+                ao[ib] = *reinterpret_cast<const f32x4 *>(&dOs[16 * ib + il][g * DQ + 4 * s4]);
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int ib = 0; ib < NIB; ++ib) {
+                    sacc[ib] = mfma16x16x4(aq[ib][e], kreg[4 * s4 + e], sacc[ib]);
+                    pacc[ib] = mfma16x16x4(ao[ib][e], vreg[4 * s4 + e], pacc[ib]);
+                }
+        }
+
+        // P = exp(S - LSE) on allowed pairs, dS = P (dP - D).
+        const int ibase = qt * BR + 4 * g;
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib) {
+            const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lse2s[16 * ib + 4 * g]);
+            const f32x4 dd = *reinterpret_cast<const f32x4 *>(&Ds[16 * ib + 4 * g]);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int i = ibase + 16 * ib + r;
+                const bool ok = (i < L) && (kj < klen) && (!causal || kj <= i);
+                const float p = ok ? exp2_fast(sacc[ib][r] * scale_log2 - l2[r]) : 0.f;
+                sacc[ib][r] = p;
+                pacc[ib][r] = p * (pacc[ib][r] - dd[r]);
+            }
+        }
+
+        // dV^T[16c + 4g + r][kj] += sum_i dO[i][16c + il'] P[i][kj]
+        // dK^T[16c + 4g + r][kj] += sum_i  Q[i][16c + il'] dS[i][kj]
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int c = 0; c < NC; ++c) {
+                    dvacc[c] = mfma16x16x4(dOs[16 * ib + 4 * g + r][16 * c + il], sacc[ib][r],
+                                           dvacc[c]);
+                    dkacc[c] = mfma16x16x4(Qs[16 * ib + 4 * g + r][16 * c + il], pacc[ib][r],
+                                           dkacc[c]);
+                }
+    }
+
+    if (kj < L) {
+        float *dkrow = dK + hoff + (size_t)kj * D;
+        float *dvrow = dV + hoff + (size_t)kj * D;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            *reinterpret_cast<f32x4 *>(dkrow + 16 * c + 4 * g) = dkacc[c] * scale;
+            *reinterpret_cast<f32x4 *>(dvrow + 16 * c + 4 * g) = dvacc[c];
+        }
+    }
+}
+
+// ------------------------------------------------------------ backward: dQ
+// Query tile of 64 rows stationary (16 per wave); key tiles stream.
+template <int D>
+__global__ __launch_bounds__(kThreads) void attn_dq_f32(
+    const float *__restrict__ Q, const float *__restrict__ K, const float *__restrict__ V,
+    const float *__restrict__ dO, const float *__restrict__ LSE, const float *__restrict__ Dws,
+    float *__restrict__ dQ, const int32_t *__restrict__ key_len, int H, int L, int causal,
+    float scale, float scale_log2, int n_qtiles, int BH) {
+    constexpr int DQ = D / 4;
+    constexpr int NC = D / 16;
+    using Stager = F32TileStager<kStream, D, kThreads>;
+    constexpr int LD = Stager::kLd;
+    __shared__ __attribute__((aligned(16))) float Ks[kStream][LD];
+    __shared__ __attribute__((aligned(16))) float Vs[kStream][LD];
+
+    const int rank = blockIdx.x / BH;
+    const int head = blockIdx.x - rank * BH;
+    const int qt = causal ? (n_qtiles - 1 - rank) : rank;
+    const int b = head / H;
+    const size_t hoff = (size_t)head * L * D;
+    const float *Kh = K + hoff;
+    const float *Vh = V + hoff;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int il = lane & 15;
+    const int g = lane >> 4;
+    const int q0 = qt * kStatRows;
+    const int qi = q0 + 16 * (tid >> 6) + il;
+
+    const int klen = key_limit(key_len, b, L);
+    const int kend = causal ? min(klen, q0 + kStatRows) : klen;
+    const int ntiles = (kend + kStream - 1) / kStream;
+
+    float qreg[DQ], oreg[DQ];
+#pragma unroll
+    for (int s4 = 0; s4 < DQ / 4; ++s4) {
+        const size_t off = hoff + (size_t)qi * D + g * DQ + 4 * s4;
+        const f32x4 qv = (qi < L) ? *reinterpret_cast<const f32x4 *>(Q + off) : zero4();
+        const f32x4 ov = (qi < L) ? *reinterpret_cast<const f32x4 *>(dO + off) : zero4();
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            qreg[4 * s4 + e] = qv[e];
+            oreg[4 * s4 + e] = ov[e];
+        }
+    }
+    const float lse2 = (qi < L) ? LSE[(size_t)head * L + qi] * kLog2e : 0.f;
+    const float Di = (qi < L) ? Dws[(size_t)head * L + qi] : 0.f;
+
+    f32x4 dqacc[NC];   // dQ^T[16c + 4g + r][qi]
+#pragma unroll
+    for (int c = 0; c < NC; ++c) dqacc[c] = zero4();
+
+    Stager kst, vst;
+    if (ntiles > 0) {
+        kst.load(Kh, 0, L, tid);
+        vst.load(Vh, 0, L, tid);
+    }
+    for (int kt = 0; kt < ntiles; ++kt) {
+        __syncthreads();
+        kst.store(Ks, tid);
+        vst.store(Vs, tid);
+        __syncthreads();
+        if (kt + 1 < ntiles) {
+            kst.load(Kh, (kt + 1) * kStream, L, tid);
+            vst.load(Vh, (kt + 1) * kStream, L, tid);
+        }
+
+        // S^T[j][qi] and dP^T[j][qi], j = 16jb + 4g + r
+        f32x4 sacc[4], pacc[4];
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb) {
+            sacc[jb] = zero4();
+            pacc[jb] = zero4();
+        }
+#pragma unroll
+        for (int s4 = 0; s4 < DQ / 4; ++s4) {
+            f32x4 ak[4], av[4];
+#pragma unroll
+            for (int jb = 0; jb < 4; ++jb) {
+                ak[jb] = *reinterpret_cast<const f32x4 *>(&Ks[16 * jb + il][g * DQ + 4 * s4]);
+                av[jb] = *reinterpret_cast<const f32x4 *>(&Vs[16 * jb + il][g * DQ + 4 * s4]);
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int jb = 0; jb < 4; ++jb) {
+                    sacc[jb] = mfma16x16x4(ak[jb][e], qreg[4 * s4 + e], sacc[jb]);
+                    pacc[jb] = mfma16x16x4(av[jb][e], oreg[4 * s4 + e], pacc[jb]);
+                }
+        }
+
+        const int j0 = kt * kStream + 4 * g;
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int j = j0 + 16 * jb + r;
+                const bool ok = (qi < L) && (j < klen) && (!causal || j <= qi);
+                const float p = ok ? exp2_fast(sacc[jb][r] * scale_log2 - lse2) : 0.f;
+                pacc[jb][r] = p * (pacc[jb][r] - Di);
+            }
+
+        // dQ^T[16c + 4g + r][qi] += sum_j K[j][16c + il'] dS^T[j][qi]
+#pragma unroll
+        for (int jb = 0; jb < 4; ++jb)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int c = 0; c < NC; ++c)
+                    dqacc[c] = mfma16x16x4(Ks[16 * jb + 4 * g + r][16 * c + il], pacc[jb][r],
+                                           dqacc[c]);
+    }
+
+    if (qi < L) {
+        float *dqrow = dQ + hoff + (size_t)qi * D;
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+            *reinterpret_cast<f32x4 *>(dqrow + 16 * c + 4 * g) = dqacc[c] * scale;
+    }
+}
+
+inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+}  // namespace
+
+// ---------------------------------------------------------------- launchers
+hipError_t launch_fwd_f32(const AttnProblem &p, const float *Q, const float *K,
+                          const float *V, float *O, float *LSE, hipStream_t s) {
+    const int BH = p.B * p.H;
+    const int nqt = cdiv(p.L, kStatRows);
+    const dim3 grid(nqt * BH), block(kThreads);
+    const float sl2 = p.scale * kLog2e;
+    switch (p.d) {
+    case 32: attn_fwd_f32<32><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.L, p.causal, sl2, nqt, BH); break;
+    case 64: attn_fwd_f32<64><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.L, p.causal, sl2, nqt, BH); break;
+    case 128: attn_fwd_f32<128><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.L, p.causal, sl2, nqt, BH); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_rowdot_f32(const AttnProblem &p, const float *O, const float *dO,
+                                 float *Dws, hipStream_t s) {
+    const int rows = p.B * p.H * p.L;
+    const dim3 block(256);
+    switch (p.d) {
+    case 32: attn_rowdot_f32<32><<<dim3(cdiv(rows, 256 / 8)), block, 0, s>>>(O, dO, Dws, rows); break;
+    case 64: attn_rowdot_f32<64><<<dim3(cdiv(rows, 256 / 16)), block, 0, s>>>(O, dO, Dws, rows); break;
+    case 128: attn_rowdot_f32<128><<<dim3(cdiv(rows, 256 / 32)), block, 0, s>>>(O, dO, Dws, rows); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_dkdv_f32(const AttnProblem &p, const float *Q, const float *K,
+                               const float *V, const float *dO, const float *LSE,
+                               const float *Dws, float *dK, float *dV, hipStream_t s) {
+    const int BH = p.B * p.H;
+    const dim3 grid(cdiv(p.L, kStatRows) * BH), block(kThreads);
+    const float sl2 = p.scale * kLog2e;
+    switch (p.d) {
+    case 32: attn_dkdv_f32<32, 4><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
+    case 64: attn_dkdv_f32<64, 4><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
+    case 128: attn_dkdv_f32<128, 2><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_dq_f32(const AttnProblem &p, const float *Q, const float *K,
+                             const float *V, const float *dO, const float *LSE,
+                             const float *Dws, float *dQ, hipStream_t s) {
+    const int BH = p.B * p.H;
+    const int nqt = cdiv(p.L, kStatRows);
+    const dim3 grid(nqt * BH), block(kThreads);
+    const float sl2 = p.scale * kLog2e;
+    switch (p.d) {
+    case 32: attn_dq_f32<32><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
+    case 64: attn_dq_f32<64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
+    case 128: attn_dq_f32<128><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace mg

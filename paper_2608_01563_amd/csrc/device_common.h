@@ -1,0 +1,78 @@
+// device_common.h -- device helpers shared by the gfx950 attention kernels.
+//
+// Matrix-core conventions used throughout (CDNA3/CDNA4 MFMA, wave64):
+//
+//   v_mfma_f32_16x16x4_f32   C[16x16] += A[16x4] * B[4x16]
+//     lane l holds A[l%16][l/16], B[l/16][l%16] (one f32 each) and
+//     C[4*(l/16) + r][l%16] in accumulator register r = 0..3.
+//
+//   v_mfma_f32_16x16x32_bf16 C[16x16] += A[16x32] * B[32x16]
+//     lane l holds 8 bf16 of A row l%16 and 8 bf16 of B column l%16; the
+//     eight contraction indices a lane holds are the same set for A and B,
+//     and C has the layout above.
+//
+// Because a contraction index only has to mean the same thing in A and B,
+// each kernel picks the contraction order that makes its loads contiguous.
+// An accumulator C[x][y] (x by lane group and register, y = lane%16) can
+// feed the next product directly as its B operand (contraction over x,
+// output columns y), which is how P and dS reach the second GEMM of each
+// pass without a trip through LDS.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mg {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.69314718055994531f;
+
+__device__ __forceinline__ f32x4 mfma16x16x4(float a, float b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x4 mfma16x16x32bf16(bf16x8 a, bf16x8 b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// 2^x on the transcendental unit (v_exp_f32); 2^-inf = 0.
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+__device__ __forceinline__ float xor_lanes(float v, int mask) { return __shfl_xor(v, mask, 64); }
+
+// Reductions across the four 16-lane groups that share one column l%16.
+__device__ __forceinline__ float max_over_groups(float v) {
+    v = fmaxf(v, xor_lanes(v, 16));
+    return fmaxf(v, xor_lanes(v, 32));
+}
+__device__ __forceinline__ float sum_over_groups(float v) {
+    v += xor_lanes(v, 16);
+    return v + xor_lanes(v, 32);
+}
+
+__device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
+
+// f32 -> bf16 bits, round to nearest even (finite inputs; NaN stays NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
+    uint32_t u = __float_as_uint(x);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+    return __uint_as_float(((uint32_t)b) << 16);
+}
+
+// Clamp a per-batch key length to [0, L]; L when no padding is given.
+__device__ __forceinline__ int key_limit(const int32_t *key_len, int b, int L) {
+    if (key_len == nullptr) return L;
+    int n = key_len[b];
+    return n < 0 ? 0 : (n > L ? L : n);
+}
+
+}  // namespace mg

@@ -1,0 +1,51 @@
+// launch.h -- host-side launchers of the attention kernels (internal).
+//
+// Each launcher enqueues exactly one kernel on `stream` and returns the
+// launch status; argument validation happens before, in mg_attn.cpp.  The
+// launch geometry of every kernel is fixed together with its template
+// instance inside its launcher, never chosen separately.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+namespace mg {
+
+struct AttnProblem {
+    int B, H, L, d;
+    int causal;
+    float scale;
+    const int32_t *key_len;  // device [B] or nullptr
+};
+
+// Forward, strict f32: O, LSE from Q, K, V.
+hipError_t launch_fwd_f32(const AttnProblem &p, const float *Q, const float *K,
+                          const float *V, float *O, float *LSE, hipStream_t s);
+// Forward, bf16 inputs/outputs, f32 accumulation.
+hipError_t launch_fwd_bf16(const AttnProblem &p, const uint16_t *Q, const uint16_t *K,
+                           const uint16_t *V, uint16_t *O, float *LSE, hipStream_t s);
+
+// Backward step 1: D_i = sum_k dO_ik O_ik (f32 out, one per row).
+hipError_t launch_bwd_rowdot_f32(const AttnProblem &p, const float *O, const float *dO,
+                                 float *Dws, hipStream_t s);
+hipError_t launch_bwd_rowdot_bf16(const AttnProblem &p, const uint16_t *O,
+                                  const uint16_t *dO, float *Dws, hipStream_t s);
+
+// Backward step 2: dK, dV with the key tile stationary.
+hipError_t launch_bwd_dkdv_f32(const AttnProblem &p, const float *Q, const float *K,
+                               const float *V, const float *dO, const float *LSE,
+                               const float *Dws, float *dK, float *dV, hipStream_t s);
+hipError_t launch_bwd_dkdv_bf16(const AttnProblem &p, const uint16_t *Q,
+                                const uint16_t *K, const uint16_t *V, const uint16_t *dO,
+                                const float *LSE, const float *Dws, uint16_t *dK,
+                                uint16_t *dV, hipStream_t s);
+
+// Backward step 3: dQ with the query tile stationary.
+hipError_t launch_bwd_dq_f32(const AttnProblem &p, const float *Q, const float *K,
+                             const float *V, const float *dO, const float *LSE,
+                             const float *Dws, float *dQ, hipStream_t s);
+hipError_t launch_bwd_dq_bf16(const AttnProblem &p, const uint16_t *Q, const uint16_t *K,
+                              const uint16_t *V, const uint16_t *dO, const float *LSE,
+                              const float *Dws, uint16_t *dQ, hipStream_t s);
+
+}  // namespace mg

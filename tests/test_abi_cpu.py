@@ -1,0 +1,105 @@
+"""Host-side checks of the C-ABI library (no GPU needed): it builds, loads,
+exports every entry point its header declares, and rejects bad arguments on
+the host before anything is enqueued."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2608_01563_amd as mg
+from paper_2608_01563_amd import _binding
+
+
+def header_functions():
+    with open(mg.HEADER_PATH) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mg_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(mg.LIB_PATH):
+        pytest.fail("libmgattn.so is not built; run __graft_entry__.build()")
+    return mg.load_library()
+
+
+def test_header_declares_the_boundary():
+    names = header_functions()
+    for required in ("mg_attn_fwd", "mg_attn_bwd", "mg_attn_bwd_workspace_bytes",
+                     "mg_status_string", "mg_last_error_detail"):
+        assert required in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", mg.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    for name in header_functions():
+        assert name in exported, name
+        assert hasattr(lib, name)
+
+
+def test_status_strings(lib):
+    for code, name in _binding.STATUS_NAMES.items():
+        assert mg.mg_status_string(code) == name
+    assert mg.mg_status_string(99) == "MG_ERR_UNKNOWN"
+
+
+def test_workspace_query(lib):
+    assert mg.mg_attn_bwd_workspace_bytes(8, 8, 1024, 64, 1, 0) == 8 * 8 * 1024 * 4
+    assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 32, 0, 0) == 256
+    assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 48, 0, 0) == 0     # unsupported d
+    assert mg.mg_attn_bwd_workspace_bytes(0, 1, 3, 32, 0, 0) == 0     # bad size
+    assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 32, 0, 7) == 0     # bad contract
+
+
+def _fwd(lib, ptrs, B=1, H=1, L=8, d=64, scale=0.125, contract=0):
+    Q, K, V, O, LSE = ptrs
+    vp = ctypes.c_void_p
+    return lib.mg_attn_fwd(vp(Q), vp(K), vp(V), vp(O), vp(LSE), None, B, H, L, d, 1,
+                           ctypes.c_float(scale), contract, None)
+
+
+GOOD = [0x1000, 0x2000, 0x3000, 0x4000, 0x5000]   # aligned, never dereferenced
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(B=0), 1), (dict(H=-1), 1), (dict(L=0), 1), (dict(d=0), 1),
+    (dict(d=48), 2), (dict(d=256), 2),
+    (dict(scale=float("inf")), 1), (dict(scale=float("nan")), 1),
+    (dict(contract=5), 1),
+    (dict(B=1 << 12, H=1 << 10, L=1 << 10, d=64), 1),   # B*H*L*d > 2^31-1
+])
+def test_forward_rejects_bad_sizes_before_any_device_call(lib, kwargs, status):
+    assert _fwd(lib, GOOD, **kwargs) == status
+    assert mg.mg_last_error_detail() != ""
+
+
+def test_forward_rejects_null_and_misaligned_pointers(lib):
+    for k in range(5):
+        ptrs = list(GOOD)
+        ptrs[k] = 0
+        assert _fwd(lib, ptrs) == 1
+        ptrs[k] = GOOD[k] + 4
+        assert _fwd(lib, ptrs) == 3
+
+
+def test_backward_rejects_missing_workspace(lib):
+    vp = ctypes.c_void_p
+    ptrs = [vp(0x1000 * (k + 1)) for k in range(9)]
+    st = lib.mg_attn_bwd(*ptrs, None, 1, 1, 8, 64, 1, ctypes.c_float(0.125), 0,
+                         None, 0, None)
+    assert st == 4                 # checked before any pointer reaches the runtime
+    st = lib.mg_attn_bwd(*ptrs, None, 1, 1, 8, 64, 1, ctypes.c_float(0.125), 9,
+                         None, 0, None)
+    assert st == 1
+
+
+def test_host_memory_is_refused(lib):
+    bufs = [ctypes.create_string_buffer(4096 + 16) for _ in range(5)]
+    ptrs = [(ctypes.addressof(b) + 15) // 16 * 16 for b in bufs]
+    assert _fwd(lib, ptrs) == 1
+    assert "device" in mg.mg_last_error_detail()

@@ -1,0 +1,166 @@
+"""GPU parity: the HIP path (through the C ABI) against the f64 oracle on the
+same seeded inputs, plus bitwise pins that need no oracle.
+
+Tolerance (normwise, per output tensor): max|gpu - oracle| / max|oracle|
+<= 1e-4 for strict_f32 and <= 2e-2 for fast_bf16.  The end-to-end cases feed
+the GPU's own O and LSE into the GPU backward; the isolation case feeds the
+oracle's O and LSE instead.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from gpu_util import TOL, compare, oracle_reference, run_gpu, say, to_device, key_len_device
+from workloads import WORKLOADS, make_inputs, workload_inputs
+
+pytestmark = pytest.mark.gpu
+
+SMALL = [(L, d, mode) for L in (1, 17, 64, 65, 200) for d in (32, 64, 128)
+         for mode in ("causal", "full", "padded")]
+
+
+def small_inputs(L, d, mode, contract="strict_f32", B=2, H=3, seed=0):
+    kl = None
+    if mode == "padded":
+        kl = [max(1, L // 2), L][:B] + [L] * max(0, B - 2)
+    return make_inputs(B, H, L, d, causal=(mode == "causal"), contract=contract,
+                       seed=seed + 1000 * L + d, key_len=kl)
+
+
+@pytest.mark.parametrize("L,d,mode", SMALL)
+def test_small_shapes_strict(gpu_lib, L, d, mode):
+    say("small strict L=%d d=%d %s" % (L, d, mode))
+    x = small_inputs(L, d, mode)
+    errs = compare(run_gpu(x), oracle_reference(x), "strict_f32")
+    assert max(errs.values()) <= TOL["strict_f32"], errs
+
+
+@pytest.mark.parametrize("wid", [1, 2, 3, 5])
+def test_workload_full_compare_strict(gpu_lib, wid):
+    w = WORKLOADS[wid]
+    say("workload %d %s" % (wid, w.name))
+    x = workload_inputs(wid)
+    errs = compare(run_gpu(x), oracle_reference(x), w.contract)
+    say("  errors %s" % {k: "%.2e" % v for k, v in errs.items()})
+    assert max(errs.values()) <= TOL[w.contract], errs
+
+
+def test_backward_isolated_with_oracle_forward(gpu_lib):
+    say("backward isolation, workload 2")
+    x = workload_inputs(2)
+    ref = oracle_reference(x)
+    got = run_gpu(x, O_in=ref["O"], LSE_in=ref["LSE"])
+    errs = compare(got, ref, "strict_f32", names=("dQ", "dK", "dV"))
+    assert max(errs.values()) <= TOL["strict_f32"], errs
+
+
+def test_bitwise_pins(gpu_lib):
+    import torch
+    import paper_2608_01563_amd as mg
+    say("bitwise pins")
+    x = make_inputs(2, 8, 192, 64, causal=True, seed=7)
+    Q, K, V, dO = (to_device(x, n) for n in ("Q", "K", "V", "dO"))
+    s = x.scale
+    O, LSE = mg.attention_forward(Q, K, V, causal=True, scale=s)
+    # causal row 0 attends only to key 0 with probability exp(0) = 1
+    assert torch.equal(O[:, :, 0, :], V[:, :, 0, :])
+    # O is linear in V with the same P; doubling is exact in binary floating point
+    O2, LSE2 = mg.attention_forward(Q, K, 2 * V, causal=True, scale=s)
+    assert torch.equal(O2, 2 * O) and torch.equal(LSE2, LSE)
+    g1 = mg.attention_backward(Q, K, V, O, LSE, dO, causal=True, scale=s)
+    g2 = mg.attention_backward(Q, K, V, O, LSE, 2 * dO, causal=True, scale=s)
+    for a, b in zip(g1, g2):
+        assert torch.equal(2 * a, b)
+    # run-to-run determinism (no atomics anywhere)
+    g3 = mg.attention_backward(Q, K, V, O, LSE, dO, causal=True, scale=s)
+    for a, b in zip(g1, g3):
+        assert torch.equal(a, b)
+    Oa, LSEa = mg.attention_forward(Q, K, V, causal=True, scale=s)
+    assert torch.equal(Oa, O) and torch.equal(LSEa, LSE)
+    # a head computed alone equals the same head computed in the batch
+    b, h = 1, 5
+    sl = lambda t: t[b:b + 1, h:h + 1].contiguous()
+    O1, L1 = mg.attention_forward(sl(Q), sl(K), sl(V), causal=True, scale=s)
+    assert torch.equal(O1, sl(O)) and torch.equal(L1, sl(LSE))
+    gs = mg.attention_backward(sl(Q), sl(K), sl(V), O1, L1, sl(dO), causal=True, scale=s)
+    for a, full in zip(gs, g1):
+        assert torch.equal(a, sl(full))
+    # rows of P sum to one: sum_j dK_j = 0 and sum_j dV_j = sum_i dO_i, up to
+    # rounding bounded by the sums of magnitudes
+    dQ, dK, dV = (t.double() for t in g1)
+    go = dO.double()
+    assert torch.all(torch.abs(dK.sum(2)) <= 1e-4 * torch.abs(dK).sum(2))
+    assert torch.all(torch.abs(dV.sum(2) - go.sum(2)) <= 1e-4 * torch.abs(go).sum(2))
+
+
+def test_padded_keys_get_exact_zero_gradients(gpu_lib):
+    import torch
+    import paper_2608_01563_amd as mg
+    say("padded zero gradients")
+    x = make_inputs(3, 2, 160, 64, causal=False, seed=11, key_len=[37, 160, 64])
+    Q, K, V, dO = (to_device(x, n) for n in ("Q", "K", "V", "dO"))
+    kl = key_len_device(x)
+    O, LSE = mg.attention_forward(Q, K, V, causal=False, scale=x.scale, key_len=kl)
+    dQ, dK, dV = mg.attention_backward(Q, K, V, O, LSE, dO, causal=False, scale=x.scale,
+                                       key_len=kl)
+    for b, n in enumerate(x.key_len):
+        assert torch.count_nonzero(dK[b, :, n:]) == 0
+        assert torch.count_nonzero(dV[b, :, n:]) == 0
+
+
+def test_fully_masked_batch_and_out_of_range_key_len(gpu_lib):
+    import torch
+    import paper_2608_01563_amd as mg
+    say("fully masked batch")
+    L = 70
+    x = make_inputs(3, 2, L, 32, causal=True, seed=3, key_len=[0, L, 1000])
+    Q, K, V, dO = (to_device(x, n) for n in ("Q", "K", "V", "dO"))
+    kl = key_len_device(x)
+    O, LSE = mg.attention_forward(Q, K, V, causal=True, scale=x.scale, key_len=kl)
+    g = mg.attention_backward(Q, K, V, O, LSE, dO, causal=True, scale=x.scale, key_len=kl)
+    assert torch.count_nonzero(O[0]) == 0
+    assert torch.all(torch.isinf(LSE[0])) and torch.all(LSE[0] < 0)
+    for t in g:
+        assert torch.count_nonzero(t[0]) == 0
+    # key_len beyond L behaves as L
+    O_nopad, L_nopad = mg.attention_forward(Q, K, V, causal=True, scale=x.scale)
+    assert torch.equal(O[1], O_nopad[1]) and torch.equal(O[2], O_nopad[2])
+    assert torch.equal(LSE[2], L_nopad[2])
+
+
+def test_every_output_element_is_written(gpu_lib):
+    import torch
+    import paper_2608_01563_amd as mg
+    say("NaN poison")
+    for L, d, causal in ((65, 64, True), (200, 32, False), (17, 128, True)):
+        x = make_inputs(1, 3, L, d, causal=causal, seed=5)
+        Q, K, V, dO = (to_device(x, n) for n in ("Q", "K", "V", "dO"))
+        O = torch.full_like(Q, float("nan"))
+        LSE = torch.full(Q.shape[:3], float("nan"), device=Q.device)
+        mg.mg_attn_fwd(Q, K, V, O, LSE, causal=causal, scale=x.scale)
+        dQ, dK, dV = (torch.full_like(Q, float("nan")) for _ in range(3))
+        mg.mg_attn_bwd(Q, K, V, O, LSE, dO, dQ, dK, dV, causal=causal, scale=x.scale)
+        torch.cuda.synchronize()
+        for t in (O, LSE, dQ, dK, dV):
+            assert not torch.isnan(t).any()
+
+
+def test_argument_errors_enqueue_nothing(gpu_lib):
+    import torch
+    import paper_2608_01563_amd as mg
+    say("argument errors")
+    x = make_inputs(1, 2, 64, 64, causal=True, seed=9)
+    Q, K, V, dO = (to_device(x, n) for n in ("Q", "K", "V", "dO"))
+    O, LSE = mg.attention_forward(Q, K, V, causal=True, scale=x.scale)
+    dQ = torch.full_like(Q, 7.0)
+    small = torch.empty(16, dtype=torch.uint8, device=Q.device)
+    with pytest.raises(mg.MgError) as e:
+        mg.mg_attn_bwd(Q, K, V, O, LSE, dO, dQ, dQ.clone(), dQ.clone(), causal=True,
+                       scale=x.scale, workspace=small)
+    assert e.value.status == 4
+    torch.cuda.synchronize()
+    assert torch.all(dQ == 7.0)
+    with pytest.raises(mg.MgError) as e:
+        mg.mg_attn_fwd(Q, K, V, O, LSE, causal=True, scale=math.inf)
+    assert e.value.status == 1
