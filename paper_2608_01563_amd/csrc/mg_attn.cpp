@@ -52,8 +52,6 @@ mg_status_t check_shape(int B, int H, int L, int d, float scale, mg_contract_t c
     if (n > kMaxElems)
         return fail(MG_ERR_INVALID_ARGUMENT, "B*H*L*d = %lld exceeds 2^31-1", (long long)n);
     if (!std::isfinite(scale)) return fail(MG_ERR_INVALID_ARGUMENT, "scale is not finite");
-    if (contract == MG_CONTRACT_FAST_BF16)
-        return fail(MG_ERR_UNSUPPORTED, "the fast_bf16 kernels are not built yet");
     return MG_OK;
 }
 

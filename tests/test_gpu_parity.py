@@ -164,3 +164,71 @@ def test_argument_errors_enqueue_nothing(gpu_lib):
     with pytest.raises(mg.MgError) as e:
         mg.mg_attn_fwd(Q, K, V, O, LSE, causal=True, scale=math.inf)
     assert e.value.status == 1
+
+
+# ------------------------------------------------------------ fast_bf16 --
+
+@pytest.mark.parametrize("L,d,mode", SMALL)
+def test_small_shapes_bf16(gpu_lib, L, d, mode):
+    say("small bf16 L=%d d=%d %s" % (L, d, mode))
+    x = small_inputs(L, d, mode, contract="fast_bf16")
+    errs = compare(run_gpu(x), oracle_reference(x), "fast_bf16")
+    assert max(errs.values()) <= TOL["fast_bf16"], errs
+
+
+WORKLOAD4_HEADS = [(0, 0), (0, 5), (0, 10), (0, 15), (1, 2), (1, 7), (1, 11), (1, 14)]
+
+
+def test_workload4_sampled_heads_bf16(gpu_lib):
+    w = WORKLOADS[4]
+    say("workload 4 %s (oracle on %d of %d heads)" % (w.name, len(WORKLOAD4_HEADS), w.B * w.H))
+    x = workload_inputs(4)
+    got = run_gpu(x)
+    ref = oracle_reference(x, heads=WORKLOAD4_HEADS)
+    errs = compare(got, ref, w.contract, heads=WORKLOAD4_HEADS)
+    say("  errors %s" % {k: "%.2e" % v for k, v in errs.items()})
+    assert max(errs.values()) <= TOL[w.contract], errs
+    # every head (not only the sampled ones) is finite and written
+    for n in ("O", "dQ", "dK", "dV"):
+        assert np.all(np.isfinite(got[n]))
+
+
+def test_bitwise_pins_bf16(gpu_lib):
+    import torch
+    import paper_2608_01563_amd as mg
+    say("bitwise pins bf16")
+    x = make_inputs(2, 8, 192, 128, causal=True, contract="fast_bf16", seed=17)
+    Q, K, V, dO = (to_device(x, n) for n in ("Q", "K", "V", "dO"))
+    s = x.scale
+    O, LSE = mg.attention_forward(Q, K, V, causal=True, scale=s)
+    assert torch.equal(O[:, :, 0, :], V[:, :, 0, :])
+    O2, LSE2 = mg.attention_forward(Q, K, 2 * V, causal=True, scale=s)
+    assert torch.equal(O2, 2 * O) and torch.equal(LSE2, LSE)
+    g1 = mg.attention_backward(Q, K, V, O, LSE, dO, causal=True, scale=s)
+    g2 = mg.attention_backward(Q, K, V, O, LSE, dO, causal=True, scale=s)
+    for a, b in zip(g1, g2):
+        assert torch.equal(a, b)
+    b, h = 0, 3
+    sl = lambda t: t[b:b + 1, h:h + 1].contiguous()
+    O1, L1 = mg.attention_forward(sl(Q), sl(K), sl(V), causal=True, scale=s)
+    assert torch.equal(O1, sl(O)) and torch.equal(L1, sl(LSE))
+    gs = mg.attention_backward(sl(Q), sl(K), sl(V), O1, L1, sl(dO), causal=True, scale=s)
+    for a, full in zip(gs, g1):
+        assert torch.equal(a, sl(full))
+
+
+def test_padded_keys_exact_zero_bf16(gpu_lib):
+    import torch
+    import paper_2608_01563_amd as mg
+    say("padded zero gradients bf16")
+    x = make_inputs(2, 2, 130, 64, causal=False, contract="fast_bf16", seed=19,
+                    key_len=[45, 0])
+    Q, K, V, dO = (to_device(x, n) for n in ("Q", "K", "V", "dO"))
+    kl = key_len_device(x)
+    O, LSE = mg.attention_forward(Q, K, V, causal=False, scale=x.scale, key_len=kl)
+    dQ, dK, dV = mg.attention_backward(Q, K, V, O, LSE, dO, causal=False, scale=x.scale,
+                                       key_len=kl)
+    assert torch.count_nonzero(dK[0, :, 45:]) == 0 and torch.count_nonzero(dV[0, :, 45:]) == 0
+    assert torch.count_nonzero(O[1]) == 0 and torch.all(torch.isinf(LSE[1]))
+    for t in (dQ, dK, dV):
+        assert torch.count_nonzero(t[1]) == 0
