@@ -19,7 +19,6 @@ and `parity` (the timed run's outputs against the oracle).
 import argparse
 import hashlib
 import json
-import math
 import os
 import sys
 import time
@@ -33,7 +32,7 @@ PEAK_TFLOPS = {"strict_f32": 157.3, "fast_bf16": 2516.6}   # MI355X dense MFMA
 HBM_PEAK_GBS = 8000.0
 KERNEL_SOURCES = {"strict_f32": "paper_2608_01563_amd/csrc/attn_f32.hip",
                   "fast_bf16": "paper_2608_01563_amd/csrc/attn_bf16.hip"}
-COUNTER_FILE = "profiles/hbm_traffic_{kernel}.json"
+COUNTER_FILE = "profiles/hbm_traffic_{workload}.json"
 
 
 def parse():
@@ -47,6 +46,9 @@ def parse():
     ap.add_argument("--cpu-repeats", type=int, default=3)
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="do not bracket kernels with events (no roofline)")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="after the run, copy one buffer of this many MiB (a plain copy "
+                         "kernel of known size, to scale HBM byte counters)")
     return ap.parse_args()
 
 
@@ -70,17 +72,18 @@ def kernel_work(name, w, pairs, rows):
     raise KeyError(name)
 
 
-def traffic_for(kernel, contract):
-    """HBM bytes per launch from committed counter runs, or None if absent or
-    taken on a different kernel source."""
-    path = os.path.join(ROOT, COUNTER_FILE.format(kernel=kernel))
+def traffic_for(kernel, w):
+    """HBM bytes per launch of `kernel` on workload `w` from the committed
+    FETCH_SIZE / WRITE_SIZE counter runs (scaled by a plain copy of known
+    size), or None if absent or taken on a different kernel source."""
+    path = os.path.join(ROOT, COUNTER_FILE.format(workload=w.name))
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("source_sha256") != sha256_of(KERNEL_SOURCES[contract]):
+    if rec.get("source_sha256") != sha256_of(KERNEL_SOURCES[w.contract]):
         return None
-    return rec.get("bytes_per_launch")
+    return rec.get("kernels", {}).get(kernel, {}).get("bytes_per_launch")
 
 
 def main():
@@ -196,7 +199,7 @@ def main():
             ach, peak, u = amount / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
         out["roofline"] = {"kernel": dom, "bound": bound, "achieved": round(ach, 3),
                            "peak": peak, "unit": u, "frac": round(ach / peak, 4),
-                           "traffic": traffic_for(dom, w.contract),
+                           "traffic": traffic_for(dom, w),
                            "algorithmic_per_launch": amount}
         out["bwd_credited_tflops"] = round(
             10.0 * w.d * pairs / (sum(kernels[k][1] / kernels[k][0] for k in kernels
@@ -205,6 +208,14 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"], out["parity"] = cpu_baseline(args, w, x, pairs,
                                                           (O, LSE, dQ, dK, dV))
+    if args.copy_calibration_mib > 0:
+        n = args.copy_calibration_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = n * 4
     print(json.dumps(out), flush=True)
 
 
