@@ -57,19 +57,36 @@ def sha256_of(path):
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def kernel_work(name, w, pairs, rows):
+def kernel_work(name, w, pairs, rows, key_len=None):
     """Algorithmic work of one launch of kernel `name`: (amount, unit, bound)."""
     d, es = w.d, (4 if w.contract == "strict_f32" else 2)
     if name.startswith("attn_fwd"):
         return 4.0 * d * pairs, "flop", "mfma"
+    if name.startswith("attn_dkdvq"):
+        return 10.0 * d * pairs, "flop", "mfma"       # S recompute, dV, dP, dK, dQ
     if name.startswith("attn_dkdv"):
         return 8.0 * d * pairs, "flop", "mfma"        # S recompute, dV, dP, dK
+    if name.startswith("attn_dqreduce"):
+        # reads one d-vector partial per (64-key tile, query row) pair that
+        # holds an allowed key, writes dQ
+        return 4.0 * d * partial_rows(w, key_len) + 4.0 * w.B * w.H * w.L * d, "byte", "hbm"
     if name.startswith("attn_dq"):
         return 2.0 * d * pairs, "flop", "mfma"        # the dQ product itself
     if name.startswith("attn_rowdot"):
         n = w.B * w.H * w.L * d
         return 2.0 * n * es + 4.0 * rows, "byte", "hbm"
     raise KeyError(name)
+
+
+def partial_rows(w, key_len, key_rows=64):
+    """(key tile, query row) pairs the fused dQ reduction reads."""
+    total = 0
+    kls = [w.L] * w.B if key_len is None else [int(n) for n in key_len]
+    for n in kls:
+        nk = -(-min(n, w.L) // key_rows)
+        for i in range(w.L):
+            total += min(nk, i // key_rows + 1) if w.causal else nk
+    return total * w.H
 
 
 def traffic_for(kernel, w):
@@ -129,10 +146,7 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    use_events = not args.no_kernel_events
-    if use_events:
-        mg.mg_profile_reset()
-        mg.mg_profile_enable(True)
+    # Timed region: exactly `steps` steps between device synchronizations.
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     stops = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -143,11 +157,23 @@ def main():
         stops[k].record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
+    samples = sorted(a.elapsed_time(b) for a, b in zip(starts, stops))
+
+    # Per-kernel durations: the same `steps` steps again, with the library
+    # bracketing every kernel launch by HIP events on the launch stream.
     kernels = {}
-    if use_events:
+    events_ms_per_step = None
+    if not args.no_kernel_events:
+        mg.mg_profile_reset()
+        mg.mg_profile_enable(True)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        events_ms_per_step = (time.perf_counter() - t1) * 1e3 / args.steps
         mg.mg_profile_enable(False)
         kernels = mg.mg_profile_collect()
-    samples = sorted(a.elapsed_time(b) for a, b in zip(starts, stops))
 
     pairs = unmasked_pairs(w.B, w.H, w.L, w.causal, x.key_len)
     rows = w.B * w.H * w.L
@@ -178,12 +204,14 @@ def main():
                     "min": round(samples[0], 4), "max": round(samples[-1], 4)},
         "pct_of_mfma_peak": round(100.0 * value / PEAK_TFLOPS[w.contract], 2),
     }
+    if events_ms_per_step is not None:
+        out["ms_per_step_with_kernel_events"] = round(events_ms_per_step, 4)
 
     if kernels:
         per = {}
         for name, (n, total) in kernels.items():
             avg = total / n
-            amount, unit, bound = kernel_work(name, w, pairs, rows)
+            amount, unit, bound = kernel_work(name, w, pairs, rows, x.key_len)
             rate = amount / (avg * 1e-3) / (1e12 if unit == "flop" else 1e9)
             per[name] = {"launches": n, "avg_ms": round(avg, 5), "bound": bound,
                          "achieved": round(rate, 3),
@@ -191,7 +219,7 @@ def main():
         out["kernels"] = per
         dom = max(kernels, key=lambda k: kernels[k][1])
         n, total = kernels[dom]
-        amount, unit, bound = kernel_work(dom, w, pairs, rows)
+        amount, unit, bound = kernel_work(dom, w, pairs, rows, x.key_len)
         avg_s = total / n * 1e-3
         if unit == "flop":
             ach, peak, u = amount / avg_s / 1e12, PEAK_TFLOPS[w.contract], "TFLOP/s"

@@ -85,9 +85,12 @@ mg_status_t mg_attn_fwd(const void *Q, const void *K, const void *V,
                         mg_contract_t contract, hipStream_t stream);
 
 /*
- * Bytes of device workspace that mg_attn_bwd needs for these arguments
- * (f32 D = rowsum(dO o O), one per query row, rounded up to 256 bytes).
- * Returns 0 when the arguments are invalid.
+ * Bytes of device workspace that mg_attn_bwd needs for these arguments:
+ * f32 D = rowsum(dO o O), one per query row, rounded up to 256 bytes, plus,
+ * for strict_f32 with d <= 64 when they fit in 1 GiB, one f32 dQ partial per
+ * (64-key tile, query row) (ceil(L/64) * B*H*L*d floats), which lets the
+ * dK/dV kernel produce dQ without a second recompute.  Returns 0 when the
+ * arguments are invalid.
  */
 size_t mg_attn_bwd_workspace_bytes(int B, int H, int L, int d, int causal,
                                    mg_contract_t contract);
@@ -96,9 +99,11 @@ size_t mg_attn_bwd_workspace_bytes(int B, int H, int L, int d, int causal,
  * Backward pass: dQ, dK, dV from Q, K, V, the forward outputs O and LSE, and
  * the upstream gradient dO (the paper's attention derivative node, Sec. 3.1,
  * lowered to a fused dK+dV kernel and a separate dQ kernel, Sec. 3.3 and
- * Sec. 8).  P is recomputed from Q, K and the saved LSE; nothing of size
- * L x L is stored.  `workspace` is caller-owned device memory of at least
- * mg_attn_bwd_workspace_bytes(...) bytes; its contents on entry are ignored
+ * Sec. 8; for strict_f32 with d <= 64 the dK+dV kernel also emits per-tile
+ * dQ partials that a reduction kernel sums).  P is recomputed from Q, K and
+ * the saved LSE; nothing of size L x L is stored.  `workspace` is
+ * caller-owned device memory of at least mg_attn_bwd_workspace_bytes(...)
+ * bytes; its contents on entry are ignored
  * and on return are unspecified.  dK and dV rows of masked (padded) keys are
  * written as exact zeros.  Deterministic: no atomics, bitwise identical
  * results for identical inputs.

@@ -16,37 +16,75 @@
 // Every product runs on v_mfma_f32_16x16x4_f32 (f32 inputs, f32 accumulate),
 // which is what the strict contract permits (Sec. 4.2).  Each wave owns 16
 // rows of the stationary tile (one per lane column l%16); the other operand
-// is staged through LDS and shared by the four waves of a workgroup.
+// is staged through LDS, 64 rows at a time, and shared by the waves of a
+// workgroup.  With double buffering the next tile is written into the other
+// LDS buffer after the current one has been consumed, so one barrier per
+// tile suffices.
 //
 // Workgroup order: the 1-D grid is numbered rank-major over heads
 // (id = rank * B*H + head) with rank 0 the tile that has the most work under
 // a causal mask, so the longest tiles start first; with B*H a multiple of 8
 // every tile of a head lands on the same XCD (workgroups are dealt to the
 // eight XCDs round-robin), so a head's K/V or Q/dO stay in one L2.
+//
+// Masking needs no per-tile branch: an element's offset inside its tile is
+// compared against one per-lane threshold (key length, causal diagonal).
+#include <climits>
+
 #include "device_common.h"
 #include "launch.h"
 #include "tiles_f32.h"
 
+// Per-kernel launch configuration: waves per workgroup, minimum waves per
+// SIMD requested from the register allocator (0 = compiler default), and
+// double-buffered LDS.  The defaults are the fastest of a sweep on MI355X at
+// B8 H8 L1024 d64 (double buffering lost there: it halves the workgroups an
+// LDS-heavy CU can hold); they can be overridden at build time.
+#ifndef MG_FWD_CFG
+#define MG_FWD_CFG 4, 3, false
+#endif
+#ifndef MG_DKDV_CFG
+#define MG_DKDV_CFG 4, 3, false
+#endif
+#ifndef MG_DQ_CFG
+#define MG_DQ_CFG 8, 0, false
+#endif
+#ifndef MG_DKDV_NIB
+#define MG_DKDV_NIB 2   // 16-row query blocks per dK/dV step (d <= 64)
+#endif
+
 namespace mg {
 namespace {
 
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
-constexpr int kStatRows = 16 * kWaves;   // stationary rows per workgroup
-constexpr int kStream = 64;              // streamed rows per step
+constexpr int kStream = 64;   // streamed rows per step
+
+template <int NW_, int OCC_, bool DB_>
+struct Cfg {
+    static constexpr int NW = NW_;             // waves per workgroup
+    static constexpr int NT = 64 * NW_;        // threads per workgroup
+    static constexpr int ROWS = 16 * NW_;      // stationary rows per workgroup
+    static constexpr int OCC = OCC_ > 0 ? OCC_ : 1;
+    // the occupancy request only holds without spills for d <= 64
+    template <int D> static constexpr int occ() { return D <= 64 ? OCC : 1; }
+    static constexpr int NBUF = DB_ ? 2 : 1;   // LDS buffers for the streamed tile
+};
+using FwdCfg = Cfg<MG_FWD_CFG>;
+using DkdvCfg = Cfg<MG_DKDV_CFG>;
+using DqCfg = Cfg<MG_DQ_CFG>;
 
 // ---------------------------------------------------------------- forward --
-template <int D>
-__global__ __launch_bounds__(kThreads) void attn_fwd_f32(
-    const float *__restrict__ Q, const float *__restrict__ K, const float *__restrict__ V,
-    float *__restrict__ O, float *__restrict__ LSE, const int32_t *__restrict__ key_len,
-    int H, int L, int causal, float scale_log2, int n_qtiles, int BH) {
+template <int D, class C>
+__global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::template occ<D>(), 8)))
+void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
+                  const float *__restrict__ V, float *__restrict__ O, float *__restrict__ LSE,
+                  const int32_t *__restrict__ key_len, int H, int L, int causal,
+                  float scale_log2, int n_qtiles, int BH) {
     constexpr int DQ = D / 4;    // contraction values per lane in one S chain
     constexpr int NC = D / 16;   // 16-column blocks of the head dimension
-    using Stager = F32TileStager<kStream, D, kThreads>;
+    using Stager = F32TileStager<kStream, D, C::NT>;
     constexpr int LD = Stager::kLd;
-    __shared__ __attribute__((aligned(16))) float Ks[kStream][LD];
-    __shared__ __attribute__((aligned(16))) float Vs[kStream][LD];
+    __shared__ __attribute__((aligned(16))) float Ks[C::NBUF][kStream][LD];
+    __shared__ __attribute__((aligned(16))) float Vs[C::NBUF][kStream][LD];
 
     const int rank = blockIdx.x / BH;
     const int head = blockIdx.x - rank * BH;
@@ -60,11 +98,11 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32(
     const int lane = tid & 63;
     const int il = lane & 15;
     const int g = lane >> 4;
-    const int q0 = qt * kStatRows;
+    const int q0 = qt * C::ROWS;
     const int qi = q0 + 16 * (tid >> 6) + il;
 
     const int klen = key_limit(key_len, b, L);
-    const int kend = causal ? min(klen, q0 + kStatRows) : klen;
+    const int kend = causal ? min(klen, q0 + C::ROWS) : klen;
     const int ntiles = (kend + kStream - 1) / kStream;
 
     // B operand of S^T = K Q^T: lane holds Q[qi][g*DQ + s].
@@ -87,12 +125,20 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32(
     if (ntiles > 0) {
         kst.load(Kh, 0, L, tid);
         vst.load(Vh, 0, L, tid);
+        if (C::NBUF == 2) {
+            kst.store(Ks[0], tid);
+            vst.store(Vs[0], tid);
+            __syncthreads();
+        }
     }
     for (int kt = 0; kt < ntiles; ++kt) {
-        __syncthreads();
-        kst.store(Ks, tid);
-        vst.store(Vs, tid);
-        __syncthreads();
+        const int cur = (C::NBUF == 2) ? (kt & 1) : 0;
+        if (C::NBUF == 1) {
+            __syncthreads();
+            kst.store(Ks[0], tid);
+            vst.store(Vs[0], tid);
+            __syncthreads();
+        }
         if (kt + 1 < ntiles) {
             kst.load(Kh, (kt + 1) * kStream, L, tid);
             vst.load(Vh, (kt + 1) * kStream, L, tid);
@@ -107,7 +153,7 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32(
             f32x4 a[4];
 #pragma unroll
             for (int jb = 0; jb < 4; ++jb)
-                a[jb] = *reinterpret_cast<const f32x4 *>(&Ks[16 * jb + il][g * DQ + 4 * s4]);
+                a[jb] = *reinterpret_cast<const f32x4 *>(&Ks[cur][16 * jb + il][g * DQ + 4 * s4]);
 #pragma unroll
             for (int e = 0; e < 4; ++e)
 #pragma unroll
@@ -115,16 +161,16 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32(
                     sacc[jb] = mfma16x16x4(a[jb][e], qreg[4 * s4 + e], sacc[jb]);
         }
 
-        // Mask, scale to base 2, and update the running max and sum.
+        // Element (jb, r) holds key j0 + 16jb + r, allowed iff that offset is
+        // below a per-lane threshold (key length; the query row if causal).
         const int j0 = kt * kStream + 4 * g;
+        const int thr = causal ? min(klen - j0, qi - j0 + 1) : klen - j0;
         float mx = -INFINITY;
 #pragma unroll
         for (int jb = 0; jb < 4; ++jb)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int j = j0 + 16 * jb + r;
-                const bool ok = (j < klen) && (!causal || j <= qi);
-                const float t = ok ? sacc[jb][r] * scale_log2 : -INFINITY;
+                const float t = (16 * jb + r < thr) ? sacc[jb][r] * scale_log2 : -INFINITY;
                 sacc[jb][r] = t;
                 mx = fmaxf(mx, t);
             }
@@ -153,8 +199,16 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_f32(
             for (int r = 0; r < 4; ++r)
 #pragma unroll
                 for (int c = 0; c < NC; ++c)
-                    oacc[c] = mfma16x16x4(Vs[16 * jb + 4 * g + r][16 * c + il], sacc[jb][r],
+                    oacc[c] = mfma16x16x4(Vs[cur][16 * jb + 4 * g + r][16 * c + il], sacc[jb][r],
                                           oacc[c]);
+
+        if (C::NBUF == 2) {
+            if (kt + 1 < ntiles) {
+                kst.store(Ks[cur ^ 1], tid);
+                vst.store(Vs[cur ^ 1], tid);
+            }
+            __syncthreads();
+        }
     }
 
     const float l = sum_over_groups(l_run);
@@ -189,23 +243,25 @@ __global__ __launch_bounds__(256) void attn_rowdot_f32(const float *__restrict__
 }
 
 // ------------------------------------------------------- backward: dK, dV
-// Key tile of 64 keys stationary (16 per wave, one per lane column); query
-// tiles of NIB*16 rows stream through LDS.
-template <int D, int NIB>
-__global__ __launch_bounds__(kThreads) void attn_dkdv_f32(
-    const float *__restrict__ Q, const float *__restrict__ K, const float *__restrict__ V,
-    const float *__restrict__ dO, const float *__restrict__ LSE, const float *__restrict__ Dws,
-    float *__restrict__ dK, float *__restrict__ dV, const int32_t *__restrict__ key_len, int H,
-    int L, int causal, float scale, float scale_log2, int BH) {
+// Key tile of C::ROWS keys stationary (16 per wave, one per lane column);
+// query tiles of NIB*16 rows stream through LDS.
+template <int D, int NIB, class C>
+__global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::template occ<D>(), 8)))
+void attn_dkdv_f32(const float *__restrict__ Q, const float *__restrict__ K,
+                   const float *__restrict__ V, const float *__restrict__ dO,
+                   const float *__restrict__ LSE, const float *__restrict__ Dws,
+                   float *__restrict__ dK, float *__restrict__ dV,
+                   const int32_t *__restrict__ key_len, int H, int L, int causal, float scale,
+                   float scale_log2, int BH) {
     constexpr int DQ = D / 4;
     constexpr int NC = D / 16;
     constexpr int BR = 16 * NIB;
-    using Stager = F32TileStager<BR, D, kThreads>;
+    using Stager = F32TileStager<BR, D, C::NT>;
     constexpr int LD = Stager::kLd;
-    __shared__ __attribute__((aligned(16))) float Qs[BR][LD];
-    __shared__ __attribute__((aligned(16))) float dOs[BR][LD];
-    __shared__ __attribute__((aligned(16))) float lse2s[BR];
-    __shared__ __attribute__((aligned(16))) float Ds[BR];
+    __shared__ __attribute__((aligned(16))) float Qs[C::NBUF][BR][LD];
+    __shared__ __attribute__((aligned(16))) float dOs[C::NBUF][BR][LD];
+    __shared__ __attribute__((aligned(16))) float lse2s[C::NBUF][BR];
+    __shared__ __attribute__((aligned(16))) float Ds[C::NBUF][BR];
 
     const int rank = blockIdx.x / BH;
     const int head = blockIdx.x - rank * BH;
@@ -219,7 +275,7 @@ __global__ __launch_bounds__(kThreads) void attn_dkdv_f32(
     const int lane = tid & 63;
     const int il = lane & 15;
     const int g = lane >> 4;
-    const int k0 = kt * kStatRows;
+    const int k0 = kt * C::ROWS;
     const int kj = k0 + 16 * (tid >> 6) + il;   // this lane's key
 
     const int klen = key_limit(key_len, b, L);
@@ -259,6 +315,208 @@ __global__ __launch_bounds__(kThreads) void attn_dkdv_f32(
             d_pre = (row < L) ? Dws[(size_t)head * L + row] : 0.f;
         }
     };
+    auto store_rows = [&](int buf) {
+        qst.store(Qs[buf], tid);
+        ost.store(dOs[buf], tid);
+        if (tid < BR) {
+            lse2s[buf][tid] = lse_pre;
+            Ds[buf][tid] = d_pre;
+        }
+    };
+    if (qstart < qstop) {
+        load_rows(qstart);
+        if (C::NBUF == 2) {
+            store_rows(0);
+            __syncthreads();
+        }
+    }
+
+    for (int qt = qstart; qt < qstop; ++qt) {
+        const int cur = (C::NBUF == 2) ? ((qt - qstart) & 1) : 0;
+        if (C::NBUF == 1) {
+            __syncthreads();
+            store_rows(0);
+            __syncthreads();
+        }
+        if (qt + 1 < qstop) load_rows(qt + 1);
+
+        // S[16ib + 4g + r][kj] and dP[..][kj]
+        f32x4 sacc[NIB], pacc[NIB];
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib) {
+            sacc[ib] = zero4();
+            pacc[ib] = zero4();
+        }
+#pragma unroll
+        for (int s4 = 0; s4 < DQ / 4; ++s4) {
+            f32x4 aq[NIB], ao[NIB];
+#pragma unroll
+            for (int ib = 0; ib < NIB; ++ib) {
+                aq[ib] = *reinterpret_cast<const f32x4 *>(&Qs[cur][16 * ib + il][g * DQ + 4 * s4]);
+                ao[ib] = *reinterpret_cast<const f32x4 *>(&dOs[cur][16 * ib + il][g * DQ + 4 * s4]);
+            }
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int ib = 0; ib < NIB; ++ib) {
+                    sacc[ib] = mfma16x16x4(aq[ib][e], kreg[4 * s4 + e], sacc[ib]);
+                    pacc[ib] = mfma16x16x4(ao[ib][e], vreg[4 * s4 + e], pacc[ib]);
+                }
+        }
+
+        // P = exp(S - LSE), dS = P (dP - D).  Under a causal mask element
+        // (ib, r) is query ibase + 16ib + r, allowed iff it is >= kj.  Padded
+        // keys (kj >= key length) are not masked here: their rows of dK and dV
+        // are overwritten with zeros at the end.  Rows past L hold Q = dO = 0
+        // and LSE = D = 0, so they contribute exactly nothing.
+        const int ibase = qt * BR + 4 * g;
+        const int thr = causal ? kj - ibase : INT_MIN;
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib) {
+            const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lse2s[cur][16 * ib + 4 * g]);
+            const f32x4 dd = *reinterpret_cast<const f32x4 *>(&Ds[cur][16 * ib + 4 * g]);
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                float p = exp2_fast(sacc[ib][r] * scale_log2 - l2[r]);
+                p = (16 * ib + r >= thr) ? p : 0.f;
+                sacc[ib][r] = p;
+                pacc[ib][r] = p * (pacc[ib][r] - dd[r]);
+            }
+        }
+
+        // dV^T[16c + 4g + r][kj] += sum_i dO[i][16c + il'] P[i][kj]
+        // dK^T[16c + 4g + r][kj] += sum_i  Q[i][16c + il'] dS[i][kj]
+#pragma unroll
+        for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+#pragma unroll
+                for (int c = 0; c < NC; ++c) {
+                    dvacc[c] = mfma16x16x4(dOs[cur][16 * ib + 4 * g + r][16 * c + il],
+                                           sacc[ib][r], dvacc[c]);
+                    dkacc[c] = mfma16x16x4(Qs[cur][16 * ib + 4 * g + r][16 * c + il],
+                                           pacc[ib][r], dkacc[c]);
+                }
+
+        if (C::NBUF == 2) {
+            if (qt + 1 < qstop) store_rows(cur ^ 1);
+            __syncthreads();
+        }
+    }
+
+    if (kj < L) {
+        const bool keep = kj < klen;   // padded keys get exact zeros
+        float *dkrow = dK + hoff + (size_t)kj * D;
+        float *dvrow = dV + hoff + (size_t)kj * D;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            *reinterpret_cast<f32x4 *>(dkrow + 16 * c + 4 * g) = keep ? dkacc[c] * scale : zero4();
+            *reinterpret_cast<f32x4 *>(dvrow + 16 * c + 4 * g) = keep ? dvacc[c] : zero4();
+        }
+    }
+}
+
+// ---------------------------------------- backward: dK, dV and dQ partials
+// The key-stationary kernel above, extended with the dQ product: after dS of
+// a query tile is known, it goes through LDS and the workgroup multiplies it
+// by its own 64-key tile, dQ_part[i][:] = sum_{j in tile} dS[i][j] K[j][:].
+// Each (key tile, query row) partial is written once to the workspace and
+// attn_dq_reduce_f32 adds the partials of a row in key-tile order: no atomics,
+// bitwise-reproducible, and no second recompute of S and dP.
+template <int D, int NIB, class C>
+__global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::template occ<D>(), 8)))
+void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
+                    const float *__restrict__ V, const float *__restrict__ dO,
+                    const float *__restrict__ LSE, const float *__restrict__ Dws,
+                    float *__restrict__ dK, float *__restrict__ dV, float *__restrict__ dQp,
+                    const int32_t *__restrict__ key_len, int H, int L, int causal, float scale,
+                    float scale_log2, int BH) {
+    constexpr int DQ = D / 4;
+    constexpr int NC = D / 16;
+    constexpr int BR = 16 * NIB;
+    constexpr int KR = C::ROWS;                 // keys per workgroup
+    constexpr int NBLK = NIB * NC;              // 16x16 blocks of a dQ partial tile
+    constexpr int PER_WAVE = NBLK / C::NW;
+    static_assert(NBLK % C::NW == 0, "dQ blocks must split evenly over waves");
+    using Stager = F32TileStager<BR, D, C::NT>;
+    constexpr int LD = Stager::kLd;
+    __shared__ __attribute__((aligned(16))) float Qs[BR][LD];
+    __shared__ __attribute__((aligned(16))) float dOs[BR][LD];
+    __shared__ __attribute__((aligned(16))) float lse2s[BR];
+    __shared__ __attribute__((aligned(16))) float Ds[BR];
+    __shared__ __attribute__((aligned(16))) float Kt[D][KR + 4];    // key tile, transposed
+    __shared__ __attribute__((aligned(16))) float dSs[BR][KR + 4];  // dS of the query tile
+
+    const int rank = blockIdx.x / BH;
+    const int head = blockIdx.x - rank * BH;
+    const int kt = rank;
+    const int b = head / H;
+    const size_t hoff = (size_t)head * L * D;
+    const float *Qh = Q + hoff;
+    const float *dOh = dO + hoff;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = tid >> 6;
+    const int il = lane & 15;
+    const int g = lane >> 4;
+    const int k0 = kt * KR;
+    const int kj = k0 + 16 * w + il;
+
+    const int klen = key_limit(key_len, b, L);
+    const int nq = (L + BR - 1) / BR;
+    const int qstart = causal ? (k0 / BR) : 0;
+    const int qstop = (k0 < klen) ? nq : qstart;
+
+    float kreg[DQ], vreg[DQ];
+#pragma unroll
+    for (int s4 = 0; s4 < DQ / 4; ++s4) {
+        const size_t off = hoff + (size_t)kj * D + g * DQ + 4 * s4;
+        const f32x4 kv = (kj < L) ? *reinterpret_cast<const f32x4 *>(K + off) : zero4();
+        const f32x4 vv = (kj < L) ? *reinterpret_cast<const f32x4 *>(V + off) : zero4();
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            kreg[4 * s4 + e] = kv[e];
+            vreg[4 * s4 + e] = vv[e];
+        }
+    }
+    // The key tile, transposed, for the A operand of the dQ product; made
+    // visible by the first barrier of the loop.
+    for (int f = tid; f < KR * (D / 4); f += C::NT) {
+        const int row = f / (D / 4);
+        const int c4 = f - row * (D / 4);
+        const f32x4 v = (k0 + row < L)
+            ? *reinterpret_cast<const f32x4 *>(K + hoff + (size_t)(k0 + row) * D + 4 * c4)
+            : zero4();
+#pragma unroll
+        for (int e = 0; e < 4; ++e) Kt[4 * c4 + e][row] = v[e];
+    }
+
+    f32x4 dkacc[NC], dvacc[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+        dkacc[c] = zero4();
+        dvacc[c] = zero4();
+    }
+
+    // Under a causal mask element (ib, r) is query ibase + 16ib + r, allowed
+    // iff it is >= kj; a padded key (kj >= key length) is masked everywhere
+    // so that it adds nothing to dQ.
+    // (sentinels +-2^30 keep kthr - ibase free of overflow)
+    constexpr int kNever = 1 << 30;
+    const int kthr = (kj >= klen) ? kNever : (causal ? kj : -kNever);
+
+    Stager qst, ost;
+    float lse_pre = 0.f, d_pre = 0.f;
+    auto load_rows = [&](int qt) {
+        qst.load(Qh, qt * BR, L, tid);
+        ost.load(dOh, qt * BR, L, tid);
+        if (tid < BR) {
+            const int row = qt * BR + tid;
+            lse_pre = (row < L) ? LSE[(size_t)head * L + row] * kLog2e : 0.f;
+            d_pre = (row < L) ? Dws[(size_t)head * L + row] : 0.f;
+        }
+    };
     if (qstart < qstop) load_rows(qstart);
 
     for (int qt = qstart; qt < qstop; ++qt) {
@@ -272,7 +530,6 @@ __global__ __launch_bounds__(kThreads) void attn_dkdv_f32(
         __syncthreads();
         if (qt + 1 < qstop) load_rows(qt + 1);
 
-        // S[16ib + 4g + r][kj] and dP[..][kj]
         f32x4 sacc[NIB], pacc[NIB];
 #pragma unroll
         for (int ib = 0; ib < NIB; ++ib) {
@@ -296,24 +553,22 @@ __global__ __launch_bounds__(kThreads) void attn_dkdv_f32(
                 }
         }
 
-        // P = exp(S - LSE) on allowed pairs, dS = P (dP - D).
         const int ibase = qt * BR + 4 * g;
+        const int thr = kthr - ibase;
 #pragma unroll
         for (int ib = 0; ib < NIB; ++ib) {
             const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lse2s[16 * ib + 4 * g]);
             const f32x4 dd = *reinterpret_cast<const f32x4 *>(&Ds[16 * ib + 4 * g]);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int i = ibase + 16 * ib + r;
-                const bool ok = (i < L) && (kj < klen) && (!causal || kj <= i);
-                const float p = ok ? exp2_fast(sacc[ib][r] * scale_log2 - l2[r]) : 0.f;
+                float p = exp2_fast(sacc[ib][r] * scale_log2 - l2[r]);
+                p = (16 * ib + r >= thr) ? p : 0.f;
                 sacc[ib][r] = p;
                 pacc[ib][r] = p * (pacc[ib][r] - dd[r]);
+                dSs[16 * ib + 4 * g + r][16 * w + il] = pacc[ib][r];
             }
         }
 
-        // dV^T[16c + 4g + r][kj] += sum_i dO[i][16c + il'] P[i][kj]
-        // dK^T[16c + 4g + r][kj] += sum_i  Q[i][16c + il'] dS[i][kj]
 #pragma unroll
         for (int ib = 0; ib < NIB; ++ib)
 #pragma unroll
@@ -325,33 +580,82 @@ __global__ __launch_bounds__(kThreads) void attn_dkdv_f32(
                     dkacc[c] = mfma16x16x4(Qs[16 * ib + 4 * g + r][16 * c + il], pacc[ib][r],
                                            dkacc[c]);
                 }
+
+        // dQ_part^T[16c + 4g + r][16ib + il] = sum_j K^T[16c + il'][j] dS^T[j][16ib + il]
+        __syncthreads();
+#pragma unroll
+        for (int bb = 0; bb < PER_WAVE; ++bb) {
+            const int blk = w * PER_WAVE + bb;
+            const int ib = blk / NC;
+            const int c = blk - ib * NC;
+            f32x4 acc = zero4();
+#pragma unroll
+            for (int q = 0; q < KR / 16; ++q) {
+                const f32x4 bv = *reinterpret_cast<const f32x4 *>(&dSs[16 * ib + il][16 * q + 4 * g]);
+                const f32x4 av = *reinterpret_cast<const f32x4 *>(&Kt[16 * c + il][16 * q + 4 * g]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc = mfma16x16x4(av[e], bv[e], acc);
+            }
+            const int row = qt * BR + 16 * ib + il;
+            if (row < L)
+                *reinterpret_cast<f32x4 *>(dQp + ((size_t)kt * BH + head) * L * D +
+                                           (size_t)row * D + 16 * c + 4 * g) = acc;
+        }
     }
 
     if (kj < L) {
+        const bool keep = kj < klen;
         float *dkrow = dK + hoff + (size_t)kj * D;
         float *dvrow = dV + hoff + (size_t)kj * D;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
-            *reinterpret_cast<f32x4 *>(dkrow + 16 * c + 4 * g) = dkacc[c] * scale;
-            *reinterpret_cast<f32x4 *>(dvrow + 16 * c + 4 * g) = dvacc[c];
+            *reinterpret_cast<f32x4 *>(dkrow + 16 * c + 4 * g) = keep ? dkacc[c] * scale : zero4();
+            *reinterpret_cast<f32x4 *>(dvrow + 16 * c + 4 * g) = keep ? dvacc[c] : zero4();
         }
     }
 }
 
-// ------------------------------------------------------------ backward: dQ
-// Query tile of 64 rows stationary (16 per wave); key tiles stream.
+// dQ[i] = scale * sum over key tiles kt that hold an allowed key for row i of
+// dQ_part[kt][i], added in increasing kt (a fixed order).
 template <int D>
-__global__ __launch_bounds__(kThreads) void attn_dq_f32(
-    const float *__restrict__ Q, const float *__restrict__ K, const float *__restrict__ V,
-    const float *__restrict__ dO, const float *__restrict__ LSE, const float *__restrict__ Dws,
-    float *__restrict__ dQ, const int32_t *__restrict__ key_len, int H, int L, int causal,
-    float scale, float scale_log2, int n_qtiles, int BH) {
+__global__ __launch_bounds__(256) void attn_dq_reduce_f32(const float *__restrict__ dQp,
+                                                          float *__restrict__ dQ,
+                                                          const int32_t *__restrict__ key_len,
+                                                          int H, int L, int causal, float scale,
+                                                          int BH, int key_rows) {
+    constexpr int C4 = D / 4;
+    const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
+    const size_t total = (size_t)BH * L * C4;
+    if (idx >= total) return;
+    const size_t rowg = idx / C4;              // head * L + i
+    const int head = (int)(rowg / L);
+    const int i = (int)(rowg - (size_t)head * L);
+    const int klen = key_limit(key_len, head / H, L);
+    const int nk = (klen + key_rows - 1) / key_rows;
+    const int kmax = causal ? min(nk, i / key_rows + 1) : nk;
+    const size_t stride = (size_t)BH * L * D;
+    const float *src = dQp + idx * 4;
+    f32x4 sum = zero4();
+    for (int kt = 0; kt < kmax; ++kt)
+        sum += *reinterpret_cast<const f32x4 *>(src + (size_t)kt * stride);
+    *reinterpret_cast<f32x4 *>(dQ + idx * 4) = sum * scale;
+}
+
+// ------------------------------------------------------------ backward: dQ
+// Query tile of C::ROWS rows stationary (16 per wave); key tiles stream.
+template <int D, class C>
+__global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::template occ<D>(), 8)))
+void attn_dq_f32(const float *__restrict__ Q, const float *__restrict__ K,
+                 const float *__restrict__ V, const float *__restrict__ dO,
+                 const float *__restrict__ LSE, const float *__restrict__ Dws,
+                 float *__restrict__ dQ, const int32_t *__restrict__ key_len, int H, int L,
+                 int causal, float scale, float scale_log2, int n_qtiles, int BH) {
     constexpr int DQ = D / 4;
     constexpr int NC = D / 16;
-    using Stager = F32TileStager<kStream, D, kThreads>;
+    using Stager = F32TileStager<kStream, D, C::NT>;
     constexpr int LD = Stager::kLd;
-    __shared__ __attribute__((aligned(16))) float Ks[kStream][LD];
-    __shared__ __attribute__((aligned(16))) float Vs[kStream][LD];
+    __shared__ __attribute__((aligned(16))) float Ks[C::NBUF][kStream][LD];
+    __shared__ __attribute__((aligned(16))) float Vs[C::NBUF][kStream][LD];
 
     const int rank = blockIdx.x / BH;
     const int head = blockIdx.x - rank * BH;
@@ -365,11 +669,11 @@ __global__ __launch_bounds__(kThreads) void attn_dq_f32(
     const int lane = tid & 63;
     const int il = lane & 15;
     const int g = lane >> 4;
-    const int q0 = qt * kStatRows;
+    const int q0 = qt * C::ROWS;
     const int qi = q0 + 16 * (tid >> 6) + il;
 
     const int klen = key_limit(key_len, b, L);
-    const int kend = causal ? min(klen, q0 + kStatRows) : klen;
+    const int kend = causal ? min(klen, q0 + C::ROWS) : klen;
     const int ntiles = (kend + kStream - 1) / kStream;
 
     float qreg[DQ], oreg[DQ];
@@ -395,12 +699,20 @@ __global__ __launch_bounds__(kThreads) void attn_dq_f32(
     if (ntiles > 0) {
         kst.load(Kh, 0, L, tid);
         vst.load(Vh, 0, L, tid);
+        if (C::NBUF == 2) {
+            kst.store(Ks[0], tid);
+            vst.store(Vs[0], tid);
+            __syncthreads();
+        }
     }
     for (int kt = 0; kt < ntiles; ++kt) {
-        __syncthreads();
-        kst.store(Ks, tid);
-        vst.store(Vs, tid);
-        __syncthreads();
+        const int cur = (C::NBUF == 2) ? (kt & 1) : 0;
+        if (C::NBUF == 1) {
+            __syncthreads();
+            kst.store(Ks[0], tid);
+            vst.store(Vs[0], tid);
+            __syncthreads();
+        }
         if (kt + 1 < ntiles) {
             kst.load(Kh, (kt + 1) * kStream, L, tid);
             vst.load(Vh, (kt + 1) * kStream, L, tid);
@@ -418,8 +730,8 @@ __global__ __launch_bounds__(kThreads) void attn_dq_f32(
             f32x4 ak[4], av[4];
 #pragma unroll
             for (int jb = 0; jb < 4; ++jb) {
-                ak[jb] = *reinterpret_cast<const f32x4 *>(&Ks[16 * jb + il][g * DQ + 4 * s4]);
-                av[jb] = *reinterpret_cast<const f32x4 *>(&Vs[16 * jb + il][g * DQ + 4 * s4]);
+                ak[jb] = *reinterpret_cast<const f32x4 *>(&Ks[cur][16 * jb + il][g * DQ + 4 * s4]);
+                av[jb] = *reinterpret_cast<const f32x4 *>(&Vs[cur][16 * jb + il][g * DQ + 4 * s4]);
             }
 #pragma unroll
             for (int e = 0; e < 4; ++e)
@@ -430,14 +742,15 @@ __global__ __launch_bounds__(kThreads) void attn_dq_f32(
                 }
         }
 
+        // Element (jb, r) holds key j0 + 16jb + r; same threshold as forward.
         const int j0 = kt * kStream + 4 * g;
+        const int thr = causal ? min(klen - j0, qi - j0 + 1) : klen - j0;
 #pragma unroll
         for (int jb = 0; jb < 4; ++jb)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int j = j0 + 16 * jb + r;
-                const bool ok = (qi < L) && (j < klen) && (!causal || j <= qi);
-                const float p = ok ? exp2_fast(sacc[jb][r] * scale_log2 - lse2) : 0.f;
+                float p = exp2_fast(sacc[jb][r] * scale_log2 - lse2);
+                p = (16 * jb + r < thr) ? p : 0.f;
                 pacc[jb][r] = p * (pacc[jb][r] - Di);
             }
 
@@ -448,8 +761,16 @@ __global__ __launch_bounds__(kThreads) void attn_dq_f32(
             for (int r = 0; r < 4; ++r)
 #pragma unroll
                 for (int c = 0; c < NC; ++c)
-                    dqacc[c] = mfma16x16x4(Ks[16 * jb + 4 * g + r][16 * c + il], pacc[jb][r],
-                                           dqacc[c]);
+                    dqacc[c] = mfma16x16x4(Ks[cur][16 * jb + 4 * g + r][16 * c + il],
+                                           pacc[jb][r], dqacc[c]);
+
+        if (C::NBUF == 2) {
+            if (kt + 1 < ntiles) {
+                kst.store(Ks[cur ^ 1], tid);
+                vst.store(Vs[cur ^ 1], tid);
+            }
+            __syncthreads();
+        }
     }
 
     if (qi < L) {
@@ -467,14 +788,15 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 // ---------------------------------------------------------------- launchers
 hipError_t launch_fwd_f32(const AttnProblem &p, const float *Q, const float *K,
                           const float *V, float *O, float *LSE, hipStream_t s) {
+    using C = FwdCfg;
     const int BH = p.B * p.H;
-    const int nqt = cdiv(p.L, kStatRows);
-    const dim3 grid(nqt * BH), block(kThreads);
+    const int nqt = cdiv(p.L, C::ROWS);
+    const dim3 grid(nqt * BH), block(C::NT);
     const float sl2 = p.scale * kLog2e;
     switch (p.d) {
-    case 32: attn_fwd_f32<32><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.L, p.causal, sl2, nqt, BH); break;
-    case 64: attn_fwd_f32<64><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.L, p.causal, sl2, nqt, BH); break;
-    case 128: attn_fwd_f32<128><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.L, p.causal, sl2, nqt, BH); break;
+    case 32: attn_fwd_f32<32, C><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.L, p.causal, sl2, nqt, BH); break;
+    case 64: attn_fwd_f32<64, C><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.L, p.causal, sl2, nqt, BH); break;
+    case 128: attn_fwd_f32<128, C><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.L, p.causal, sl2, nqt, BH); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -496,13 +818,45 @@ hipError_t launch_bwd_rowdot_f32(const AttnProblem &p, const float *O, const flo
 hipError_t launch_bwd_dkdv_f32(const AttnProblem &p, const float *Q, const float *K,
                                const float *V, const float *dO, const float *LSE,
                                const float *Dws, float *dK, float *dV, hipStream_t s) {
+    using C = DkdvCfg;
     const int BH = p.B * p.H;
-    const dim3 grid(cdiv(p.L, kStatRows) * BH), block(kThreads);
+    const dim3 grid(cdiv(p.L, C::ROWS) * BH), block(C::NT);
     const float sl2 = p.scale * kLog2e;
     switch (p.d) {
-    case 32: attn_dkdv_f32<32, 4><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
-    case 64: attn_dkdv_f32<64, 4><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
-    case 128: attn_dkdv_f32<128, 2><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
+    case 32: attn_dkdv_f32<32, MG_DKDV_NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
+    case 64: attn_dkdv_f32<64, MG_DKDV_NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
+    case 128: attn_dkdv_f32<128, 2, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+int fused_dq_key_rows() { return DkdvCfg::ROWS; }
+
+hipError_t launch_bwd_dkdvq_f32(const AttnProblem &p, const float *Q, const float *K,
+                                const float *V, const float *dO, const float *LSE,
+                                const float *Dws, float *dK, float *dV, float *dQp,
+                                hipStream_t s) {
+    using C = DkdvCfg;
+    const int BH = p.B * p.H;
+    const dim3 grid(cdiv(p.L, C::ROWS) * BH), block(C::NT);
+    const float sl2 = p.scale * kLog2e;
+    switch (p.d) {
+    case 32: attn_dkdvq_f32<32, MG_DKDV_NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
+    case 64: attn_dkdvq_f32<64, MG_DKDV_NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+hipError_t launch_bwd_dq_reduce_f32(const AttnProblem &p, const float *dQp, float *dQ,
+                                    hipStream_t s) {
+    const int BH = p.B * p.H;
+    const size_t total = (size_t)BH * p.L * (p.d / 4);
+    const dim3 grid((unsigned)((total + 255) / 256)), block(256);
+    switch (p.d) {
+    case 32: attn_dq_reduce_f32<32><<<grid, block, 0, s>>>(dQp, dQ, p.key_len, p.H, p.L, p.causal, p.scale, BH, DkdvCfg::ROWS); break;
+    case 64: attn_dq_reduce_f32<64><<<grid, block, 0, s>>>(dQp, dQ, p.key_len, p.H, p.L, p.causal, p.scale, BH, DkdvCfg::ROWS); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -511,14 +865,15 @@ hipError_t launch_bwd_dkdv_f32(const AttnProblem &p, const float *Q, const float
 hipError_t launch_bwd_dq_f32(const AttnProblem &p, const float *Q, const float *K,
                              const float *V, const float *dO, const float *LSE,
                              const float *Dws, float *dQ, hipStream_t s) {
+    using C = DqCfg;
     const int BH = p.B * p.H;
-    const int nqt = cdiv(p.L, kStatRows);
-    const dim3 grid(nqt * BH), block(kThreads);
+    const int nqt = cdiv(p.L, C::ROWS);
+    const dim3 grid(nqt * BH), block(C::NT);
     const float sl2 = p.scale * kLog2e;
     switch (p.d) {
-    case 32: attn_dq_f32<32><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
-    case 64: attn_dq_f32<64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
-    case 128: attn_dq_f32<128><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
+    case 32: attn_dq_f32<32, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
+    case 64: attn_dq_f32<64, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
+    case 128: attn_dq_f32<128, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -40,6 +40,17 @@ hipError_t launch_bwd_dkdv_bf16(const AttnProblem &p, const uint16_t *Q,
                                 const float *LSE, const float *Dws, uint16_t *dK,
                                 uint16_t *dV, hipStream_t s);
 
+// Backward steps 2+3 fused (strict f32, d <= 64): dK, dV as above plus one
+// f32 dQ partial per (key tile, query row) written to dQp, laid out
+// [key tile][B*H][L][d]; then dQ = scale * sum of a row's partials.
+int fused_dq_key_rows();
+hipError_t launch_bwd_dkdvq_f32(const AttnProblem &p, const float *Q, const float *K,
+                                const float *V, const float *dO, const float *LSE,
+                                const float *Dws, float *dK, float *dV, float *dQp,
+                                hipStream_t s);
+hipError_t launch_bwd_dq_reduce_f32(const AttnProblem &p, const float *dQp, float *dQ,
+                                    hipStream_t s);
+
 // Backward step 3: dQ with the query tile stationary.
 hipError_t launch_bwd_dq_f32(const AttnProblem &p, const float *Q, const float *K,
                              const float *V, const float *dO, const float *LSE,

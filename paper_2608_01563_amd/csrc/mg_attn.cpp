@@ -174,9 +174,28 @@ const char *kernel_name(const char *stage, mg_contract_t c, int d) {
     return it->second.c_str();
 }
 
-size_t workspace_bytes(int B, int H, int L) {
-    const size_t raw = (size_t)B * H * L * sizeof(float);
-    return (raw + 255) / 256 * 256;
+size_t round256(size_t n) { return (n + 255) / 256 * 256; }
+
+// Strict f32 with d <= 64 fuses dQ into the key-stationary kernel when its
+// per-key-tile partials fit under this many bytes; otherwise (and for bf16)
+// a separate query-stationary dQ kernel recomputes what it needs.
+constexpr size_t kFusedPartialLimit = size_t(1) << 30;
+
+size_t dq_partial_bytes(int B, int H, int L, int d) {
+    const int kr = mg::fused_dq_key_rows();
+    return (size_t)((L + kr - 1) / kr) * B * H * L * d * sizeof(float);
+}
+
+bool use_fused_dq(int B, int H, int L, int d, mg_contract_t contract) {
+    return contract == MG_CONTRACT_STRICT_F32 && d <= 64 &&
+           dq_partial_bytes(B, H, L, d) <= kFusedPartialLimit;
+}
+
+// Layout: D (f32 per row) first, then the dQ partials when fused.
+size_t workspace_bytes(int B, int H, int L, int d, mg_contract_t contract) {
+    size_t n = round256((size_t)B * H * L * sizeof(float));
+    if (use_fused_dq(B, H, L, d, contract)) n += dq_partial_bytes(B, H, L, d);
+    return n;
 }
 
 }  // namespace
@@ -211,7 +230,7 @@ size_t mg_attn_bwd_workspace_bytes(int B, int H, int L, int d, int causal,
     mg_status_t st = check_shape(B, H, L, d, 1.0f, contract);
     g_detail = saved;
     if (st != MG_OK) return 0;
-    return workspace_bytes(B, H, L);
+    return workspace_bytes(B, H, L, d, contract);
 }
 
 mg_status_t mg_attn_bwd(const void *Q, const void *K, const void *V, const void *O,
@@ -220,7 +239,7 @@ mg_status_t mg_attn_bwd(const void *Q, const void *K, const void *V, const void 
                         float scale, mg_contract_t contract, void *workspace,
                         size_t ws_bytes, hipStream_t stream) {
     MG_TRY(check_shape(B, H, L, d, scale, contract));
-    const size_t need = workspace_bytes(B, H, L);
+    const size_t need = workspace_bytes(B, H, L, d, contract);
     if (workspace == nullptr || ws_bytes < need)
         return fail(MG_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed",
                     workspace ? ws_bytes : (size_t)0, need);
@@ -234,6 +253,17 @@ mg_status_t mg_attn_bwd(const void *Q, const void *K, const void *V, const void 
         const float *o = (const float *)O, *go = (const float *)dO;
         MG_TRY(run_kernel(kernel_name("attn_rowdot", contract, d), stream,
                           [&] { return mg::launch_bwd_rowdot_f32(p, o, go, Dws, stream); }));
+        if (use_fused_dq(B, H, L, d, contract)) {
+            float *dQp = (float *)((char *)workspace + round256((size_t)B * H * L * sizeof(float)));
+            MG_TRY(run_kernel(kernel_name("attn_dkdvq", contract, d), stream, [&] {
+                return mg::launch_bwd_dkdvq_f32(p, q, k, v, go, LSE, Dws, (float *)dK,
+                                                (float *)dV, dQp, stream);
+            }));
+            MG_TRY(run_kernel(kernel_name("attn_dqreduce", contract, d), stream, [&] {
+                return mg::launch_bwd_dq_reduce_f32(p, dQp, (float *)dQ, stream);
+            }));
+            return ok();
+        }
         MG_TRY(run_kernel(kernel_name("attn_dkdv", contract, d), stream, [&] {
             return mg::launch_bwd_dkdv_f32(p, q, k, v, go, LSE, Dws, (float *)dK, (float *)dV,
                                            stream);

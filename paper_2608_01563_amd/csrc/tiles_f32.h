@@ -52,3 +52,63 @@ struct F32TileStager {
 };
 
 }  // namespace mg
+
+namespace mg {
+
+// Quad staging: each thread moves a 4-row x 4-column block of an f32 tile and
+// writes it row-major R[ROWS][D+4] and/or transposed T[D][ROWS+4], both with
+// 16-byte LDS stores (the 4x4 transpose happens in registers).  Quads are
+// numbered row-group fastest, so a wave's transposed stores are contiguous.
+// The transposed copy lets a lane read four consecutive rows of one column
+// (the B-operand order of an accumulator) with a single 16-byte read.
+template <int ROWS, int D, int NTHREADS, bool ROW_MAJOR, bool TRANSPOSED>
+struct F32QuadStager {
+    static constexpr int kLdR = D + 4;
+    static constexpr int kLdT = ROWS + 4;
+    static constexpr int kGroups = ROWS / 4;
+    static constexpr int kQuads = kGroups * (D / 4);
+    static constexpr int kIters = (kQuads + NTHREADS - 1) / NTHREADS;
+    static_assert(ROWS % 4 == 0 && D % 4 == 0, "tile shape");
+
+    f32x4 buf[kIters][4];
+
+    __device__ __forceinline__ void load(const float *__restrict__ src, int row0, int L,
+                                         int tid) {
+#pragma unroll
+        for (int it = 0; it < kIters; ++it) {
+            const int q = tid + it * NTHREADS;
+            const int rg = q % kGroups;
+            const int c4 = q / kGroups;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int row = row0 + 4 * rg + k;
+                buf[it][k] = (q < kQuads && row < L)
+                    ? *reinterpret_cast<const f32x4 *>(src + (size_t)row * D + 4 * c4)
+                    : zero4();
+            }
+        }
+    }
+
+    __device__ __forceinline__ void store(float (*R)[kLdR], float (*T)[kLdT], int tid) const {
+#pragma unroll
+        for (int it = 0; it < kIters; ++it) {
+            const int q = tid + it * NTHREADS;
+            if (kQuads % NTHREADS != 0 && q >= kQuads) continue;
+            const int rg = q % kGroups;
+            const int c4 = q / kGroups;
+            if constexpr (ROW_MAJOR) {
+#pragma unroll
+                for (int k = 0; k < 4; ++k)
+                    *reinterpret_cast<f32x4 *>(&R[4 * rg + k][4 * c4]) = buf[it][k];
+            }
+            if constexpr (TRANSPOSED) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    *reinterpret_cast<f32x4 *>(&T[4 * c4 + e][4 * rg]) =
+                        f32x4{buf[it][0][e], buf[it][1][e], buf[it][2][e], buf[it][3][e]};
+            }
+        }
+    }
+};
+
+}  // namespace mg

@@ -49,8 +49,15 @@ def test_status_strings(lib):
 
 
 def test_workspace_query(lib):
-    assert mg.mg_attn_bwd_workspace_bytes(8, 8, 1024, 64, 1, 0) == 8 * 8 * 1024 * 4
-    assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 32, 0, 0) == 256
+    rows = 8 * 8 * 1024
+    # strict f32, d <= 64: D plus one dQ partial per (64-key tile, query row)
+    assert mg.mg_attn_bwd_workspace_bytes(8, 8, 1024, 64, 1, 0) == rows * 4 + 16 * rows * 64 * 4
+    # bf16, or d = 128: D only
+    assert mg.mg_attn_bwd_workspace_bytes(8, 8, 1024, 64, 1, 1) == rows * 4
+    assert mg.mg_attn_bwd_workspace_bytes(8, 8, 1024, 128, 1, 0) == rows * 4
+    # partials above 1 GiB fall back to the separate dQ kernel (D only)
+    assert mg.mg_attn_bwd_workspace_bytes(8, 8, 8192, 64, 1, 0) == 8 * 8 * 8192 * 4
+    assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 32, 0, 0) == 256 + 3 * 32 * 4
     assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 48, 0, 0) == 0     # unsupported d
     assert mg.mg_attn_bwd_workspace_bytes(0, 1, 3, 32, 0, 0) == 0     # bad size
     assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 32, 0, 7) == 0     # bad contract
