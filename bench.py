@@ -78,8 +78,10 @@ def kernel_work(name, w, pairs, rows, key_len=None):
     raise KeyError(name)
 
 
-def partial_rows(w, key_len, key_rows=64):
-    """(key tile, query row) pairs the fused dQ reduction reads."""
+def partial_rows(w, key_len):
+    """(key tile, query row) pairs the fused dQ reduction reads (key tiles of
+    128 keys when causal with >= 512 such tiles, else 64)."""
+    key_rows = 128 if (w.causal and -(-w.L // 128) * w.B * w.H >= 512) else 64
     total = 0
     kls = [w.L] * w.B if key_len is None else [int(n) for n in key_len]
     for n in kls:

@@ -88,8 +88,9 @@ mg_status_t mg_attn_fwd(const void *Q, const void *K, const void *V,
  * Bytes of device workspace that mg_attn_bwd needs for these arguments:
  * f32 D = rowsum(dO o O), one per query row, rounded up to 256 bytes, plus,
  * for strict_f32 with d <= 64 when they fit in 1 GiB, one f32 dQ partial per
- * (64-key tile, query row) (ceil(L/64) * B*H*L*d floats), which lets the
- * dK/dV kernel produce dQ without a second recompute.  Returns 0 when the
+ * (key tile, query row): ceil(L/T) * B*H*L*d floats with key tiles of
+ * T = 128 keys when causal and ceil(L/128)*B*H >= 512, else T = 64.  The partials let the dK/dV
+ * kernel produce dQ without a second recompute.  Returns 0 when the
  * arguments are invalid.
  */
 size_t mg_attn_bwd_workspace_bytes(int B, int H, int L, int d, int causal,

@@ -46,8 +46,14 @@
 #ifndef MG_DKDV_CFG
 #define MG_DKDV_CFG 4, 3, false
 #endif
+#ifndef MG_DKDVQ_CAUSAL_CFG
+#define MG_DKDVQ_CAUSAL_CFG 8, 3, false   // 128-key tiles: half the dQ partials
+#endif
 #ifndef MG_DQ_CFG
 #define MG_DQ_CFG 8, 0, false
+#endif
+#ifndef MG_FWD_STREAM
+#define MG_FWD_STREAM 64   // keys per streamed forward tile (32 or 64)
 #endif
 #ifndef MG_DKDV_NIB
 #define MG_DKDV_NIB 2   // 16-row query blocks per dK/dV step (d <= 64)
@@ -57,6 +63,7 @@ namespace mg {
 namespace {
 
 constexpr int kStream = 64;   // streamed rows per step
+constexpr int kFwdStream = MG_FWD_STREAM;
 
 template <int NW_, int OCC_, bool DB_>
 struct Cfg {
@@ -70,6 +77,7 @@ struct Cfg {
 };
 using FwdCfg = Cfg<MG_FWD_CFG>;
 using DkdvCfg = Cfg<MG_DKDV_CFG>;
+using DkdvqCausalCfg = Cfg<MG_DKDVQ_CAUSAL_CFG>;
 using DqCfg = Cfg<MG_DQ_CFG>;
 
 // ---------------------------------------------------------------- forward --
@@ -81,10 +89,12 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
                   float scale_log2, int n_qtiles, int BH) {
     constexpr int DQ = D / 4;    // contraction values per lane in one S chain
     constexpr int NC = D / 16;   // 16-column blocks of the head dimension
-    using Stager = F32TileStager<kStream, D, C::NT>;
+    constexpr int KS = kFwdStream;
+    constexpr int NJB = KS / 16; // 16-key blocks per streamed tile
+    using Stager = F32TileStager<KS, D, C::NT>;
     constexpr int LD = Stager::kLd;
-    __shared__ __attribute__((aligned(16))) float Ks[C::NBUF][kStream][LD];
-    __shared__ __attribute__((aligned(16))) float Vs[C::NBUF][kStream][LD];
+    __shared__ __attribute__((aligned(16))) float Ks[C::NBUF][KS][LD];
+    __shared__ __attribute__((aligned(16))) float Vs[C::NBUF][KS][LD];
 
     const int rank = blockIdx.x / BH;
     const int head = blockIdx.x - rank * BH;
@@ -103,7 +113,7 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
     const int klen = key_limit(key_len, b, L);
     const int kend = causal ? min(klen, q0 + C::ROWS) : klen;
-    const int ntiles = (kend + kStream - 1) / kStream;
+    const int ntiles = (kend + KS - 1) / KS;
 
     // B operand of S^T = K Q^T: lane holds Q[qi][g*DQ + s].
     float qreg[DQ];
@@ -140,34 +150,34 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
             __syncthreads();
         }
         if (kt + 1 < ntiles) {
-            kst.load(Kh, (kt + 1) * kStream, L, tid);
-            vst.load(Vh, (kt + 1) * kStream, L, tid);
+            kst.load(Kh, (kt + 1) * KS, L, tid);
+            vst.load(Vh, (kt + 1) * KS, L, tid);
         }
 
         // S^T[16jb + 4g + r][qi] = sum_k K[j][k] Q[qi][k]
-        f32x4 sacc[4];
+        f32x4 sacc[NJB];
 #pragma unroll
-        for (int jb = 0; jb < 4; ++jb) sacc[jb] = zero4();
+        for (int jb = 0; jb < NJB; ++jb) sacc[jb] = zero4();
 #pragma unroll
         for (int s4 = 0; s4 < DQ / 4; ++s4) {
-            f32x4 a[4];
+            f32x4 a[NJB];
 #pragma unroll
-            for (int jb = 0; jb < 4; ++jb)
+            for (int jb = 0; jb < NJB; ++jb)
                 a[jb] = *reinterpret_cast<const f32x4 *>(&Ks[cur][16 * jb + il][g * DQ + 4 * s4]);
 #pragma unroll
             for (int e = 0; e < 4; ++e)
 #pragma unroll
-                for (int jb = 0; jb < 4; ++jb)
+                for (int jb = 0; jb < NJB; ++jb)
                     sacc[jb] = mfma16x16x4(a[jb][e], qreg[4 * s4 + e], sacc[jb]);
         }
 
         // Element (jb, r) holds key j0 + 16jb + r, allowed iff that offset is
         // below a per-lane threshold (key length; the query row if causal).
-        const int j0 = kt * kStream + 4 * g;
+        const int j0 = kt * KS + 4 * g;
         const int thr = causal ? min(klen - j0, qi - j0 + 1) : klen - j0;
         float mx = -INFINITY;
 #pragma unroll
-        for (int jb = 0; jb < 4; ++jb)
+        for (int jb = 0; jb < NJB; ++jb)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const float t = (16 * jb + r < thr) ? sacc[jb][r] * scale_log2 : -INFINITY;
@@ -180,7 +190,7 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
         const float alpha = exp2_fast(m_run - m_use);
         float psum = 0.f;
 #pragma unroll
-        for (int jb = 0; jb < 4; ++jb)
+        for (int jb = 0; jb < NJB; ++jb)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const float p = exp2_fast(sacc[jb][r] - m_use);
@@ -194,7 +204,7 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
         // O^T[16c + 4g + r][qi] += sum_j V[j][16c + il'] P^T[j][qi]
 #pragma unroll
-        for (int jb = 0; jb < 4; ++jb)
+        for (int jb = 0; jb < NJB; ++jb)
 #pragma unroll
             for (int r = 0; r < 4; ++r)
 #pragma unroll
@@ -436,8 +446,7 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     constexpr int BR = 16 * NIB;
     constexpr int KR = C::ROWS;                 // keys per workgroup
     constexpr int NBLK = NIB * NC;              // 16x16 blocks of a dQ partial tile
-    constexpr int PER_WAVE = NBLK / C::NW;
-    static_assert(NBLK % C::NW == 0, "dQ blocks must split evenly over waves");
+    constexpr int PER_WAVE = (NBLK + C::NW - 1) / C::NW;
     using Stager = F32TileStager<BR, D, C::NT>;
     constexpr int LD = Stager::kLd;
     __shared__ __attribute__((aligned(16))) float Qs[BR][LD];
@@ -585,7 +594,10 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
         __syncthreads();
 #pragma unroll
         for (int bb = 0; bb < PER_WAVE; ++bb) {
-            const int blk = w * PER_WAVE + bb;
+            // consecutive blocks (same query rows, shared dS reads) per wave
+            // when they split evenly; otherwise strided, wave-uniform skip
+            const int blk = (NBLK % C::NW == 0) ? w * PER_WAVE + bb : w + bb * C::NW;
+            if (NBLK % C::NW != 0 && blk >= NBLK) break;
             const int ib = blk / NC;
             const int c = blk - ib * NC;
             f32x4 acc = zero4();
@@ -831,13 +843,21 @@ hipError_t launch_bwd_dkdv_f32(const AttnProblem &p, const float *Q, const float
     return hipGetLastError();
 }
 
-int fused_dq_key_rows() { return DkdvCfg::ROWS; }
+// Fused dQ: causal problems with enough work use 128-key tiles (heavy-first
+// ordering keeps the fewer workgroups balanced, and the partials halve);
+// the rest keep 64-key tiles, which measured faster there.
+bool wide_key_tiles(const AttnProblem &p) {
+    return p.causal && (long)cdiv(p.L, DkdvqCausalCfg::ROWS) * p.B * p.H >= 512;
+}
+int fused_dq_key_rows(const AttnProblem &p) {
+    return wide_key_tiles(p) ? DkdvqCausalCfg::ROWS : DkdvCfg::ROWS;
+}
 
-hipError_t launch_bwd_dkdvq_f32(const AttnProblem &p, const float *Q, const float *K,
-                                const float *V, const float *dO, const float *LSE,
-                                const float *Dws, float *dK, float *dV, float *dQp,
-                                hipStream_t s) {
-    using C = DkdvCfg;
+template <class C>
+static hipError_t launch_dkdvq(const AttnProblem &p, const float *Q, const float *K,
+                               const float *V, const float *dO, const float *LSE,
+                               const float *Dws, float *dK, float *dV, float *dQp,
+                               hipStream_t s) {
     const int BH = p.B * p.H;
     const dim3 grid(cdiv(p.L, C::ROWS) * BH), block(C::NT);
     const float sl2 = p.scale * kLog2e;
@@ -849,14 +869,23 @@ hipError_t launch_bwd_dkdvq_f32(const AttnProblem &p, const float *Q, const floa
     return hipGetLastError();
 }
 
+hipError_t launch_bwd_dkdvq_f32(const AttnProblem &p, const float *Q, const float *K,
+                                const float *V, const float *dO, const float *LSE,
+                                const float *Dws, float *dK, float *dV, float *dQp,
+                                hipStream_t s) {
+    return wide_key_tiles(p) ? launch_dkdvq<DkdvqCausalCfg>(p, Q, K, V, dO, LSE, Dws, dK, dV, dQp, s)
+                             : launch_dkdvq<DkdvCfg>(p, Q, K, V, dO, LSE, Dws, dK, dV, dQp, s);
+}
+
 hipError_t launch_bwd_dq_reduce_f32(const AttnProblem &p, const float *dQp, float *dQ,
                                     hipStream_t s) {
     const int BH = p.B * p.H;
     const size_t total = (size_t)BH * p.L * (p.d / 4);
     const dim3 grid((unsigned)((total + 255) / 256)), block(256);
+    const int kr = fused_dq_key_rows(p);
     switch (p.d) {
-    case 32: attn_dq_reduce_f32<32><<<grid, block, 0, s>>>(dQp, dQ, p.key_len, p.H, p.L, p.causal, p.scale, BH, DkdvCfg::ROWS); break;
-    case 64: attn_dq_reduce_f32<64><<<grid, block, 0, s>>>(dQp, dQ, p.key_len, p.H, p.L, p.causal, p.scale, BH, DkdvCfg::ROWS); break;
+    case 32: attn_dq_reduce_f32<32><<<grid, block, 0, s>>>(dQp, dQ, p.key_len, p.H, p.L, p.causal, p.scale, BH, kr); break;
+    case 64: attn_dq_reduce_f32<64><<<grid, block, 0, s>>>(dQp, dQ, p.key_len, p.H, p.L, p.causal, p.scale, BH, kr); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

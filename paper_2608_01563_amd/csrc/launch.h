@@ -42,8 +42,9 @@ hipError_t launch_bwd_dkdv_bf16(const AttnProblem &p, const uint16_t *Q,
 
 // Backward steps 2+3 fused (strict f32, d <= 64): dK, dV as above plus one
 // f32 dQ partial per (key tile, query row) written to dQp, laid out
-// [key tile][B*H][L][d]; then dQ = scale * sum of a row's partials.
-int fused_dq_key_rows();
+// [key tile][B*H][L][d]; then dQ = scale * sum of a row's partials.  The
+// key-tile height (64 or 128) depends on the problem.
+int fused_dq_key_rows(const AttnProblem &p);
 hipError_t launch_bwd_dkdvq_f32(const AttnProblem &p, const float *Q, const float *K,
                                 const float *V, const float *dO, const float *LSE,
                                 const float *Dws, float *dK, float *dV, float *dQp,

@@ -181,20 +181,21 @@ size_t round256(size_t n) { return (n + 255) / 256 * 256; }
 // a separate query-stationary dQ kernel recomputes what it needs.
 constexpr size_t kFusedPartialLimit = size_t(1) << 30;
 
-size_t dq_partial_bytes(int B, int H, int L, int d) {
-    const int kr = mg::fused_dq_key_rows();
+size_t dq_partial_bytes(int B, int H, int L, int d, int causal) {
+    const mg::AttnProblem p{B, H, L, d, causal ? 1 : 0, 1.0f, nullptr};
+    const int kr = mg::fused_dq_key_rows(p);
     return (size_t)((L + kr - 1) / kr) * B * H * L * d * sizeof(float);
 }
 
-bool use_fused_dq(int B, int H, int L, int d, mg_contract_t contract) {
+bool use_fused_dq(int B, int H, int L, int d, int causal, mg_contract_t contract) {
     return contract == MG_CONTRACT_STRICT_F32 && d <= 64 &&
-           dq_partial_bytes(B, H, L, d) <= kFusedPartialLimit;
+           dq_partial_bytes(B, H, L, d, causal) <= kFusedPartialLimit;
 }
 
 // Layout: D (f32 per row) first, then the dQ partials when fused.
-size_t workspace_bytes(int B, int H, int L, int d, mg_contract_t contract) {
+size_t workspace_bytes(int B, int H, int L, int d, int causal, mg_contract_t contract) {
     size_t n = round256((size_t)B * H * L * sizeof(float));
-    if (use_fused_dq(B, H, L, d, contract)) n += dq_partial_bytes(B, H, L, d);
+    if (use_fused_dq(B, H, L, d, causal, contract)) n += dq_partial_bytes(B, H, L, d, causal);
     return n;
 }
 
@@ -225,12 +226,11 @@ mg_status_t mg_attn_fwd(const void *Q, const void *K, const void *V, void *O, fl
 
 size_t mg_attn_bwd_workspace_bytes(int B, int H, int L, int d, int causal,
                                    mg_contract_t contract) {
-    (void)causal;
     std::string saved = g_detail;
     mg_status_t st = check_shape(B, H, L, d, 1.0f, contract);
     g_detail = saved;
     if (st != MG_OK) return 0;
-    return workspace_bytes(B, H, L, d, contract);
+    return workspace_bytes(B, H, L, d, causal, contract);
 }
 
 mg_status_t mg_attn_bwd(const void *Q, const void *K, const void *V, const void *O,
@@ -239,7 +239,7 @@ mg_status_t mg_attn_bwd(const void *Q, const void *K, const void *V, const void 
                         float scale, mg_contract_t contract, void *workspace,
                         size_t ws_bytes, hipStream_t stream) {
     MG_TRY(check_shape(B, H, L, d, scale, contract));
-    const size_t need = workspace_bytes(B, H, L, d, contract);
+    const size_t need = workspace_bytes(B, H, L, d, causal, contract);
     if (workspace == nullptr || ws_bytes < need)
         return fail(MG_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed",
                     workspace ? ws_bytes : (size_t)0, need);
@@ -253,7 +253,7 @@ mg_status_t mg_attn_bwd(const void *Q, const void *K, const void *V, const void 
         const float *o = (const float *)O, *go = (const float *)dO;
         MG_TRY(run_kernel(kernel_name("attn_rowdot", contract, d), stream,
                           [&] { return mg::launch_bwd_rowdot_f32(p, o, go, Dws, stream); }));
-        if (use_fused_dq(B, H, L, d, contract)) {
+        if (use_fused_dq(B, H, L, d, causal, contract)) {
             float *dQp = (float *)((char *)workspace + round256((size_t)B * H * L * sizeof(float)));
             MG_TRY(run_kernel(kernel_name("attn_dkdvq", contract, d), stream, [&] {
                 return mg::launch_bwd_dkdvq_f32(p, q, k, v, go, LSE, Dws, (float *)dK,

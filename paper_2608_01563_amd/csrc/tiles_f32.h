@@ -18,8 +18,8 @@ template <int ROWS, int D, int NTHREADS>
 struct F32TileStager {
     static constexpr int kChunksPerRow = D / 4;
     static constexpr int kChunks = ROWS * kChunksPerRow;
-    static_assert(kChunks % NTHREADS == 0, "tile must split evenly over threads");
-    static constexpr int kPerThread = kChunks / NTHREADS;
+    static constexpr int kPerThread = (kChunks + NTHREADS - 1) / NTHREADS;
+    static constexpr bool kExact = kChunks % NTHREADS == 0;   // no idle threads
     static constexpr int kLd = D + 4;
 
     f32x4 buf[kPerThread];
@@ -33,7 +33,7 @@ struct F32TileStager {
             const int r = f / kChunksPerRow;
             const int c4 = f - r * kChunksPerRow;
             const int row = row0 + r;
-            buf[u] = (row < L)
+            buf[u] = ((kExact || f < kChunks) && row < L)
                 ? *reinterpret_cast<const f32x4 *>(src + (size_t)row * D + 4 * c4)
                 : zero4();
         }
@@ -44,6 +44,7 @@ struct F32TileStager {
 #pragma unroll
         for (int u = 0; u < kPerThread; ++u) {
             const int f = tid + u * NTHREADS;
+            if (!kExact && f >= kChunks) continue;
             const int r = f / kChunksPerRow;
             const int c4 = f - r * kChunksPerRow;
             *reinterpret_cast<f32x4 *>(&dst[r][4 * c4]) = buf[u];

@@ -50,14 +50,18 @@ def test_status_strings(lib):
 
 def test_workspace_query(lib):
     rows = 8 * 8 * 1024
-    # strict f32, d <= 64: D plus one dQ partial per (64-key tile, query row)
-    assert mg.mg_attn_bwd_workspace_bytes(8, 8, 1024, 64, 1, 0) == rows * 4 + 16 * rows * 64 * 4
+    # strict f32, d <= 64: D plus one dQ partial per (key tile, query row);
+    # key tiles hold 128 keys under a causal mask with >= 512 such tiles, else 64
+    assert mg.mg_attn_bwd_workspace_bytes(8, 8, 1024, 64, 1, 0) == rows * 4 + 8 * rows * 64 * 4
+    assert mg.mg_attn_bwd_workspace_bytes(8, 8, 1024, 64, 0, 0) == rows * 4 + 16 * rows * 64 * 4
     # bf16, or d = 128: D only
     assert mg.mg_attn_bwd_workspace_bytes(8, 8, 1024, 64, 1, 1) == rows * 4
     assert mg.mg_attn_bwd_workspace_bytes(8, 8, 1024, 128, 1, 0) == rows * 4
     # partials above 1 GiB fall back to the separate dQ kernel (D only)
-    assert mg.mg_attn_bwd_workspace_bytes(8, 8, 8192, 64, 1, 0) == 8 * 8 * 8192 * 4
+    assert mg.mg_attn_bwd_workspace_bytes(8, 8, 8192, 64, 0, 0) == 8 * 8 * 8192 * 4
     assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 32, 0, 0) == 256 + 3 * 32 * 4
+    # causal but too few 128-key tiles: 64-key tiles (B4 H4 L256 -> 4 tiles)
+    assert mg.mg_attn_bwd_workspace_bytes(4, 4, 256, 64, 1, 0) == 4096 * 4 + 4 * 4096 * 64 * 4
     assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 48, 0, 0) == 0     # unsupported d
     assert mg.mg_attn_bwd_workspace_bytes(0, 1, 3, 32, 0, 0) == 0     # bad size
     assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 32, 0, 7) == 0     # bad contract

@@ -232,3 +232,17 @@ def test_padded_keys_exact_zero_bf16(gpu_lib):
     assert torch.count_nonzero(O[1]) == 0 and torch.all(torch.isinf(LSE[1]))
     for t in (dQ, dK, dV):
         assert torch.count_nonzero(t[1]) == 0
+
+
+def test_strict_separate_dq_fallback_sampled_heads(gpu_lib):
+    """Non-causal B32 H16 L1024 d64 needs 2 GiB of dQ partials, above the
+    1 GiB cap, so dQ comes from the separate query-stationary kernel."""
+    import paper_2608_01563_amd as mg
+    B, H, L, d = 32, 16, 1024, 64
+    need = mg.mg_attn_bwd_workspace_bytes(B, H, L, d, 0, "strict_f32")
+    assert need == B * H * L * 4       # D only: the fallback path
+    say("separate dQ fallback B%d H%d L%d d%d" % (B, H, L, d))
+    x = make_inputs(B, H, L, d, causal=False, seed=23, key_len_range=(1, L))
+    heads = [(0, 0), (7, 3), (19, 15), (31, 8)]
+    errs = compare(run_gpu(x), oracle_reference(x, heads=heads), "strict_f32", heads=heads)
+    assert max(errs.values()) <= TOL["strict_f32"], errs
