@@ -44,14 +44,27 @@ __device__ __forceinline__ void load_stationary(bf16x8 (&reg)[D / 32], const uin
 }
 
 // ---------------------------------------------------------------- forward --
-template <int D>
-__global__ __launch_bounds__(kThreads) void attn_fwd_bf16(
-    const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
-    const uint16_t *__restrict__ V, uint16_t *__restrict__ O, float *__restrict__ LSE,
-    const int32_t *__restrict__ key_len, int H, int L, int causal, float scale_log2,
-    int n_qtiles, int BH) {
-    constexpr int NS = D / 32;
-    constexpr int NC = D / 16;
+// 32x32x16 products: each wave owns 32 queries (lane column l%32), so every
+// 16-byte K fragment and 2x8-byte V^T fragment read from LDS feeds a
+// 32-query product (half the LDS bytes per flop of 16-query waves).  The
+// softmax keeps the VALU work per score low, because at bf16 matrix rates
+// the vector unit, not the matrix core, is the tighter resource:
+//   - the row max is taken on raw scores (POS_SCALE: scale > 0 keeps the
+//     order) and each probability is one fma + one exp2;
+//   - only tiles that straddle the causal diagonal or the key length are
+//     masked (a workgroup-uniform branch);
+//   - the output is rescaled only when some row's max moved.
+constexpr int kFwdRows = 128;   // queries per workgroup (4 waves x 32)
+
+template <int D, bool POS_SCALE>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
+void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
+                   const uint16_t *__restrict__ V, uint16_t *__restrict__ O,
+                   float *__restrict__ LSE, const int32_t *__restrict__ key_len, int H, int L,
+                   int causal, float scale_log2, int n_qtiles, int BH) {
+    constexpr int NS = D / 16;    // 16-deep contraction steps over d
+    constexpr int NCB = D / 32;   // 32-column blocks of d
+    constexpr int NKB = kStream / 32;
     using KSt = Bf16TileStager<kStream, D, kThreads, true, false>;
     using VSt = Bf16TileStager<kStream, D, kThreads, false, true>;
     __shared__ __attribute__((aligned(16))) uint16_t Kr[kStream][KSt::kLdR];
@@ -65,22 +78,27 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int il = lane & 15;
-    const int g = lane >> 4;
-    const int q0 = qt * kStatRows;
-    const int qi = q0 + 16 * (tid >> 6) + il;
+    const int c = lane & 31;
+    const int h = lane >> 5;
+    const int q0 = qt * kFwdRows;
+    const int qi = q0 + 32 * (tid >> 6) + c;
 
     const int klen = key_limit(key_len, b, L);
-    const int kend = causal ? min(klen, q0 + kStatRows) : klen;
+    const int kend = causal ? min(klen, q0 + kFwdRows) : klen;
     const int ntiles = (kend + kStream - 1) / kStream;
 
+    // B operand of S^T = K Q^T: lane holds Q[qi][16s + 8h + e].
     bf16x8 qreg[NS];
-    load_stationary<D>(qreg, Q + hoff, qi, L, g);
-
-    float m_run = -INFINITY, l_run = 0.f;
-    f32x4 oacc[NC];   // O^T[16c + 4g + r][qi]
 #pragma unroll
-    for (int c = 0; c < NC; ++c) oacc[c] = zero4();
+    for (int s = 0; s < NS; ++s)
+        qreg[s] = (qi < L) ? load_bf16x8(Q + hoff + (size_t)qi * D + 16 * s + 8 * h)
+                           : __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+
+    // Running max in raw-score units when POS_SCALE, else in base-2 units.
+    float m_run = -INFINITY, l_run = 0.f;
+    f32x16 oacc[NCB];   // O^T[32cb + 8a + 4h + r][qi] in register 4a + r
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) oacc[cb] = zero16();
 
     KSt kst;
     VSt vst;
@@ -98,67 +116,93 @@ __global__ __launch_bounds__(kThreads) void attn_fwd_bf16(
             vst.load(V + hoff, (kt + 1) * kStream, L, tid);
         }
 
-        f32x4 sacc[kBlk];
+        // S^T[32kb + 8a + 4h + r][qi] in sacc[kb] register 4a + r
+        f32x16 sacc[NKB];
 #pragma unroll
-        for (int jb = 0; jb < kBlk; ++jb) sacc[jb] = zero4();
+        for (int kb = 0; kb < NKB; ++kb) {
+            sacc[kb] = zero16();
 #pragma unroll
-        for (int s = 0; s < NS; ++s)
+            for (int s = 0; s < NS; ++s)
+                sacc[kb] = mfma32x32x16bf16(load_bf16x8(&Kr[32 * kb + c][16 * s + 8 * h]),
+                                            qreg[s], sacc[kb]);
+        }
+        if (!POS_SCALE) {
 #pragma unroll
-            for (int jb = 0; jb < kBlk; ++jb)
-                sacc[jb] = mfma16x16x32bf16(load_bf16x8(&Kr[16 * jb + il][32 * s + 8 * g]),
-                                            qreg[s], sacc[jb]);
+            for (int kb = 0; kb < NKB; ++kb) sacc[kb] *= scale_log2;
+        }
 
-        const int j0 = kt * kStream + 4 * g;
+        // Masking only where the tile crosses the diagonal or the key length.
+        const bool full = (kt + 1) * kStream <= klen &&
+                          (!causal || (kt + 1) * kStream - 1 <= q0);
+        if (!full) {
+            const int j0 = kt * kStream + 4 * h;
+            const int thr = causal ? min(klen - j0, qi - j0 + 1) : klen - j0;
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    if (32 * kb + 8 * (v >> 2) + (v & 3) >= thr) sacc[kb][v] = -INFINITY;
+        }
         float mx = -INFINITY;
 #pragma unroll
-        for (int jb = 0; jb < kBlk; ++jb)
+        for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int j = j0 + 16 * jb + r;
-                const bool ok = (j < klen) && (!causal || j <= qi);
-                const float t = ok ? sacc[jb][r] * scale_log2 : -INFINITY;
-                sacc[jb][r] = t;
-                mx = fmaxf(mx, t);
-            }
-        mx = max_over_groups(mx);
+            for (int v = 0; v < 16; v += 2) mx = fmaxf(mx, fmaxf(sacc[kb][v], sacc[kb][v + 1]));
+        mx = fmaxf(mx, xor_lanes(mx, 32));
         const float m_new = fmaxf(m_run, mx);
-        const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-        const float alpha = exp2_fast(m_run - m_use);
+        // exponent offset in base-2 units; a row with nothing allowed yet
+        // keeps all-zero probabilities
+        const float m2 = (m_new == -INFINITY) ? 0.f : (POS_SCALE ? m_new * scale_log2 : m_new);
+        if (__any(m_new != m_run)) {
+            const float m2_old = POS_SCALE ? m_run * scale_log2 : m_run;
+            const float alpha = exp2_fast(m2_old - m2);
+            l_run *= alpha;
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) oacc[cb] *= alpha;
+        }
+        m_run = m_new;
         float psum = 0.f;
 #pragma unroll
-        for (int jb = 0; jb < kBlk; ++jb)
+        for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float p = exp2_fast(sacc[jb][r] - m_use);
-                sacc[jb][r] = p;
+            for (int v = 0; v < 16; ++v) {
+                const float p = POS_SCALE ? exp2_fast(fmaf(sacc[kb][v], scale_log2, -m2))
+                                          : exp2_fast(sacc[kb][v] - m2);
+                sacc[kb][v] = p;
                 psum += p;
             }
-        l_run = l_run * alpha + psum;
-        m_run = m_new;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) oacc[c] *= alpha;
+        l_run += psum;
 
-        // O^T[16c + 4g + r][qi] += sum_j V^T[16c + il'][j] P^T[j][qi]
+        // O^T[32cb + .][qi] += sum_j V^T[32cb + c'][j] P^T[j][qi], 16 keys per step
 #pragma unroll
-        for (int t = 0; t < kBlk / 2; ++t) {
-            const bf16x8 pb = pack_bf16(sacc[2 * t], sacc[2 * t + 1]);
+        for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-            for (int c = 0; c < NC; ++c)
-                oacc[c] = mfma16x16x32bf16(
-                    load_bf16x4x2(&Vt[16 * c + il][32 * t + 4 * g],
-                                  &Vt[16 * c + il][32 * t + 16 + 4 * g]),
-                    pb, oacc[c]);
-        }
+            for (int t = 0; t < 2; ++t) {
+                const bf16x8 pb = pack_bf16_half(sacc[kb], t);
+                const int col = 32 * kb + 16 * t + 4 * h;
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb)
+                    oacc[cb] = mfma32x32x16bf16(
+                        load_bf16x4x2(&Vt[32 * cb + c][col], &Vt[32 * cb + c][col + 8]), pb,
+                        oacc[cb]);
+            }
     }
 
-    const float l = sum_over_groups(l_run);
+    const float l = l_run + xor_lanes(l_run, 32);
     if (qi < L) {
         const float inv = (l > 0.f) ? 1.f / l : 0.f;
         uint16_t *orow = O + hoff + (size_t)qi * D;
 #pragma unroll
-        for (int c = 0; c < NC; ++c) store_bf16x4(orow + 16 * c + 4 * g, oacc[c] * inv);
-        if (g == 0)
-            LSE[(size_t)head * L + qi] = (l > 0.f) ? (m_run + log2f(l)) * kLn2 : -INFINITY;
+        for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+            for (int a = 0; a < 4; ++a)
+                store_bf16x4(orow + 32 * cb + 8 * a + 4 * h,
+                             f32x4{oacc[cb][4 * a], oacc[cb][4 * a + 1], oacc[cb][4 * a + 2],
+                                   oacc[cb][4 * a + 3]} * inv);
+        if (h == 0) {
+            const float m2 = POS_SCALE ? m_run * scale_log2 : m_run;
+            LSE[(size_t)head * L + qi] = (l > 0.f) ? (m2 + log2f(l)) * kLn2 : -INFINITY;
+        }
     }
 }
 
@@ -429,15 +473,22 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 hipError_t launch_fwd_bf16(const AttnProblem &p, const uint16_t *Q, const uint16_t *K,
                            const uint16_t *V, uint16_t *O, float *LSE, hipStream_t s) {
     const int BH = p.B * p.H;
-    const int nqt = cdiv(p.L, kStatRows);
+    const int nqt = cdiv(p.L, kFwdRows);
     const dim3 grid(nqt * BH), block(kThreads);
     const float sl2 = p.scale * kLog2e;
+#define MG_FWD_BF16(DD)                                                                     \
+    (p.scale > 0.f                                                                         \
+         ? (attn_fwd_bf16<DD, true><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H,  \
+                                                          p.L, p.causal, sl2, nqt, BH), 0) \
+         : (attn_fwd_bf16<DD, false><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, \
+                                                           p.L, p.causal, sl2, nqt, BH), 0))
     switch (p.d) {
-    case 32: attn_fwd_bf16<32><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.L, p.causal, sl2, nqt, BH); break;
-    case 64: attn_fwd_bf16<64><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.L, p.causal, sl2, nqt, BH); break;
-    case 128: attn_fwd_bf16<128><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.L, p.causal, sl2, nqt, BH); break;
+    case 32: MG_FWD_BF16(32); break;
+    case 64: MG_FWD_BF16(64); break;
+    case 128: MG_FWD_BF16(128); break;
     default: return hipErrorInvalidValue;
     }
+#undef MG_FWD_BF16
     return hipGetLastError();
 }
 

@@ -7,9 +7,12 @@
 // rows read it transposed (two runs of 4 consecutive rows = two 8-byte LDS
 // reads).  Both layouts are written from one pass over global memory.
 //
-// Work unit: a quad = 4 consecutive rows x one 8-column chunk.  Quads are
-// numbered row-group fastest, so the transposed 8-byte writes of a wave fall
-// on consecutive LDS words.  Rows at or beyond L are zero-filled.
+// Work unit: a quad = 4 consecutive rows x one 8-column chunk.  When a
+// transposed copy is written, quads are numbered row-group fastest so the
+// transposed 8-byte writes of a wave fall on consecutive LDS words; a
+// row-major-only tile numbers them chunk fastest, so global reads and LDS
+// writes of a wave are contiguous along each row.  Rows at or beyond L are
+// zero-filled.
 //
 //   row-major  R[ROWS][D + 8]   (row stride 16-byte aligned; D+8 u16 words
 //                                is 4 words past a multiple of 64 banks)
@@ -37,8 +40,8 @@ struct Bf16TileStager {
 #pragma unroll
         for (int it = 0; it < kIters; ++it) {
             const int q = tid + it * NTHREADS;
-            const int rg = q % kGroups;
-            const int c8 = q / kGroups;
+            const int rg = TRANSPOSED ? q % kGroups : q / kChunks;
+            const int c8 = TRANSPOSED ? q / kGroups : q % kChunks;
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const int row = row0 + 4 * rg + k;
@@ -55,8 +58,8 @@ struct Bf16TileStager {
         for (int it = 0; it < kIters; ++it) {
             const int q = tid + it * NTHREADS;
             if (q >= kQuads) continue;
-            const int rg = q % kGroups;
-            const int c8 = q / kGroups;
+            const int rg = TRANSPOSED ? q % kGroups : q / kChunks;
+            const int c8 = TRANSPOSED ? q / kGroups : q % kChunks;
             if constexpr (ROW_MAJOR) {
 #pragma unroll
                 for (int k = 0; k < 4; ++k)
@@ -105,6 +108,15 @@ __device__ __forceinline__ bf16x8 pack_bf16(f32x4 a, f32x4 b) {
         v[r] = (__bf16)a[r];
         v[4 + r] = (__bf16)b[r];
     }
+    return v;
+}
+
+// Accumulator registers [8t, 8t+8) of a 32x32 block, rounded to bf16 (nearest
+// even), as the B operand of a 32x32x16 product contracting over its rows.
+__device__ __forceinline__ bf16x8 pack_bf16_half(const f32x16 &a, int t) {
+    bf16x8 v;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = (__bf16)a[8 * t + e];
     return v;
 }
 
