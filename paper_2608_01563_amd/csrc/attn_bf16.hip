@@ -3,19 +3,19 @@
 //
 // Same three-kernel structure as the strict-f32 path (tiled forward, fused
 // dK+dV with the key tile stationary, separate dQ; the paper's attention
-// archetype, Sec. 3.3 and Sec. 8), on v_mfma_f32_16x16x32_bf16.  The
-// reduced-input contract of Sec. 4.2 rounds matrix inputs locally and
-// accumulates in f32; here Q, K, V, O, dO and the gradients are stored bf16,
-// and the softmax probabilities P and dS are rounded to bf16 (nearest even)
-// only as inputs of the second product of each pass.  Softmax statistics,
-// LSE and D stay f32.
+// archetype, Sec. 3.3 and Sec. 8).  The reduced-input contract of Sec. 4.2
+// rounds matrix inputs locally and accumulates in f32; here Q, K, V, O, dO
+// and the gradients are stored bf16, and the softmax probabilities P and dS
+// are rounded to bf16 (nearest even) only as inputs of the second product of
+// each pass.  Softmax statistics, LSE and D stay f32.
 //
-// Contraction order inside one 16x16x32 product: for products over the head
-// dimension a lane holds d = 32s + 8g + e (e = 0..7, g = lane/16), one
-// 16-byte load; for products over streamed rows it holds row
-// 32t + 16*(e/4) + 4g + e%4, which is exactly the pair of 16x16 accumulator
-// blocks (2t, 2t+1) a lane already owns, so P and dS become the B operand
-// without leaving registers, and the LDS operand is read transposed.
+// Contraction order: for products over the head dimension a lane holds 8
+// consecutive d values (one 16-byte LDS read); for products over streamed
+// rows it holds the rows of the accumulator registers it already owns, so
+// P and dS become the B operand without leaving registers, and the LDS
+// operand (a column of the row-major tile) comes from transpose reads.
+//   16x16x32 (dK/dV): rows 32t + 16*(e/4) + 4g + e%4, g = lane/16
+//   32x32x16 (forward, dQ): rows 16t + 8*(e/4) + 4h + e%4, h = lane/32
 #include "device_common.h"
 #include "launch.h"
 #include "tiles_bf16.h"
@@ -65,10 +65,10 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
     constexpr int NS = D / 16;    // 16-deep contraction steps over d
     constexpr int NCB = D / 32;   // 32-column blocks of d
     constexpr int NKB = kStream / 32;
-    using KSt = Bf16TileStager<kStream, D, kThreads, true, false>;
-    using VSt = Bf16TileStager<kStream, D, kThreads, false, true>;
-    __shared__ __attribute__((aligned(16))) uint16_t Kr[kStream][KSt::kLdR];
-    __shared__ __attribute__((aligned(16))) uint16_t Vt[D][VSt::kLdT];
+    using St = Bf16TileStager<kStream, D, kThreads>;
+    constexpr int LD = St::kLd;
+    __shared__ __attribute__((aligned(16))) uint16_t Kr[kStream][LD];
+    __shared__ __attribute__((aligned(16))) uint16_t Vr[kStream][LD];
 
     const int rank = blockIdx.x / BH;
     const int head = blockIdx.x - rank * BH;
@@ -80,6 +80,7 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
     const int lane = tid & 63;
     const int c = lane & 31;
     const int h = lane >> 5;
+    const int jr = (lane & 15) >> 2, jc = 4 * (lane & 3);   // transpose-read block offsets
     const int q0 = qt * kFwdRows;
     const int qi = q0 + 32 * (tid >> 6) + c;
 
@@ -100,16 +101,15 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) oacc[cb] = zero16();
 
-    KSt kst;
-    VSt vst;
+    St kst, vst;
     if (ntiles > 0) {
         kst.load(K + hoff, 0, L, tid);
         vst.load(V + hoff, 0, L, tid);
     }
     for (int kt = 0; kt < ntiles; ++kt) {
         __syncthreads();
-        kst.store(Kr, nullptr, tid);
-        vst.store(nullptr, Vt, tid);
+        kst.store(Kr, tid);
+        vst.store(Vr, tid);
         __syncthreads();
         if (kt + 1 < ntiles) {
             kst.load(K + hoff, (kt + 1) * kStream, L, tid);
@@ -179,11 +179,11 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
                 const bf16x8 pb = pack_bf16_half(sacc[kb], t);
-                const int col = 32 * kb + 16 * t + 4 * h;
+                const int r0 = 32 * kb + 16 * t + 4 * h;
 #pragma unroll
                 for (int cb = 0; cb < NCB; ++cb)
                     oacc[cb] = mfma32x32x16bf16(
-                        load_bf16x4x2(&Vt[32 * cb + c][col], &Vt[32 * cb + c][col + 8]), pb,
+                        load_tr_pair<LD>(Vr, r0, r0 + 8, 32 * cb + 16 * (c >> 4), jr, jc), pb,
                         oacc[cb]);
             }
     }
@@ -230,20 +230,24 @@ __global__ __launch_bounds__(256) void attn_rowdot_bf16(const uint16_t *__restri
 }
 
 // ------------------------------------------------------- backward: dK, dV
+// Key tile of 64 keys stationary (16 per wave, one per lane column) on
+// 16x16x32 products; query tiles of 64 rows stream through LDS row-major.
+// Masks as in the strict-f32 kernel: a causal threshold per lane, padded
+// keys overwritten with zeros at the end, rows past L inert.
 template <int D>
-__global__ __launch_bounds__(kThreads) void attn_dkdv_bf16(
-    const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
-    const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
-    const float *__restrict__ LSE, const float *__restrict__ Dws, uint16_t *__restrict__ dK,
-    uint16_t *__restrict__ dV, const int32_t *__restrict__ key_len, int H, int L, int causal,
-    float scale, float scale_log2, int BH) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
+void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
+                    const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
+                    const float *__restrict__ LSE, const float *__restrict__ Dws,
+                    uint16_t *__restrict__ dK, uint16_t *__restrict__ dV,
+                    const int32_t *__restrict__ key_len, int H, int L, int causal, float scale,
+                    float scale_log2, int BH) {
     constexpr int NS = D / 32;
     constexpr int NC = D / 16;
-    using St = Bf16TileStager<kStream, D, kThreads, true, true>;
-    __shared__ __attribute__((aligned(16))) uint16_t Qr[kStream][St::kLdR];
-    __shared__ __attribute__((aligned(16))) uint16_t Qt[D][St::kLdT];
-    __shared__ __attribute__((aligned(16))) uint16_t Or[kStream][St::kLdR];
-    __shared__ __attribute__((aligned(16))) uint16_t Ot[D][St::kLdT];
+    using St = Bf16TileStager<kStream, D, kThreads>;
+    constexpr int LD = St::kLd;
+    __shared__ __attribute__((aligned(16))) uint16_t Qr[kStream][LD];
+    __shared__ __attribute__((aligned(16))) uint16_t Or[kStream][LD];
     __shared__ __attribute__((aligned(16))) float lse2s[kStream];
     __shared__ __attribute__((aligned(16))) float Ds[kStream];
 
@@ -257,6 +261,7 @@ __global__ __launch_bounds__(kThreads) void attn_dkdv_bf16(
     const int lane = tid & 63;
     const int il = lane & 15;
     const int g = lane >> 4;
+    const int jr = il >> 2, jc = 4 * (il & 3);   // transpose-read block offsets
     const int k0 = kt * kStatRows;
     const int kj = k0 + 16 * (tid >> 6) + il;
 
@@ -291,8 +296,8 @@ __global__ __launch_bounds__(kThreads) void attn_dkdv_bf16(
 
     for (int qt = qstart; qt < qstop; ++qt) {
         __syncthreads();
-        qst.store(Qr, Qt, tid);
-        ost.store(Or, Ot, tid);
+        qst.store(Qr, tid);
+        ost.store(Or, tid);
         if (tid < kStream) {
             lse2s[tid] = lse_pre;
             Ds[tid] = d_pre;
@@ -317,64 +322,68 @@ __global__ __launch_bounds__(kThreads) void attn_dkdv_bf16(
             }
 
         const int ibase = qt * kStream + 4 * g;
+        const int thr = causal ? kj - ibase : -(1 << 30);
 #pragma unroll
         for (int ib = 0; ib < kBlk; ++ib) {
             const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lse2s[16 * ib + 4 * g]);
             const f32x4 dd = *reinterpret_cast<const f32x4 *>(&Ds[16 * ib + 4 * g]);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
-                const int i = ibase + 16 * ib + r;
-                const bool ok = (i < L) && (kj < klen) && (!causal || kj <= i);
-                const float p = ok ? exp2_fast(sacc[ib][r] * scale_log2 - l2[r]) : 0.f;
+                float p = exp2_fast(fmaf(sacc[ib][r], scale_log2, -l2[r]));
+                p = (16 * ib + r >= thr) ? p : 0.f;
                 sacc[ib][r] = p;
                 pacc[ib][r] = p * (pacc[ib][r] - dd[r]);
             }
         }
 
+        // dV^T[16c + .][kj] += dO^T[16c + il'][i] P[i][kj]; dK^T likewise with Q, dS
 #pragma unroll
         for (int t = 0; t < kBlk / 2; ++t) {
             const bf16x8 pb = pack_bf16(sacc[2 * t], sacc[2 * t + 1]);
             const bf16x8 sb = pack_bf16(pacc[2 * t], pacc[2 * t + 1]);
+            const int r0 = 32 * t + 4 * g;
 #pragma unroll
             for (int c = 0; c < NC; ++c) {
-                dvacc[c] = mfma16x16x32bf16(
-                    load_bf16x4x2(&Ot[16 * c + il][32 * t + 4 * g],
-                                  &Ot[16 * c + il][32 * t + 16 + 4 * g]),
-                    pb, dvacc[c]);
-                dkacc[c] = mfma16x16x32bf16(
-                    load_bf16x4x2(&Qt[16 * c + il][32 * t + 4 * g],
-                                  &Qt[16 * c + il][32 * t + 16 + 4 * g]),
-                    sb, dkacc[c]);
+                dvacc[c] = mfma16x16x32bf16(load_tr_pair<LD>(Or, r0, r0 + 16, 16 * c, jr, jc),
+                                            pb, dvacc[c]);
+                dkacc[c] = mfma16x16x32bf16(load_tr_pair<LD>(Qr, r0, r0 + 16, 16 * c, jr, jc),
+                                            sb, dkacc[c]);
             }
         }
     }
 
     if (kj < L) {
+        const bool keep = kj < klen;   // padded keys get exact zeros
         uint16_t *dkrow = dK + hoff + (size_t)kj * D;
         uint16_t *dvrow = dV + hoff + (size_t)kj * D;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
-            store_bf16x4(dkrow + 16 * c + 4 * g, dkacc[c] * scale);
-            store_bf16x4(dvrow + 16 * c + 4 * g, dvacc[c]);
+            store_bf16x4(dkrow + 16 * c + 4 * g, keep ? dkacc[c] * scale : zero4());
+            store_bf16x4(dvrow + 16 * c + 4 * g, keep ? dvacc[c] : zero4());
         }
     }
 }
 
 // ------------------------------------------------------------ backward: dQ
-template <int D>
-__global__ __launch_bounds__(kThreads) void attn_dq_bf16(
-    const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
-    const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
-    const float *__restrict__ LSE, const float *__restrict__ Dws, uint16_t *__restrict__ dQ,
-    const int32_t *__restrict__ key_len, int H, int L, int causal, float scale,
-    float scale_log2, int n_qtiles, int BH) {
-    constexpr int NS = D / 32;
-    constexpr int NC = D / 16;
-    using KSt = Bf16TileStager<kStream, D, kThreads, true, true>;
-    using VSt = Bf16TileStager<kStream, D, kThreads, true, false>;
-    __shared__ __attribute__((aligned(16))) uint16_t Kr[kStream][KSt::kLdR];
-    __shared__ __attribute__((aligned(16))) uint16_t Kt[D][KSt::kLdT];
-    __shared__ __attribute__((aligned(16))) uint16_t Vr[kStream][VSt::kLdR];
+// Query-stationary, 32 queries per wave on 32x32x16 products (as the forward):
+// S^T = K Q^T and dP^T = V dO^T from row-major K and V tiles, then
+// dQ^T += K^T dS^T with dS^T straight from registers and K^T from transpose
+// reads of the row-major K tile.  KS keys per streamed tile (32 for d = 128,
+// which keeps the kernel within 256 registers).
+template <int D, int KS>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
+void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
+                  const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
+                  const float *__restrict__ LSE, const float *__restrict__ Dws,
+                  uint16_t *__restrict__ dQ, const int32_t *__restrict__ key_len, int H, int L,
+                  int causal, float scale, float scale_log2, int n_qtiles, int BH) {
+    constexpr int NS = D / 16;
+    constexpr int NCB = D / 32;
+    constexpr int NKB = KS / 32;
+    using St = Bf16TileStager<KS, D, kThreads>;
+    constexpr int LD = St::kLd;
+    __shared__ __attribute__((aligned(16))) uint16_t Kr[KS][LD];
+    __shared__ __attribute__((aligned(16))) uint16_t Vr[KS][LD];
 
     const int rank = blockIdx.x / BH;
     const int head = blockIdx.x - rank * BH;
@@ -384,84 +393,89 @@ __global__ __launch_bounds__(kThreads) void attn_dq_bf16(
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int il = lane & 15;
-    const int g = lane >> 4;
-    const int q0 = qt * kStatRows;
-    const int qi = q0 + 16 * (tid >> 6) + il;
+    const int c = lane & 31;
+    const int h = lane >> 5;
+    const int jr = (lane & 15) >> 2, jc = 4 * (lane & 3);
+    const int q0 = qt * kFwdRows;
+    const int qi = q0 + 32 * (tid >> 6) + c;
 
     const int klen = key_limit(key_len, b, L);
-    const int kend = causal ? min(klen, q0 + kStatRows) : klen;
-    const int ntiles = (kend + kStream - 1) / kStream;
+    const int kend = causal ? min(klen, q0 + kFwdRows) : klen;
+    const int ntiles = (kend + KS - 1) / KS;
 
     bf16x8 qreg[NS], oreg[NS];
-    load_stationary<D>(qreg, Q + hoff, qi, L, g);
-    load_stationary<D>(oreg, dO + hoff, qi, L, g);
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        const size_t off = hoff + (size_t)qi * D + 16 * s + 8 * h;
+        qreg[s] = (qi < L) ? load_bf16x8(Q + off) : __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+        oreg[s] = (qi < L) ? load_bf16x8(dO + off) : __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    }
+    // Rows past L: Q = dO = 0 and LSE = D = 0, so their dS is exactly 0.
     const float lse2 = (qi < L) ? LSE[(size_t)head * L + qi] * kLog2e : 0.f;
     const float Di = (qi < L) ? Dws[(size_t)head * L + qi] : 0.f;
 
-    f32x4 dqacc[NC];   // dQ^T[16c + 4g + r][qi]
+    f32x16 dqacc[NCB];   // dQ^T[32cb + 8a + 4h + r][qi]
 #pragma unroll
-    for (int c = 0; c < NC; ++c) dqacc[c] = zero4();
+    for (int cb = 0; cb < NCB; ++cb) dqacc[cb] = zero16();
 
-    KSt kst;
-    VSt vst;
+    St kst, vst;
     if (ntiles > 0) {
         kst.load(K + hoff, 0, L, tid);
         vst.load(V + hoff, 0, L, tid);
     }
     for (int kt = 0; kt < ntiles; ++kt) {
         __syncthreads();
-        kst.store(Kr, Kt, tid);
-        vst.store(Vr, nullptr, tid);
+        kst.store(Kr, tid);
+        vst.store(Vr, tid);
         __syncthreads();
         if (kt + 1 < ntiles) {
-            kst.load(K + hoff, (kt + 1) * kStream, L, tid);
-            vst.load(V + hoff, (kt + 1) * kStream, L, tid);
+            kst.load(K + hoff, (kt + 1) * KS, L, tid);
+            vst.load(V + hoff, (kt + 1) * KS, L, tid);
         }
+        const bool full = (kt + 1) * KS <= klen &&
+                          (!causal || (kt + 1) * KS - 1 <= q0);
+        const int j0 = kt * KS + 4 * h;
+        const int thr = causal ? min(klen - j0, qi - j0 + 1) : klen - j0;
 
-        f32x4 sacc[kBlk], pacc[kBlk];
 #pragma unroll
-        for (int jb = 0; jb < kBlk; ++jb) {
-            sacc[jb] = zero4();
-            pacc[jb] = zero4();
-        }
+        for (int kb = 0; kb < NKB; ++kb) {
+            f32x16 sacc = zero16(), pacc = zero16();
 #pragma unroll
-        for (int s = 0; s < NS; ++s)
-#pragma unroll
-            for (int jb = 0; jb < kBlk; ++jb) {
-                sacc[jb] = mfma16x16x32bf16(load_bf16x8(&Kr[16 * jb + il][32 * s + 8 * g]),
-                                            qreg[s], sacc[jb]);
-                pacc[jb] = mfma16x16x32bf16(load_bf16x8(&Vr[16 * jb + il][32 * s + 8 * g]),
-                                            oreg[s], pacc[jb]);
+            for (int s = 0; s < NS; ++s) {
+                sacc = mfma32x32x16bf16(load_bf16x8(&Kr[32 * kb + c][16 * s + 8 * h]), qreg[s],
+                                        sacc);
+                pacc = mfma32x32x16bf16(load_bf16x8(&Vr[32 * kb + c][16 * s + 8 * h]), oreg[s],
+                                        pacc);
             }
-
-        const int j0 = kt * kStream + 4 * g;
+            // dS^T = P^T (dP^T - D), P^T = exp2(S^T * scale*log2e - LSE*log2e)
 #pragma unroll
-        for (int jb = 0; jb < kBlk; ++jb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int j = j0 + 16 * jb + r;
-                const bool ok = (qi < L) && (j < klen) && (!causal || j <= qi);
-                const float p = ok ? exp2_fast(sacc[jb][r] * scale_log2 - lse2) : 0.f;
-                pacc[jb][r] = p * (pacc[jb][r] - Di);
+            for (int v = 0; v < 16; ++v) {
+                float p = exp2_fast(fmaf(sacc[v], scale_log2, -lse2));
+                if (!full && 32 * kb + 8 * (v >> 2) + (v & 3) >= thr) p = 0.f;
+                pacc[v] = p * (pacc[v] - Di);
             }
-
 #pragma unroll
-        for (int t = 0; t < kBlk / 2; ++t) {
-            const bf16x8 sb = pack_bf16(pacc[2 * t], pacc[2 * t + 1]);
+            for (int t = 0; t < 2; ++t) {
+                const bf16x8 sb = pack_bf16_half(pacc, t);
+                const int r0 = 32 * kb + 16 * t + 4 * h;
 #pragma unroll
-            for (int c = 0; c < NC; ++c)
-                dqacc[c] = mfma16x16x32bf16(
-                    load_bf16x4x2(&Kt[16 * c + il][32 * t + 4 * g],
-                                  &Kt[16 * c + il][32 * t + 16 + 4 * g]),
-                    sb, dqacc[c]);
+                for (int cb = 0; cb < NCB; ++cb)
+                    dqacc[cb] = mfma32x32x16bf16(
+                        load_tr_pair<LD>(Kr, r0, r0 + 8, 32 * cb + 16 * (c >> 4), jr, jc), sb,
+                        dqacc[cb]);
+            }
         }
     }
 
     if (qi < L) {
         uint16_t *dqrow = dQ + hoff + (size_t)qi * D;
 #pragma unroll
-        for (int c = 0; c < NC; ++c) store_bf16x4(dqrow + 16 * c + 4 * g, dqacc[c] * scale);
+        for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+            for (int a = 0; a < 4; ++a)
+                store_bf16x4(dqrow + 32 * cb + 8 * a + 4 * h,
+                             f32x4{dqacc[cb][4 * a], dqacc[cb][4 * a + 1], dqacc[cb][4 * a + 2],
+                                   dqacc[cb][4 * a + 3]} * scale);
     }
 }
 
@@ -524,13 +538,13 @@ hipError_t launch_bwd_dq_bf16(const AttnProblem &p, const uint16_t *Q, const uin
                               const uint16_t *V, const uint16_t *dO, const float *LSE,
                               const float *Dws, uint16_t *dQ, hipStream_t s) {
     const int BH = p.B * p.H;
-    const int nqt = cdiv(p.L, kStatRows);
+    const int nqt = cdiv(p.L, kFwdRows);
     const dim3 grid(nqt * BH), block(kThreads);
     const float sl2 = p.scale * kLog2e;
     switch (p.d) {
-    case 32: attn_dq_bf16<32><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
-    case 64: attn_dq_bf16<64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
-    case 128: attn_dq_bf16<128><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
+    case 32: attn_dq_bf16<32, 64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
+    case 64: attn_dq_bf16<64, 64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
+    case 128: attn_dq_bf16<128, 32><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -1,32 +1,34 @@
-// tiles_bf16.h -- cooperative global->LDS staging of bf16 row tiles, in
-// row-major and/or transposed layout.
+// tiles_bf16.h -- cooperative global->LDS staging of bf16 row tiles and the
+// LDS reads that feed bf16 MFMA operands.
 //
-// bf16 MFMA (16x16x32) takes 8 contraction values per lane.  Products that
-// contract over the head dimension read a tile row-major (8 consecutive d
-// values = one 16-byte LDS read); products that contract over the streamed
-// rows read it transposed (two runs of 4 consecutive rows = two 8-byte LDS
-// reads).  Both layouts are written from one pass over global memory.
+// A streamed tile is stored row-major only.  Products that contract over the
+// head dimension read 8 consecutive d values of a row (one 16-byte read);
+// products that contract over the streamed rows read 4 consecutive rows of
+// one column with gfx950's 16-bit transpose read (ds_read_b64_tr_b16): in
+// each 16-lane group, lane i receives element i%4 of the 8-byte chunks that
+// lanes i/4, i/4+4, i/4+8 and i/4+12 address, so when lane j addresses row
+// j/4, columns 4*(j%4)..+3 of a 4 x 16 block, lane i gets rows 0..3 of
+// column i.  No transposed copy of any tile is needed.
 //
-// Work unit: a quad = 4 consecutive rows x one 8-column chunk.  When a
-// transposed copy is written, quads are numbered row-group fastest so the
-// transposed 8-byte writes of a wave fall on consecutive LDS words; a
-// row-major-only tile numbers them chunk fastest, so global reads and LDS
-// writes of a wave are contiguous along each row.  Rows at or beyond L are
-// zero-filled.
-//
-//   row-major  R[ROWS][D + 8]   (row stride 16-byte aligned; D+8 u16 words
-//                                is 4 words past a multiple of 64 banks)
-//   transposed T[D][ROWS + 4]   (row stride 8-byte aligned)
+// Row stride (u16): the smallest padding for which both the 16-row 16-byte
+// reads and the 4-row transpose reads of a 16-lane group hit 16 distinct
+// 4-bank groups: d=32 -> 56, d=64 -> 72, d=128 -> 152.  Quads (4 rows x 8
+// columns) are numbered chunk-first so global reads and LDS writes of a wave
+// are contiguous along each row.  Rows at or beyond L are zero-filled.
 #pragma once
 
 #include "device_common.h"
 
 namespace mg {
 
-template <int ROWS, int D, int NTHREADS, bool ROW_MAJOR, bool TRANSPOSED>
+template <int D> struct Bf16Ld;
+template <> struct Bf16Ld<32> { static constexpr int value = 56; };
+template <> struct Bf16Ld<64> { static constexpr int value = 72; };
+template <> struct Bf16Ld<128> { static constexpr int value = 152; };
+
+template <int ROWS, int D, int NTHREADS>
 struct Bf16TileStager {
-    static constexpr int kLdR = D + 8;
-    static constexpr int kLdT = ROWS + 4;
+    static constexpr int kLd = Bf16Ld<D>::value;
     static constexpr int kGroups = ROWS / 4;          // row groups of 4
     static constexpr int kChunks = D / 8;             // 8-column chunks per row
     static constexpr int kQuads = kGroups * kChunks;
@@ -40,8 +42,8 @@ struct Bf16TileStager {
 #pragma unroll
         for (int it = 0; it < kIters; ++it) {
             const int q = tid + it * NTHREADS;
-            const int rg = TRANSPOSED ? q % kGroups : q / kChunks;
-            const int c8 = TRANSPOSED ? q / kGroups : q % kChunks;
+            const int rg = q / kChunks;
+            const int c8 = q % kChunks;
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
                 const int row = row0 + 4 * rg + k;
@@ -52,51 +54,44 @@ struct Bf16TileStager {
         }
     }
 
-    __device__ __forceinline__ void store(uint16_t (*R)[kLdR], uint16_t (*T)[kLdT],
-                                          int tid) const {
+    __device__ __forceinline__ void store(uint16_t (*R)[kLd], int tid) const {
 #pragma unroll
         for (int it = 0; it < kIters; ++it) {
             const int q = tid + it * NTHREADS;
             if (q >= kQuads) continue;
-            const int rg = TRANSPOSED ? q % kGroups : q / kChunks;
-            const int c8 = TRANSPOSED ? q / kGroups : q % kChunks;
-            if constexpr (ROW_MAJOR) {
+            const int rg = q / kChunks;
+            const int c8 = q % kChunks;
 #pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    *reinterpret_cast<u32x4 *>(&R[4 * rg + k][8 * c8]) = buf[it][k];
-            }
-            if constexpr (TRANSPOSED) {
-                // column 8*c8 + e of rows 4rg..4rg+3 -> T[8*c8 + e][4rg..4rg+3]
-#pragma unroll
-                for (int m = 0; m < 4; ++m) {
-                    const uint32_t w0 = buf[it][0][m], w1 = buf[it][1][m];
-                    const uint32_t w2 = buf[it][2][m], w3 = buf[it][3][m];
-                    // even element 2m: low halves; odd element 2m+1: high halves
-                    const uint32_t lo01 = (w0 & 0xffffu) | (w1 << 16);
-                    const uint32_t lo23 = (w2 & 0xffffu) | (w3 << 16);
-                    const uint32_t hi01 = (w0 >> 16) | (w1 & 0xffff0000u);
-                    const uint32_t hi23 = (w2 >> 16) | (w3 & 0xffff0000u);
-                    *reinterpret_cast<uint64_t *>(&T[8 * c8 + 2 * m][4 * rg]) =
-                        (uint64_t)lo01 | ((uint64_t)lo23 << 32);
-                    *reinterpret_cast<uint64_t *>(&T[8 * c8 + 2 * m + 1][4 * rg]) =
-                        (uint64_t)hi01 | ((uint64_t)hi23 << 32);
-                }
-            }
+            for (int k = 0; k < 4; ++k)
+                *reinterpret_cast<u32x4 *>(&R[4 * rg + k][8 * c8]) = buf[it][k];
         }
     }
 };
 
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+// Transpose read (see above): `p` is this lane's 8-byte chunk address.
+__device__ __forceinline__ s16x4 lds_read_tr16(const uint16_t *p) {
+    typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4 *)p);
+}
+
+// A operand of a product contracting over the rows of row-major tile X:
+// positions 0..3 are rows r0..r0+3 and 4..7 rows r1..r1+3 of column col0 + i
+// (i = lane%16); `jr`, `jc` are this lane's row / column offsets in its
+// 4 x 16 transpose block (lane%16 / 4 and 4*(lane%4)).
+template <int LD>
+__device__ __forceinline__ bf16x8 load_tr_pair(const uint16_t (*X)[LD], int r0, int r1,
+                                               int col0, int jr, int jc) {
+    const s16x4 lo = lds_read_tr16(&X[r0 + jr][col0 + jc]);
+    const s16x4 hi = lds_read_tr16(&X[r1 + jr][col0 + jc]);
+    return __builtin_bit_cast(bf16x8, (short __attribute__((ext_vector_type(8)))){
+        lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+}
+
 // Eight bf16 from 16 bytes of LDS or global memory.
 __device__ __forceinline__ bf16x8 load_bf16x8(const uint16_t *p) {
     return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4 *>(p));
-}
-
-// Eight bf16 from two 8-byte runs (contraction positions 0..3 and 4..7).
-__device__ __forceinline__ bf16x8 load_bf16x4x2(const uint16_t *lo, const uint16_t *hi) {
-    typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-    const u32x2 a = *reinterpret_cast<const u32x2 *>(lo);
-    const u32x2 b = *reinterpret_cast<const u32x2 *>(hi);
-    return __builtin_bit_cast(bf16x8, u32x4{a[0], a[1], b[0], b[1]});
 }
 
 // Round two accumulator blocks (4 values each) to bf16 as one B operand:
