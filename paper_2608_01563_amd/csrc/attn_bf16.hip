@@ -148,7 +148,7 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
         for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
             for (int v = 0; v < 16; v += 2) mx = fmaxf(mx, fmaxf(sacc[kb][v], sacc[kb][v + 1]));
-        mx = fmaxf(mx, xor_lanes(mx, 32));
+        mx = max_xor32(mx);
         const float m_new = fmaxf(m_run, mx);
         // exponent offset in base-2 units; a row with nothing allowed yet
         // keeps all-zero probabilities
@@ -188,7 +188,7 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
             }
     }
 
-    const float l = l_run + xor_lanes(l_run, 32);
+    const float l = sum_xor32(l_run);
     if (qi < L) {
         const float inv = (l > 0.f) ? 1.f / l : 0.f;
         uint16_t *orow = O + hoff + (size_t)qi * D;

@@ -60,15 +60,31 @@ __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_ex
 
 __device__ __forceinline__ float xor_lanes(float v, int mask) { return __shfl_xor(v, mask, 64); }
 
+// Cross-row exchanges on the VALU (no LDS crossbar round trip).  For
+// v_permlane16_swap(x, x) every lane receives {x of the even 16-lane row,
+// x of the odd row} of its row pair, in that order; v_permlane32_swap does the
+// same for the two 32-lane halves.  Combining the pair therefore yields the
+// same value, bit for bit, on both partners.
+__device__ __forceinline__ float max_xor16(float v) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor32(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_xor16(float v) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float sum_xor32(float v) {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Reductions across the four 16-lane groups that share one column l%16.
-__device__ __forceinline__ float max_over_groups(float v) {
-    v = fmaxf(v, xor_lanes(v, 16));
-    return fmaxf(v, xor_lanes(v, 32));
-}
-__device__ __forceinline__ float sum_over_groups(float v) {
-    v += xor_lanes(v, 16);
-    return v + xor_lanes(v, 32);
-}
+__device__ __forceinline__ float max_over_groups(float v) { return max_xor32(max_xor16(v)); }
+__device__ __forceinline__ float sum_over_groups(float v) { return sum_xor32(sum_xor16(v)); }
 
 __device__ __forceinline__ f32x4 zero4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
