@@ -288,7 +288,9 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
         ost.load(dO + hoff, qt * kStream, L, tid);
         if (tid < kStream) {
             const int row = qt * kStream + tid;
-            lse_pre = (row < L) ? LSE[(size_t)head * L + row] * kLog2e : 0.f;
+            // natural log; scaled to base 2 at the LDS store so that nothing waits
+            // for this load before the next tile's rows are consumed
+            lse_pre = (row < L) ? LSE[(size_t)head * L + row] : 0.f;
             d_pre = (row < L) ? Dws[(size_t)head * L + row] : 0.f;
         }
     };
@@ -299,7 +301,7 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
         qst.store(Qr, tid);
         ost.store(Or, tid);
         if (tid < kStream) {
-            lse2s[tid] = lse_pre;
+            lse2s[tid] = lse_pre * kLog2e;
             Ds[tid] = d_pre;
         }
         __syncthreads();

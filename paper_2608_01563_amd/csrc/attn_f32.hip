@@ -9,17 +9,24 @@
 //   attn_rowdot_f32   D_i = sum_k dO_ik O_ik (HBM-bound row reduction).
 //   attn_dkdv_f32     key tile stationary: recomputes P from LSE, then
 //                     dV += P^T dO, dP = dO V^T, dS = P(dP - D), dK += dS^T Q.
+//   attn_dkdvq_f32    attn_dkdv_f32 plus the dQ product of its key tile:
+//                     dQ_part = dS K_tile goes to the workspace, one partial
+//                     per (key tile, query row) (d <= 64).
+//   attn_dq_reduce_f32  dQ = scale * sum of a row's partials, in key-tile
+//                     order (fixed order: bitwise-reproducible, no atomics).
 //   attn_dq_f32       query tile stationary: recomputes P and dS, then
-//                     dQ += dS K.  Separate from dK/dV, so no atomics and
-//                     bitwise-reproducible results.
+//                     dQ += dS K (used when the partials do not fit: d = 128
+//                     or a workspace above 1 GiB).
 //
 // Every product runs on v_mfma_f32_16x16x4_f32 (f32 inputs, f32 accumulate),
 // which is what the strict contract permits (Sec. 4.2).  Each wave owns 16
 // rows of the stationary tile (one per lane column l%16); the other operand
 // is staged through LDS, 64 rows at a time, and shared by the waves of a
-// workgroup.  With double buffering the next tile is written into the other
-// LDS buffer after the current one has been consumed, so one barrier per
-// tile suffices.
+// workgroup.  The forward kernel copies its K and V tiles with gfx950's
+// direct-to-LDS buffer loads (no staging registers) and fetches the next K
+// tile during P V and the next V tile during S = K Q^T.  The backward
+// kernels stage Q and dO through registers: the loads for the next tile are
+// issued before the current one is consumed and written to LDS after it.
 //
 // Workgroup order: the 1-D grid is numbered rank-major over heads
 // (id = rank * B*H + head) with rank 0 the tile that has the most work under
@@ -27,8 +34,9 @@
 // every tile of a head lands on the same XCD (workgroups are dealt to the
 // eight XCDs round-robin), so a head's K/V or Q/dO stay in one L2.
 //
-// Masking needs no per-tile branch: an element's offset inside its tile is
-// compared against one per-lane threshold (key length, causal diagonal).
+// Masking: an element's offset inside its tile is compared against one
+// per-lane threshold (key length, causal diagonal); the forward kernel skips
+// the comparison on tiles that hold no masked element.
 #include <climits>
 
 #include "device_common.h"
@@ -37,9 +45,11 @@
 
 // Per-kernel launch configuration: waves per workgroup, minimum waves per
 // SIMD requested from the register allocator (0 = compiler default), and
-// double-buffered LDS.  The defaults are the fastest of a sweep on MI355X at
-// B8 H8 L1024 d64 (double buffering lost there: it halves the workgroups an
-// LDS-heavy CU can hold); they can be overridden at build time.
+// double-buffered LDS for the streamed tile of the backward kernels (the
+// forward kernel always alternates its K and V fetches).  The defaults are
+// the fastest of sweeps on MI355X at B8 H8 L1024 d64 and B16 H12 L512 d64
+// (double buffering lost there: it halves the workgroups an LDS-heavy CU can
+// hold); they can be overridden at build time.
 #ifndef MG_FWD_CFG
 #define MG_FWD_CFG 4, 3, false
 #endif
@@ -52,9 +62,6 @@
 #ifndef MG_DQ_CFG
 #define MG_DQ_CFG 8, 0, false
 #endif
-#ifndef MG_FWD_STREAM
-#define MG_FWD_STREAM 64   // keys per streamed forward tile (32 or 64)
-#endif
 #ifndef MG_DKDV_NIB
 #define MG_DKDV_NIB 2   // 16-row query blocks per dK/dV step (d <= 64)
 #endif
@@ -63,7 +70,7 @@ namespace mg {
 namespace {
 
 constexpr int kStream = 64;   // streamed rows per step
-constexpr int kFwdStream = MG_FWD_STREAM;
+constexpr int kFwdStream = 64;   // keys per streamed forward tile
 
 template <int NW_, int OCC_, bool DB_>
 struct Cfg {
@@ -81,20 +88,28 @@ using DkdvqCausalCfg = Cfg<MG_DKDVQ_CAUSAL_CFG>;
 using DqCfg = Cfg<MG_DQ_CFG>;
 
 // ---------------------------------------------------------------- forward --
+// Query tile of C::ROWS rows stationary (16 per wave); 64-key K and V tiles
+// stream through LDS by direct-to-LDS loads.  The next K tile is fetched
+// while the softmax and P V of the current tile run, the next V tile while
+// the next S = K Q^T runs, so each iteration has two barriers and no staging
+// registers:
+//   S(kt) from K | wait V(kt), barrier | fetch K(kt+1) | softmax, P V(kt)
+//   | wait K(kt+1), barrier | fetch V(kt+1)
 template <int D, class C>
 __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::template occ<D>(), 8)))
 void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
                   const float *__restrict__ V, float *__restrict__ O, float *__restrict__ LSE,
                   const int32_t *__restrict__ key_len, int H, int L, int causal,
                   float scale_log2, int n_qtiles, int BH) {
+    constexpr int KS = kFwdStream;
     constexpr int DQ = D / 4;    // contraction values per lane in one S chain
     constexpr int NC = D / 16;   // 16-column blocks of the head dimension
-    constexpr int KS = kFwdStream;
     constexpr int NJB = KS / 16; // 16-key blocks per streamed tile
-    using Stager = F32TileStager<KS, D, C::NT>;
-    constexpr int LD = Stager::kLd;
-    __shared__ __attribute__((aligned(16))) float Ks[C::NBUF][KS][LD];
-    __shared__ __attribute__((aligned(16))) float Vs[C::NBUF][KS][LD];
+    using Tile = DirectTile<KS, D, C::NW>;
+    static_assert(Tile::kEven, "the vmcnt waits below count kPerWave loads per fetch");
+    constexpr int NL = Tile::kPerWave;   // vector-memory operations per tile fetch
+    __shared__ __attribute__((aligned(16))) float Ks[KS * D];
+    __shared__ __attribute__((aligned(16))) float Vs[KS * D];
 
     const int rank = blockIdx.x / BH;
     const int head = blockIdx.x - rank * BH;
@@ -106,23 +121,42 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int il = lane & 15;
     const int g = lane >> 4;
     const int q0 = qt * C::ROWS;
-    const int qi = q0 + 16 * (tid >> 6) + il;
+    const int qw0 = q0 + 16 * w;   // first query row of this wave
+    const int qi = qw0 + il;
 
     const int klen = key_limit(key_len, b, L);
     const int kend = causal ? min(klen, q0 + C::ROWS) : klen;
     const int ntiles = (kend + KS - 1) / KS;
 
-    // B operand of S^T = K Q^T: lane holds Q[qi][g*DQ + s].
+    Tile tile;
+    tile.init(w, lane);
+    // LDS float offsets of this lane's operands in key block jb = 0; block jb
+    // adds 16*jb*D (the chunk permutation repeats every 16 rows).
+    int koff[DQ / 4], voffs[4][NC];
+#pragma unroll
+    for (int s4 = 0; s4 < DQ / 4; ++s4) koff[s4] = Tile::at(il, g * DQ + 4 * s4);
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int c = 0; c < NC; ++c) voffs[r][c] = Tile::at(4 * g + r, 16 * c + il);
+    if (ntiles > 0) {
+        tile.issue(Ks, Kh, 0, L, w);
+        tile.issue(Vs, Vh, 0, L, w);
+    }
+
+    // B operand of S^T = K Q^T: lane holds Q[qi][g*DQ + s] times
+    // scale*log2(e), so that the product is the exponent in base 2.
     float qreg[DQ];
 #pragma unroll
     for (int s4 = 0; s4 < DQ / 4; ++s4) {
         f32x4 v = (qi < L) ? *reinterpret_cast<const f32x4 *>(Qh + (size_t)qi * D + g * DQ + 4 * s4)
                            : zero4();
 #pragma unroll
-        for (int e = 0; e < 4; ++e) qreg[4 * s4 + e] = v[e];
+        for (int e = 0; e < 4; ++e) qreg[4 * s4 + e] = v[e] * scale_log2;
     }
 
     float m_run = -INFINITY;   // running max of this lane's row, base-2 units
@@ -131,29 +165,9 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
 #pragma unroll
     for (int c = 0; c < NC; ++c) oacc[c] = zero4();
 
-    Stager kst, vst;
-    if (ntiles > 0) {
-        kst.load(Kh, 0, L, tid);
-        vst.load(Vh, 0, L, tid);
-        if (C::NBUF == 2) {
-            kst.store(Ks[0], tid);
-            vst.store(Vs[0], tid);
-            __syncthreads();
-        }
-    }
+    wait_vmcnt<NL>();   // K(0) landed (V(0) may still be in flight)
+    __syncthreads();
     for (int kt = 0; kt < ntiles; ++kt) {
-        const int cur = (C::NBUF == 2) ? (kt & 1) : 0;
-        if (C::NBUF == 1) {
-            __syncthreads();
-            kst.store(Ks[0], tid);
-            vst.store(Vs[0], tid);
-            __syncthreads();
-        }
-        if (kt + 1 < ntiles) {
-            kst.load(Kh, (kt + 1) * KS, L, tid);
-            vst.load(Vh, (kt + 1) * KS, L, tid);
-        }
-
         // S^T[16jb + 4g + r][qi] = sum_k K[j][k] Q[qi][k]
         f32x4 sacc[NJB];
 #pragma unroll
@@ -163,31 +177,48 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
             f32x4 a[NJB];
 #pragma unroll
             for (int jb = 0; jb < NJB; ++jb)
-                a[jb] = *reinterpret_cast<const f32x4 *>(&Ks[cur][16 * jb + il][g * DQ + 4 * s4]);
+                a[jb] = *reinterpret_cast<const f32x4 *>(&Ks[koff[s4] + 16 * jb * D]);
 #pragma unroll
             for (int e = 0; e < 4; ++e)
 #pragma unroll
                 for (int jb = 0; jb < NJB; ++jb)
                     sacc[jb] = mfma16x16x4(a[jb][e], qreg[4 * s4 + e], sacc[jb]);
         }
+        wait_vmcnt<0>();   // V(kt) landed
+        __syncthreads();   // every wave is done with K(kt) and sees V(kt)
+        if (kt + 1 < ntiles) tile.issue(Ks, Kh, (kt + 1) * KS, L, w);
 
         // Element (jb, r) holds key j0 + 16jb + r, allowed iff that offset is
         // below a per-lane threshold (key length; the query row if causal).
-        const int j0 = kt * KS + 4 * g;
-        const int thr = causal ? min(klen - j0, qi - j0 + 1) : klen - j0;
+        // Only tiles that reach past the key length or past the wave's first
+        // query row (causal) hold masked elements.
+        const int jt = kt * KS;
+        if (jt + KS > klen || (causal && jt + KS - 1 > qw0)) {
+            const int j0 = jt + 4 * g;
+            const int thr = causal ? min(klen - j0, qi - j0 + 1) : klen - j0;
+#pragma unroll
+            for (int jb = 0; jb < NJB; ++jb)
+#pragma unroll
+                for (int r = 0; r < 4; ++r)
+                    sacc[jb][r] = (16 * jb + r < thr) ? sacc[jb][r] : -INFINITY;
+        }
         float mx = -INFINITY;
 #pragma unroll
         for (int jb = 0; jb < NJB; ++jb)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float t = (16 * jb + r < thr) ? sacc[jb][r] * scale_log2 : -INFINITY;
-                sacc[jb][r] = t;
-                mx = fmaxf(mx, t);
-            }
+            for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sacc[jb][r]);
         mx = max_over_groups(mx);
         const float m_new = fmaxf(m_run, mx);
         const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-        const float alpha = exp2_fast(m_run - m_use);
+        // Rescaling by 2^(m_run - m_new) is a multiplication by one on every
+        // lane whose maximum did not move; skip it when that holds wave-wide.
+        if (__any(m_new != m_run)) {
+            const float alpha = exp2_fast(m_run - m_use);
+            l_run *= alpha;
+#pragma unroll
+            for (int c = 0; c < NC; ++c) oacc[c] *= alpha;
+        }
+        m_run = m_new;
         float psum = 0.f;
 #pragma unroll
         for (int jb = 0; jb < NJB; ++jb)
@@ -197,10 +228,7 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
                 sacc[jb][r] = p;
                 psum += p;
             }
-        l_run = l_run * alpha + psum;
-        m_run = m_new;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) oacc[c] *= alpha;
+        l_run += psum;
 
         // O^T[16c + 4g + r][qi] += sum_j V[j][16c + il'] P^T[j][qi]
 #pragma unroll
@@ -209,16 +237,11 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
             for (int r = 0; r < 4; ++r)
 #pragma unroll
                 for (int c = 0; c < NC; ++c)
-                    oacc[c] = mfma16x16x4(Vs[cur][16 * jb + 4 * g + r][16 * c + il], sacc[jb][r],
-                                          oacc[c]);
+                    oacc[c] = mfma16x16x4(Vs[voffs[r][c] + 16 * jb * D], sacc[jb][r], oacc[c]);
 
-        if (C::NBUF == 2) {
-            if (kt + 1 < ntiles) {
-                kst.store(Ks[cur ^ 1], tid);
-                vst.store(Vs[cur ^ 1], tid);
-            }
-            __syncthreads();
-        }
+        wait_vmcnt<0>();   // K(kt+1) landed
+        __syncthreads();   // every wave is done with V(kt) and sees K(kt+1)
+        if (kt + 1 < ntiles) tile.issue(Vs, Vh, (kt + 1) * KS, L, w);
     }
 
     const float l = sum_over_groups(l_run);
@@ -321,7 +344,9 @@ void attn_dkdv_f32(const float *__restrict__ Q, const float *__restrict__ K,
         ost.load(dOh, qt * BR, L, tid);
         if (tid < BR) {
             const int row = qt * BR + tid;
-            lse_pre = (row < L) ? LSE[(size_t)head * L + row] * kLog2e : 0.f;
+            // natural log; scaled to base 2 at the LDS store so that nothing waits
+            // for this load before the next tile's rows are consumed
+            lse_pre = (row < L) ? LSE[(size_t)head * L + row] : 0.f;
             d_pre = (row < L) ? Dws[(size_t)head * L + row] : 0.f;
         }
     };
@@ -329,7 +354,7 @@ void attn_dkdv_f32(const float *__restrict__ Q, const float *__restrict__ K,
         qst.store(Qs[buf], tid);
         ost.store(dOs[buf], tid);
         if (tid < BR) {
-            lse2s[buf][tid] = lse_pre;
+            lse2s[buf][tid] = lse_pre * kLog2e;
             Ds[buf][tid] = d_pre;
         }
     };
@@ -429,10 +454,16 @@ void attn_dkdv_f32(const float *__restrict__ Q, const float *__restrict__ K,
 // ---------------------------------------- backward: dK, dV and dQ partials
 // The key-stationary kernel above, extended with the dQ product: after dS of
 // a query tile is known, it goes through LDS and the workgroup multiplies it
-// by its own 64-key tile, dQ_part[i][:] = sum_{j in tile} dS[i][j] K[j][:].
+// by its own key tile, dQ_part[i][:] = sum_{j in tile} dS[i][j] K[j][:].
 // Each (key tile, query row) partial is written once to the workspace and
 // attn_dq_reduce_f32 adds the partials of a row in key-tile order: no atomics,
 // bitwise-reproducible, and no second recompute of S and dP.
+//
+// The Q and dO tiles reach LDS by row-wise direct-to-LDS loads (no staging
+// registers, padded rows as in the kernel above).  With two LDS buffers (C::NBUF == 2) the next tile is fetched
+// during the whole current iteration; with one, during the dQ product.  A
+// tile's dQ partials are stored at the start of the next iteration, so the
+// wait for the next tile never waits on a just-issued store.
 template <int D, int NIB, class C>
 __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::template occ<D>(), 8)))
 void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
@@ -447,12 +478,13 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     constexpr int KR = C::ROWS;                 // keys per workgroup
     constexpr int NBLK = NIB * NC;              // 16x16 blocks of a dQ partial tile
     constexpr int PER_WAVE = (NBLK + C::NW - 1) / C::NW;
-    using Stager = F32TileStager<BR, D, C::NT>;
-    constexpr int LD = Stager::kLd;
-    __shared__ __attribute__((aligned(16))) float Qs[BR][LD];
-    __shared__ __attribute__((aligned(16))) float dOs[BR][LD];
-    __shared__ __attribute__((aligned(16))) float lse2s[BR];
-    __shared__ __attribute__((aligned(16))) float Ds[BR];
+    constexpr int NB = C::NBUF;
+    constexpr int LD = D + 4;
+    using Tile = RowDirectTile<BR, D, C::NW, LD>;
+    __shared__ __attribute__((aligned(16))) float Qs[NB][BR][LD];
+    __shared__ __attribute__((aligned(16))) float dOs[NB][BR][LD];
+    __shared__ __attribute__((aligned(16))) float lse2s[NB][BR];
+    __shared__ __attribute__((aligned(16))) float Ds[NB][BR];
     __shared__ __attribute__((aligned(16))) float Kt[D][KR + 4];    // key tile, transposed
     __shared__ __attribute__((aligned(16))) float dSs[BR][KR + 4];  // dS of the query tile
 
@@ -466,7 +498,7 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int w = tid >> 6;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int il = lane & 15;
     const int g = lane >> 4;
     const int k0 = kt * KR;
@@ -476,6 +508,26 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     const int nq = (L + BR - 1) / BR;
     const int qstart = causal ? (k0 / BR) : 0;
     const int qstop = (k0 < klen) ? nq : qstart;
+
+    const Tile tile;
+
+    float lse_pre = 0.f, d_pre = 0.f;
+    auto fetch = [&](int qt, int buf) {   // direct loads of Q, dO; LSE, D to registers
+        tile.issue(Qs[buf], Qh, qt * BR, L, w, lane);
+        tile.issue(dOs[buf], dOh, qt * BR, L, w, lane);
+        if (tid < BR) {
+            const int row = qt * BR + tid;
+            lse_pre = (row < L) ? LSE[(size_t)head * L + row] : 0.f;
+            d_pre = (row < L) ? Dws[(size_t)head * L + row] : 0.f;
+        }
+    };
+    auto publish = [&](int buf) {   // LSE (base 2) and D of the fetched rows
+        if (tid < BR) {
+            lse2s[buf][tid] = lse_pre * kLog2e;
+            Ds[buf][tid] = d_pre;
+        }
+    };
+    if (qstart < qstop) fetch(qstart, 0);
 
     float kreg[DQ], vreg[DQ];
 #pragma unroll
@@ -489,8 +541,7 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
             vreg[4 * s4 + e] = vv[e];
         }
     }
-    // The key tile, transposed, for the A operand of the dQ product; made
-    // visible by the first barrier of the loop.
+    // The key tile, transposed, for the A operand of the dQ product.
     for (int f = tid; f < KR * (D / 4); f += C::NT) {
         const int row = f / (D / 4);
         const int c4 = f - row * (D / 4);
@@ -515,29 +566,36 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     constexpr int kNever = 1 << 30;
     const int kthr = (kj >= klen) ? kNever : (causal ? kj : -kNever);
 
-    Stager qst, ost;
-    float lse_pre = 0.f, d_pre = 0.f;
-    auto load_rows = [&](int qt) {
-        qst.load(Qh, qt * BR, L, tid);
-        ost.load(dOh, qt * BR, L, tid);
-        if (tid < BR) {
-            const int row = qt * BR + tid;
-            lse_pre = (row < L) ? LSE[(size_t)head * L + row] * kLog2e : 0.f;
-            d_pre = (row < L) ? Dws[(size_t)head * L + row] : 0.f;
+    // dQ partial blocks of this wave: consecutive blocks (same query rows,
+    // shared dS reads) when they split evenly, else strided
+    auto dq_block = [&](int bb) {
+        return (NBLK % C::NW == 0) ? w * PER_WAVE + bb : w + bb * C::NW;
+    };
+    f32x4 dqacc[PER_WAVE];   // partials of the previous query tile, not yet stored
+    auto store_dq = [&](int qt) {
+#pragma unroll
+        for (int bb = 0; bb < PER_WAVE; ++bb) {
+            const int blk = dq_block(bb);
+            if (NBLK % C::NW != 0 && blk >= NBLK) break;
+            const int ib = blk / NC;
+            const int c = blk - ib * NC;
+            const int row = qt * BR + 16 * ib + il;
+            if (row < L)
+                *reinterpret_cast<f32x4 *>(dQp + ((size_t)kt * BH + head) * L * D +
+                                           (size_t)row * D + 16 * c + 4 * g) = dqacc[bb];
         }
     };
-    if (qstart < qstop) load_rows(qstart);
+
+    if (qstart < qstop) {
+        wait_vmcnt<0>();
+        publish(0);
+    }
+    __syncthreads();   // first tile, its LSE/D and Kt visible
 
     for (int qt = qstart; qt < qstop; ++qt) {
-        __syncthreads();
-        qst.store(Qs, tid);
-        ost.store(dOs, tid);
-        if (tid < BR) {
-            lse2s[tid] = lse_pre;
-            Ds[tid] = d_pre;
-        }
-        __syncthreads();
-        if (qt + 1 < qstop) load_rows(qt + 1);
+        const int cb = (NB == 2) ? ((qt - qstart) & 1) : 0;
+        if (qt > qstart) store_dq(qt - 1);
+        if (NB == 2 && qt + 1 < qstop) fetch(qt + 1, cb ^ 1);
 
         f32x4 sacc[NIB], pacc[NIB];
 #pragma unroll
@@ -550,8 +608,8 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
             f32x4 aq[NIB], ao[NIB];
 #pragma unroll
             for (int ib = 0; ib < NIB; ++ib) {
-                aq[ib] = *reinterpret_cast<const f32x4 *>(&Qs[16 * ib + il][g * DQ + 4 * s4]);
-                ao[ib] = *reinterpret_cast<const f32x4 *>(&dOs[16 * ib + il][g * DQ + 4 * s4]);
+                aq[ib] = *reinterpret_cast<const f32x4 *>(&Qs[cb][16 * ib + il][g * DQ + 4 * s4]);
+                ao[ib] = *reinterpret_cast<const f32x4 *>(&dOs[cb][16 * ib + il][g * DQ + 4 * s4]);
             }
 #pragma unroll
             for (int e = 0; e < 4; ++e)
@@ -566,8 +624,8 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
         const int thr = kthr - ibase;
 #pragma unroll
         for (int ib = 0; ib < NIB; ++ib) {
-            const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lse2s[16 * ib + 4 * g]);
-            const f32x4 dd = *reinterpret_cast<const f32x4 *>(&Ds[16 * ib + 4 * g]);
+            const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lse2s[cb][16 * ib + 4 * g]);
+            const f32x4 dd = *reinterpret_cast<const f32x4 *>(&Ds[cb][16 * ib + 4 * g]);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 float p = exp2_fast(sacc[ib][r] * scale_log2 - l2[r]);
@@ -584,19 +642,19 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
             for (int r = 0; r < 4; ++r)
 #pragma unroll
                 for (int c = 0; c < NC; ++c) {
-                    dvacc[c] = mfma16x16x4(dOs[16 * ib + 4 * g + r][16 * c + il], sacc[ib][r],
-                                           dvacc[c]);
-                    dkacc[c] = mfma16x16x4(Qs[16 * ib + 4 * g + r][16 * c + il], pacc[ib][r],
-                                           dkacc[c]);
+                    dvacc[c] = mfma16x16x4(dOs[cb][16 * ib + 4 * g + r][16 * c + il],
+                                           sacc[ib][r], dvacc[c]);
+                    dkacc[c] = mfma16x16x4(Qs[cb][16 * ib + 4 * g + r][16 * c + il],
+                                           pacc[ib][r], dkacc[c]);
                 }
 
+        __syncthreads();   // dS complete (and, single-buffered, Q/dO consumed)
+        if (NB == 1 && qt + 1 < qstop) fetch(qt + 1, 0);
+
         // dQ_part^T[16c + 4g + r][16ib + il] = sum_j K^T[16c + il'][j] dS^T[j][16ib + il]
-        __syncthreads();
 #pragma unroll
         for (int bb = 0; bb < PER_WAVE; ++bb) {
-            // consecutive blocks (same query rows, shared dS reads) per wave
-            // when they split evenly; otherwise strided, wave-uniform skip
-            const int blk = (NBLK % C::NW == 0) ? w * PER_WAVE + bb : w + bb * C::NW;
+            const int blk = dq_block(bb);
             if (NBLK % C::NW != 0 && blk >= NBLK) break;
             const int ib = blk / NC;
             const int c = blk - ib * NC;
@@ -608,12 +666,16 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
 #pragma unroll
                 for (int e = 0; e < 4; ++e) acc = mfma16x16x4(av[e], bv[e], acc);
             }
-            const int row = qt * BR + 16 * ib + il;
-            if (row < L)
-                *reinterpret_cast<f32x4 *>(dQp + ((size_t)kt * BH + head) * L * D +
-                                           (size_t)row * D + 16 * c + 4 * g) = acc;
+            dqacc[bb] = acc;
         }
+
+        if (qt + 1 < qstop) {
+            wait_vmcnt<0>();   // next Q/dO tile landed, its LSE/D in registers
+            publish(NB == 2 ? (cb ^ 1) : 0);
+        }
+        __syncthreads();   // next tile visible; dS and this tile's buffer free
     }
+    if (qstart < qstop) store_dq(qstop - 1);
 
     if (kj < L) {
         const bool keep = kj < klen;

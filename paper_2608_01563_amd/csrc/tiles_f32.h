@@ -6,13 +6,38 @@
 // row) and land in a row-padded LDS array with stride D+4 floats, which keeps
 // both the row-fragment reads (16 lanes on 16 rows, 16 bytes each) and the
 // column reads (16 lanes along one row, 4 rows apart) free of bank conflicts.
-// Rows at or beyond L are filled with zeros, so nothing past the tensor is
-// read and masked rows stay finite.
+//
+// The reads are raw buffer loads through a descriptor that covers exactly the
+// tile's rows below L: a chunk past the end reads as zero without touching
+// memory, so the tail tile needs neither a branch nor a per-lane bounds test,
+// and the only per-lane address is the thread's fixed byte offset in the tile.
 #pragma once
 
 #include "device_common.h"
 
 namespace mg {
+
+// Word 3 of a gfx9-family buffer descriptor: 32-bit data format, every other
+// field zero (no swizzle, no index stride); untyped dword loads need a
+// non-zero data format.
+constexpr int kBufferWord3 = 0x00020000;
+
+// Descriptor of `bytes` bytes starting at `base` (stride 0: offsets are plain
+// byte offsets; loads at offsets >= bytes return zero).  Both arguments must
+// be the same on every lane of the wave; they are read from the first active
+// lane so that the descriptor lives in scalar registers.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, int bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+    void *p = reinterpret_cast<void *>(((uint64_t)hi << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, __builtin_amdgcn_readfirstlane(bytes),
+                                             kBufferWord3);
+}
+
+__device__ __forceinline__ f32x4 buffer_load_f32x4(__amdgpu_buffer_rsrc_t r, int byte_offset) {
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_offset, 0, 0));
+}
 
 template <int ROWS, int D, int NTHREADS>
 struct F32TileStager {
@@ -24,19 +49,16 @@ struct F32TileStager {
 
     f32x4 buf[kPerThread];
 
-    // Issue the global loads of rows [row0, row0+ROWS) of `src` (one head).
+    // Issue the global loads of rows [row0, row0+ROWS) of `src` (one head);
+    // rows at or beyond L read as zero.  Chunk f of the tile sits at byte
+    // 16*f from the tile's first row, because tile rows are contiguous.
     __device__ __forceinline__ void load(const float *__restrict__ src, int row0, int L,
                                          int tid) {
+        const int rows = min(max(L - row0, 0), ROWS);
+        const auto rsrc = buffer_rsrc(src + (size_t)row0 * D, rows * D * 4);
 #pragma unroll
-        for (int u = 0; u < kPerThread; ++u) {
-            const int f = tid + u * NTHREADS;
-            const int r = f / kChunksPerRow;
-            const int c4 = f - r * kChunksPerRow;
-            const int row = row0 + r;
-            buf[u] = ((kExact || f < kChunks) && row < L)
-                ? *reinterpret_cast<const f32x4 *>(src + (size_t)row * D + 4 * c4)
-                : zero4();
-        }
+        for (int u = 0; u < kPerThread; ++u)
+            buf[u] = buffer_load_f32x4(rsrc, 16 * (tid + u * NTHREADS));
     }
 
     // Write the loaded chunks into dst[ROWS][D+4].
@@ -56,58 +78,105 @@ struct F32TileStager {
 
 namespace mg {
 
-// Quad staging: each thread moves a 4-row x 4-column block of an f32 tile and
-// writes it row-major R[ROWS][D+4] and/or transposed T[D][ROWS+4], both with
-// 16-byte LDS stores (the 4x4 transpose happens in registers).  Quads are
-// numbered row-group fastest, so a wave's transposed stores are contiguous.
-// The transposed copy lets a lane read four consecutive rows of one column
-// (the B-operand order of an accumulator) with a single 16-byte read.
-template <int ROWS, int D, int NTHREADS, bool ROW_MAJOR, bool TRANSPOSED>
-struct F32QuadStager {
-    static constexpr int kLdR = D + 4;
-    static constexpr int kLdT = ROWS + 4;
-    static constexpr int kGroups = ROWS / 4;
-    static constexpr int kQuads = kGroups * (D / 4);
-    static constexpr int kIters = (kQuads + NTHREADS - 1) / NTHREADS;
-    static_assert(ROWS % 4 == 0 && D % 4 == 0, "tile shape");
+// s_waitcnt immediate that waits until at most `n` vector-memory operations
+// of this wave are outstanding (gfx9 encoding: vmcnt in bits 3:0, expcnt and
+// lgkmcnt left at their maxima, i.e. not waited for).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 16, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
 
-    f32x4 buf[kIters][4];
+// A [ROWS][D] f32 tile copied from global memory straight into LDS with
+// 16-byte buffer loads that write LDS themselves (no staging registers, no
+// LDS store instructions).  One such load moves 64 chunks of 16 bytes, one
+// per lane, into 1 KB of contiguous LDS, so rows cannot be padded; instead
+// the 16-byte chunks of a row are permuted (chunk c of row r is stored at
+// position c ^ swz(r)), which makes both operand read patterns of the
+// forward pass bank-conflict free for d = 64 and 128:
+//   16 lanes reading 16 consecutive rows, same logical chunk (16-byte reads);
+//   64 lanes reading rows 4g + r, columns 16c + lane%16 (4-byte reads).
+// The lane -> chunk assignment is fixed per thread, so each lane's global
+// offset is computed once.  Rows at or beyond L arrive as zeros.
+template <int ROWS, int D, int NW>
+struct DirectTile {
+    static constexpr int kCpr = D / 4;                  // chunks per row
+    static constexpr int kWaveLoads = ROWS * kCpr / 64; // 1 KB loads per tile
+    static constexpr int kPerWave = (kWaveLoads + NW - 1) / NW;
+    // every wave issues exactly kPerWave loads per tile (else some issue fewer)
+    static constexpr bool kEven = kWaveLoads % NW == 0;
+    static_assert(ROWS * kCpr % 64 == 0, "tile must be a whole number of 1 KB loads");
 
-    __device__ __forceinline__ void load(const float *__restrict__ src, int row0, int L,
-                                         int tid) {
+    __device__ static constexpr int swz(int row) {
+        return D == 32 ? ((row >> 1) & 7) : (row & 15);
+    }
+    // Float offset of logical element (row, col) inside the tile.
+    __device__ static constexpr int at(int row, int col) {
+        return row * D + 4 * ((col >> 2) ^ swz(row)) + (col & 3);
+    }
+
+    int voff[kPerWave];   // byte offset, relative to the tile's first row
+
+    __device__ __forceinline__ void init(int w, int lane) {
 #pragma unroll
-        for (int it = 0; it < kIters; ++it) {
-            const int q = tid + it * NTHREADS;
-            const int rg = q % kGroups;
-            const int c4 = q / kGroups;
-#pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const int row = row0 + 4 * rg + k;
-                buf[it][k] = (q < kQuads && row < L)
-                    ? *reinterpret_cast<const f32x4 *>(src + (size_t)row * D + 4 * c4)
-                    : zero4();
-            }
+        for (int u = 0; u < kPerWave; ++u) {
+            const int pos = (u * NW + w) * 64 + lane;   // chunk position in LDS
+            const int row = pos / kCpr;
+            const int chunk = (pos % kCpr) ^ swz(row);   // logical chunk stored there
+            voff[u] = (row * D + 4 * chunk) * 4;
         }
     }
 
-    __device__ __forceinline__ void store(float (*R)[kLdR], float (*T)[kLdT], int tid) const {
+    // Issue this wave's share of the copy of rows [row0, row0 + ROWS) of
+    // `src` into `dst` (float[ROWS * D] in LDS).  Completion is tracked by
+    // the wave's vmcnt: kPerWave operations per call when kEven, at most
+    // that many otherwise.  `w` is the wave index (wave-uniform).
+    __device__ __forceinline__ void issue(float *dst, const float *__restrict__ src, int row0,
+                                          int L, int w) const {
+        const int rows = min(max(L - row0, 0), ROWS);
+        const auto rsrc = buffer_rsrc(src + (size_t)row0 * D, rows * D * 4);
 #pragma unroll
-        for (int it = 0; it < kIters; ++it) {
-            const int q = tid + it * NTHREADS;
-            if (kQuads % NTHREADS != 0 && q >= kQuads) continue;
-            const int rg = q % kGroups;
-            const int c4 = q / kGroups;
-            if constexpr (ROW_MAJOR) {
+        for (int u = 0; u < kPerWave; ++u)
+            if (kEven || u * NW + w < kWaveLoads)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rsrc, (__attribute__((address_space(3))) void *)(dst + (u * NW + w) * 256),
+                    16, voff[u], 0, 0, 0);
+    }
+};
+
+}  // namespace mg
+
+namespace mg {
+
+// A [ROWS][D] f32 tile copied row by row straight into a padded LDS array
+// dst[ROWS][LD]: one wave-wide 4-byte direct-to-LDS buffer load moves 64
+// consecutive floats of a row (256 bytes, fully coalesced), so every row
+// keeps the padded stride and all operand reads keep immediate offsets from
+// one per-lane base.  For D = 32 the upper half of the wave stays idle.  Rows
+// at or beyond L arrive as zeros.  Loads are dealt to the waves round-robin.
+template <int ROWS, int D, int NW, int LD>
+struct RowDirectTile {
+    static constexpr int kPart = D < 64 ? D : 64;       // floats per load
+    static constexpr int kParts = D / kPart;            // loads per row
+    static constexpr int kLoads = ROWS * kParts;        // loads per tile
+    static constexpr int kPerWave = (kLoads + NW - 1) / NW;
+    static constexpr bool kEven = kLoads % NW == 0;
+    static_assert(D % kPart == 0 && LD >= D, "row shape");
+
+    __device__ __forceinline__ void issue(float (*dst)[LD], const float *__restrict__ src,
+                                          int row0, int L, int w, int lane) const {
+        const int rows = min(max(L - row0, 0), ROWS);
+        const auto rsrc = buffer_rsrc(src + (size_t)row0 * D, rows * D * 4);
 #pragma unroll
-                for (int k = 0; k < 4; ++k)
-                    *reinterpret_cast<f32x4 *>(&R[4 * rg + k][4 * c4]) = buf[it][k];
-            }
-            if constexpr (TRANSPOSED) {
-#pragma unroll
-                for (int e = 0; e < 4; ++e)
-                    *reinterpret_cast<f32x4 *>(&T[4 * c4 + e][4 * rg]) =
-                        f32x4{buf[it][0][e], buf[it][1][e], buf[it][2][e], buf[it][3][e]};
-            }
+        for (int u = 0; u < kPerWave; ++u) {
+            const int t = u * NW + w;
+            if (!kEven && t >= kLoads) break;
+            const int row = t / kParts;
+            const int part = t - row * kParts;
+            if (kPart == 64 || lane < kPart)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rsrc, (__attribute__((address_space(3))) void *)&dst[row][kPart * part], 4,
+                    (row * D + kPart * part + lane) * 4, 0, 0, 0);
         }
     }
 };
