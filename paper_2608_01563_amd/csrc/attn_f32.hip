@@ -168,21 +168,45 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
     wait_vmcnt<NL>();   // K(0) landed (V(0) may still be in flight)
     __syncthreads();
     for (int kt = 0; kt < ntiles; ++kt) {
+        // 16-key blocks of this tile that hold an allowed key for some row
+        // of this wave (a prefix: keys past the key length, or past the
+        // wave's last row under a causal mask, are masked for every row).
+        // The products of the other blocks are skipped; their scores are
+        // masked below and their probabilities are exactly zero.
+        const int jt = kt * KS;
+        const int kcut = causal ? min(klen, qw0 + 16) : klen;
+        const int nlive = min(NJB, (kcut - jt + 15) / 16);
+
         // S^T[16jb + 4g + r][qi] = sum_k K[j][k] Q[qi][k]
         f32x4 sacc[NJB];
 #pragma unroll
         for (int jb = 0; jb < NJB; ++jb) sacc[jb] = zero4();
+        if (nlive == NJB) {
 #pragma unroll
-        for (int s4 = 0; s4 < DQ / 4; ++s4) {
-            f32x4 a[NJB];
-#pragma unroll
-            for (int jb = 0; jb < NJB; ++jb)
-                a[jb] = *reinterpret_cast<const f32x4 *>(&Ks[koff[s4] + 16 * jb * D]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
+            for (int s4 = 0; s4 < DQ / 4; ++s4) {
+                f32x4 a[NJB];
 #pragma unroll
                 for (int jb = 0; jb < NJB; ++jb)
-                    sacc[jb] = mfma16x16x4(a[jb][e], qreg[4 * s4 + e], sacc[jb]);
+                    a[jb] = *reinterpret_cast<const f32x4 *>(&Ks[koff[s4] + 16 * jb * D]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+#pragma unroll
+                    for (int jb = 0; jb < NJB; ++jb)
+                        sacc[jb] = mfma16x16x4(a[jb][e], qreg[4 * s4 + e], sacc[jb]);
+            }
+        } else {
+#pragma unroll
+            for (int jb = 0; jb < NJB; ++jb) {
+                if (jb >= nlive) break;
+#pragma unroll
+                for (int s4 = 0; s4 < DQ / 4; ++s4) {
+                    const f32x4 a =
+                        *reinterpret_cast<const f32x4 *>(&Ks[koff[s4] + 16 * jb * D]);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e)
+                        sacc[jb] = mfma16x16x4(a[e], qreg[4 * s4 + e], sacc[jb]);
+                }
+            }
         }
         wait_vmcnt<0>();   // V(kt) landed
         __syncthreads();   // every wave is done with K(kt) and sees V(kt)
@@ -192,7 +216,6 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
         // below a per-lane threshold (key length; the query row if causal).
         // Only tiles that reach past the key length or past the wave's first
         // query row (causal) hold masked elements.
-        const int jt = kt * KS;
         if (jt + KS > klen || (causal && jt + KS - 1 > qw0)) {
             const int j0 = jt + 4 * g;
             const int thr = causal ? min(klen - j0, qi - j0 + 1) : klen - j0;
@@ -232,12 +255,14 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
         // O^T[16c + 4g + r][qi] += sum_j V[j][16c + il'] P^T[j][qi]
 #pragma unroll
-        for (int jb = 0; jb < NJB; ++jb)
+        for (int jb = 0; jb < NJB; ++jb) {
+            if (jb >= nlive) break;
 #pragma unroll
             for (int r = 0; r < 4; ++r)
 #pragma unroll
                 for (int c = 0; c < NC; ++c)
                     oacc[c] = mfma16x16x4(Vs[voffs[r][c] + 16 * jb * D], sacc[jb][r], oacc[c]);
+        }
 
         wait_vmcnt<0>();   // K(kt+1) landed
         __syncthreads();   // every wave is done with V(kt) and sees K(kt+1)
@@ -502,7 +527,8 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     const int il = lane & 15;
     const int g = lane >> 4;
     const int k0 = kt * KR;
-    const int kj = k0 + 16 * w + il;
+    const int wkey0 = k0 + 16 * w;   // first key of this wave (wave-uniform)
+    const int kj = wkey0 + il;
 
     const int klen = key_limit(key_len, b, L);
     const int nq = (L + BR - 1) / BR;
@@ -597,56 +623,67 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
         if (qt > qstart) store_dq(qt - 1);
         if (NB == 2 && qt + 1 < qstop) fetch(qt + 1, cb ^ 1);
 
-        f32x4 sacc[NIB], pacc[NIB];
-#pragma unroll
-        for (int ib = 0; ib < NIB; ++ib) {
-            sacc[ib] = zero4();
-            pacc[ib] = zero4();
-        }
-#pragma unroll
-        for (int s4 = 0; s4 < DQ / 4; ++s4) {
-            f32x4 aq[NIB], ao[NIB];
+        // A wave whose 16 keys are all masked for every row of this query
+        // tile (padded keys, or keys past the tile's last row under a causal
+        // mask) contributes nothing but its zero block of dS.
+        const bool live = wkey0 < klen && (!causal || wkey0 <= qt * BR + BR - 1);
+        if (live) {
+            f32x4 sacc[NIB], pacc[NIB];
 #pragma unroll
             for (int ib = 0; ib < NIB; ++ib) {
-                aq[ib] = *reinterpret_cast<const f32x4 *>(&Qs[cb][16 * ib + il][g * DQ + 4 * s4]);
-                ao[ib] = *reinterpret_cast<const f32x4 *>(&dOs[cb][16 * ib + il][g * DQ + 4 * s4]);
+                sacc[ib] = zero4();
+                pacc[ib] = zero4();
             }
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
+            for (int s4 = 0; s4 < DQ / 4; ++s4) {
+                f32x4 aq[NIB], ao[NIB];
 #pragma unroll
                 for (int ib = 0; ib < NIB; ++ib) {
-                    sacc[ib] = mfma16x16x4(aq[ib][e], kreg[4 * s4 + e], sacc[ib]);
-                    pacc[ib] = mfma16x16x4(ao[ib][e], vreg[4 * s4 + e], pacc[ib]);
+                    aq[ib] = *reinterpret_cast<const f32x4 *>(&Qs[cb][16 * ib + il][g * DQ + 4 * s4]);
+                    ao[ib] = *reinterpret_cast<const f32x4 *>(&dOs[cb][16 * ib + il][g * DQ + 4 * s4]);
                 }
-        }
-
-        const int ibase = qt * BR + 4 * g;
-        const int thr = kthr - ibase;
 #pragma unroll
-        for (int ib = 0; ib < NIB; ++ib) {
-            const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lse2s[cb][16 * ib + 4 * g]);
-            const f32x4 dd = *reinterpret_cast<const f32x4 *>(&Ds[cb][16 * ib + 4 * g]);
+                for (int e = 0; e < 4; ++e)
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                float p = exp2_fast(sacc[ib][r] * scale_log2 - l2[r]);
-                p = (16 * ib + r >= thr) ? p : 0.f;
-                sacc[ib][r] = p;
-                pacc[ib][r] = p * (pacc[ib][r] - dd[r]);
-                dSs[16 * ib + 4 * g + r][16 * w + il] = pacc[ib][r];
+                    for (int ib = 0; ib < NIB; ++ib) {
+                        sacc[ib] = mfma16x16x4(aq[ib][e], kreg[4 * s4 + e], sacc[ib]);
+                        pacc[ib] = mfma16x16x4(ao[ib][e], vreg[4 * s4 + e], pacc[ib]);
+                    }
             }
-        }
+
+            const int ibase = qt * BR + 4 * g;
+            const int thr = kthr - ibase;
+#pragma unroll
+            for (int ib = 0; ib < NIB; ++ib) {
+                const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lse2s[cb][16 * ib + 4 * g]);
+                const f32x4 dd = *reinterpret_cast<const f32x4 *>(&Ds[cb][16 * ib + 4 * g]);
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    float p = exp2_fast(sacc[ib][r] * scale_log2 - l2[r]);
+                    p = (16 * ib + r >= thr) ? p : 0.f;
+                    sacc[ib][r] = p;
+                    pacc[ib][r] = p * (pacc[ib][r] - dd[r]);
+                    dSs[16 * ib + 4 * g + r][16 * w + il] = pacc[ib][r];
+                }
+            }
 
 #pragma unroll
-        for (int ib = 0; ib < NIB; ++ib)
+            for (int ib = 0; ib < NIB; ++ib)
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
+                for (int r = 0; r < 4; ++r)
 #pragma unroll
-                for (int c = 0; c < NC; ++c) {
-                    dvacc[c] = mfma16x16x4(dOs[cb][16 * ib + 4 * g + r][16 * c + il],
-                                           sacc[ib][r], dvacc[c]);
-                    dkacc[c] = mfma16x16x4(Qs[cb][16 * ib + 4 * g + r][16 * c + il],
-                                           pacc[ib][r], dkacc[c]);
-                }
+                    for (int c = 0; c < NC; ++c) {
+                        dvacc[c] = mfma16x16x4(dOs[cb][16 * ib + 4 * g + r][16 * c + il],
+                                               sacc[ib][r], dvacc[c]);
+                        dkacc[c] = mfma16x16x4(Qs[cb][16 * ib + 4 * g + r][16 * c + il],
+                                               pacc[ib][r], dkacc[c]);
+                    }
+        } else {
+#pragma unroll
+            for (int ib = 0; ib < NIB; ++ib)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) dSs[16 * ib + 4 * g + r][16 * w + il] = 0.f;
+        }
 
         __syncthreads();   // dS complete (and, single-buffered, Q/dO consumed)
         if (NB == 1 && qt + 1 < qstop) fetch(qt + 1, 0);
