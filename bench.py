@@ -30,8 +30,7 @@ if ROOT not in sys.path:
 METRIC = "attention fwd+bwd TFLOP/s (strict f32) at B8 H8 L1024 d64; % MFMA peak"
 PEAK_TFLOPS = {"strict_f32": 157.3, "fast_bf16": 2516.6}   # MI355X dense MFMA
 HBM_PEAK_GBS = 8000.0
-KERNEL_SOURCES = {"strict_f32": "paper_2608_01563_amd/csrc/attn_f32.hip",
-                  "fast_bf16": "paper_2608_01563_amd/csrc/attn_bf16.hip"}
+KERNEL_SOURCE_DIR = "paper_2608_01563_amd/csrc"
 COUNTER_FILE = "profiles/hbm_traffic_{workload}.json"
 
 
@@ -52,9 +51,19 @@ def parse():
     return ap.parse_args()
 
 
-def sha256_of(path):
-    with open(os.path.join(ROOT, path), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+def kernel_source_digest():
+    """sha256 over the names and contents of every file the library is built
+    from (kernels, headers, host code): a counter record taken on any other
+    source is stale."""
+    h = hashlib.sha256()
+    base = os.path.join(ROOT, KERNEL_SOURCE_DIR)
+    for name in sorted(os.listdir(base)):
+        path = os.path.join(base, name)
+        if os.path.isfile(path):
+            h.update(name.encode() + b"\0")
+            with open(path, "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()
 
 
 def kernel_work(name, w, pairs, rows, key_len=None):
@@ -67,7 +76,7 @@ def kernel_work(name, w, pairs, rows, key_len=None):
     if name.startswith("attn_dkdv"):
         return 8.0 * d * pairs, "flop", "mfma"        # S recompute, dV, dP, dK
     if name.startswith("attn_dqreduce"):
-        # reads one d-vector partial per (64-key tile, query row) pair that
+        # reads one d-vector partial per (key tile, query row) pair that
         # holds an allowed key, writes dQ
         return 4.0 * d * partial_rows(w, key_len) + 4.0 * w.B * w.H * w.L * d, "byte", "hbm"
     if name.startswith("attn_dq"):
@@ -100,7 +109,7 @@ def traffic_for(kernel, w):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("source_sha256") != sha256_of(KERNEL_SOURCES[w.contract]):
+    if rec.get("source_sha256") != kernel_source_digest():
         return None
     return rec.get("kernels", {}).get(kernel, {}).get("bytes_per_launch")
 
