@@ -42,7 +42,8 @@ def parse():
     ap.add_argument("--workload", type=int, default=3,
                     help="workload id (3 = causal B8 H8 L1024 d64 strict f32)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-repeats", type=int, default=3)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="repeat the oracle sample until this much CPU wall time (>= 3 runs)")
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="do not bracket kernels with events (no roofline)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -267,20 +268,22 @@ def cpu_baseline(args, w, x, pairs, gpu_outputs):
     heads = None
     if B * H * w.L * w.L * w.d > 2 ** 33:          # keep the CPU leg to seconds
         heads = [(b, h) for b in range(B) for h in range(H)][:: max(1, (B * H) // 4)][:4]
+    # repeat the sample until about --cpu-seconds of oracle work (at least 3
+    # runs, at most 100), so the figure is a bounded, stable CPU measurement
     times = []
-    for _ in range(max(1, args.cpu_repeats)):
+    while len(times) < 3 or (sum(times) < args.cpu_seconds and len(times) < 100):
         t0 = time.perf_counter()
         O, LSE = oracle_forward(x.Q, x.K, x.V, w.causal, w.scale, key_len=x.key_len, heads=heads)
         dQ, dK, dV, _ = oracle_backward(x.Q, x.K, x.V, x.dO, w.causal, w.scale,
                                         key_len=x.key_len, heads=heads)
         times.append(time.perf_counter() - t0)
-    t = float(np.median(times))
+    total = float(sum(times))
     frac = 1.0 if heads is None else len(heads) / float(B * H)
-    value = 14.0 * w.d * pairs * frac / t / 1e12
-    sample = ("whole workload (%d heads), fwd+bwd, median of %d runs, %.2f s each"
-              % (B * H, len(times), t)) if heads is None else (
-        "%d of %d heads, fwd+bwd, median of %d runs, %.2f s each"
-        % (len(heads), B * H, len(times), t))
+    value = 14.0 * w.d * pairs * frac * len(times) / total / 1e12
+    what = ("the whole workload (%d heads)" % (B * H)) if heads is None else (
+        "%d of %d heads" % (len(heads), B * H))
+    sample = ("%s, fwd+bwd, run %d times back to back (%.1f s of CPU wall time, "
+              "%.2f s per run)" % (what, len(times), total, total / len(times)))
     base = {"value": round(value, 6), "unit": "TFLOP/s", "cores": oracle_num_threads(),
             "kind": "oracle", "sample": sample}
     ref = {"O": O, "LSE": LSE, "dQ": dQ, "dK": dK, "dV": dV}
