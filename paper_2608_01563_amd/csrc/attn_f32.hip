@@ -62,6 +62,9 @@
 #ifndef MG_DQ_CFG
 #define MG_DQ_CFG 8, 0, false
 #endif
+#ifndef MG_DKDVQ_CAUSAL_NIB
+#define MG_DKDVQ_CAUSAL_NIB 2   // 16-row query blocks per step, 128-key fused kernel
+#endif
 #ifndef MG_DKDV_NIB
 #define MG_DKDV_NIB 2   // 16-row query blocks per dK/dV step (d <= 64)
 #endif
@@ -952,7 +955,7 @@ int fused_dq_key_rows(const AttnProblem &p) {
     return wide_key_tiles(p) ? DkdvqCausalCfg::ROWS : DkdvCfg::ROWS;
 }
 
-template <class C>
+template <class C, int NIB>
 static hipError_t launch_dkdvq(const AttnProblem &p, const float *Q, const float *K,
                                const float *V, const float *dO, const float *LSE,
                                const float *Dws, float *dK, float *dV, float *dQp,
@@ -961,8 +964,8 @@ static hipError_t launch_dkdvq(const AttnProblem &p, const float *Q, const float
     const dim3 grid(cdiv(p.L, C::ROWS) * BH), block(C::NT);
     const float sl2 = p.scale * kLog2e;
     switch (p.d) {
-    case 32: attn_dkdvq_f32<32, MG_DKDV_NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
-    case 64: attn_dkdvq_f32<64, MG_DKDV_NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
+    case 32: attn_dkdvq_f32<32, NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
+    case 64: attn_dkdvq_f32<64, NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -972,8 +975,9 @@ hipError_t launch_bwd_dkdvq_f32(const AttnProblem &p, const float *Q, const floa
                                 const float *V, const float *dO, const float *LSE,
                                 const float *Dws, float *dK, float *dV, float *dQp,
                                 hipStream_t s) {
-    return wide_key_tiles(p) ? launch_dkdvq<DkdvqCausalCfg>(p, Q, K, V, dO, LSE, Dws, dK, dV, dQp, s)
-                             : launch_dkdvq<DkdvCfg>(p, Q, K, V, dO, LSE, Dws, dK, dV, dQp, s);
+    return wide_key_tiles(p)
+        ? launch_dkdvq<DkdvqCausalCfg, MG_DKDVQ_CAUSAL_NIB>(p, Q, K, V, dO, LSE, Dws, dK, dV, dQp, s)
+        : launch_dkdvq<DkdvCfg, MG_DKDV_NIB>(p, Q, K, V, dO, LSE, Dws, dK, dV, dQp, s);
 }
 
 hipError_t launch_bwd_dq_reduce_f32(const AttnProblem &p, const float *dQp, float *dQ,

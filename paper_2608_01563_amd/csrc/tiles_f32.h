@@ -78,13 +78,14 @@ struct F32TileStager {
 
 namespace mg {
 
-// s_waitcnt immediate that waits until at most `n` vector-memory operations
-// of this wave are outstanding (gfx9 encoding: vmcnt in bits 3:0, expcnt and
-// lgkmcnt left at their maxima, i.e. not waited for).
+// s_waitcnt immediate that waits until at most `N` vector-memory operations
+// of this wave are outstanding (gfx9 encoding: vmcnt bits 3:0 in bits 3:0 and
+// bits 5:4 in bits 15:14; expcnt and lgkmcnt left at their maxima, i.e. not
+// waited for).
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 16, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
 }
 
 // A [ROWS][D] f32 tile copied from global memory straight into LDS with
@@ -92,13 +93,19 @@ __device__ __forceinline__ void wait_vmcnt() {
 // LDS store instructions).  One such load moves 64 chunks of 16 bytes, one
 // per lane, into 1 KB of contiguous LDS, so rows cannot be padded; instead
 // the 16-byte chunks of a row are permuted (chunk c of row r is stored at
-// position c ^ swz(r)), which makes both operand read patterns of the
-// forward pass bank-conflict free for d = 64 and 128:
-//   16 lanes reading 16 consecutive rows, same logical chunk (16-byte reads);
-//   64 lanes reading rows 4g + r, columns 16c + lane%16 (4-byte reads).
+// position c ^ SW::f(r)), chosen so that the operand reads of the kernel that
+// uses the tile are bank-conflict free for d = 64 and 128.
 // The lane -> chunk assignment is fixed per thread, so each lane's global
 // offset is computed once.  Rows at or beyond L arrive as zeros.
-template <int ROWS, int D, int NW>
+// Chunk permutation for DirectTile (a function of the row index, values in
+// [0, D/4)): chunk c of row r at c ^ (r mod 16) (d = 32: c ^ (r/2 mod 8)).
+// Conflict-free for 16-byte reads of 16 consecutive rows at one chunk
+// position and for 4-byte reads of rows {4g + r : g < 4} x 16 columns.
+template <int D> struct RowXor {
+    __device__ static constexpr int f(int row) { return D == 32 ? ((row >> 1) & 7) : (row & 15); }
+};
+
+template <int ROWS, int D, int NW, class SW = RowXor<D>>
 struct DirectTile {
     static constexpr int kCpr = D / 4;                  // chunks per row
     static constexpr int kWaveLoads = ROWS * kCpr / 64; // 1 KB loads per tile
@@ -107,9 +114,7 @@ struct DirectTile {
     static constexpr bool kEven = kWaveLoads % NW == 0;
     static_assert(ROWS * kCpr % 64 == 0, "tile must be a whole number of 1 KB loads");
 
-    __device__ static constexpr int swz(int row) {
-        return D == 32 ? ((row >> 1) & 7) : (row & 15);
-    }
+    __device__ static constexpr int swz(int row) { return SW::f(row); }
     // Float offset of logical element (row, col) inside the tile.
     __device__ static constexpr int at(int row, int col) {
         return row * D + 4 * ((col >> 2) ^ swz(row)) + (col & 3);

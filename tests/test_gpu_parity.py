@@ -246,3 +246,18 @@ def test_strict_separate_dq_fallback_sampled_heads(gpu_lib):
     heads = [(0, 0), (7, 3), (19, 15), (31, 8)]
     errs = compare(run_gpu(x), oracle_reference(x, heads=heads), "strict_f32", heads=heads)
     assert max(errs.values()) <= TOL["strict_f32"], errs
+
+
+@pytest.mark.parametrize("d", [32, 64])
+@pytest.mark.parametrize("padded", [False, True])
+def test_wide_key_tiles_ragged(gpu_lib, d, padded):
+    """Causal problems with ceil(L/128)*B*H >= 512 take the 128-key fused
+    backward (8 waves); a ragged L exercises its tail tiles, key padding its
+    masked waves."""
+    B, H, L = 4, 16, 1000
+    kl = [1000, 517, 128, 1] if padded else None
+    say("wide key tiles B%d H%d L%d d%d padded=%s" % (B, H, L, d, padded))
+    x = make_inputs(B, H, L, d, causal=True, seed=77 + d, key_len=kl)
+    errs = compare(run_gpu(x), oracle_reference(x), "strict_f32")
+    say("  errors %s" % {k: "%.2e" % v for k, v in errs.items()})
+    assert max(errs.values()) <= TOL["strict_f32"], errs
