@@ -99,6 +99,38 @@ __device__ __forceinline__ float bf16_to_f32(uint16_t b) {
     return __uint_as_float(((uint32_t)b) << 16);
 }
 
+// Word 3 of a gfx9-family buffer descriptor: 32-bit data format, every other
+// field zero (no swizzle, no index stride); untyped dword loads need a
+// non-zero data format.
+constexpr int kBufferWord3 = 0x00020000;
+
+// Descriptor of `bytes` bytes starting at `base` (stride 0: offsets are plain
+// byte offsets; loads at offsets >= bytes return zero).  Both arguments must
+// be the same on every lane of the wave; they are read from the first active
+// lane so that the descriptor lives in scalar registers.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void *base, int bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+    void *p = reinterpret_cast<void *>(((uint64_t)hi << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, __builtin_amdgcn_readfirstlane(bytes),
+                                             kBufferWord3);
+}
+
+__device__ __forceinline__ f32x4 buffer_load_f32x4(__amdgpu_buffer_rsrc_t r, int byte_offset) {
+    return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_offset, 0, 0));
+}
+
+// s_waitcnt immediate that waits until at most `N` vector-memory operations
+// of this wave are outstanding (gfx9 encoding: vmcnt bits 3:0 in bits 3:0 and
+// bits 5:4 in bits 15:14; expcnt and lgkmcnt left at their maxima, i.e. not
+// waited for).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
+}
+
 // Clamp a per-batch key length to [0, L]; L when no padding is given.
 __device__ __forceinline__ int key_limit(const int32_t *key_len, int b, int L) {
     if (key_len == nullptr) return L;

@@ -37,20 +37,22 @@ struct Bf16TileStager {
 
     u32x4 buf[kIters][4];
 
+    // Rows at or beyond L (and quads past the tile) read as zero: the loads go
+    // through a buffer descriptor covering only the tile's rows below L.
     __device__ __forceinline__ void load(const uint16_t *__restrict__ src, int row0, int L,
                                          int tid) {
+        const int rows = min(max(L - row0, 0), ROWS);
+        const auto rsrc = buffer_rsrc(src + (size_t)row0 * D, rows * D * 2);
 #pragma unroll
         for (int it = 0; it < kIters; ++it) {
             const int q = tid + it * NTHREADS;
             const int rg = q / kChunks;
             const int c8 = q % kChunks;
 #pragma unroll
-            for (int k = 0; k < 4; ++k) {
-                const int row = row0 + 4 * rg + k;
-                buf[it][k] = (q < kQuads && row < L)
-                    ? *reinterpret_cast<const u32x4 *>(src + (size_t)row * D + 8 * c8)
-                    : u32x4{0u, 0u, 0u, 0u};
-            }
+            for (int k = 0; k < 4; ++k)
+                buf[it][k] = __builtin_bit_cast(
+                    u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                               rsrc, ((4 * rg + k) * D + 8 * c8) * 2, 0, 0));
         }
     }
 
