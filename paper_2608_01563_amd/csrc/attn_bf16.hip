@@ -19,6 +19,7 @@
 #include "device_common.h"
 #include "launch.h"
 #include "tiles_bf16.h"
+#include "tiles_direct.h"
 
 namespace mg {
 namespace {
@@ -65,10 +66,15 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
     constexpr int NS = D / 16;    // 16-deep contraction steps over d
     constexpr int NCB = D / 32;   // 32-column blocks of d
     constexpr int NKB = kStream / 32;
-    using St = Bf16TileStager<kStream, D, kThreads>;
-    constexpr int LD = St::kLd;
+    constexpr int LD = Bf16Ld<D>::value;
+    // rows move as D/2 floats into LDS rows of LD/2 floats (the padded layout)
+    using Tile = RowDirectTile<kStream, D / 2, kWaves, LD / 2>;
+    static_assert(Tile::kEven, "the vmcnt waits below count kPerWave loads per fetch");
+    constexpr int NL = Tile::kPerWave;
     __shared__ __attribute__((aligned(16))) uint16_t Kr[kStream][LD];
     __shared__ __attribute__((aligned(16))) uint16_t Vr[kStream][LD];
+    auto kdst = reinterpret_cast<float (*)[LD / 2]>(&Kr[0][0]);
+    auto vdst = reinterpret_cast<float (*)[LD / 2]>(&Vr[0][0]);
 
     const int rank = blockIdx.x / BH;
     const int head = blockIdx.x - rank * BH;
@@ -78,15 +84,26 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int c = lane & 31;
     const int h = lane >> 5;
     const int jr = (lane & 15) >> 2, jc = 4 * (lane & 3);   // transpose-read block offsets
     const int q0 = qt * kFwdRows;
-    const int qi = q0 + 32 * (tid >> 6) + c;
+    const int qi = q0 + 32 * w + c;
 
     const int klen = key_limit(key_len, b, L);
     const int kend = causal ? min(klen, q0 + kFwdRows) : klen;
     const int ntiles = (kend + kStream - 1) / kStream;
+
+    // K and V tiles: direct-to-LDS row loads; the next K tile is fetched
+    // during P V, the next V tile during the next S = K Q^T.
+    const Tile tile;
+    const float *Kf = reinterpret_cast<const float *>(K + hoff);
+    const float *Vf = reinterpret_cast<const float *>(V + hoff);
+    if (ntiles > 0) {
+        tile.issue(kdst, Kf, 0, L, w, lane);
+        tile.issue(vdst, Vf, 0, L, w, lane);
+    }
 
     // B operand of S^T = K Q^T: lane holds Q[qi][16s + 8h + e].
     bf16x8 qreg[NS];
@@ -101,20 +118,9 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) oacc[cb] = zero16();
 
-    St kst, vst;
-    if (ntiles > 0) {
-        kst.load(K + hoff, 0, L, tid);
-        vst.load(V + hoff, 0, L, tid);
-    }
+    wait_vmcnt<NL>();   // K(0) landed (V(0) may still be in flight)
+    __syncthreads();
     for (int kt = 0; kt < ntiles; ++kt) {
-        __syncthreads();
-        kst.store(Kr, tid);
-        vst.store(Vr, tid);
-        __syncthreads();
-        if (kt + 1 < ntiles) {
-            kst.load(K + hoff, (kt + 1) * kStream, L, tid);
-            vst.load(V + hoff, (kt + 1) * kStream, L, tid);
-        }
 
         // S^T[32kb + 8a + 4h + r][qi] in sacc[kb] register 4a + r
         f32x16 sacc[NKB];
@@ -126,6 +132,9 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
                 sacc[kb] = mfma32x32x16bf16(load_bf16x8(&Kr[32 * kb + c][16 * s + 8 * h]),
                                             qreg[s], sacc[kb]);
         }
+        wait_vmcnt<0>();   // V(kt) landed
+        __syncthreads();   // every wave is done with K(kt) and sees V(kt)
+        if (kt + 1 < ntiles) tile.issue(kdst, Kf, (kt + 1) * kStream, L, w, lane);
         if (!POS_SCALE) {
 #pragma unroll
             for (int kb = 0; kb < NKB; ++kb) sacc[kb] *= scale_log2;
@@ -186,6 +195,10 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
                         load_tr_pair<LD>(Vr, r0, r0 + 8, 32 * cb + 16 * (c >> 4), jr, jc), pb,
                         oacc[cb]);
             }
+
+        wait_vmcnt<0>();   // K(kt+1) landed
+        __syncthreads();   // every wave is done with V(kt) and sees K(kt+1)
+        if (kt + 1 < ntiles) tile.issue(vdst, Vf, (kt + 1) * kStream, L, w, lane);
     }
 
     const float l = sum_xor32(l_run);

@@ -41,6 +41,7 @@
 
 #include "device_common.h"
 #include "launch.h"
+#include "tiles_direct.h"
 #include "tiles_f32.h"
 
 // Per-kernel launch configuration: waves per workgroup, minimum waves per
