@@ -257,12 +257,15 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
                     float scale_log2, int BH) {
     constexpr int NS = D / 32;
     constexpr int NC = D / 16;
-    using St = Bf16TileStager<kStream, D, kThreads>;
-    constexpr int LD = St::kLd;
-    __shared__ __attribute__((aligned(16))) uint16_t Qr[kStream][LD];
-    __shared__ __attribute__((aligned(16))) uint16_t Or[kStream][LD];
-    __shared__ __attribute__((aligned(16))) float lse2s[kStream];
-    __shared__ __attribute__((aligned(16))) float Ds[kStream];
+    constexpr int LD = Bf16Ld<D>::value;
+    // Q and dO rows move as D/2 floats into double-buffered padded LDS tiles
+    // by direct-to-LDS loads: the next tile is fetched during the whole
+    // current iteration, and one barrier per iteration suffices.
+    using Tile = RowDirectTile<kStream, D / 2, kWaves, LD / 2>;
+    __shared__ __attribute__((aligned(16))) uint16_t Qr[2][kStream][LD];
+    __shared__ __attribute__((aligned(16))) uint16_t Or[2][kStream][LD];
+    __shared__ __attribute__((aligned(16))) float lse2s[2][kStream];
+    __shared__ __attribute__((aligned(16))) float Ds[2][kStream];
 
     const int rank = blockIdx.x / BH;
     const int head = blockIdx.x - rank * BH;
@@ -272,11 +275,12 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int il = lane & 15;
     const int g = lane >> 4;
     const int jr = il >> 2, jc = 4 * (il & 3);   // transpose-read block offsets
     const int k0 = kt * kStatRows;
-    const int kj = k0 + 16 * (tid >> 6) + il;
+    const int kj = k0 + 16 * w + il;
 
     const int klen = key_limit(key_len, b, L);
     const int nq = (L + kStream - 1) / kStream;
@@ -294,31 +298,37 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
         dvacc[c] = zero4();
     }
 
-    St qst, ost;
+    const Tile tile;
+    const float *Qf = reinterpret_cast<const float *>(Q + hoff);
+    const float *Of = reinterpret_cast<const float *>(dO + hoff);
     float lse_pre = 0.f, d_pre = 0.f;
-    auto load_rows = [&](int qt) {
-        qst.load(Q + hoff, qt * kStream, L, tid);
-        ost.load(dO + hoff, qt * kStream, L, tid);
+    auto fetch = [&](int qt, int buf) {   // direct loads of Q, dO; LSE, D to registers
+        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Qr[buf][0][0]), Qf, qt * kStream, L, w,
+                   lane);
+        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Or[buf][0][0]), Of, qt * kStream, L, w,
+                   lane);
         if (tid < kStream) {
             const int row = qt * kStream + tid;
-            // natural log; scaled to base 2 at the LDS store so that nothing waits
-            // for this load before the next tile's rows are consumed
-            lse_pre = (row < L) ? LSE[(size_t)head * L + row] : 0.f;
+            lse_pre = (row < L) ? LSE[(size_t)head * L + row] : 0.f;   // natural log
             d_pre = (row < L) ? Dws[(size_t)head * L + row] : 0.f;
         }
     };
-    if (qstart < qstop) load_rows(qstart);
+    auto publish = [&](int buf) {   // LSE (base 2) and D of the fetched rows
+        if (tid < kStream) {
+            lse2s[buf][tid] = lse_pre * kLog2e;
+            Ds[buf][tid] = d_pre;
+        }
+    };
+    if (qstart < qstop) {
+        fetch(qstart, 0);
+        wait_vmcnt<0>();
+        publish(0);
+    }
+    __syncthreads();
 
     for (int qt = qstart; qt < qstop; ++qt) {
-        __syncthreads();
-        qst.store(Qr, tid);
-        ost.store(Or, tid);
-        if (tid < kStream) {
-            lse2s[tid] = lse_pre * kLog2e;
-            Ds[tid] = d_pre;
-        }
-        __syncthreads();
-        if (qt + 1 < qstop) load_rows(qt + 1);
+        const int cb = (qt - qstart) & 1;
+        if (qt + 1 < qstop) fetch(qt + 1, cb ^ 1);   // buffer cb^1 was freed by the last barrier
 
         f32x4 sacc[kBlk], pacc[kBlk];
 #pragma unroll
@@ -330,9 +340,9 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
         for (int s = 0; s < NS; ++s)
 #pragma unroll
             for (int ib = 0; ib < kBlk; ++ib) {
-                sacc[ib] = mfma16x16x32bf16(load_bf16x8(&Qr[16 * ib + il][32 * s + 8 * g]),
+                sacc[ib] = mfma16x16x32bf16(load_bf16x8(&Qr[cb][16 * ib + il][32 * s + 8 * g]),
                                             kreg[s], sacc[ib]);
-                pacc[ib] = mfma16x16x32bf16(load_bf16x8(&Or[16 * ib + il][32 * s + 8 * g]),
+                pacc[ib] = mfma16x16x32bf16(load_bf16x8(&Or[cb][16 * ib + il][32 * s + 8 * g]),
                                             vreg[s], pacc[ib]);
             }
 
@@ -340,8 +350,8 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
         const int thr = causal ? kj - ibase : -(1 << 30);
 #pragma unroll
         for (int ib = 0; ib < kBlk; ++ib) {
-            const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lse2s[16 * ib + 4 * g]);
-            const f32x4 dd = *reinterpret_cast<const f32x4 *>(&Ds[16 * ib + 4 * g]);
+            const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lse2s[cb][16 * ib + 4 * g]);
+            const f32x4 dd = *reinterpret_cast<const f32x4 *>(&Ds[cb][16 * ib + 4 * g]);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 float p = exp2_fast(fmaf(sacc[ib][r], scale_log2, -l2[r]));
@@ -359,12 +369,18 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
             const int r0 = 32 * t + 4 * g;
 #pragma unroll
             for (int c = 0; c < NC; ++c) {
-                dvacc[c] = mfma16x16x32bf16(load_tr_pair<LD>(Or, r0, r0 + 16, 16 * c, jr, jc),
-                                            pb, dvacc[c]);
-                dkacc[c] = mfma16x16x32bf16(load_tr_pair<LD>(Qr, r0, r0 + 16, 16 * c, jr, jc),
-                                            sb, dkacc[c]);
+                dvacc[c] = mfma16x16x32bf16(
+                    load_tr_pair<LD>(Or[cb], r0, r0 + 16, 16 * c, jr, jc), pb, dvacc[c]);
+                dkacc[c] = mfma16x16x32bf16(
+                    load_tr_pair<LD>(Qr[cb], r0, r0 + 16, 16 * c, jr, jc), sb, dkacc[c]);
             }
         }
+
+        if (qt + 1 < qstop) {
+            wait_vmcnt<0>();   // next Q/dO tile landed, its LSE/D in registers
+            publish(cb ^ 1);
+        }
+        __syncthreads();   // next tile visible; buffer cb free
     }
 
     if (kj < L) {
@@ -383,8 +399,9 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
 // Query-stationary, 32 queries per wave on 32x32x16 products (as the forward):
 // S^T = K Q^T and dP^T = V dO^T from row-major K and V tiles, then
 // dQ^T += K^T dS^T with dS^T straight from registers and K^T from transpose
-// reads of the row-major K tile.  KS keys per streamed tile (32 for d = 128,
-// which keeps the kernel within 256 registers).
+// reads of the row-major K tile.  KS keys per streamed tile; K and V tiles
+// are double-buffered in LDS and arrive by direct-to-LDS row loads, so the
+// next tile is fetched during the whole current iteration.
 template <int D, int KS>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
 void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
@@ -395,10 +412,12 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
     constexpr int NS = D / 16;
     constexpr int NCB = D / 32;
     constexpr int NKB = KS / 32;
-    using St = Bf16TileStager<KS, D, kThreads>;
-    constexpr int LD = St::kLd;
-    __shared__ __attribute__((aligned(16))) uint16_t Kr[KS][LD];
-    __shared__ __attribute__((aligned(16))) uint16_t Vr[KS][LD];
+    constexpr int LD = Bf16Ld<D>::value;
+    // K and V rows move as D/2 floats into double-buffered padded LDS tiles:
+    // the next tile is fetched during the whole current iteration.
+    using Tile = RowDirectTile<KS, D / 2, kWaves, LD / 2>;
+    __shared__ __attribute__((aligned(16))) uint16_t Kr[2][KS][LD];
+    __shared__ __attribute__((aligned(16))) uint16_t Vr[2][KS][LD];
 
     const int rank = blockIdx.x / BH;
     const int head = blockIdx.x - rank * BH;
@@ -408,11 +427,12 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int c = lane & 31;
     const int h = lane >> 5;
     const int jr = (lane & 15) >> 2, jc = 4 * (lane & 3);
     const int q0 = qt * kFwdRows;
-    const int qi = q0 + 32 * (tid >> 6) + c;
+    const int qi = q0 + 32 * w + c;
 
     const int klen = key_limit(key_len, b, L);
     const int kend = causal ? min(klen, q0 + kFwdRows) : klen;
@@ -433,20 +453,19 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) dqacc[cb] = zero16();
 
-    St kst, vst;
-    if (ntiles > 0) {
-        kst.load(K + hoff, 0, L, tid);
-        vst.load(V + hoff, 0, L, tid);
-    }
+    const Tile tile;
+    const float *Kf = reinterpret_cast<const float *>(K + hoff);
+    const float *Vf = reinterpret_cast<const float *>(V + hoff);
+    auto fetch = [&](int t, int buf) {
+        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Kr[buf][0][0]), Kf, t * KS, L, w, lane);
+        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Vr[buf][0][0]), Vf, t * KS, L, w, lane);
+    };
+    if (ntiles > 0) fetch(0, 0);
+    wait_vmcnt<0>();
+    __syncthreads();
     for (int kt = 0; kt < ntiles; ++kt) {
-        __syncthreads();
-        kst.store(Kr, tid);
-        vst.store(Vr, tid);
-        __syncthreads();
-        if (kt + 1 < ntiles) {
-            kst.load(K + hoff, (kt + 1) * KS, L, tid);
-            vst.load(V + hoff, (kt + 1) * KS, L, tid);
-        }
+        const int cb = kt & 1;
+        if (kt + 1 < ntiles) fetch(kt + 1, cb ^ 1);   // buffer cb^1 was freed by the last barrier
         const bool full = (kt + 1) * KS <= klen &&
                           (!causal || (kt + 1) * KS - 1 <= q0);
         const int j0 = kt * KS + 4 * h;
@@ -457,10 +476,10 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
             f32x16 sacc = zero16(), pacc = zero16();
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
-                sacc = mfma32x32x16bf16(load_bf16x8(&Kr[32 * kb + c][16 * s + 8 * h]), qreg[s],
-                                        sacc);
-                pacc = mfma32x32x16bf16(load_bf16x8(&Vr[32 * kb + c][16 * s + 8 * h]), oreg[s],
-                                        pacc);
+                sacc = mfma32x32x16bf16(load_bf16x8(&Kr[cb][32 * kb + c][16 * s + 8 * h]),
+                                        qreg[s], sacc);
+                pacc = mfma32x32x16bf16(load_bf16x8(&Vr[cb][32 * kb + c][16 * s + 8 * h]),
+                                        oreg[s], pacc);
             }
             // dS^T = P^T (dP^T - D), P^T = exp2(S^T * scale*log2e - LSE*log2e)
 #pragma unroll
@@ -474,12 +493,14 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
                 const bf16x8 sb = pack_bf16_half(pacc, t);
                 const int r0 = 32 * kb + 16 * t + 4 * h;
 #pragma unroll
-                for (int cb = 0; cb < NCB; ++cb)
-                    dqacc[cb] = mfma32x32x16bf16(
-                        load_tr_pair<LD>(Kr, r0, r0 + 8, 32 * cb + 16 * (c >> 4), jr, jc), sb,
-                        dqacc[cb]);
+                for (int cb2 = 0; cb2 < NCB; ++cb2)
+                    dqacc[cb2] = mfma32x32x16bf16(
+                        load_tr_pair<LD>(Kr[cb], r0, r0 + 8, 32 * cb2 + 16 * (c >> 4), jr, jc),
+                        sb, dqacc[cb2]);
             }
         }
+        wait_vmcnt<0>();   // next K/V tile landed
+        __syncthreads();   // it is visible; buffer cb is free
     }
 
     if (qi < L) {
@@ -559,7 +580,7 @@ hipError_t launch_bwd_dq_bf16(const AttnProblem &p, const uint16_t *Q, const uin
     switch (p.d) {
     case 32: attn_dq_bf16<32, 64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
     case 64: attn_dq_bf16<64, 64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
-    case 128: attn_dq_bf16<128, 32><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
+    case 128: attn_dq_bf16<128, 64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -1,5 +1,6 @@
-// tiles_bf16.h -- cooperative global->LDS staging of bf16 row tiles and the
-// LDS reads that feed bf16 MFMA operands.
+// tiles_bf16.h -- LDS layout of bf16 row tiles and the LDS reads that feed
+// bf16 MFMA operands (the tiles themselves arrive by the direct-to-LDS row
+// loads of tiles_direct.h).
 //
 // A streamed tile is stored row-major only.  Products that contract over the
 // head dimension read 8 consecutive d values of a row (one 16-byte read);
@@ -12,9 +13,8 @@
 //
 // Row stride (u16): the smallest padding for which both the 16-row 16-byte
 // reads and the 4-row transpose reads of a 16-lane group hit 16 distinct
-// 4-bank groups: d=32 -> 56, d=64 -> 72, d=128 -> 152.  Quads (4 rows x 8
-// columns) are numbered chunk-first so global reads and LDS writes of a wave
-// are contiguous along each row.  Rows at or beyond L are zero-filled.
+// 4-bank groups: d=32 -> 56, d=64 -> 72, d=128 -> 152.  Rows at or beyond L
+// arrive as zeros.
 #pragma once
 
 #include "device_common.h"
@@ -25,50 +25,6 @@ template <int D> struct Bf16Ld;
 template <> struct Bf16Ld<32> { static constexpr int value = 56; };
 template <> struct Bf16Ld<64> { static constexpr int value = 72; };
 template <> struct Bf16Ld<128> { static constexpr int value = 152; };
-
-template <int ROWS, int D, int NTHREADS>
-struct Bf16TileStager {
-    static constexpr int kLd = Bf16Ld<D>::value;
-    static constexpr int kGroups = ROWS / 4;          // row groups of 4
-    static constexpr int kChunks = D / 8;             // 8-column chunks per row
-    static constexpr int kQuads = kGroups * kChunks;
-    static constexpr int kIters = (kQuads + NTHREADS - 1) / NTHREADS;
-    static_assert(ROWS % 4 == 0 && D % 8 == 0, "tile shape");
-
-    u32x4 buf[kIters][4];
-
-    // Rows at or beyond L (and quads past the tile) read as zero: the loads go
-    // through a buffer descriptor covering only the tile's rows below L.
-    __device__ __forceinline__ void load(const uint16_t *__restrict__ src, int row0, int L,
-                                         int tid) {
-        const int rows = min(max(L - row0, 0), ROWS);
-        const auto rsrc = buffer_rsrc(src + (size_t)row0 * D, rows * D * 2);
-#pragma unroll
-        for (int it = 0; it < kIters; ++it) {
-            const int q = tid + it * NTHREADS;
-            const int rg = q / kChunks;
-            const int c8 = q % kChunks;
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-                buf[it][k] = __builtin_bit_cast(
-                    u32x4, __builtin_amdgcn_raw_buffer_load_b128(
-                               rsrc, ((4 * rg + k) * D + 8 * c8) * 2, 0, 0));
-        }
-    }
-
-    __device__ __forceinline__ void store(uint16_t (*R)[kLd], int tid) const {
-#pragma unroll
-        for (int it = 0; it < kIters; ++it) {
-            const int q = tid + it * NTHREADS;
-            if (q >= kQuads) continue;
-            const int rg = q / kChunks;
-            const int c8 = q % kChunks;
-#pragma unroll
-            for (int k = 0; k < 4; ++k)
-                *reinterpret_cast<u32x4 *>(&R[4 * rg + k][8 * c8]) = buf[it][k];
-        }
-    }
-};
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
