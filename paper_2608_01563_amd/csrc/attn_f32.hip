@@ -74,7 +74,10 @@ namespace mg {
 namespace {
 
 constexpr int kStream = 64;   // streamed rows per step
-constexpr int kFwdStream = 64;   // keys per streamed forward tile
+#ifndef MG_FWD_KS
+#define MG_FWD_KS 64
+#endif
+constexpr int kFwdStream = MG_FWD_KS;   // keys per streamed forward tile
 
 template <int NW_, int OCC_, bool DB_>
 struct Cfg {
