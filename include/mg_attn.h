@@ -24,6 +24,11 @@
  *                           paper's reduced-input mode uses f16 and keeps the
  *                           backward f32; this contract uses bf16 (f32
  *                           exponent range) for both passes.
+ *   MG_CONTRACT_ACCELERATED the paper's practical default: every tensor f32;
+ *                           the forward rounds Q, K, V (and P as the operand
+ *                           of P V) to f16, nearest even, and multiplies on
+ *                           f16 matrix cores with f32 accumulation; the
+ *                           backward is exactly the strict_f32 backward.
  *   LSE and the workspace are always f32.
  *
  * Layout: Q, K, V, O, dO, dQ, dK, dV are contiguous [B][H][L][d] with d
@@ -58,7 +63,8 @@ extern "C" {
 
 typedef enum {
     MG_CONTRACT_STRICT_F32 = 0,
-    MG_CONTRACT_FAST_BF16 = 1
+    MG_CONTRACT_FAST_BF16 = 1,
+    MG_CONTRACT_ACCELERATED = 2
 } mg_contract_t;
 
 typedef enum {
@@ -87,10 +93,10 @@ mg_status_t mg_attn_fwd(const void *Q, const void *K, const void *V,
 /*
  * Bytes of device workspace that mg_attn_bwd needs for these arguments:
  * f32 D = rowsum(dO o O), one per query row, rounded up to 256 bytes, plus,
- * for strict_f32 with d <= 64 when they fit in 1 GiB, one f32 dQ partial per
- * (key tile, query row): ceil(L/T) * B*H*L*d floats with key tiles of
- * T = 128 keys when causal and ceil(L/128)*B*H >= 512, else T = 64.  The partials let the dK/dV
- * kernel produce dQ without a second recompute.  Returns 0 when the
+ * for strict_f32 and accelerated with d <= 64 when they fit in 1 GiB, one f32
+ * dQ partial per (key tile, query row): ceil(L/T) * B*H*L*d floats with key
+ * tiles of T = 128 keys when causal and ceil(L/128)*B*H >= 512, else T = 64.
+ * The partials let the dK/dV kernel produce dQ without a second recompute.  Returns 0 when the
  * arguments are invalid.
  */
 size_t mg_attn_bwd_workspace_bytes(int B, int H, int L, int d, int causal,

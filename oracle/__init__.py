@@ -16,5 +16,6 @@ from .oracle import (  # noqa: F401
     oracle_backward,
     oracle_head_matrices,
     oracle_num_threads,
+    round_to_f16,
     ORACLE_SRC,
 )

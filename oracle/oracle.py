@@ -127,6 +127,16 @@ def oracle_backward(Q, K, V, dO, causal, scale, key_len=None, heads=None, lib=No
     return dQ, dK, dV, D
 
 
+def round_to_f16(x):
+    """Values of `x` rounded to IEEE binary16 (nearest even, overflow to inf),
+    returned as float64: the local input rounding of the paper's practical
+    default contract, whose eligible forward matrix inputs are rounded to f16
+    before an f32-accumulated product (Sec. 4.2, table of arithmetic
+    permissions).  numpy's float16 conversion is the IEEE operation."""
+    with np.errstate(over="ignore"):
+        return np.asarray(x, dtype=np.float64).astype(np.float16).astype(np.float64)
+
+
 def oracle_num_threads(lib=None):
     """Threads the oracle's parallel loops use."""
     return int((lib or load_oracle()).oracle_num_threads())

@@ -16,7 +16,8 @@ HEADER_PATH = os.path.join(os.path.dirname(HERE), "include", "mg_attn.h")
 
 STRICT_F32 = 0
 FAST_BF16 = 1
-CONTRACTS = {"strict_f32": STRICT_F32, "fast_bf16": FAST_BF16}
+ACCELERATED = 2   # f32 tensors; f16 forward matrix inputs; strict-f32 backward
+CONTRACTS = {"strict_f32": STRICT_F32, "fast_bf16": FAST_BF16, "accelerated": ACCELERATED}
 
 MG_OK = 0
 STATUS_NAMES = {0: "MG_OK", 1: "MG_ERR_INVALID_ARGUMENT", 2: "MG_ERR_UNSUPPORTED",
@@ -96,7 +97,7 @@ def _ptr(t):
 
 def _check_tensors(contract, ref, named):
     import torch
-    want = torch.float32 if contract == STRICT_F32 else torch.bfloat16
+    want = torch.bfloat16 if contract == FAST_BF16 else torch.float32
     for name, t in named:
         if not t.is_cuda:
             raise ValueError("%s must be a GPU tensor" % name)

@@ -1,0 +1,282 @@
+// attn_accel.hip -- forward attention under the paper's practical default
+// (accelerated) arithmetic contract, for gfx950.
+//
+// The paper's arithmetic permissions (Sec. 4.2, table of arithmetic
+// permissions): persistent tensors and outputs are f32; eligible forward
+// matrix and attention inputs may be rounded locally to f16 and multiplied
+// with f32 accumulation; backward matrices stay f32.  Here Q, K, V are f32 in
+// HBM, rounded to f16 (nearest even) as they enter the matrix cores, the
+// probabilities P are rounded to f16 as the operand of P V, and O and LSE are
+// written in f32.  The backward under this contract is the strict-f32 one.
+//
+// Structure as the bf16 forward (32 queries per wave on
+// v_mfma_f32_32x32x16_f16, K and V streamed 64 keys at a time through padded
+// row-major LDS tiles, V^T operands by 16-bit transpose reads), except that
+// the f32 tiles pass through registers to be rounded: the next K tile is
+// loaded while S of the current tile runs and written to LDS (as f16) after
+// the barrier that frees it; the next V tile likewise during P V.  K and V
+// staging never overlap in time, so one set of staging registers serves both.
+#include "device_common.h"
+#include "launch.h"
+#include "tiles_bf16.h"
+
+namespace mg {
+namespace {
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWaves = 4;
+constexpr int kThreads = 64 * kWaves;
+constexpr int kRows = 32 * kWaves;   // queries per workgroup
+constexpr int kKeys = 64;            // keys per streamed tile
+
+__device__ __forceinline__ f32x16 mfma32x32x16f16(f16x8 a, f16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+// Eight f32 -> eight f16 (nearest even).
+__device__ __forceinline__ f16x8 to_f16x8(f32x4 lo, f32x4 hi) {
+    f16x8 v;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        v[e] = (_Float16)lo[e];
+        v[4 + e] = (_Float16)hi[e];
+    }
+    return v;
+}
+
+// Accumulator registers [8t, 8t+8) of a 32x32 block rounded to f16, as the B
+// operand of a 32x32x16 product contracting over its rows.
+__device__ __forceinline__ f16x8 pack_f16_half(const f32x16 &a, int t) {
+    f16x8 v;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = (_Float16)a[8 * t + e];
+    return v;
+}
+
+// An f32 [ROWS][D] tile staged through registers and written to LDS as f16
+// (row stride LD in 16-bit units).  Chunk f (4 floats) of the tile is row
+// f / (D/4), columns 4*(f % (D/4)); consecutive threads take consecutive
+// chunks, so global reads are coalesced and LDS writes contiguous per row.
+// Rows at or beyond L read as zeros (buffer descriptor over rows below L).
+template <int ROWS, int D, int NT, int LD>
+struct F16ConvStager {
+    static constexpr int kCpr = D / 4;
+    static constexpr int kPer = ROWS * kCpr / NT;
+    static_assert(ROWS * kCpr % NT == 0, "tile must split evenly over the threads");
+    f32x4 buf[kPer];
+
+    __device__ __forceinline__ void load(const float *__restrict__ src, int row0, int L,
+                                         int tid) {
+        const int rows = min(max(L - row0, 0), ROWS);
+        const auto rsrc = buffer_rsrc(src + (size_t)row0 * D, rows * D * 4);
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) buf[u] = buffer_load_f32x4(rsrc, 16 * (tid + u * NT));
+    }
+    __device__ __forceinline__ void store(uint16_t (*dst)[LD], int tid) const {
+#pragma unroll
+        for (int u = 0; u < kPer; ++u) {
+            const int f = tid + u * NT;
+            const int r = f / kCpr;
+            const int c4 = f - r * kCpr;
+            f16x4 h;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) h[e] = (_Float16)buf[u][e];
+            *reinterpret_cast<uint64_t *>(&dst[r][4 * c4]) = __builtin_bit_cast(uint64_t, h);
+        }
+    }
+};
+
+template <int D, bool POS_SCALE>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
+void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
+                    const float *__restrict__ V, float *__restrict__ O, float *__restrict__ LSE,
+                    const int32_t *__restrict__ key_len, int H, int L, int causal,
+                    float scale_log2, int n_qtiles, int BH) {
+    constexpr int NS = D / 16;    // 16-deep contraction steps over d
+    constexpr int NCB = D / 32;   // 32-column blocks of d
+    constexpr int NKB = kKeys / 32;
+    constexpr int LD = Bf16Ld<D>::value;   // 16-bit row stride (bank-conflict free)
+    using St = F16ConvStager<kKeys, D, kThreads, LD>;
+    __shared__ __attribute__((aligned(16))) uint16_t Kr[kKeys][LD];
+    __shared__ __attribute__((aligned(16))) uint16_t Vr[kKeys][LD];
+
+    const int rank = blockIdx.x / BH;
+    const int head = blockIdx.x - rank * BH;
+    const int qt = causal ? (n_qtiles - 1 - rank) : rank;
+    const int b = head / H;
+    const size_t hoff = (size_t)head * L * D;
+    const float *Kh = K + hoff;
+    const float *Vh = V + hoff;
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int c = lane & 31;
+    const int h = lane >> 5;
+    const int jr = (lane & 15) >> 2, jc = 4 * (lane & 3);   // transpose-read block offsets
+    const int q0 = qt * kRows;
+    const int qi = q0 + 32 * w + c;
+
+    const int klen = key_limit(key_len, b, L);
+    const int kend = causal ? min(klen, q0 + kRows) : klen;
+    const int ntiles = (kend + kKeys - 1) / kKeys;
+
+    // B operand of S^T = K Q^T: lane holds f16(Q[qi][16s + 8h + e]).
+    f16x8 qreg[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        const float *qp = Q + hoff + (size_t)qi * D + 16 * s + 8 * h;
+        qreg[s] = (qi < L) ? to_f16x8(*reinterpret_cast<const f32x4 *>(qp),
+                                      *reinterpret_cast<const f32x4 *>(qp + 4))
+                           : f16x8{};
+    }
+
+    St st;
+    if (ntiles > 0) {
+        st.load(Kh, 0, L, tid);
+        st.store(Kr, tid);
+        st.load(Vh, 0, L, tid);
+        st.store(Vr, tid);
+        if (ntiles > 1) st.load(Kh, kKeys, L, tid);
+    }
+    __syncthreads();
+
+    // Running max in raw-score units when POS_SCALE, else in base-2 units.
+    float m_run = -INFINITY, l_run = 0.f;
+    f32x16 oacc[NCB];   // O^T[32cb + 8a + 4h + r][qi] in register 4a + r
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) oacc[cb] = zero16();
+
+    for (int kt = 0; kt < ntiles; ++kt) {
+        // S^T[32kb + 8a + 4h + r][qi] in sacc[kb] register 4a + r
+        f32x16 sacc[NKB];
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) {
+            sacc[kb] = zero16();
+#pragma unroll
+            for (int s = 0; s < NS; ++s)
+                sacc[kb] = mfma32x32x16f16(
+                    __builtin_bit_cast(f16x8, *reinterpret_cast<const u32x4 *>(
+                                                  &Kr[32 * kb + c][16 * s + 8 * h])),
+                    qreg[s], sacc[kb]);
+        }
+        __syncthreads();   // every wave is done with K(kt)
+        if (kt + 1 < ntiles) {
+            st.store(Kr, tid);                      // K(kt+1), loaded during S(kt)
+            st.load(Vh, (kt + 1) * kKeys, L, tid);  // V(kt+1), lands during P V(kt)
+        }
+        if (!POS_SCALE) {
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) sacc[kb] *= scale_log2;
+        }
+
+        // Masking only where the tile crosses the diagonal or the key length.
+        const bool full = (kt + 1) * kKeys <= klen && (!causal || (kt + 1) * kKeys - 1 <= q0);
+        if (!full) {
+            const int j0 = kt * kKeys + 4 * h;
+            const int thr = causal ? min(klen - j0, qi - j0 + 1) : klen - j0;
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    if (32 * kb + 8 * (v >> 2) + (v & 3) >= thr) sacc[kb][v] = -INFINITY;
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+            for (int v = 0; v < 16; v += 2) mx = fmaxf(mx, fmaxf(sacc[kb][v], sacc[kb][v + 1]));
+        mx = max_xor32(mx);
+        const float m_new = fmaxf(m_run, mx);
+        const float m2 = (m_new == -INFINITY) ? 0.f : (POS_SCALE ? m_new * scale_log2 : m_new);
+        if (__any(m_new != m_run)) {
+            const float m2_old = POS_SCALE ? m_run * scale_log2 : m_run;
+            const float alpha = exp2_fast(m2_old - m2);
+            l_run *= alpha;
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) oacc[cb] *= alpha;
+        }
+        m_run = m_new;
+        float psum = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const float p = POS_SCALE ? exp2_fast(fmaf(sacc[kb][v], scale_log2, -m2))
+                                          : exp2_fast(sacc[kb][v] - m2);
+                sacc[kb][v] = p;
+                psum += p;
+            }
+        l_run += psum;
+
+        // O^T[32cb + .][qi] += sum_j V^T[32cb + c'][j] P^T[j][qi], 16 keys per step
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                const f16x8 pb = pack_f16_half(sacc[kb], t);
+                const int r0 = 32 * kb + 16 * t + 4 * h;
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb)
+                    oacc[cb] = mfma32x32x16f16(
+                        __builtin_bit_cast(f16x8, load_tr_pair<LD>(Vr, r0, r0 + 8,
+                                                                   32 * cb + 16 * (c >> 4), jr, jc)),
+                        pb, oacc[cb]);
+            }
+
+        __syncthreads();   // every wave is done with V(kt); K(kt+1) is visible
+        if (kt + 1 < ntiles) {
+            st.store(Vr, tid);                                       // V(kt+1)
+            if (kt + 2 < ntiles) st.load(Kh, (kt + 2) * kKeys, L, tid);   // K(kt+2)
+        }
+        // V(kt+1) becomes visible at the first barrier of the next iteration,
+        // before P V reads it
+    }
+
+    const float l = sum_xor32(l_run);
+    if (qi < L) {
+        const float inv = (l > 0.f) ? 1.f / l : 0.f;
+        float *orow = O + hoff + (size_t)qi * D;
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+            for (int a = 0; a < 4; ++a)
+                *reinterpret_cast<f32x4 *>(orow + 32 * cb + 8 * a + 4 * h) =
+                    f32x4{oacc[cb][4 * a], oacc[cb][4 * a + 1], oacc[cb][4 * a + 2],
+                          oacc[cb][4 * a + 3]} * inv;
+        if (h == 0) {
+            const float m2 = POS_SCALE ? m_run * scale_log2 : m_run;
+            LSE[(size_t)head * L + qi] = (l > 0.f) ? (m2 + log2f(l)) * kLn2 : -INFINITY;
+        }
+    }
+}
+
+inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+}  // namespace
+
+hipError_t launch_fwd_accel(const AttnProblem &p, const float *Q, const float *K,
+                            const float *V, float *O, float *LSE, hipStream_t s) {
+    const int BH = p.B * p.H;
+    const int nqt = cdiv(p.L, kRows);
+    const dim3 grid(nqt * BH), block(kThreads);
+    const float sl2 = p.scale * kLog2e;
+#define MG_FWD_ACCEL(DD)                                                                     \
+    (p.scale > 0.f                                                                          \
+         ? (attn_fwd_accel<DD, true><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, \
+                                                            p.L, p.causal, sl2, nqt, BH))     \
+         : (attn_fwd_accel<DD, false><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len,     \
+                                                             p.H, p.L, p.causal, sl2, nqt, BH)))
+    switch (p.d) {
+    case 32: MG_FWD_ACCEL(32); break;
+    case 64: MG_FWD_ACCEL(64); break;
+    case 128: MG_FWD_ACCEL(128); break;
+    default: return hipErrorInvalidValue;
+    }
+#undef MG_FWD_ACCEL
+    return hipGetLastError();
+}
+
+}  // namespace mg

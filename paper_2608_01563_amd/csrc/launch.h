@@ -25,6 +25,11 @@ hipError_t launch_fwd_f32(const AttnProblem &p, const float *Q, const float *K,
 hipError_t launch_fwd_bf16(const AttnProblem &p, const uint16_t *Q, const uint16_t *K,
                            const uint16_t *V, uint16_t *O, float *LSE, hipStream_t s);
 
+// Forward under the accelerated contract: f32 Q, K, V, O, LSE; Q, K, V and
+// P rounded to f16 as matrix-core inputs, f32 accumulation.
+hipError_t launch_fwd_accel(const AttnProblem &p, const float *Q, const float *K,
+                            const float *V, float *O, float *LSE, hipStream_t s);
+
 // Backward step 1: D_i = sum_k dO_ik O_ik (f32 out, one per row).
 hipError_t launch_bwd_rowdot_f32(const AttnProblem &p, const float *O, const float *dO,
                                  float *Dws, hipStream_t s);

@@ -41,7 +41,8 @@ mg_status_t ok() {
 constexpr int64_t kMaxElems = INT32_MAX;
 
 mg_status_t check_shape(int B, int H, int L, int d, float scale, mg_contract_t contract) {
-    if (contract != MG_CONTRACT_STRICT_F32 && contract != MG_CONTRACT_FAST_BF16)
+    if (contract != MG_CONTRACT_STRICT_F32 && contract != MG_CONTRACT_FAST_BF16 &&
+        contract != MG_CONTRACT_ACCELERATED)
         return fail(MG_ERR_INVALID_ARGUMENT, "unknown contract %d", (int)contract);
     if (B < 1 || H < 1 || L < 1 || d < 1)
         return fail(MG_ERR_INVALID_ARGUMENT, "sizes must be >= 1 (B=%d H=%d L=%d d=%d)", B, H,
@@ -166,8 +167,9 @@ const char *kernel_name(const char *stage, mg_contract_t c, int d) {
     static std::mutex mu;
     static std::map<std::string, std::string> names;
     char buf[96];
-    snprintf(buf, sizeof buf, "%s_%s_d%d", stage, c == MG_CONTRACT_STRICT_F32 ? "f32" : "bf16",
-             d);
+    const char *suffix = c == MG_CONTRACT_STRICT_F32 ? "f32"
+                         : c == MG_CONTRACT_FAST_BF16 ? "bf16" : "accel";
+    snprintf(buf, sizeof buf, "%s_%s_d%d", stage, suffix, d);
     std::lock_guard<std::mutex> g(mu);
     auto it = names.find(buf);
     if (it == names.end()) it = names.emplace(buf, buf).first;
@@ -175,6 +177,12 @@ const char *kernel_name(const char *stage, mg_contract_t c, int d) {
 }
 
 size_t round256(size_t n) { return (n + 255) / 256 * 256; }
+
+// The accelerated contract's backward is the strict-f32 backward (its
+// tensors are f32 and its backward matrices stay f32).
+mg_contract_t backward_contract(mg_contract_t c) {
+    return c == MG_CONTRACT_ACCELERATED ? MG_CONTRACT_STRICT_F32 : c;
+}
 
 // Strict f32 with d <= 64 fuses dQ into the key-stationary kernel when its
 // per-key-tile partials fit under this many bytes; otherwise (and for bf16)
@@ -194,6 +202,7 @@ bool use_fused_dq(int B, int H, int L, int d, int causal, mg_contract_t contract
 
 // Layout: D (f32 per row) first, then the dQ partials when fused.
 size_t workspace_bytes(int B, int H, int L, int d, int causal, mg_contract_t contract) {
+    contract = backward_contract(contract);
     size_t n = round256((size_t)B * H * L * sizeof(float));
     if (use_fused_dq(B, H, L, d, causal, contract)) n += dq_partial_bytes(B, H, L, d, causal);
     return n;
@@ -214,6 +223,11 @@ mg_status_t mg_attn_fwd(const void *Q, const void *K, const void *V, void *O, fl
         MG_TRY(run_kernel(kernel_name("attn_fwd", contract, d), stream, [&] {
             return mg::launch_fwd_f32(p, (const float *)Q, (const float *)K, (const float *)V,
                                       (float *)O, LSE, stream);
+        }));
+    } else if (contract == MG_CONTRACT_ACCELERATED) {
+        MG_TRY(run_kernel(kernel_name("attn_fwd", contract, d), stream, [&] {
+            return mg::launch_fwd_accel(p, (const float *)Q, (const float *)K, (const float *)V,
+                                        (float *)O, LSE, stream);
         }));
     } else {
         MG_TRY(run_kernel(kernel_name("attn_fwd", contract, d), stream, [&] {
@@ -248,6 +262,7 @@ mg_status_t mg_attn_bwd(const void *Q, const void *K, const void *V, const void 
     MG_TRY(check_key_len(key_len));
     const mg::AttnProblem p{B, H, L, d, causal ? 1 : 0, scale, key_len};
     float *Dws = (float *)workspace;
+    contract = backward_contract(contract);
     if (contract == MG_CONTRACT_STRICT_F32) {
         const float *q = (const float *)Q, *k = (const float *)K, *v = (const float *)V;
         const float *o = (const float *)O, *go = (const float *)dO;

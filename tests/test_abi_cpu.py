@@ -65,6 +65,10 @@ def test_workspace_query(lib):
     assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 48, 0, 0) == 0     # unsupported d
     assert mg.mg_attn_bwd_workspace_bytes(0, 1, 3, 32, 0, 0) == 0     # bad size
     assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 32, 0, 7) == 0     # bad contract
+    # the accelerated contract's backward is the strict one: same workspace
+    for args in ((8, 8, 1024, 64, 1), (8, 8, 1024, 64, 0), (8, 8, 1024, 128, 1),
+                 (4, 4, 256, 64, 1), (1, 1, 3, 32, 0)):
+        assert mg.mg_attn_bwd_workspace_bytes(*args, 2) == mg.mg_attn_bwd_workspace_bytes(*args, 0)
 
 
 def _fwd(lib, ptrs, B=1, H=1, L=8, d=64, scale=0.125, contract=0):

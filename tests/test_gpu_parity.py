@@ -11,7 +11,8 @@ import math
 import numpy as np
 import pytest
 
-from gpu_util import TOL, compare, oracle_reference, run_gpu, say, to_device, key_len_device
+from gpu_util import (TOL, TOL_ACCEL_ROUNDED, compare, key_len_device, normwise_error,
+                      oracle_reference, run_gpu, say, to_device)
 from workloads import WORKLOADS, make_inputs, workload_inputs
 
 pytestmark = pytest.mark.gpu
@@ -261,3 +262,74 @@ def test_wide_key_tiles_ragged(gpu_lib, d, padded):
     errs = compare(run_gpu(x), oracle_reference(x), "strict_f32")
     say("  errors %s" % {k: "%.2e" % v for k, v in errs.items()})
     assert max(errs.values()) <= TOL["strict_f32"], errs
+
+
+# ---- accelerated contract: f32 tensors, f16 forward matrix inputs, strict backward
+
+ACCEL_SMALL = [(L, d, mode) for L in (1, 17, 65, 200) for d in (32, 64, 128)
+               for mode in ("causal", "full", "padded")]
+
+
+def accel_check(x):
+    from oracle import oracle_forward, round_to_f16
+    got = run_gpu(x)
+    Or, Lr = oracle_forward(round_to_f16(x.Q), round_to_f16(x.K), round_to_f16(x.V), x.causal,
+                            x.scale, key_len=x.key_len)
+    e_o, e_l = normwise_error(got["O"], Or), normwise_error(got["LSE"], Lr)
+    assert e_o <= TOL_ACCEL_ROUNDED["O"] and e_l <= TOL_ACCEL_ROUNDED["LSE"], (e_o, e_l)
+    errs = compare(got, oracle_reference(x), "accelerated")
+    assert max(errs.values()) <= TOL["accelerated"], errs
+    return e_o, e_l, errs
+
+
+@pytest.mark.parametrize("L,d,mode", ACCEL_SMALL)
+def test_small_shapes_accelerated(gpu_lib, L, d, mode):
+    say("small accelerated L=%d d=%d %s" % (L, d, mode))
+    accel_check(small_inputs(L, d, mode, contract="accelerated"))
+
+
+def test_workload6_accelerated(gpu_lib):
+    w = WORKLOADS[6]
+    say("workload 6 %s" % w.name)
+    e_o, e_l, errs = accel_check(workload_inputs(6))
+    say("  rounded-input O %.2e LSE %.2e; exact %s" % (e_o, e_l,
+                                                        {k: "%.2e" % v for k, v in errs.items()}))
+
+
+def test_accelerated_backward_is_the_strict_backward(gpu_lib):
+    """Given the same O and LSE, the accelerated backward is the strict one:
+    bitwise equal outputs, and the oracle's O/LSE in gives strict parity."""
+    import torch
+    import paper_2608_01563_amd as mg
+    say("accelerated backward vs strict backward")
+    x = workload_inputs(2)
+    ref = oracle_reference(x)
+    got = run_gpu(x, O_in=ref["O"], LSE_in=ref["LSE"])
+    errs = compare(got, ref, "strict_f32", names=("dQ", "dK", "dV"))
+    assert max(errs.values()) <= TOL["strict_f32"], errs
+    Q, K, V, dO = (to_device(x, n) for n in ("Q", "K", "V", "dO"))
+    O = torch.from_numpy(ref["O"].astype(np.float32)).cuda()
+    LSE = torch.from_numpy(ref["LSE"].astype(np.float32)).cuda()
+    ga = mg.attention_backward(Q, K, V, O, LSE, dO, causal=True, scale=x.scale,
+                               contract="accelerated")
+    gs = mg.attention_backward(Q, K, V, O, LSE, dO, causal=True, scale=x.scale,
+                               contract="strict_f32")
+    for a, b in zip(ga, gs):
+        assert torch.equal(a, b)
+
+
+def test_bitwise_pins_accelerated(gpu_lib):
+    import torch
+    import paper_2608_01563_amd as mg
+    from oracle import round_to_f16
+    say("bitwise pins accelerated")
+    x = make_inputs(2, 4, 130, 64, causal=True, contract="accelerated", seed=21)
+    Q, K, V = (to_device(x, n) for n in ("Q", "K", "V"))
+    O, LSE = mg.attention_forward(Q, K, V, causal=True, scale=x.scale, contract="accelerated")
+    # causal row 0 attends only to key 0 with probability exactly 1, so O is
+    # the f16-rounded V row, exactly
+    v0 = torch.from_numpy(round_to_f16(x.V[:, :, 0, :]).astype(np.float32)).cuda()
+    assert torch.equal(O[:, :, 0, :], v0)
+    # run-to-run determinism
+    O2, LSE2 = mg.attention_forward(Q, K, V, causal=True, scale=x.scale, contract="accelerated")
+    assert torch.equal(O, O2) and torch.equal(LSE, LSE2)

@@ -13,7 +13,7 @@ import numpy as np
 import pytest
 import scipy.special
 
-from oracle import oracle_forward, oracle_backward, oracle_head_matrices
+from oracle import oracle_forward, oracle_backward, oracle_head_matrices, round_to_f16
 
 RNG = np.random.default_rng(12345)
 
@@ -329,3 +329,54 @@ def test_bwd_linear_in_upstream_gradient_and_masked_batch():
         assert np.array_equal(2 * a, b)
     for g in g1[:3]:
         assert np.all(g[0] == 0.0)
+
+
+# ---- f16 input rounding of the accelerated contract (Sec. 4.2 permissions)
+
+def test_round_to_f16_closed_forms():
+    """IEEE binary16: 10 fraction bits, ties to even, max finite 65504,
+    smallest subnormal 2^-24."""
+    cases = [
+        (1.0 + 2.0 ** -11, 1.0),                  # halfway, ties to the even 1.0
+        (1.0 + 3 * 2.0 ** -11, 1.0 + 2.0 ** -9),  # halfway, ties to the even neighbour
+        (1.0 + 2.0 ** -10, 1.0 + 2.0 ** -10),     # representable
+        (-2049.0, -2048.0),                       # spacing 2 above 2048, tie to even
+        (65504.0, 65504.0),                       # largest finite
+        (65519.0, 65504.0),                       # below the overflow midpoint
+        (65520.0, math.inf),                      # overflow midpoint rounds to inf
+        (2.0 ** -24, 2.0 ** -24),                 # smallest subnormal
+        (2.0 ** -25, 0.0),                        # half of it ties to zero
+        (3 * 2.0 ** -25, 2.0 ** -23),             # 1.5 subnormal steps -> 2 (even)
+        (1.0 / 3.0, 1365.0 / 4096.0),             # 0.0101010101|01... -> 1365/4096
+    ]
+    got = round_to_f16(np.array([c[0] for c in cases]))
+    assert np.array_equal(got, np.array([c[1] for c in cases]))
+
+
+def test_round_to_f16_error_bound_and_identity():
+    rng = np.random.default_rng(11)
+    x = rng.standard_normal(100000) * np.exp(rng.uniform(-8, 8, 100000))
+    r = round_to_f16(x)
+    normal = np.abs(x) >= 2.0 ** -14
+    # relative error at most half an ulp: 2^-11 for normal numbers
+    assert np.all(np.abs(r[normal] - x[normal]) <= 2.0 ** -11 * np.abs(x[normal]))
+    # values already in binary16 are fixed points; rounding is idempotent
+    assert np.array_equal(round_to_f16(r), r)
+    ints = np.arange(-2048, 2049, dtype=np.float64)
+    assert np.array_equal(round_to_f16(ints), ints)
+
+
+def test_round_to_f16_inputs_change_attention_only_through_rounding():
+    """The oracle on f16-rounded inputs equals the oracle on inputs that were
+    f16-representable to begin with, and differs from the unrounded result by
+    about the rounding size."""
+    B, H, L, d = 1, 2, 9, 8
+    Q, K, V = (round_to_f16(rand(B, H, L, d)) for _ in range(3))
+    O1, L1 = oracle_forward(round_to_f16(Q), round_to_f16(K), round_to_f16(V), True, 0.5)
+    O0, L0 = oracle_forward(Q, K, V, True, 0.5)
+    assert np.array_equal(O1, O0) and np.array_equal(L1, L0)
+    Qf, Kf, Vf = (rand(B, H, L, d) for _ in range(3))
+    Or, _ = oracle_forward(round_to_f16(Qf), round_to_f16(Kf), round_to_f16(Vf), True, 0.5)
+    Oe, _ = oracle_forward(Qf, Kf, Vf, True, 0.5)
+    err = normwise(Or, Oe)
+    assert 1e-6 < err < 2e-2
