@@ -5,6 +5,7 @@ include/mg_attn.h); this package is its ctypes binding.  PyTorch is used only
 for device memory and streams.
 """
 from ._binding import (  # noqa: F401
+    ACCELERATED,
     FAST_BF16,
     HEADER_PATH,
     LIB_PATH,
