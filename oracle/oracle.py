@@ -34,12 +34,12 @@ def _bind(lib):
     ip = ctypes.POINTER(ctypes.c_int)
     up = ctypes.POINTER(ctypes.c_ubyte)
     ci, cd = ctypes.c_int, ctypes.c_double
-    lib.oracle_attn_fwd.argtypes = [dp, dp, dp, ip, ci, ci, ci, ci, ci, cd, up, dp, dp]
+    lib.oracle_attn_fwd.argtypes = [dp, dp, dp, ip, ci, ci, ci, ci, ci, ci, cd, up, dp, dp]
     lib.oracle_attn_fwd.restype = ci
-    lib.oracle_attn_bwd.argtypes = [dp, dp, dp, dp, ip, ci, ci, ci, ci, ci, cd, up,
+    lib.oracle_attn_bwd.argtypes = [dp, dp, dp, dp, ip, ci, ci, ci, ci, ci, ci, cd, up,
                                     dp, dp, dp, dp]
     lib.oracle_attn_bwd.restype = ci
-    lib.oracle_head_matrices.argtypes = [dp, dp, dp, dp, ip, ci, ci, ci, ci, ci, cd,
+    lib.oracle_head_matrices.argtypes = [dp, dp, dp, dp, ip, ci, ci, ci, ci, ci, ci, cd,
                                          ci, ci, dp, dp, dp]
     lib.oracle_head_matrices.restype = ci
     lib.oracle_num_threads.argtypes = []
@@ -70,10 +70,13 @@ def _ptr(a, ctype=ctypes.c_double):
 
 
 def _prep(Q, K, V, key_len, heads):
+    """Q [B,H,Lq,d]; K, V [B,H,Lk,d] (Lq == Lk for self-attention)."""
     Q, K, V = _f64(Q), _f64(K), _f64(V)
-    if Q.ndim != 4 or K.shape != Q.shape or V.shape != Q.shape:
-        raise ValueError("Q, K, V must share one [B,H,L,d] shape")
-    B, H, L, d = Q.shape
+    if Q.ndim != 4 or K.ndim != 4 or V.shape != K.shape or \
+            K.shape[:2] != Q.shape[:2] or K.shape[3] != Q.shape[3]:
+        raise ValueError("Q [B,H,Lq,d], K and V [B,H,Lk,d] expected")
+    B, H, Lq, d = Q.shape
+    Lk = K.shape[2]
     kl = None
     if key_len is not None:
         kl = np.ascontiguousarray(np.asarray(key_len, dtype=np.int32))
@@ -84,21 +87,23 @@ def _prep(Q, K, V, key_len, heads):
         mask = np.zeros(B * H, dtype=np.uint8)
         for b, h in heads:
             mask[b * H + h] = 1
-    return Q, K, V, kl, mask, (B, H, L, d)
+    return Q, K, V, kl, mask, (B, H, Lq, Lk, d)
 
 
 def oracle_forward(Q, K, V, causal, scale, key_len=None, heads=None, lib=None):
-    """O [B,H,L,d] and LSE [B,H,L] (natural log) in float64.
+    """O [B,H,Lq,d] and LSE [B,H,Lq] (natural log) in float64.  K and V may
+    have their own length Lk (cross-attention); the causal mask is then
+    bottom-right aligned (row i sees keys j <= i + Lk - Lq).
 
     heads: optional iterable of (b, h) to compute; other heads are NaN.
     """
     lib = lib or load_oracle()
-    Q, K, V, kl, mask, (B, H, L, d) = _prep(Q, K, V, key_len, heads)
-    O = np.full((B, H, L, d), np.nan)
-    LSE = np.full((B, H, L), np.nan)
+    Q, K, V, kl, mask, (B, H, Lq, Lk, d) = _prep(Q, K, V, key_len, heads)
+    O = np.full((B, H, Lq, d), np.nan)
+    LSE = np.full((B, H, Lq), np.nan)
     rc = lib.oracle_attn_fwd(_ptr(Q), _ptr(K), _ptr(V),
                              None if kl is None else _ptr(kl, ctypes.c_int),
-                             B, H, L, d, int(bool(causal)), float(scale),
+                             B, H, Lq, Lk, d, int(bool(causal)), float(scale),
                              None if mask is None else _ptr(mask, ctypes.c_ubyte),
                              _ptr(O), _ptr(LSE))
     if rc != 0:
@@ -107,19 +112,20 @@ def oracle_forward(Q, K, V, causal, scale, key_len=None, heads=None, lib=None):
 
 
 def oracle_backward(Q, K, V, dO, causal, scale, key_len=None, heads=None, lib=None):
-    """dQ, dK, dV [B,H,L,d] and D [B,H,L] in float64 (recomputing O and LSE)."""
+    """dQ [B,H,Lq,d], dK, dV [B,H,Lk,d] and D [B,H,Lq] in float64
+    (recomputing O and LSE)."""
     lib = lib or load_oracle()
-    Q, K, V, kl, mask, (B, H, L, d) = _prep(Q, K, V, key_len, heads)
+    Q, K, V, kl, mask, (B, H, Lq, Lk, d) = _prep(Q, K, V, key_len, heads)
     dO = _f64(dO)
     if dO.shape != Q.shape:
         raise ValueError("dO must have the shape of Q")
-    dQ = np.full((B, H, L, d), np.nan)
-    dK = np.full((B, H, L, d), np.nan)
-    dV = np.full((B, H, L, d), np.nan)
-    D = np.full((B, H, L), np.nan)
+    dQ = np.full((B, H, Lq, d), np.nan)
+    dK = np.full((B, H, Lk, d), np.nan)
+    dV = np.full((B, H, Lk, d), np.nan)
+    D = np.full((B, H, Lq), np.nan)
     rc = lib.oracle_attn_bwd(_ptr(Q), _ptr(K), _ptr(V), _ptr(dO),
                              None if kl is None else _ptr(kl, ctypes.c_int),
-                             B, H, L, d, int(bool(causal)), float(scale),
+                             B, H, Lq, Lk, d, int(bool(causal)), float(scale),
                              None if mask is None else _ptr(mask, ctypes.c_ubyte),
                              _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(D))
     if rc != 0:
@@ -143,16 +149,16 @@ def oracle_num_threads(lib=None):
 
 
 def oracle_head_matrices(Q, K, V, dO, causal, scale, b, h, key_len=None, lib=None):
-    """P, dS [L,L] and Dalt [L] (= sum_j P_ij dP_ij) of head (b, h)."""
+    """P, dS [Lq,Lk] and Dalt [Lq] (= sum_j P_ij dP_ij) of head (b, h)."""
     lib = lib or load_oracle()
-    Q, K, V, kl, _, (B, H, L, d) = _prep(Q, K, V, key_len, None)
+    Q, K, V, kl, _, (B, H, Lq, Lk, d) = _prep(Q, K, V, key_len, None)
     dO = _f64(dO)
-    P = np.empty((L, L))
-    dS = np.empty((L, L))
-    Dalt = np.empty(L)
+    P = np.empty((Lq, Lk))
+    dS = np.empty((Lq, Lk))
+    Dalt = np.empty(Lq)
     rc = lib.oracle_head_matrices(_ptr(Q), _ptr(K), _ptr(V), _ptr(dO),
                                   None if kl is None else _ptr(kl, ctypes.c_int),
-                                  B, H, L, d, int(bool(causal)), float(scale),
+                                  B, H, Lq, Lk, d, int(bool(causal)), float(scale),
                                   int(b), int(h), _ptr(P), _ptr(dS), _ptr(Dalt))
     if rc != 0:
         raise RuntimeError("oracle_head_matrices failed")

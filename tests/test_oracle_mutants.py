@@ -14,10 +14,14 @@ import oracle.oracle as oracle_mod
 import test_oracle_pins as pins
 
 MUTANTS = {
-    "causal_off_by_one": ("return (!causal || j <= i) && j < klen;",
-                          "return (!causal || j < i) && j < klen;"),
-    "padding_off_by_one": ("return (!causal || j <= i) && j < klen;",
-                           "return (!causal || j <= i) && j <= klen;"),
+    "causal_off_by_one": ("return (!causal || j <= i + off) && j < klen;",
+                          "return (!causal || j < i + off) && j < klen;"),
+    "padding_off_by_one": ("return (!causal || j <= i + off) && j < klen;",
+                           "return (!causal || j <= i + off) && j <= klen;"),
+    "causal_top_left_for_cross": ("return (!causal || j <= i + off) && j < klen;",
+                                  "return (!causal || j <= i) && j < klen;"),
+    "cross_offset_sign": ("const int off = Lk - Lq;\n    for (int i = 0; i < Lq; ++i) {",
+                          "const int off = Lq - Lk;\n    for (int i = 0; i < Lq; ++i) {"),
     "fwd_scores_unscaled": ("S[j] = scale * dot(q, K + (size_t)j * d, d);",
                             "S[j] = dot(q, K + (size_t)j * d, d);"),
     "lse_base_two": ("LSE[i] = m + log(sum);", "LSE[i] = m + log2(sum);"),
@@ -34,7 +38,8 @@ MUTANTS = {
     "dP_wrong_operand": ("double dPij = dot(go, vj, d);", "double dPij = dot(go, kj, d);"),
     "bwd_probs_unscaled": ("double Pij = exp(scale * dot(q, kj, d) - LSE[i]);",
                            "double Pij = exp(dot(q, kj, d) - LSE[i]);"),
-    "key_len_batch_index": ("key_limit(key_len, bh / H, L)", "key_limit(key_len, bh % H, L)"),
+    "key_len_batch_index": ("key_limit(key_len, bh / H, Lk)", "key_limit(key_len, bh % H, Lk)"),
+    "key_len_clamped_to_Lq": ("key_limit(key_len, bh / H, Lk)", "key_limit(key_len, bh / H, Lq)"),
 }
 
 PINS = [
@@ -53,6 +58,10 @@ PINS = [
     lambda: pins.test_fwd_bwd_match_torch_autograd_f64(False, True, 12, 4),
     pins.test_bwd_invariants,
     pins.test_bwd_single_key_special_case,
+    pins.test_cross_causal_is_the_bottom_rows_of_square_causal,
+    pins.test_cross_single_key,
+    lambda: pins.test_cross_matches_torch_autograd_f64(12, 30, False, True),
+    lambda: pins.test_cross_central_finite_differences(3, 5, True, False),
 ]
 
 

@@ -236,13 +236,16 @@ def test_bwd_central_finite_differences(L, d, causal, padded):
 
 
 def _torch_reference(Q, K, V, dO, causal, scale, kl):
+    """Unfused f64 attention by torch autograd; Q [B,H,Lq,d], K, V [B,H,Lk,d],
+    causal mask bottom-right aligned (the usual lower triangle when Lq == Lk)."""
     import torch
-    B, H, L, d = Q.shape
+    B, H, Lq, d = Q.shape
+    Lk = K.shape[2]
     q, k, v = (torch.tensor(x, dtype=torch.float64, requires_grad=True) for x in (Q, K, V))
     S = scale * torch.matmul(q, k.transpose(-1, -2))
-    mask = torch.ones(B, 1, L, L, dtype=torch.bool)
+    mask = torch.ones(B, 1, Lq, Lk, dtype=torch.bool)
     if causal:
-        mask &= torch.ones(L, L, dtype=torch.bool).tril()
+        mask &= torch.ones(Lq, Lk, dtype=torch.bool).tril(diagonal=Lk - Lq)
     if kl is not None:
         for b in range(B):
             mask[b, :, :, int(kl[b]):] = False
@@ -380,3 +383,93 @@ def test_round_to_f16_inputs_change_attention_only_through_rounding():
     Oe, _ = oracle_forward(Qf, Kf, Vf, True, 0.5)
     err = normwise(Or, Oe)
     assert 1e-6 < err < 2e-2
+
+
+# ---- cross-attention: Lq != Lk, causal mask bottom-right aligned
+
+CROSS_FD_CASES = [(Lq, Lk, causal, padded) for (Lq, Lk) in ((3, 5), (5, 2), (4, 7))
+                  for causal, padded in ((True, False), (False, False), (False, True))]
+
+
+def _loss_cross(Q, K, V, dO, causal, scale, kl):
+    O, _ = oracle_forward(Q, K, V, causal, scale, key_len=kl)
+    return float(np.sum(O * dO))
+
+
+@pytest.mark.parametrize("Lq,Lk,causal,padded", CROSS_FD_CASES)
+def test_cross_central_finite_differences(Lq, Lk, causal, padded):
+    B, H, d = 1, 2, 3
+    Q, dO = rand(B, H, Lq, d), rand(B, H, Lq, d)
+    K, V = rand(B, H, Lk, d), rand(B, H, Lk, d)
+    kl = np.array([max(1, (Lk + 1) // 2)], dtype=np.int32) if padded else None
+    scale = 0.77
+    dQ, dK, dV, _ = oracle_backward(Q, K, V, dO, causal, scale, key_len=kl)
+    assert dQ.shape == Q.shape and dK.shape == K.shape and dV.shape == V.shape
+    h = 1e-5
+    for X, G in ((Q, dQ), (K, dK), (V, dV)):
+        num = np.zeros_like(X)
+        it = np.nditer(X, flags=["multi_index"])
+        for _ in it:
+            idx = it.multi_index
+            old = X[idx]
+            X[idx] = old + h
+            fp = _loss_cross(Q, K, V, dO, causal, scale, kl)
+            X[idx] = old - h
+            fm = _loss_cross(Q, K, V, dO, causal, scale, kl)
+            X[idx] = old
+            num[idx] = (fp - fm) / (2 * h)
+        assert np.max(np.abs(num - G)) <= 1e-7 * max(1.0, np.max(np.abs(G)))
+
+
+@pytest.mark.parametrize("Lq,Lk,causal,padded", [(9, 23, True, False), (17, 6, False, False),
+                                                 (12, 30, False, True), (20, 20, True, False)])
+def test_cross_matches_torch_autograd_f64(Lq, Lk, causal, padded):
+    B, H, d = 2, 2, 8
+    Q, dO = rand(B, H, Lq, d), rand(B, H, Lq, d)
+    K, V = rand(B, H, Lk, d), rand(B, H, Lk, d)
+    kl = np.array([Lk, max(1, Lk // 3)], dtype=np.int32) if padded else None
+    scale = 1 / math.sqrt(d)
+    O, LSE = oracle_forward(Q, K, V, causal, scale, key_len=kl)
+    dQ, dK, dV, _ = oracle_backward(Q, K, V, dO, causal, scale, key_len=kl)
+    tO, tL, tdQ, tdK, tdV = _torch_reference(Q, K, V, dO, causal, scale, kl)
+    assert normwise(O, tO) < 1e-13 and normwise(LSE, tL) < 1e-13
+    assert normwise(dQ, tdQ) < 1e-12 and normwise(dK, tdK) < 1e-12
+    assert normwise(dV, tdV) < 1e-12
+
+
+def test_cross_causal_is_the_bottom_rows_of_square_causal():
+    """Bottom-right alignment: with Lq < Lk, causal cross-attention of the
+    last Lq queries equals those rows of square causal attention over all Lk
+    (and, with dO zero on the other rows, the same dK and dV); with Lq > Lk,
+    the first Lq - Lk rows see no key and the rest are square causal
+    attention of the last Lk queries."""
+    B, H, d, Lk, Lq = 2, 2, 5, 13, 6
+    Qall, dOall = rand(B, H, Lk, d), rand(B, H, Lk, d)
+    K, V = rand(B, H, Lk, d), rand(B, H, Lk, d)
+    dOall[:, :, :Lk - Lq] = 0.0
+    Osq, Lsq = oracle_forward(Qall, K, V, True, 0.4)
+    gsq = oracle_backward(Qall, K, V, dOall, True, 0.4)
+    Q, dO = Qall[:, :, Lk - Lq:].copy(), dOall[:, :, Lk - Lq:].copy()
+    O, LSE = oracle_forward(Q, K, V, True, 0.4)
+    g = oracle_backward(Q, K, V, dO, True, 0.4)
+    assert np.array_equal(O, Osq[:, :, Lk - Lq:]) and np.array_equal(LSE, Lsq[:, :, Lk - Lq:])
+    assert np.array_equal(g[0], gsq[0][:, :, Lk - Lq:])
+    assert np.array_equal(g[1], gsq[1]) and np.array_equal(g[2], gsq[2])
+    # Lq > Lk: queries longer than keys
+    Lq2, Lk2 = 11, 4
+    Q2, K2, V2 = rand(B, H, Lq2, d), rand(B, H, Lk2, d), rand(B, H, Lk2, d)
+    O2, L2 = oracle_forward(Q2, K2, V2, True, 0.4)
+    assert np.all(O2[:, :, :Lq2 - Lk2] == 0.0) and np.all(L2[:, :, :Lq2 - Lk2] == -np.inf)
+    O3, L3 = oracle_forward(Q2[:, :, Lq2 - Lk2:].copy(), K2, V2, True, 0.4)
+    assert np.array_equal(O2[:, :, Lq2 - Lk2:], O3) and np.array_equal(L2[:, :, Lq2 - Lk2:], L3)
+
+
+def test_cross_single_key():
+    B, H, d = 1, 2, 4
+    Q, K, V = rand(B, H, 5, d), rand(B, H, 1, d), rand(B, H, 1, d)
+    O, LSE = oracle_forward(Q, K, V, False, 0.3)
+    assert np.array_equal(O, np.broadcast_to(V, O.shape))
+    assert normwise(LSE, 0.3 * np.einsum("bhid,bhjd->bhi", Q, K)) < 1e-15
+    O, LSE = oracle_forward(Q, K, V, True, 0.3)   # only the last row sees the key
+    assert np.all(O[:, :, :4] == 0.0) and np.all(LSE[:, :, :4] == -np.inf)
+    assert np.array_equal(O[:, :, 4], V[:, :, 0])
