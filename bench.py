@@ -103,13 +103,15 @@ def kernel_peak(name):
 def partial_rows(w, key_len):
     """(key tile, query row) pairs the fused dQ reduction reads (key tiles of
     128 keys when causal with >= 512 such tiles, else 64)."""
-    key_rows = 128 if (w.causal and -(-w.L // 128) * w.B * w.H >= 512) else 64
+    Lk = w.key_length
+    key_rows = 128 if (w.causal and -(-Lk // 128) * w.B * w.H >= 512) else 64
     total = 0
-    kls = [w.L] * w.B if key_len is None else [int(n) for n in key_len]
+    kls = [Lk] * w.B if key_len is None else [int(n) for n in key_len]
     for n in kls:
-        nk = -(-min(n, w.L) // key_rows)
+        nk = -(-max(0, min(n, Lk)) // key_rows)
         for i in range(w.L):
-            total += min(nk, i // key_rows + 1) if w.causal else nk
+            last = i + Lk - w.L          # causal: last key row i sees
+            total += (0 if last < 0 else min(nk, last // key_rows + 1)) if w.causal else nk
     return total * w.H
 
 
@@ -156,15 +158,16 @@ def main():
     O = torch.empty_like(Q)
     LSE = torch.empty(Q.shape[:3], dtype=torch.float32, device=dev)
     dQ, dK, dV = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
-    ws = torch.empty(mg.mg_attn_bwd_workspace_bytes(w.B, w.H, w.L, w.d, w.causal, w.contract),
+    ws = torch.empty(mg.mg_attn_bwd_cross_workspace_bytes(w.B, w.H, w.L, w.key_length, w.d,
+                                                          w.causal, w.contract),
                      dtype=torch.uint8, device=dev)
     stream = torch.cuda.current_stream()
 
     def step():
-        mg.mg_attn_fwd(Q, K, V, O, LSE, kl, causal=w.causal, scale=w.scale,
-                       contract=w.contract, stream=stream)
-        mg.mg_attn_bwd(Q, K, V, O, LSE, dO, dQ, dK, dV, kl, causal=w.causal, scale=w.scale,
-                       contract=w.contract, workspace=ws, stream=stream)
+        mg.mg_attn_fwd_cross(Q, K, V, O, LSE, kl, causal=w.causal, scale=w.scale,
+                             contract=w.contract, stream=stream)
+        mg.mg_attn_bwd_cross(Q, K, V, O, LSE, dO, dQ, dK, dV, kl, causal=w.causal,
+                             scale=w.scale, contract=w.contract, workspace=ws, stream=stream)
 
     for _ in range(args.warmup):
         step()
@@ -199,7 +202,7 @@ def main():
         mg.mg_profile_enable(False)
         kernels = mg.mg_profile_collect()
 
-    pairs = unmasked_pairs(w.B, w.H, w.L, w.causal, x.key_len)
+    pairs = unmasked_pairs(w.B, w.H, w.L, w.causal, x.key_len, Lk=w.key_length)
     rows = w.B * w.H * w.L
     flops = 14.0 * w.d * pairs
     ms_per_step = elapsed * 1e3 / args.steps
@@ -219,7 +222,8 @@ def main():
         "vs_baseline": None,
         "dtype": DTYPE[w.contract],
         "data": "synthetic",
-        "config": {"workload": w.name, "B": w.B, "H": w.H, "L": w.L, "d": w.d,
+        "config": {"workload": w.name, "B": w.B, "H": w.H, "L": w.L, "Lk": w.key_length,
+                   "d": w.d,
                    "causal": w.causal, "key_padding": w.padded, "contract": w.contract,
                    "unmasked_pairs": pairs, "credited_gflop_per_step": flops / 1e9},
         "step_ms": {"median": round(float(np.median(samples)), 4),
@@ -278,7 +282,7 @@ def cpu_baseline(args, w, x, pairs, gpu_outputs):
     from oracle import oracle_forward, oracle_backward, oracle_num_threads
     B, H = w.B, w.H
     heads = None
-    if B * H * w.L * w.L * w.d > 2 ** 33:          # keep the CPU leg to seconds
+    if B * H * w.L * w.key_length * w.d > 2 ** 33:   # keep the CPU leg to seconds
         heads = [(b, h) for b in range(B) for h in range(H)][:: max(1, (B * H) // 4)][:4]
     # repeat the sample until about --cpu-seconds of oracle work (at least 3
     # runs, at most 100), so the figure is a bounded, stable CPU measurement

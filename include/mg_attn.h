@@ -35,7 +35,8 @@
  * fastest; LSE is [B][H][L].  key_len is an int32 device array [B] or NULL
  * (no padding); its values are clamped to [0, L] on the device.  A row with
  * no allowed key (key_len[b] == 0) yields O = 0, LSE = -inf and zero
- * gradients.  Causal masking is top-left aligned (equal query/key length).
+ * gradients.  Causal masking: query row i sees keys j <= i (equal query and
+ * key lengths; see mg_attn_fwd_cross for the general case).
  *
  * Ownership: the caller owns every buffer, including the backward workspace.
  * The library allocates no device memory, keeps no per-call state and is
@@ -70,7 +71,8 @@ typedef enum {
 typedef enum {
     MG_OK = 0,
     MG_ERR_INVALID_ARGUMENT = 1, /* null pointer, size < 1, non-finite scale,
-                                    bad contract, B*H*L*d > 2^31-1         */
+                                    bad contract, B*H*L*d > 2^31-1
+                                    (cross: B*H*max(Lq,Lk)*d)               */
     MG_ERR_UNSUPPORTED = 2,      /* head dimension d not in {32, 64, 128}   */
     MG_ERR_MISALIGNED = 3,       /* a tensor pointer not 16-byte aligned    */
     MG_ERR_WORKSPACE = 4,        /* backward workspace missing or too small */
@@ -123,6 +125,38 @@ mg_status_t mg_attn_bwd(const void *Q, const void *K, const void *V,
                         mg_contract_t contract,
                         void *workspace, size_t workspace_bytes,
                         hipStream_t stream);
+
+/*
+ * Cross-attention: queries and keys of different lengths (Sec. 10 workloads:
+ * the U-Net's 77-token text cross-attention, the action expert's action and
+ * context tokens).  Q, O, dO, dQ are [B][H][Lq][d]; K, V, dK, dV are
+ * [B][H][Lk][d]; LSE and the workspace's D are [B][H][Lq]; key_len values
+ * are clamped to [0, Lk].  The causal mask is bottom-right aligned: query row
+ * i sees keys j <= i + Lk - Lq, so the last query row sees every key and,
+ * when Lk < Lq, the first Lq - Lk rows see none (O = 0, LSE = -inf, no
+ * gradient).  With Lq == Lk these are exactly mg_attn_fwd / mg_attn_bwd,
+ * which call them.  Arguments, contracts, ownership, asynchrony and errors
+ * are otherwise as there; the workspace holds D and, for strict_f32 and
+ * accelerated with d <= 64 when they fit in 1 GiB, ceil(Lk/T) * B*H*Lq*d
+ * f32 dQ partials (T as above, decided from Lk).
+ */
+mg_status_t mg_attn_fwd_cross(const void *Q, const void *K, const void *V,
+                              void *O, float *LSE,
+                              const int32_t *key_len,
+                              int B, int H, int Lq, int Lk, int d, int causal, float scale,
+                              mg_contract_t contract, hipStream_t stream);
+
+size_t mg_attn_bwd_cross_workspace_bytes(int B, int H, int Lq, int Lk, int d, int causal,
+                                         mg_contract_t contract);
+
+mg_status_t mg_attn_bwd_cross(const void *Q, const void *K, const void *V,
+                              const void *O, const float *LSE, const void *dO,
+                              void *dQ, void *dK, void *dV,
+                              const int32_t *key_len,
+                              int B, int H, int Lq, int Lk, int d, int causal, float scale,
+                              mg_contract_t contract,
+                              void *workspace, size_t workspace_bytes,
+                              hipStream_t stream);
 
 /* Static, human-readable name of a status code. */
 const char *mg_status_string(mg_status_t status);

@@ -15,8 +15,11 @@ from ._binding import (  # noqa: F401
     attention_forward,
     load_library,
     mg_attn_bwd,
+    mg_attn_bwd_cross,
+    mg_attn_bwd_cross_workspace_bytes,
     mg_attn_bwd_workspace_bytes,
     mg_attn_fwd,
+    mg_attn_fwd_cross,
     mg_last_error_detail,
     mg_profile_collect,
     mg_profile_enable,

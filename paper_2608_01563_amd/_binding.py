@@ -44,6 +44,15 @@ def _declare(lib):
     lib.mg_attn_bwd.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, c_int, c_int, c_int,
                                 c_int, c_int, c_float, c_int, vp, c_size, vp]
     lib.mg_attn_bwd.restype = c_int
+    lib.mg_attn_fwd_cross.argtypes = [vp, vp, vp, vp, vp, vp, c_int, c_int, c_int, c_int,
+                                      c_int, c_int, c_float, c_int, vp]
+    lib.mg_attn_fwd_cross.restype = c_int
+    lib.mg_attn_bwd_cross_workspace_bytes.argtypes = [c_int, c_int, c_int, c_int, c_int, c_int,
+                                                      c_int]
+    lib.mg_attn_bwd_cross_workspace_bytes.restype = c_size
+    lib.mg_attn_bwd_cross.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, c_int, c_int,
+                                      c_int, c_int, c_int, c_int, c_float, c_int, vp, c_size, vp]
+    lib.mg_attn_bwd_cross.restype = c_int
     lib.mg_status_string.argtypes = [c_int]
     lib.mg_status_string.restype = ctypes.c_char_p
     lib.mg_last_error_detail.argtypes = []
@@ -95,7 +104,9 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
-def _check_tensors(contract, ref, named):
+def _check_tensors(contract, shape, named):
+    """Each tensor in `named` must be a contiguous GPU tensor of the
+    contract's dtype and of `shape`."""
     import torch
     want = torch.bfloat16 if contract == FAST_BF16 else torch.float32
     for name, t in named:
@@ -103,11 +114,21 @@ def _check_tensors(contract, ref, named):
             raise ValueError("%s must be a GPU tensor" % name)
         if t.dtype != want:
             raise ValueError("%s has dtype %s, contract needs %s" % (name, t.dtype, want))
-        if tuple(t.shape) != tuple(ref.shape):
+        if tuple(t.shape) != tuple(shape):
             raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape),
-                                                               tuple(ref.shape)))
+                                                               tuple(shape)))
         if not t.is_contiguous():
             raise ValueError("%s must be contiguous" % name)
+
+
+def _cross_shapes(Q, K):
+    """(B, H, Lq, Lk, d) from Q [B,H,Lq,d] and K [B,H,Lk,d]."""
+    if Q.dim() != 4 or K.dim() != 4:
+        raise ValueError("Q must be [B,H,Lq,d] and K [B,H,Lk,d]")
+    B, H, Lq, d = Q.shape
+    if tuple(K.shape) != (B, H, K.shape[2], d):
+        raise ValueError("K has shape %s, expected [%d,%d,Lk,%d]" % (tuple(K.shape), B, H, d))
+    return B, H, Lq, K.shape[2], d
 
 
 def _check_lse(LSE, shape):
@@ -135,7 +156,7 @@ def mg_attn_fwd(Q, K, V, O, LSE, key_len=None, *, causal, scale, contract=STRICT
     if Q.dim() != 4:
         raise ValueError("Q must be [B,H,L,d]")
     B, H, L, d = Q.shape
-    _check_tensors(c, Q, (("Q", Q), ("K", K), ("V", V), ("O", O)))
+    _check_tensors(c, Q.shape, (("Q", Q), ("K", K), ("V", V), ("O", O)))
     _check_lse(LSE, Q.shape)
     _check_key_len(key_len, B)
     _check(lib.mg_attn_fwd(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(LSE), _ptr(key_len),
@@ -159,8 +180,8 @@ def mg_attn_bwd(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len=None, *, causal, scale,
     if Q.dim() != 4:
         raise ValueError("Q must be [B,H,L,d]")
     B, H, L, d = Q.shape
-    _check_tensors(c, Q, (("Q", Q), ("K", K), ("V", V), ("O", O), ("dO", dO), ("dQ", dQ),
-                          ("dK", dK), ("dV", dV)))
+    _check_tensors(c, Q.shape, (("Q", Q), ("K", K), ("V", V), ("O", O), ("dO", dO),
+                                ("dQ", dQ), ("dK", dK), ("dV", dV)))
     _check_lse(LSE, Q.shape)
     _check_key_len(key_len, B)
     need = mg_attn_bwd_workspace_bytes(B, H, L, d, causal, c)
@@ -170,6 +191,51 @@ def mg_attn_bwd(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len=None, *, causal, scale,
     _check(lib.mg_attn_bwd(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(LSE), _ptr(dO), _ptr(dQ),
                            _ptr(dK), _ptr(dV), _ptr(key_len), B, H, L, d, int(bool(causal)),
                            float(scale), c, _ptr(workspace), nbytes, _stream_handle(stream)))
+
+
+def mg_attn_fwd_cross(Q, K, V, O, LSE, key_len=None, *, causal, scale, contract=STRICT_F32,
+                      stream=None):
+    """Cross-attention forward: Q, O [B,H,Lq,d]; K, V [B,H,Lk,d]; LSE
+    [B,H,Lq]; the causal mask is bottom-right aligned (row i sees keys
+    j <= i + Lk - Lq)."""
+    lib = load_library()
+    c = _contract_id(contract)
+    B, H, Lq, Lk, d = _cross_shapes(Q, K)
+    _check_tensors(c, Q.shape, (("Q", Q), ("O", O)))
+    _check_tensors(c, K.shape, (("K", K), ("V", V)))
+    _check_lse(LSE, Q.shape)
+    _check_key_len(key_len, B)
+    _check(lib.mg_attn_fwd_cross(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(LSE), _ptr(key_len),
+                                 B, H, Lq, Lk, d, int(bool(causal)), float(scale), c,
+                                 _stream_handle(stream)))
+
+
+def mg_attn_bwd_cross_workspace_bytes(B, H, Lq, Lk, d, causal, contract=STRICT_F32):
+    return int(load_library().mg_attn_bwd_cross_workspace_bytes(
+        B, H, Lq, Lk, d, int(bool(causal)), _contract_id(contract)))
+
+
+def mg_attn_bwd_cross(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len=None, *, causal, scale,
+                      contract=STRICT_F32, workspace=None, stream=None):
+    """Cross-attention backward: Q, O, dO, dQ [B,H,Lq,d]; K, V, dK, dV
+    [B,H,Lk,d].  `workspace` as for mg_attn_bwd (sized by
+    mg_attn_bwd_cross_workspace_bytes)."""
+    import torch
+    lib = load_library()
+    c = _contract_id(contract)
+    B, H, Lq, Lk, d = _cross_shapes(Q, K)
+    _check_tensors(c, Q.shape, (("Q", Q), ("O", O), ("dO", dO), ("dQ", dQ)))
+    _check_tensors(c, K.shape, (("K", K), ("V", V), ("dK", dK), ("dV", dV)))
+    _check_lse(LSE, Q.shape)
+    _check_key_len(key_len, B)
+    need = mg_attn_bwd_cross_workspace_bytes(B, H, Lq, Lk, d, causal, c)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=Q.device)
+    nbytes = workspace.numel() * workspace.element_size()
+    _check(lib.mg_attn_bwd_cross(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(LSE), _ptr(dO),
+                                 _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(key_len), B, H, Lq, Lk, d,
+                                 int(bool(causal)), float(scale), c, _ptr(workspace), nbytes,
+                                 _stream_handle(stream)))
 
 
 def mg_status_string(status):
@@ -203,24 +269,26 @@ def mg_profile_collect(max_entries=32):
 
 # ------------------------------------------------------------ conveniences --
 def attention_forward(Q, K, V, *, causal, scale, key_len=None, contract=None, stream=None):
-    """Allocate O and LSE with torch and run mg_attn_fwd; returns (O, LSE)."""
+    """Allocate O and LSE with torch and run the forward; returns (O, LSE).
+    K and V may have their own sequence length (cross-attention)."""
     import torch
     c = _contract_id(contract) if contract is not None else (
         FAST_BF16 if Q.dtype == torch.bfloat16 else STRICT_F32)
     O = torch.empty_like(Q)
     LSE = torch.empty(Q.shape[:3], dtype=torch.float32, device=Q.device)
-    mg_attn_fwd(Q, K, V, O, LSE, key_len, causal=causal, scale=scale, contract=c,
-                stream=stream)
+    mg_attn_fwd_cross(Q, K, V, O, LSE, key_len, causal=causal, scale=scale, contract=c,
+                      stream=stream)
     return O, LSE
 
 
 def attention_backward(Q, K, V, O, LSE, dO, *, causal, scale, key_len=None, contract=None,
                        workspace=None, stream=None):
-    """Allocate dQ, dK, dV with torch and run mg_attn_bwd; returns (dQ, dK, dV)."""
+    """Allocate dQ, dK, dV with torch and run the backward; returns (dQ, dK,
+    dV).  K and V may have their own sequence length (cross-attention)."""
     import torch
     c = _contract_id(contract) if contract is not None else (
         FAST_BF16 if Q.dtype == torch.bfloat16 else STRICT_F32)
     dQ, dK, dV = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
-    mg_attn_bwd(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len, causal=causal, scale=scale,
-                contract=c, workspace=workspace, stream=stream)
+    mg_attn_bwd_cross(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len, causal=causal, scale=scale,
+                      contract=c, workspace=workspace, stream=stream)
     return dQ, dK, dV

@@ -92,7 +92,7 @@ template <int D, bool POS_SCALE>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
 void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
                     const float *__restrict__ V, float *__restrict__ O, float *__restrict__ LSE,
-                    const int32_t *__restrict__ key_len, int H, int L, int causal,
+                    const int32_t *__restrict__ key_len, int H, int Lq, int Lk, int causal,
                     float scale_log2, int n_qtiles, int BH) {
     constexpr int NS = D / 16;    // 16-deep contraction steps over d
     constexpr int NCB = D / 32;   // 32-column blocks of d
@@ -106,9 +106,10 @@ void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
     const int head = blockIdx.x - rank * BH;
     const int qt = causal ? (n_qtiles - 1 - rank) : rank;
     const int b = head / H;
-    const size_t hoff = (size_t)head * L * D;
+    const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
     const float *Kh = K + hoff;
     const float *Vh = V + hoff;
+    const int diag = Lk - Lq;   // causal: row i sees keys j <= i + diag
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -119,27 +120,27 @@ void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
     const int q0 = qt * kRows;
     const int qi = q0 + 32 * w + c;
 
-    const int klen = key_limit(key_len, b, L);
-    const int kend = causal ? min(klen, q0 + kRows) : klen;
+    const int klen = key_limit(key_len, b, Lk);
+    const int kend = causal ? min(klen, q0 + kRows + diag) : klen;
     const int ntiles = (kend + kKeys - 1) / kKeys;
 
     // B operand of S^T = K Q^T: lane holds f16(Q[qi][16s + 8h + e]).
     f16x8 qreg[NS];
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-        const float *qp = Q + hoff + (size_t)qi * D + 16 * s + 8 * h;
-        qreg[s] = (qi < L) ? to_f16x8(*reinterpret_cast<const f32x4 *>(qp),
+        const float *qp = Q + qoff + (size_t)qi * D + 16 * s + 8 * h;
+        qreg[s] = (qi < Lq) ? to_f16x8(*reinterpret_cast<const f32x4 *>(qp),
                                       *reinterpret_cast<const f32x4 *>(qp + 4))
                            : f16x8{};
     }
 
     St st;
     if (ntiles > 0) {
-        st.load(Kh, 0, L, tid);
+        st.load(Kh, 0, Lk, tid);
         st.store(Kr, tid);
-        st.load(Vh, 0, L, tid);
+        st.load(Vh, 0, Lk, tid);
         st.store(Vr, tid);
-        if (ntiles > 1) st.load(Kh, kKeys, L, tid);
+        if (ntiles > 1) st.load(Kh, kKeys, Lk, tid);
     }
     __syncthreads();
 
@@ -165,7 +166,7 @@ void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
         __syncthreads();   // every wave is done with K(kt)
         if (kt + 1 < ntiles) {
             st.store(Kr, tid);                      // K(kt+1), loaded during S(kt)
-            st.load(Vh, (kt + 1) * kKeys, L, tid);  // V(kt+1), lands during P V(kt)
+            st.load(Vh, (kt + 1) * kKeys, Lk, tid);  // V(kt+1), lands during P V(kt)
         }
         if (!POS_SCALE) {
 #pragma unroll
@@ -173,10 +174,10 @@ void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
         }
 
         // Masking only where the tile crosses the diagonal or the key length.
-        const bool full = (kt + 1) * kKeys <= klen && (!causal || (kt + 1) * kKeys - 1 <= q0);
+        const bool full = (kt + 1) * kKeys <= klen && (!causal || (kt + 1) * kKeys - 1 <= q0 + diag);
         if (!full) {
             const int j0 = kt * kKeys + 4 * h;
-            const int thr = causal ? min(klen - j0, qi - j0 + 1) : klen - j0;
+            const int thr = causal ? min(klen - j0, qi + diag - j0 + 1) : klen - j0;
 #pragma unroll
             for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
@@ -229,16 +230,16 @@ void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
         __syncthreads();   // every wave is done with V(kt); K(kt+1) is visible
         if (kt + 1 < ntiles) {
             st.store(Vr, tid);                                       // V(kt+1)
-            if (kt + 2 < ntiles) st.load(Kh, (kt + 2) * kKeys, L, tid);   // K(kt+2)
+            if (kt + 2 < ntiles) st.load(Kh, (kt + 2) * kKeys, Lk, tid);   // K(kt+2)
         }
         // V(kt+1) becomes visible at the first barrier of the next iteration,
         // before P V reads it
     }
 
     const float l = sum_xor32(l_run);
-    if (qi < L) {
+    if (qi < Lq) {
         const float inv = (l > 0.f) ? 1.f / l : 0.f;
-        float *orow = O + hoff + (size_t)qi * D;
+        float *orow = O + qoff + (size_t)qi * D;
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
@@ -248,7 +249,7 @@ void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
                           oacc[cb][4 * a + 3]} * inv;
         if (h == 0) {
             const float m2 = POS_SCALE ? m_run * scale_log2 : m_run;
-            LSE[(size_t)head * L + qi] = (l > 0.f) ? (m2 + log2f(l)) * kLn2 : -INFINITY;
+            LSE[(size_t)head * Lq + qi] = (l > 0.f) ? (m2 + log2f(l)) * kLn2 : -INFINITY;
         }
     }
 }
@@ -260,15 +261,15 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 hipError_t launch_fwd_accel(const AttnProblem &p, const float *Q, const float *K,
                             const float *V, float *O, float *LSE, hipStream_t s) {
     const int BH = p.B * p.H;
-    const int nqt = cdiv(p.L, kRows);
+    const int nqt = cdiv(p.Lq, kRows);
     const dim3 grid(nqt * BH), block(kThreads);
     const float sl2 = p.scale * kLog2e;
 #define MG_FWD_ACCEL(DD)                                                                     \
     (p.scale > 0.f                                                                          \
          ? (attn_fwd_accel<DD, true><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, \
-                                                            p.L, p.causal, sl2, nqt, BH))     \
+                                                            p.Lq, p.Lk, p.causal, sl2, nqt, BH))     \
          : (attn_fwd_accel<DD, false><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len,     \
-                                                             p.H, p.L, p.causal, sl2, nqt, BH)))
+                                                             p.H, p.Lq, p.Lk, p.causal, sl2, nqt, BH)))
     switch (p.d) {
     case 32: MG_FWD_ACCEL(32); break;
     case 64: MG_FWD_ACCEL(64); break;

@@ -61,7 +61,7 @@ template <int D, bool POS_SCALE>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
 void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                    const uint16_t *__restrict__ V, uint16_t *__restrict__ O,
-                   float *__restrict__ LSE, const int32_t *__restrict__ key_len, int H, int L,
+                   float *__restrict__ LSE, const int32_t *__restrict__ key_len, int H, int Lq, int Lk,
                    int causal, float scale_log2, int n_qtiles, int BH) {
     constexpr int NS = D / 16;    // 16-deep contraction steps over d
     constexpr int NCB = D / 32;   // 32-column blocks of d
@@ -80,7 +80,8 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
     const int head = blockIdx.x - rank * BH;
     const int qt = causal ? (n_qtiles - 1 - rank) : rank;
     const int b = head / H;
-    const size_t hoff = (size_t)head * L * D;
+    const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
+    const int diag = Lk - Lq;   // causal: row i sees keys j <= i + diag
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -91,8 +92,8 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
     const int q0 = qt * kFwdRows;
     const int qi = q0 + 32 * w + c;
 
-    const int klen = key_limit(key_len, b, L);
-    const int kend = causal ? min(klen, q0 + kFwdRows) : klen;
+    const int klen = key_limit(key_len, b, Lk);
+    const int kend = causal ? min(klen, q0 + kFwdRows + diag) : klen;
     const int ntiles = (kend + kStream - 1) / kStream;
 
     // K and V tiles: direct-to-LDS row loads; the next K tile is fetched
@@ -101,15 +102,15 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
     const float *Kf = reinterpret_cast<const float *>(K + hoff);
     const float *Vf = reinterpret_cast<const float *>(V + hoff);
     if (ntiles > 0) {
-        tile.issue(kdst, Kf, 0, L, w, lane);
-        tile.issue(vdst, Vf, 0, L, w, lane);
+        tile.issue(kdst, Kf, 0, Lk, w, lane);
+        tile.issue(vdst, Vf, 0, Lk, w, lane);
     }
 
     // B operand of S^T = K Q^T: lane holds Q[qi][16s + 8h + e].
     bf16x8 qreg[NS];
 #pragma unroll
     for (int s = 0; s < NS; ++s)
-        qreg[s] = (qi < L) ? load_bf16x8(Q + hoff + (size_t)qi * D + 16 * s + 8 * h)
+        qreg[s] = (qi < Lq) ? load_bf16x8(Q + qoff + (size_t)qi * D + 16 * s + 8 * h)
                            : __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
 
     // Running max in raw-score units when POS_SCALE, else in base-2 units.
@@ -134,7 +135,7 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
         }
         wait_vmcnt<0>();   // V(kt) landed
         __syncthreads();   // every wave is done with K(kt) and sees V(kt)
-        if (kt + 1 < ntiles) tile.issue(kdst, Kf, (kt + 1) * kStream, L, w, lane);
+        if (kt + 1 < ntiles) tile.issue(kdst, Kf, (kt + 1) * kStream, Lk, w, lane);
         if (!POS_SCALE) {
 #pragma unroll
             for (int kb = 0; kb < NKB; ++kb) sacc[kb] *= scale_log2;
@@ -142,10 +143,10 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
 
         // Masking only where the tile crosses the diagonal or the key length.
         const bool full = (kt + 1) * kStream <= klen &&
-                          (!causal || (kt + 1) * kStream - 1 <= q0);
+                          (!causal || (kt + 1) * kStream - 1 <= q0 + diag);
         if (!full) {
             const int j0 = kt * kStream + 4 * h;
-            const int thr = causal ? min(klen - j0, qi - j0 + 1) : klen - j0;
+            const int thr = causal ? min(klen - j0, qi + diag - j0 + 1) : klen - j0;
 #pragma unroll
             for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
@@ -198,13 +199,13 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
 
         wait_vmcnt<0>();   // K(kt+1) landed
         __syncthreads();   // every wave is done with V(kt) and sees K(kt+1)
-        if (kt + 1 < ntiles) tile.issue(vdst, Vf, (kt + 1) * kStream, L, w, lane);
+        if (kt + 1 < ntiles) tile.issue(vdst, Vf, (kt + 1) * kStream, Lk, w, lane);
     }
 
     const float l = sum_xor32(l_run);
-    if (qi < L) {
+    if (qi < Lq) {
         const float inv = (l > 0.f) ? 1.f / l : 0.f;
-        uint16_t *orow = O + hoff + (size_t)qi * D;
+        uint16_t *orow = O + qoff + (size_t)qi * D;
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
@@ -214,7 +215,7 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
                                    oacc[cb][4 * a + 3]} * inv);
         if (h == 0) {
             const float m2 = POS_SCALE ? m_run * scale_log2 : m_run;
-            LSE[(size_t)head * L + qi] = (l > 0.f) ? (m2 + log2f(l)) * kLn2 : -INFINITY;
+            LSE[(size_t)head * Lq + qi] = (l > 0.f) ? (m2 + log2f(l)) * kLn2 : -INFINITY;
         }
     }
 }
@@ -246,14 +247,14 @@ __global__ __launch_bounds__(256) void attn_rowdot_bf16(const uint16_t *__restri
 // Key tile of 64 keys stationary (16 per wave, one per lane column) on
 // 16x16x32 products; query tiles of 64 rows stream through LDS row-major.
 // Masks as in the strict-f32 kernel: a causal threshold per lane, padded
-// keys overwritten with zeros at the end, rows past L inert.
+// keys overwritten with zeros at the end, rows past Lq inert.
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
 void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                     const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
                     const float *__restrict__ LSE, const float *__restrict__ Dws,
                     uint16_t *__restrict__ dK, uint16_t *__restrict__ dV,
-                    const int32_t *__restrict__ key_len, int H, int L, int causal, float scale,
+                    const int32_t *__restrict__ key_len, int H, int Lq, int Lk, int causal, float scale,
                     float scale_log2, int BH) {
     constexpr int NS = D / 32;
     constexpr int NC = D / 16;
@@ -271,7 +272,8 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
     const int head = blockIdx.x - rank * BH;
     const int kt = rank;
     const int b = head / H;
-    const size_t hoff = (size_t)head * L * D;
+    const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
+    const int diag = Lk - Lq;   // causal: row i sees keys j <= i + diag
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -282,14 +284,15 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
     const int k0 = kt * kStatRows;
     const int kj = k0 + 16 * w + il;
 
-    const int klen = key_limit(key_len, b, L);
-    const int nq = (L + kStream - 1) / kStream;
-    const int qstart = causal ? (k0 / kStream) : 0;
+    const int klen = key_limit(key_len, b, Lk);
+    const int nq = (Lq + kStream - 1) / kStream;
+    // first query tile holding a row that sees key k0
+    const int qstart = causal ? min(nq, max(0, k0 - diag) / kStream) : 0;
     const int qstop = (k0 < klen) ? nq : qstart;
 
     bf16x8 kreg[NS], vreg[NS];
-    load_stationary<D>(kreg, K + hoff, kj, L, g);
-    load_stationary<D>(vreg, V + hoff, kj, L, g);
+    load_stationary<D>(kreg, K + hoff, kj, Lk, g);
+    load_stationary<D>(vreg, V + hoff, kj, Lk, g);
 
     f32x4 dkacc[NC], dvacc[NC];   // dK^T[16c + 4g + r][kj], dV^T likewise
 #pragma unroll
@@ -299,18 +302,18 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
     }
 
     const Tile tile;
-    const float *Qf = reinterpret_cast<const float *>(Q + hoff);
-    const float *Of = reinterpret_cast<const float *>(dO + hoff);
+    const float *Qf = reinterpret_cast<const float *>(Q + qoff);
+    const float *Of = reinterpret_cast<const float *>(dO + qoff);
     float lse_pre = 0.f, d_pre = 0.f;
     auto fetch = [&](int qt, int buf) {   // direct loads of Q, dO; LSE, D to registers
-        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Qr[buf][0][0]), Qf, qt * kStream, L, w,
+        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Qr[buf][0][0]), Qf, qt * kStream, Lq, w,
                    lane);
-        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Or[buf][0][0]), Of, qt * kStream, L, w,
+        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Or[buf][0][0]), Of, qt * kStream, Lq, w,
                    lane);
         if (tid < kStream) {
             const int row = qt * kStream + tid;
-            lse_pre = (row < L) ? LSE[(size_t)head * L + row] : 0.f;   // natural log
-            d_pre = (row < L) ? Dws[(size_t)head * L + row] : 0.f;
+            lse_pre = (row < Lq) ? LSE[(size_t)head * Lq + row] : 0.f;   // natural log
+            d_pre = (row < Lq) ? Dws[(size_t)head * Lq + row] : 0.f;
         }
     };
     auto publish = [&](int buf) {   // LSE (base 2) and D of the fetched rows
@@ -347,7 +350,7 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
             }
 
         const int ibase = qt * kStream + 4 * g;
-        const int thr = causal ? kj - ibase : -(1 << 30);
+        const int thr = causal ? kj - diag - ibase : -(1 << 30);
 #pragma unroll
         for (int ib = 0; ib < kBlk; ++ib) {
             const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lse2s[cb][16 * ib + 4 * g]);
@@ -383,7 +386,7 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
         __syncthreads();   // next tile visible; buffer cb free
     }
 
-    if (kj < L) {
+    if (kj < Lk) {
         const bool keep = kj < klen;   // padded keys get exact zeros
         uint16_t *dkrow = dK + hoff + (size_t)kj * D;
         uint16_t *dvrow = dV + hoff + (size_t)kj * D;
@@ -407,7 +410,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
 void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                   const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
                   const float *__restrict__ LSE, const float *__restrict__ Dws,
-                  uint16_t *__restrict__ dQ, const int32_t *__restrict__ key_len, int H, int L,
+                  uint16_t *__restrict__ dQ, const int32_t *__restrict__ key_len, int H, int Lq, int Lk,
                   int causal, float scale, float scale_log2, int n_qtiles, int BH) {
     constexpr int NS = D / 16;
     constexpr int NCB = D / 32;
@@ -423,7 +426,8 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
     const int head = blockIdx.x - rank * BH;
     const int qt = causal ? (n_qtiles - 1 - rank) : rank;
     const int b = head / H;
-    const size_t hoff = (size_t)head * L * D;
+    const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
+    const int diag = Lk - Lq;   // causal: row i sees keys j <= i + diag
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -434,20 +438,20 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
     const int q0 = qt * kFwdRows;
     const int qi = q0 + 32 * w + c;
 
-    const int klen = key_limit(key_len, b, L);
-    const int kend = causal ? min(klen, q0 + kFwdRows) : klen;
+    const int klen = key_limit(key_len, b, Lk);
+    const int kend = causal ? min(klen, q0 + kFwdRows + diag) : klen;
     const int ntiles = (kend + KS - 1) / KS;
 
     bf16x8 qreg[NS], oreg[NS];
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-        const size_t off = hoff + (size_t)qi * D + 16 * s + 8 * h;
-        qreg[s] = (qi < L) ? load_bf16x8(Q + off) : __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
-        oreg[s] = (qi < L) ? load_bf16x8(dO + off) : __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+        const size_t off = qoff + (size_t)qi * D + 16 * s + 8 * h;
+        qreg[s] = (qi < Lq) ? load_bf16x8(Q + off) : __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+        oreg[s] = (qi < Lq) ? load_bf16x8(dO + off) : __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
     }
-    // Rows past L: Q = dO = 0 and LSE = D = 0, so their dS is exactly 0.
-    const float lse2 = (qi < L) ? LSE[(size_t)head * L + qi] * kLog2e : 0.f;
-    const float Di = (qi < L) ? Dws[(size_t)head * L + qi] : 0.f;
+    // Rows past Lq: Q = dO = 0 and LSE = D = 0, so their dS is exactly 0.
+    const float lse2 = (qi < Lq) ? LSE[(size_t)head * Lq + qi] * kLog2e : 0.f;
+    const float Di = (qi < Lq) ? Dws[(size_t)head * Lq + qi] : 0.f;
 
     f32x16 dqacc[NCB];   // dQ^T[32cb + 8a + 4h + r][qi]
 #pragma unroll
@@ -457,8 +461,8 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
     const float *Kf = reinterpret_cast<const float *>(K + hoff);
     const float *Vf = reinterpret_cast<const float *>(V + hoff);
     auto fetch = [&](int t, int buf) {
-        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Kr[buf][0][0]), Kf, t * KS, L, w, lane);
-        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Vr[buf][0][0]), Vf, t * KS, L, w, lane);
+        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Kr[buf][0][0]), Kf, t * KS, Lk, w, lane);
+        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Vr[buf][0][0]), Vf, t * KS, Lk, w, lane);
     };
     if (ntiles > 0) fetch(0, 0);
     wait_vmcnt<0>();
@@ -467,9 +471,9 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
         const int cb = kt & 1;
         if (kt + 1 < ntiles) fetch(kt + 1, cb ^ 1);   // buffer cb^1 was freed by the last barrier
         const bool full = (kt + 1) * KS <= klen &&
-                          (!causal || (kt + 1) * KS - 1 <= q0);
+                          (!causal || (kt + 1) * KS - 1 <= q0 + diag);
         const int j0 = kt * KS + 4 * h;
-        const int thr = causal ? min(klen - j0, qi - j0 + 1) : klen - j0;
+        const int thr = causal ? min(klen - j0, qi + diag - j0 + 1) : klen - j0;
 
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb) {
@@ -503,8 +507,8 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
         __syncthreads();   // it is visible; buffer cb is free
     }
 
-    if (qi < L) {
-        uint16_t *dqrow = dQ + hoff + (size_t)qi * D;
+    if (qi < Lq) {
+        uint16_t *dqrow = dQ + qoff + (size_t)qi * D;
 #pragma unroll
         for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
@@ -523,15 +527,15 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 hipError_t launch_fwd_bf16(const AttnProblem &p, const uint16_t *Q, const uint16_t *K,
                            const uint16_t *V, uint16_t *O, float *LSE, hipStream_t s) {
     const int BH = p.B * p.H;
-    const int nqt = cdiv(p.L, kFwdRows);
+    const int nqt = cdiv(p.Lq, kFwdRows);
     const dim3 grid(nqt * BH), block(kThreads);
     const float sl2 = p.scale * kLog2e;
 #define MG_FWD_BF16(DD)                                                                     \
     (p.scale > 0.f                                                                         \
          ? (attn_fwd_bf16<DD, true><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H,  \
-                                                          p.L, p.causal, sl2, nqt, BH), 0) \
+                                                          p.Lq, p.Lk, p.causal, sl2, nqt, BH), 0) \
          : (attn_fwd_bf16<DD, false><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, \
-                                                           p.L, p.causal, sl2, nqt, BH), 0))
+                                                           p.Lq, p.Lk, p.causal, sl2, nqt, BH), 0))
     switch (p.d) {
     case 32: MG_FWD_BF16(32); break;
     case 64: MG_FWD_BF16(64); break;
@@ -544,7 +548,7 @@ hipError_t launch_fwd_bf16(const AttnProblem &p, const uint16_t *Q, const uint16
 
 hipError_t launch_bwd_rowdot_bf16(const AttnProblem &p, const uint16_t *O, const uint16_t *dO,
                                   float *Dws, hipStream_t s) {
-    const int rows = p.B * p.H * p.L;
+    const int rows = p.B * p.H * p.Lq;
     const dim3 block(256);
     switch (p.d) {
     case 32: attn_rowdot_bf16<32><<<dim3(cdiv(rows, 256 / 4)), block, 0, s>>>(O, dO, Dws, rows); break;
@@ -559,12 +563,12 @@ hipError_t launch_bwd_dkdv_bf16(const AttnProblem &p, const uint16_t *Q, const u
                                 const uint16_t *V, const uint16_t *dO, const float *LSE,
                                 const float *Dws, uint16_t *dK, uint16_t *dV, hipStream_t s) {
     const int BH = p.B * p.H;
-    const dim3 grid(cdiv(p.L, kStatRows) * BH), block(kThreads);
+    const dim3 grid(cdiv(p.Lk, kStatRows) * BH), block(kThreads);
     const float sl2 = p.scale * kLog2e;
     switch (p.d) {
-    case 32: attn_dkdv_bf16<32><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
-    case 64: attn_dkdv_bf16<64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
-    case 128: attn_dkdv_bf16<128><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
+    case 32: attn_dkdv_bf16<32><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
+    case 64: attn_dkdv_bf16<64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
+    case 128: attn_dkdv_bf16<128><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -574,13 +578,13 @@ hipError_t launch_bwd_dq_bf16(const AttnProblem &p, const uint16_t *Q, const uin
                               const uint16_t *V, const uint16_t *dO, const float *LSE,
                               const float *Dws, uint16_t *dQ, hipStream_t s) {
     const int BH = p.B * p.H;
-    const int nqt = cdiv(p.L, kFwdRows);
+    const int nqt = cdiv(p.Lq, kFwdRows);
     const dim3 grid(nqt * BH), block(kThreads);
     const float sl2 = p.scale * kLog2e;
     switch (p.d) {
-    case 32: attn_dq_bf16<32, 64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
-    case 64: attn_dq_bf16<64, 64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
-    case 128: attn_dq_bf16<128, 64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
+    case 32: attn_dq_bf16<32, 64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, nqt, BH); break;
+    case 64: attn_dq_bf16<64, 64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, nqt, BH); break;
+    case 128: attn_dq_bf16<128, 64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, nqt, BH); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

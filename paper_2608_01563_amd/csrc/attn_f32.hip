@@ -106,7 +106,7 @@ template <int D, class C>
 __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::template occ<D>(), 8)))
 void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
                   const float *__restrict__ V, float *__restrict__ O, float *__restrict__ LSE,
-                  const int32_t *__restrict__ key_len, int H, int L, int causal,
+                  const int32_t *__restrict__ key_len, int H, int Lq, int Lk, int causal,
                   float scale_log2, int n_qtiles, int BH) {
     constexpr int KS = kFwdStream;
     constexpr int DQ = D / 4;    // contraction values per lane in one S chain
@@ -122,9 +122,10 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
     const int head = blockIdx.x - rank * BH;
     const int qt = causal ? (n_qtiles - 1 - rank) : rank;
     const int b = head / H;
-    const float *Qh = Q + (size_t)head * L * D;
-    const float *Kh = K + (size_t)head * L * D;
-    const float *Vh = V + (size_t)head * L * D;
+    const float *Qh = Q + (size_t)head * Lq * D;
+    const float *Kh = K + (size_t)head * Lk * D;
+    const float *Vh = V + (size_t)head * Lk * D;
+    const int diag = Lk - Lq;   // causal: row i sees keys j <= i + diag
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -135,8 +136,8 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
     const int qw0 = q0 + 16 * w;   // first query row of this wave
     const int qi = qw0 + il;
 
-    const int klen = key_limit(key_len, b, L);
-    const int kend = causal ? min(klen, q0 + C::ROWS) : klen;
+    const int klen = key_limit(key_len, b, Lk);
+    const int kend = causal ? min(klen, q0 + C::ROWS + diag) : klen;
     const int ntiles = (kend + KS - 1) / KS;
 
     Tile tile;
@@ -151,8 +152,8 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
 #pragma unroll
         for (int c = 0; c < NC; ++c) voffs[r][c] = Tile::at(4 * g + r, 16 * c + il);
     if (ntiles > 0) {
-        tile.issue(Ks, Kh, 0, L, w);
-        tile.issue(Vs, Vh, 0, L, w);
+        tile.issue(Ks, Kh, 0, Lk, w);
+        tile.issue(Vs, Vh, 0, Lk, w);
     }
 
     // B operand of S^T = K Q^T: lane holds Q[qi][g*DQ + s] times
@@ -160,7 +161,7 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
     float qreg[DQ];
 #pragma unroll
     for (int s4 = 0; s4 < DQ / 4; ++s4) {
-        f32x4 v = (qi < L) ? *reinterpret_cast<const f32x4 *>(Qh + (size_t)qi * D + g * DQ + 4 * s4)
+        f32x4 v = (qi < Lq) ? *reinterpret_cast<const f32x4 *>(Qh + (size_t)qi * D + g * DQ + 4 * s4)
                            : zero4();
 #pragma unroll
         for (int e = 0; e < 4; ++e) qreg[4 * s4 + e] = v[e] * scale_log2;
@@ -181,7 +182,7 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
         // The products of the other blocks are skipped; their scores are
         // masked below and their probabilities are exactly zero.
         const int jt = kt * KS;
-        const int kcut = causal ? min(klen, qw0 + 16) : klen;
+        const int kcut = causal ? min(klen, qw0 + 16 + diag) : klen;
         const int nlive = min(NJB, (kcut - jt + 15) / 16);
 
         // S^T[16jb + 4g + r][qi] = sum_k K[j][k] Q[qi][k]
@@ -217,15 +218,15 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
         }
         wait_vmcnt<0>();   // V(kt) landed
         __syncthreads();   // every wave is done with K(kt) and sees V(kt)
-        if (kt + 1 < ntiles) tile.issue(Ks, Kh, (kt + 1) * KS, L, w);
+        if (kt + 1 < ntiles) tile.issue(Ks, Kh, (kt + 1) * KS, Lk, w);
 
         // Element (jb, r) holds key j0 + 16jb + r, allowed iff that offset is
         // below a per-lane threshold (key length; the query row if causal).
         // Only tiles that reach past the key length or past the wave's first
         // query row (causal) hold masked elements.
-        if (jt + KS > klen || (causal && jt + KS - 1 > qw0)) {
+        if (jt + KS > klen || (causal && jt + KS - 1 > qw0 + diag)) {
             const int j0 = jt + 4 * g;
-            const int thr = causal ? min(klen - j0, qi - j0 + 1) : klen - j0;
+            const int thr = causal ? min(klen - j0, qi + diag - j0 + 1) : klen - j0;
 #pragma unroll
             for (int jb = 0; jb < NJB; ++jb)
 #pragma unroll
@@ -273,18 +274,18 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
         wait_vmcnt<0>();   // K(kt+1) landed
         __syncthreads();   // every wave is done with V(kt) and sees K(kt+1)
-        if (kt + 1 < ntiles) tile.issue(Vs, Vh, (kt + 1) * KS, L, w);
+        if (kt + 1 < ntiles) tile.issue(Vs, Vh, (kt + 1) * KS, Lk, w);
     }
 
     const float l = sum_over_groups(l_run);
-    if (qi < L) {
+    if (qi < Lq) {
         const float inv = (l > 0.f) ? 1.f / l : 0.f;
-        float *orow = O + ((size_t)head * L + qi) * D;
+        float *orow = O + ((size_t)head * Lq + qi) * D;
 #pragma unroll
         for (int c = 0; c < NC; ++c)
             *reinterpret_cast<f32x4 *>(orow + 16 * c + 4 * g) = oacc[c] * inv;
         if (g == 0)
-            LSE[(size_t)head * L + qi] = (l > 0.f) ? (m_run + log2f(l)) * kLn2 : -INFINITY;
+            LSE[(size_t)head * Lq + qi] = (l > 0.f) ? (m_run + log2f(l)) * kLn2 : -INFINITY;
     }
 }
 
@@ -316,7 +317,7 @@ void attn_dkdv_f32(const float *__restrict__ Q, const float *__restrict__ K,
                    const float *__restrict__ V, const float *__restrict__ dO,
                    const float *__restrict__ LSE, const float *__restrict__ Dws,
                    float *__restrict__ dK, float *__restrict__ dV,
-                   const int32_t *__restrict__ key_len, int H, int L, int causal, float scale,
+                   const int32_t *__restrict__ key_len, int H, int Lq, int Lk, int causal, float scale,
                    float scale_log2, int BH) {
     constexpr int DQ = D / 4;
     constexpr int NC = D / 16;
@@ -332,9 +333,10 @@ void attn_dkdv_f32(const float *__restrict__ Q, const float *__restrict__ K,
     const int head = blockIdx.x - rank * BH;
     const int kt = rank;   // low key tiles see the most queries under a causal mask
     const int b = head / H;
-    const size_t hoff = (size_t)head * L * D;
-    const float *Qh = Q + hoff;
-    const float *dOh = dO + hoff;
+    const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
+    const float *Qh = Q + qoff;
+    const float *dOh = dO + qoff;
+    const int diag = Lk - Lq;   // causal: row i sees keys j <= i + diag
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -343,9 +345,10 @@ void attn_dkdv_f32(const float *__restrict__ Q, const float *__restrict__ K,
     const int k0 = kt * C::ROWS;
     const int kj = k0 + 16 * (tid >> 6) + il;   // this lane's key
 
-    const int klen = key_limit(key_len, b, L);
-    const int nq = (L + BR - 1) / BR;
-    const int qstart = causal ? (k0 / BR) : 0;
+    const int klen = key_limit(key_len, b, Lk);
+    const int nq = (Lq + BR - 1) / BR;
+    // first query tile holding a row that sees key k0
+    const int qstart = causal ? min(nq, max(0, k0 - diag) / BR) : 0;
     const int qstop = (k0 < klen) ? nq : qstart;   // a fully padded key tile does no work
 
     // B operands of S = Q K^T and dP = dO V^T: lane holds K[kj][g*DQ + s].
@@ -353,8 +356,8 @@ void attn_dkdv_f32(const float *__restrict__ Q, const float *__restrict__ K,
 #pragma unroll
     for (int s4 = 0; s4 < DQ / 4; ++s4) {
         const size_t off = hoff + (size_t)kj * D + g * DQ + 4 * s4;
-        const f32x4 kv = (kj < L) ? *reinterpret_cast<const f32x4 *>(K + off) : zero4();
-        const f32x4 vv = (kj < L) ? *reinterpret_cast<const f32x4 *>(V + off) : zero4();
+        const f32x4 kv = (kj < Lk) ? *reinterpret_cast<const f32x4 *>(K + off) : zero4();
+        const f32x4 vv = (kj < Lk) ? *reinterpret_cast<const f32x4 *>(V + off) : zero4();
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             kreg[4 * s4 + e] = kv[e];
@@ -372,14 +375,14 @@ void attn_dkdv_f32(const float *__restrict__ Q, const float *__restrict__ K,
     Stager qst, ost;
     float lse_pre = 0.f, d_pre = 0.f;
     auto load_rows = [&](int qt) {
-        qst.load(Qh, qt * BR, L, tid);
-        ost.load(dOh, qt * BR, L, tid);
+        qst.load(Qh, qt * BR, Lq, tid);
+        ost.load(dOh, qt * BR, Lq, tid);
         if (tid < BR) {
             const int row = qt * BR + tid;
             // natural log; scaled to base 2 at the LDS store so that nothing waits
             // for this load before the next tile's rows are consumed
-            lse_pre = (row < L) ? LSE[(size_t)head * L + row] : 0.f;
-            d_pre = (row < L) ? Dws[(size_t)head * L + row] : 0.f;
+            lse_pre = (row < Lq) ? LSE[(size_t)head * Lq + row] : 0.f;
+            d_pre = (row < Lq) ? Dws[(size_t)head * Lq + row] : 0.f;
         }
     };
     auto store_rows = [&](int buf) {
@@ -432,12 +435,12 @@ void attn_dkdv_f32(const float *__restrict__ Q, const float *__restrict__ K,
         }
 
         // P = exp(S - LSE), dS = P (dP - D).  Under a causal mask element
-        // (ib, r) is query ibase + 16ib + r, allowed iff it is >= kj.  Padded
+        // (ib, r) is query ibase + 16ib + r, allowed iff it is >= kj - diag.  Padded
         // keys (kj >= key length) are not masked here: their rows of dK and dV
-        // are overwritten with zeros at the end.  Rows past L hold Q = dO = 0
+        // are overwritten with zeros at the end.  Rows past Lq hold Q = dO = 0
         // and LSE = D = 0, so they contribute exactly nothing.
         const int ibase = qt * BR + 4 * g;
-        const int thr = causal ? kj - ibase : INT_MIN;
+        const int thr = causal ? kj - diag - ibase : INT_MIN;
 #pragma unroll
         for (int ib = 0; ib < NIB; ++ib) {
             const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lse2s[cur][16 * ib + 4 * g]);
@@ -471,7 +474,7 @@ void attn_dkdv_f32(const float *__restrict__ Q, const float *__restrict__ K,
         }
     }
 
-    if (kj < L) {
+    if (kj < Lk) {
         const bool keep = kj < klen;   // padded keys get exact zeros
         float *dkrow = dK + hoff + (size_t)kj * D;
         float *dvrow = dV + hoff + (size_t)kj * D;
@@ -502,7 +505,7 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
                     const float *__restrict__ V, const float *__restrict__ dO,
                     const float *__restrict__ LSE, const float *__restrict__ Dws,
                     float *__restrict__ dK, float *__restrict__ dV, float *__restrict__ dQp,
-                    const int32_t *__restrict__ key_len, int H, int L, int causal, float scale,
+                    const int32_t *__restrict__ key_len, int H, int Lq, int Lk, int causal, float scale,
                     float scale_log2, int BH) {
     constexpr int DQ = D / 4;
     constexpr int NC = D / 16;
@@ -524,9 +527,10 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     const int head = blockIdx.x - rank * BH;
     const int kt = rank;
     const int b = head / H;
-    const size_t hoff = (size_t)head * L * D;
-    const float *Qh = Q + hoff;
-    const float *dOh = dO + hoff;
+    const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
+    const float *Qh = Q + qoff;
+    const float *dOh = dO + qoff;
+    const int diag = Lk - Lq;   // causal: row i sees keys j <= i + diag
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -537,21 +541,22 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     const int wkey0 = k0 + 16 * w;   // first key of this wave (wave-uniform)
     const int kj = wkey0 + il;
 
-    const int klen = key_limit(key_len, b, L);
-    const int nq = (L + BR - 1) / BR;
-    const int qstart = causal ? (k0 / BR) : 0;
+    const int klen = key_limit(key_len, b, Lk);
+    const int nq = (Lq + BR - 1) / BR;
+    // first query tile holding a row that sees key k0
+    const int qstart = causal ? min(nq, max(0, k0 - diag) / BR) : 0;
     const int qstop = (k0 < klen) ? nq : qstart;
 
     const Tile tile;
 
     float lse_pre = 0.f, d_pre = 0.f;
     auto fetch = [&](int qt, int buf) {   // direct loads of Q, dO; LSE, D to registers
-        tile.issue(Qs[buf], Qh, qt * BR, L, w, lane);
-        tile.issue(dOs[buf], dOh, qt * BR, L, w, lane);
+        tile.issue(Qs[buf], Qh, qt * BR, Lq, w, lane);
+        tile.issue(dOs[buf], dOh, qt * BR, Lq, w, lane);
         if (tid < BR) {
             const int row = qt * BR + tid;
-            lse_pre = (row < L) ? LSE[(size_t)head * L + row] : 0.f;
-            d_pre = (row < L) ? Dws[(size_t)head * L + row] : 0.f;
+            lse_pre = (row < Lq) ? LSE[(size_t)head * Lq + row] : 0.f;
+            d_pre = (row < Lq) ? Dws[(size_t)head * Lq + row] : 0.f;
         }
     };
     auto publish = [&](int buf) {   // LSE (base 2) and D of the fetched rows
@@ -566,8 +571,8 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
 #pragma unroll
     for (int s4 = 0; s4 < DQ / 4; ++s4) {
         const size_t off = hoff + (size_t)kj * D + g * DQ + 4 * s4;
-        const f32x4 kv = (kj < L) ? *reinterpret_cast<const f32x4 *>(K + off) : zero4();
-        const f32x4 vv = (kj < L) ? *reinterpret_cast<const f32x4 *>(V + off) : zero4();
+        const f32x4 kv = (kj < Lk) ? *reinterpret_cast<const f32x4 *>(K + off) : zero4();
+        const f32x4 vv = (kj < Lk) ? *reinterpret_cast<const f32x4 *>(V + off) : zero4();
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             kreg[4 * s4 + e] = kv[e];
@@ -578,7 +583,7 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     for (int f = tid; f < KR * (D / 4); f += C::NT) {
         const int row = f / (D / 4);
         const int c4 = f - row * (D / 4);
-        const f32x4 v = (k0 + row < L)
+        const f32x4 v = (k0 + row < Lk)
             ? *reinterpret_cast<const f32x4 *>(K + hoff + (size_t)(k0 + row) * D + 4 * c4)
             : zero4();
 #pragma unroll
@@ -593,11 +598,11 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     }
 
     // Under a causal mask element (ib, r) is query ibase + 16ib + r, allowed
-    // iff it is >= kj; a padded key (kj >= key length) is masked everywhere
+    // iff it is >= kj - diag; a padded key (kj >= key length) is masked everywhere
     // so that it adds nothing to dQ.
     // (sentinels +-2^30 keep kthr - ibase free of overflow)
     constexpr int kNever = 1 << 30;
-    const int kthr = (kj >= klen) ? kNever : (causal ? kj : -kNever);
+    const int kthr = (kj >= klen) ? kNever : (causal ? kj - diag : -kNever);
 
     // dQ partial blocks of this wave: consecutive blocks (same query rows,
     // shared dS reads) when they split evenly, else strided
@@ -613,8 +618,8 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
             const int ib = blk / NC;
             const int c = blk - ib * NC;
             const int row = qt * BR + 16 * ib + il;
-            if (row < L)
-                *reinterpret_cast<f32x4 *>(dQp + ((size_t)kt * BH + head) * L * D +
+            if (row < Lq)
+                *reinterpret_cast<f32x4 *>(dQp + ((size_t)kt * BH + head) * Lq * D +
                                            (size_t)row * D + 16 * c + 4 * g) = dqacc[bb];
         }
     };
@@ -633,7 +638,7 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
         // A wave whose 16 keys are all masked for every row of this query
         // tile (padded keys, or keys past the tile's last row under a causal
         // mask) contributes nothing but its zero block of dS.
-        const bool live = wkey0 < klen && (!causal || wkey0 <= qt * BR + BR - 1);
+        const bool live = wkey0 < klen && (!causal || wkey0 - diag <= qt * BR + BR - 1);
         if (live) {
             f32x4 sacc[NIB], pacc[NIB];
 #pragma unroll
@@ -721,7 +726,7 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     }
     if (qstart < qstop) store_dq(qstop - 1);
 
-    if (kj < L) {
+    if (kj < Lk) {
         const bool keep = kj < klen;
         float *dkrow = dK + hoff + (size_t)kj * D;
         float *dvrow = dV + hoff + (size_t)kj * D;
@@ -734,24 +739,28 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
 }
 
 // dQ[i] = scale * sum over key tiles kt that hold an allowed key for row i of
-// dQ_part[kt][i], added in increasing kt (a fixed order).
+// dQ_part[kt][i], added in increasing kt (a fixed order).  Partials are laid
+// out [key tile][B*H][Lq][d].
 template <int D>
 __global__ __launch_bounds__(256) void attn_dq_reduce_f32(const float *__restrict__ dQp,
                                                           float *__restrict__ dQ,
                                                           const int32_t *__restrict__ key_len,
-                                                          int H, int L, int causal, float scale,
+                                                          int H, int Lq, int Lk, int causal,
+                                                          float scale,
                                                           int BH, int key_rows) {
     constexpr int C4 = D / 4;
     const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
-    const size_t total = (size_t)BH * L * C4;
+    const size_t total = (size_t)BH * Lq * C4;
     if (idx >= total) return;
-    const size_t rowg = idx / C4;              // head * L + i
-    const int head = (int)(rowg / L);
-    const int i = (int)(rowg - (size_t)head * L);
-    const int klen = key_limit(key_len, head / H, L);
+    const size_t rowg = idx / C4;              // head * Lq + i
+    const int head = (int)(rowg / Lq);
+    const int i = (int)(rowg - (size_t)head * Lq);
+    const int klen = key_limit(key_len, head / H, Lk);
     const int nk = (klen + key_rows - 1) / key_rows;
-    const int kmax = causal ? min(nk, i / key_rows + 1) : nk;
-    const size_t stride = (size_t)BH * L * D;
+    // causal: row i sees keys j <= i + Lk - Lq, i.e. key tiles up to that key's
+    const int last = i + Lk - Lq;
+    const int kmax = causal ? (last < 0 ? 0 : min(nk, last / key_rows + 1)) : nk;
+    const size_t stride = (size_t)BH * Lq * D;
     const float *src = dQp + idx * 4;
     f32x4 sum = zero4();
     for (int kt = 0; kt < kmax; ++kt)
@@ -766,8 +775,8 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::templa
 void attn_dq_f32(const float *__restrict__ Q, const float *__restrict__ K,
                  const float *__restrict__ V, const float *__restrict__ dO,
                  const float *__restrict__ LSE, const float *__restrict__ Dws,
-                 float *__restrict__ dQ, const int32_t *__restrict__ key_len, int H, int L,
-                 int causal, float scale, float scale_log2, int n_qtiles, int BH) {
+                 float *__restrict__ dQ, const int32_t *__restrict__ key_len, int H, int Lq,
+                 int Lk, int causal, float scale, float scale_log2, int n_qtiles, int BH) {
     constexpr int DQ = D / 4;
     constexpr int NC = D / 16;
     using Stager = F32TileStager<kStream, D, C::NT>;
@@ -779,9 +788,10 @@ void attn_dq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     const int head = blockIdx.x - rank * BH;
     const int qt = causal ? (n_qtiles - 1 - rank) : rank;
     const int b = head / H;
-    const size_t hoff = (size_t)head * L * D;
+    const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
     const float *Kh = K + hoff;
     const float *Vh = V + hoff;
+    const int diag = Lk - Lq;   // causal: row i sees keys j <= i + diag
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -790,24 +800,24 @@ void attn_dq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     const int q0 = qt * C::ROWS;
     const int qi = q0 + 16 * (tid >> 6) + il;
 
-    const int klen = key_limit(key_len, b, L);
-    const int kend = causal ? min(klen, q0 + C::ROWS) : klen;
+    const int klen = key_limit(key_len, b, Lk);
+    const int kend = causal ? min(klen, q0 + C::ROWS + diag) : klen;
     const int ntiles = (kend + kStream - 1) / kStream;
 
     float qreg[DQ], oreg[DQ];
 #pragma unroll
     for (int s4 = 0; s4 < DQ / 4; ++s4) {
-        const size_t off = hoff + (size_t)qi * D + g * DQ + 4 * s4;
-        const f32x4 qv = (qi < L) ? *reinterpret_cast<const f32x4 *>(Q + off) : zero4();
-        const f32x4 ov = (qi < L) ? *reinterpret_cast<const f32x4 *>(dO + off) : zero4();
+        const size_t off = qoff + (size_t)qi * D + g * DQ + 4 * s4;
+        const f32x4 qv = (qi < Lq) ? *reinterpret_cast<const f32x4 *>(Q + off) : zero4();
+        const f32x4 ov = (qi < Lq) ? *reinterpret_cast<const f32x4 *>(dO + off) : zero4();
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
             qreg[4 * s4 + e] = qv[e];
             oreg[4 * s4 + e] = ov[e];
         }
     }
-    const float lse2 = (qi < L) ? LSE[(size_t)head * L + qi] * kLog2e : 0.f;
-    const float Di = (qi < L) ? Dws[(size_t)head * L + qi] : 0.f;
+    const float lse2 = (qi < Lq) ? LSE[(size_t)head * Lq + qi] * kLog2e : 0.f;
+    const float Di = (qi < Lq) ? Dws[(size_t)head * Lq + qi] : 0.f;
 
     f32x4 dqacc[NC];   // dQ^T[16c + 4g + r][qi]
 #pragma unroll
@@ -815,8 +825,8 @@ void attn_dq_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
     Stager kst, vst;
     if (ntiles > 0) {
-        kst.load(Kh, 0, L, tid);
-        vst.load(Vh, 0, L, tid);
+        kst.load(Kh, 0, Lk, tid);
+        vst.load(Vh, 0, Lk, tid);
         if (C::NBUF == 2) {
             kst.store(Ks[0], tid);
             vst.store(Vs[0], tid);
@@ -832,8 +842,8 @@ void attn_dq_f32(const float *__restrict__ Q, const float *__restrict__ K,
             __syncthreads();
         }
         if (kt + 1 < ntiles) {
-            kst.load(Kh, (kt + 1) * kStream, L, tid);
-            vst.load(Vh, (kt + 1) * kStream, L, tid);
+            kst.load(Kh, (kt + 1) * kStream, Lk, tid);
+            vst.load(Vh, (kt + 1) * kStream, Lk, tid);
         }
 
         // S^T[j][qi] and dP^T[j][qi], j = 16jb + 4g + r
@@ -862,7 +872,7 @@ void attn_dq_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
         // Element (jb, r) holds key j0 + 16jb + r; same threshold as forward.
         const int j0 = kt * kStream + 4 * g;
-        const int thr = causal ? min(klen - j0, qi - j0 + 1) : klen - j0;
+        const int thr = causal ? min(klen - j0, qi + diag - j0 + 1) : klen - j0;
 #pragma unroll
         for (int jb = 0; jb < 4; ++jb)
 #pragma unroll
@@ -891,8 +901,8 @@ void attn_dq_f32(const float *__restrict__ Q, const float *__restrict__ K,
         }
     }
 
-    if (qi < L) {
-        float *dqrow = dQ + hoff + (size_t)qi * D;
+    if (qi < Lq) {
+        float *dqrow = dQ + qoff + (size_t)qi * D;
 #pragma unroll
         for (int c = 0; c < NC; ++c)
             *reinterpret_cast<f32x4 *>(dqrow + 16 * c + 4 * g) = dqacc[c] * scale;
@@ -908,13 +918,13 @@ hipError_t launch_fwd_f32(const AttnProblem &p, const float *Q, const float *K,
                           const float *V, float *O, float *LSE, hipStream_t s) {
     using C = FwdCfg;
     const int BH = p.B * p.H;
-    const int nqt = cdiv(p.L, C::ROWS);
+    const int nqt = cdiv(p.Lq, C::ROWS);
     const dim3 grid(nqt * BH), block(C::NT);
     const float sl2 = p.scale * kLog2e;
     switch (p.d) {
-    case 32: attn_fwd_f32<32, C><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.L, p.causal, sl2, nqt, BH); break;
-    case 64: attn_fwd_f32<64, C><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.L, p.causal, sl2, nqt, BH); break;
-    case 128: attn_fwd_f32<128, C><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.L, p.causal, sl2, nqt, BH); break;
+    case 32: attn_fwd_f32<32, C><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal, sl2, nqt, BH); break;
+    case 64: attn_fwd_f32<64, C><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal, sl2, nqt, BH); break;
+    case 128: attn_fwd_f32<128, C><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal, sl2, nqt, BH); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -922,7 +932,7 @@ hipError_t launch_fwd_f32(const AttnProblem &p, const float *Q, const float *K,
 
 hipError_t launch_bwd_rowdot_f32(const AttnProblem &p, const float *O, const float *dO,
                                  float *Dws, hipStream_t s) {
-    const int rows = p.B * p.H * p.L;
+    const int rows = p.B * p.H * p.Lq;
     const dim3 block(256);
     switch (p.d) {
     case 32: attn_rowdot_f32<32><<<dim3(cdiv(rows, 256 / 8)), block, 0, s>>>(O, dO, Dws, rows); break;
@@ -938,12 +948,12 @@ hipError_t launch_bwd_dkdv_f32(const AttnProblem &p, const float *Q, const float
                                const float *Dws, float *dK, float *dV, hipStream_t s) {
     using C = DkdvCfg;
     const int BH = p.B * p.H;
-    const dim3 grid(cdiv(p.L, C::ROWS) * BH), block(C::NT);
+    const dim3 grid(cdiv(p.Lk, C::ROWS) * BH), block(C::NT);
     const float sl2 = p.scale * kLog2e;
     switch (p.d) {
-    case 32: attn_dkdv_f32<32, MG_DKDV_NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
-    case 64: attn_dkdv_f32<64, MG_DKDV_NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
-    case 128: attn_dkdv_f32<128, 2, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
+    case 32: attn_dkdv_f32<32, MG_DKDV_NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
+    case 64: attn_dkdv_f32<64, MG_DKDV_NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
+    case 128: attn_dkdv_f32<128, 2, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -953,7 +963,7 @@ hipError_t launch_bwd_dkdv_f32(const AttnProblem &p, const float *Q, const float
 // ordering keeps the fewer workgroups balanced, and the partials halve);
 // the rest keep 64-key tiles, which measured faster there.
 bool wide_key_tiles(const AttnProblem &p) {
-    return p.causal && (long)cdiv(p.L, DkdvqCausalCfg::ROWS) * p.B * p.H >= 512;
+    return p.causal && (long)cdiv(p.Lk, DkdvqCausalCfg::ROWS) * p.B * p.H >= 512;
 }
 int fused_dq_key_rows(const AttnProblem &p) {
     return wide_key_tiles(p) ? DkdvqCausalCfg::ROWS : DkdvCfg::ROWS;
@@ -965,11 +975,11 @@ static hipError_t launch_dkdvq(const AttnProblem &p, const float *Q, const float
                                const float *Dws, float *dK, float *dV, float *dQp,
                                hipStream_t s) {
     const int BH = p.B * p.H;
-    const dim3 grid(cdiv(p.L, C::ROWS) * BH), block(C::NT);
+    const dim3 grid(cdiv(p.Lk, C::ROWS) * BH), block(C::NT);
     const float sl2 = p.scale * kLog2e;
     switch (p.d) {
-    case 32: attn_dkdvq_f32<32, NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
-    case 64: attn_dkdvq_f32<64, NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, p.key_len, p.H, p.L, p.causal, p.scale, sl2, BH); break;
+    case 32: attn_dkdvq_f32<32, NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
+    case 64: attn_dkdvq_f32<64, NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -987,12 +997,12 @@ hipError_t launch_bwd_dkdvq_f32(const AttnProblem &p, const float *Q, const floa
 hipError_t launch_bwd_dq_reduce_f32(const AttnProblem &p, const float *dQp, float *dQ,
                                     hipStream_t s) {
     const int BH = p.B * p.H;
-    const size_t total = (size_t)BH * p.L * (p.d / 4);
+    const size_t total = (size_t)BH * p.Lq * (p.d / 4);
     const dim3 grid((unsigned)((total + 255) / 256)), block(256);
     const int kr = fused_dq_key_rows(p);
     switch (p.d) {
-    case 32: attn_dq_reduce_f32<32><<<grid, block, 0, s>>>(dQp, dQ, p.key_len, p.H, p.L, p.causal, p.scale, BH, kr); break;
-    case 64: attn_dq_reduce_f32<64><<<grid, block, 0, s>>>(dQp, dQ, p.key_len, p.H, p.L, p.causal, p.scale, BH, kr); break;
+    case 32: attn_dq_reduce_f32<32><<<grid, block, 0, s>>>(dQp, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, BH, kr); break;
+    case 64: attn_dq_reduce_f32<64><<<grid, block, 0, s>>>(dQp, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, BH, kr); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -1003,13 +1013,13 @@ hipError_t launch_bwd_dq_f32(const AttnProblem &p, const float *Q, const float *
                              const float *Dws, float *dQ, hipStream_t s) {
     using C = DqCfg;
     const int BH = p.B * p.H;
-    const int nqt = cdiv(p.L, C::ROWS);
+    const int nqt = cdiv(p.Lq, C::ROWS);
     const dim3 grid(nqt * BH), block(C::NT);
     const float sl2 = p.scale * kLog2e;
     switch (p.d) {
-    case 32: attn_dq_f32<32, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
-    case 64: attn_dq_f32<64, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
-    case 128: attn_dq_f32<128, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.L, p.causal, p.scale, sl2, nqt, BH); break;
+    case 32: attn_dq_f32<32, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, nqt, BH); break;
+    case 64: attn_dq_f32<64, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, nqt, BH); break;
+    case 128: attn_dq_f32<128, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, nqt, BH); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

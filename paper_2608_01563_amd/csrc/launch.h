@@ -11,8 +11,11 @@
 
 namespace mg {
 
+// Q, O, dO, dQ are [B][H][Lq][d]; K, V, dK, dV are [B][H][Lk][d]; LSE and D
+// are [B][H][Lq].  Under a causal mask query row i sees keys j <= i + Lk - Lq
+// (bottom-right alignment; j <= i when Lq == Lk).
 struct AttnProblem {
-    int B, H, L, d;
+    int B, H, Lq, Lk, d;
     int causal;
     float scale;
     const int32_t *key_len;  // device [B] or nullptr

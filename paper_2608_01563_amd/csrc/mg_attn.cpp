@@ -6,6 +6,7 @@
 // launch geometry are chosen together by the per-kernel launchers.
 #include "mg_attn.h"
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdint>
@@ -40,18 +41,20 @@ mg_status_t ok() {
 
 constexpr int64_t kMaxElems = INT32_MAX;
 
-mg_status_t check_shape(int B, int H, int L, int d, float scale, mg_contract_t contract) {
+mg_status_t check_shape(int B, int H, int Lq, int Lk, int d, float scale,
+                        mg_contract_t contract) {
     if (contract != MG_CONTRACT_STRICT_F32 && contract != MG_CONTRACT_FAST_BF16 &&
         contract != MG_CONTRACT_ACCELERATED)
         return fail(MG_ERR_INVALID_ARGUMENT, "unknown contract %d", (int)contract);
-    if (B < 1 || H < 1 || L < 1 || d < 1)
-        return fail(MG_ERR_INVALID_ARGUMENT, "sizes must be >= 1 (B=%d H=%d L=%d d=%d)", B, H,
-                    L, d);
+    if (B < 1 || H < 1 || Lq < 1 || Lk < 1 || d < 1)
+        return fail(MG_ERR_INVALID_ARGUMENT,
+                    "sizes must be >= 1 (B=%d H=%d Lq=%d Lk=%d d=%d)", B, H, Lq, Lk, d);
     if (d != 32 && d != 64 && d != 128)
         return fail(MG_ERR_UNSUPPORTED, "head dimension d=%d not in {32, 64, 128}", d);
-    const int64_t n = (int64_t)B * H * L * d;
+    const int64_t n = (int64_t)B * H * std::max(Lq, Lk) * d;
     if (n > kMaxElems)
-        return fail(MG_ERR_INVALID_ARGUMENT, "B*H*L*d = %lld exceeds 2^31-1", (long long)n);
+        return fail(MG_ERR_INVALID_ARGUMENT, "B*H*max(Lq,Lk)*d = %lld exceeds 2^31-1",
+                    (long long)n);
     if (!std::isfinite(scale)) return fail(MG_ERR_INVALID_ARGUMENT, "scale is not finite");
     return MG_OK;
 }
@@ -189,22 +192,24 @@ mg_contract_t backward_contract(mg_contract_t c) {
 // a separate query-stationary dQ kernel recomputes what it needs.
 constexpr size_t kFusedPartialLimit = size_t(1) << 30;
 
-size_t dq_partial_bytes(int B, int H, int L, int d, int causal) {
-    const mg::AttnProblem p{B, H, L, d, causal ? 1 : 0, 1.0f, nullptr};
+size_t dq_partial_bytes(int B, int H, int Lq, int Lk, int d, int causal) {
+    const mg::AttnProblem p{B, H, Lq, Lk, d, causal ? 1 : 0, 1.0f, nullptr};
     const int kr = mg::fused_dq_key_rows(p);
-    return (size_t)((L + kr - 1) / kr) * B * H * L * d * sizeof(float);
+    return (size_t)((Lk + kr - 1) / kr) * B * H * Lq * d * sizeof(float);
 }
 
-bool use_fused_dq(int B, int H, int L, int d, int causal, mg_contract_t contract) {
+bool use_fused_dq(int B, int H, int Lq, int Lk, int d, int causal, mg_contract_t contract) {
     return contract == MG_CONTRACT_STRICT_F32 && d <= 64 &&
-           dq_partial_bytes(B, H, L, d, causal) <= kFusedPartialLimit;
+           dq_partial_bytes(B, H, Lq, Lk, d, causal) <= kFusedPartialLimit;
 }
 
-// Layout: D (f32 per row) first, then the dQ partials when fused.
-size_t workspace_bytes(int B, int H, int L, int d, int causal, mg_contract_t contract) {
+// Layout: D (f32 per query row) first, then the dQ partials when fused.
+size_t workspace_bytes(int B, int H, int Lq, int Lk, int d, int causal,
+                       mg_contract_t contract) {
     contract = backward_contract(contract);
-    size_t n = round256((size_t)B * H * L * sizeof(float));
-    if (use_fused_dq(B, H, L, d, causal, contract)) n += dq_partial_bytes(B, H, L, d, causal);
+    size_t n = round256((size_t)B * H * Lq * sizeof(float));
+    if (use_fused_dq(B, H, Lq, Lk, d, causal, contract))
+        n += dq_partial_bytes(B, H, Lq, Lk, d, causal);
     return n;
 }
 
@@ -212,13 +217,14 @@ size_t workspace_bytes(int B, int H, int L, int d, int causal, mg_contract_t con
 
 extern "C" {
 
-mg_status_t mg_attn_fwd(const void *Q, const void *K, const void *V, void *O, float *LSE,
-                        const int32_t *key_len, int B, int H, int L, int d, int causal,
-                        float scale, mg_contract_t contract, hipStream_t stream) {
-    MG_TRY(check_shape(B, H, L, d, scale, contract));
+mg_status_t mg_attn_fwd_cross(const void *Q, const void *K, const void *V, void *O, float *LSE,
+                              const int32_t *key_len, int B, int H, int Lq, int Lk, int d,
+                              int causal, float scale, mg_contract_t contract,
+                              hipStream_t stream) {
+    MG_TRY(check_shape(B, H, Lq, Lk, d, scale, contract));
     MG_TRY(check_tensors({{Q, "Q"}, {K, "K"}, {V, "V"}, {O, "O"}, {LSE, "LSE"}}));
     MG_TRY(check_key_len(key_len));
-    const mg::AttnProblem p{B, H, L, d, causal ? 1 : 0, scale, key_len};
+    const mg::AttnProblem p{B, H, Lq, Lk, d, causal ? 1 : 0, scale, key_len};
     if (contract == MG_CONTRACT_STRICT_F32) {
         MG_TRY(run_kernel(kernel_name("attn_fwd", contract, d), stream, [&] {
             return mg::launch_fwd_f32(p, (const float *)Q, (const float *)K, (const float *)V,
@@ -238,29 +244,29 @@ mg_status_t mg_attn_fwd(const void *Q, const void *K, const void *V, void *O, fl
     return ok();
 }
 
-size_t mg_attn_bwd_workspace_bytes(int B, int H, int L, int d, int causal,
-                                   mg_contract_t contract) {
+size_t mg_attn_bwd_cross_workspace_bytes(int B, int H, int Lq, int Lk, int d, int causal,
+                                         mg_contract_t contract) {
     std::string saved = g_detail;
-    mg_status_t st = check_shape(B, H, L, d, 1.0f, contract);
+    mg_status_t st = check_shape(B, H, Lq, Lk, d, 1.0f, contract);
     g_detail = saved;
     if (st != MG_OK) return 0;
-    return workspace_bytes(B, H, L, d, causal, contract);
+    return workspace_bytes(B, H, Lq, Lk, d, causal, contract);
 }
 
-mg_status_t mg_attn_bwd(const void *Q, const void *K, const void *V, const void *O,
-                        const float *LSE, const void *dO, void *dQ, void *dK, void *dV,
-                        const int32_t *key_len, int B, int H, int L, int d, int causal,
-                        float scale, mg_contract_t contract, void *workspace,
-                        size_t ws_bytes, hipStream_t stream) {
-    MG_TRY(check_shape(B, H, L, d, scale, contract));
-    const size_t need = workspace_bytes(B, H, L, d, causal, contract);
+mg_status_t mg_attn_bwd_cross(const void *Q, const void *K, const void *V, const void *O,
+                              const float *LSE, const void *dO, void *dQ, void *dK, void *dV,
+                              const int32_t *key_len, int B, int H, int Lq, int Lk, int d,
+                              int causal, float scale, mg_contract_t contract, void *workspace,
+                              size_t ws_bytes, hipStream_t stream) {
+    MG_TRY(check_shape(B, H, Lq, Lk, d, scale, contract));
+    const size_t need = workspace_bytes(B, H, Lq, Lk, d, causal, contract);
     if (workspace == nullptr || ws_bytes < need)
         return fail(MG_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed",
                     workspace ? ws_bytes : (size_t)0, need);
     MG_TRY(check_tensors({{Q, "Q"}, {K, "K"}, {V, "V"}, {O, "O"}, {LSE, "LSE"}, {dO, "dO"},
                           {dQ, "dQ"}, {dK, "dK"}, {dV, "dV"}, {workspace, "workspace"}}));
     MG_TRY(check_key_len(key_len));
-    const mg::AttnProblem p{B, H, L, d, causal ? 1 : 0, scale, key_len};
+    const mg::AttnProblem p{B, H, Lq, Lk, d, causal ? 1 : 0, scale, key_len};
     float *Dws = (float *)workspace;
     contract = backward_contract(contract);
     if (contract == MG_CONTRACT_STRICT_F32) {
@@ -268,8 +274,8 @@ mg_status_t mg_attn_bwd(const void *Q, const void *K, const void *V, const void 
         const float *o = (const float *)O, *go = (const float *)dO;
         MG_TRY(run_kernel(kernel_name("attn_rowdot", contract, d), stream,
                           [&] { return mg::launch_bwd_rowdot_f32(p, o, go, Dws, stream); }));
-        if (use_fused_dq(B, H, L, d, causal, contract)) {
-            float *dQp = (float *)((char *)workspace + round256((size_t)B * H * L * sizeof(float)));
+        if (use_fused_dq(B, H, Lq, Lk, d, causal, contract)) {
+            float *dQp = (float *)((char *)workspace + round256((size_t)B * H * Lq * sizeof(float)));
             MG_TRY(run_kernel(kernel_name("attn_dkdvq", contract, d), stream, [&] {
                 return mg::launch_bwd_dkdvq_f32(p, q, k, v, go, LSE, Dws, (float *)dK,
                                                 (float *)dV, dQp, stream);
@@ -301,6 +307,27 @@ mg_status_t mg_attn_bwd(const void *Q, const void *K, const void *V, const void 
         }));
     }
     return ok();
+}
+
+mg_status_t mg_attn_fwd(const void *Q, const void *K, const void *V, void *O, float *LSE,
+                        const int32_t *key_len, int B, int H, int L, int d, int causal,
+                        float scale, mg_contract_t contract, hipStream_t stream) {
+    return mg_attn_fwd_cross(Q, K, V, O, LSE, key_len, B, H, L, L, d, causal, scale, contract,
+                             stream);
+}
+
+size_t mg_attn_bwd_workspace_bytes(int B, int H, int L, int d, int causal,
+                                   mg_contract_t contract) {
+    return mg_attn_bwd_cross_workspace_bytes(B, H, L, L, d, causal, contract);
+}
+
+mg_status_t mg_attn_bwd(const void *Q, const void *K, const void *V, const void *O,
+                        const float *LSE, const void *dO, void *dQ, void *dK, void *dV,
+                        const int32_t *key_len, int B, int H, int L, int d, int causal,
+                        float scale, mg_contract_t contract, void *workspace,
+                        size_t ws_bytes, hipStream_t stream) {
+    return mg_attn_bwd_cross(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len, B, H, L, L, d, causal,
+                             scale, contract, workspace, ws_bytes, stream);
 }
 
 const char *mg_status_string(mg_status_t s) {

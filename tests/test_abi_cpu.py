@@ -71,6 +71,44 @@ def test_workspace_query(lib):
         assert mg.mg_attn_bwd_workspace_bytes(*args, 2) == mg.mg_attn_bwd_workspace_bytes(*args, 0)
 
 
+def test_cross_workspace_query(lib):
+    # D has one f32 per query row; the fused dQ partials are
+    # ceil(Lk / key_rows) * B*H*Lq*d f32, key tiles decided from Lk
+    B, H, Lq, Lk, d = 4, 8, 1024, 77, 64
+    rows = B * H * Lq
+    assert mg.mg_attn_bwd_cross_workspace_bytes(B, H, Lq, Lk, d, 0, 0) == \
+        rows * 4 + 2 * rows * d * 4
+    assert mg.mg_attn_bwd_cross_workspace_bytes(B, H, Lq, Lk, d, 0, 1) == rows * 4
+    assert mg.mg_attn_bwd_cross_workspace_bytes(B, H, Lq, Lk, d, 0, 2) == \
+        mg.mg_attn_bwd_cross_workspace_bytes(B, H, Lq, Lk, d, 0, 0)
+    # 50 action queries onto 66 keys: D rounded up to 256 bytes
+    assert mg.mg_attn_bwd_cross_workspace_bytes(1, 1, 50, 66, 32, 1, 0) == 256 + 2 * 50 * 32 * 4
+    # causal, Lk = 1024 with 8*8 heads -> 512 tiles of 128 keys over Lq = 300 rows
+    assert mg.mg_attn_bwd_cross_workspace_bytes(8, 8, 300, 1024, 64, 1, 0) == \
+        64 * 300 * 4 + 8 * 64 * 300 * 64 * 4
+    # the square entry points are the cross ones with Lq = Lk
+    for args in ((8, 8, 1024, 64, 1, 0), (4, 4, 256, 64, 1, 0), (1, 1, 3, 32, 0, 1)):
+        B, H, L, d, c, k = args
+        assert mg.mg_attn_bwd_workspace_bytes(*args) == \
+            mg.mg_attn_bwd_cross_workspace_bytes(B, H, L, L, d, c, k)
+    assert mg.mg_attn_bwd_cross_workspace_bytes(1, 1, 3, 0, 32, 0, 0) == 0    # Lk < 1
+    assert mg.mg_attn_bwd_cross_workspace_bytes(1, 1, 0, 3, 32, 0, 0) == 0    # Lq < 1
+
+
+def test_cross_forward_size_checks(lib):
+    vp = ctypes.c_void_p
+    Q, K, V, O, LSE = (vp(p) for p in GOOD)
+
+    def fwd(Lq, Lk, B=1, H=1, d=64):
+        return lib.mg_attn_fwd_cross(Q, K, V, O, LSE, None, B, H, Lq, Lk, d, 1,
+                                     ctypes.c_float(0.125), 0, None)
+    assert fwd(8, 0) == 1 and fwd(0, 8) == 1
+    # the element-count limit applies to the longer of the two lengths
+    assert fwd(4, 1 << 22, B=1 << 4, H=1 << 1) == 1
+    assert fwd(1 << 22, 4, B=1 << 4, H=1 << 1) == 1
+    assert "2^31" in mg.mg_last_error_detail()
+
+
 def _fwd(lib, ptrs, B=1, H=1, L=8, d=64, scale=0.125, contract=0):
     Q, K, V, O, LSE = ptrs
     vp = ctypes.c_void_p

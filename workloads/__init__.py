@@ -11,12 +11,18 @@ runs attention in two arithmetic contracts (Sec. 4.2): strict f32, and a
 reduced-input mode with f32 accumulation.  Workloads 1-5 are the attention
 shapes this library is measured and parity-tested on; workload 6 is the
 headline shape under the paper's own practical default ("accelerated":
-f32 tensors, f16 forward matrix inputs, strict backward).
+f32 tensors, f16 forward matrix inputs, strict backward).  Workloads 7 and 8
+take the attention shapes of two of the paper's model workloads (Sec. 10):
+the U-Net's cross-attention of 32x32 latent positions onto a 77-token
+context, and the Whisper-tiny encoder's non-causal self-attention over 1,500
+positions (6 heads of 64), a length that is no multiple of any tile.
 
 Draw recipe (fixed so that every run sees identical values):
   rng = numpy.random.default_rng(seed)
   if padded: key_len = rng.integers(key_len_lo, key_len_hi + 1, size=B)
-  Q, K, V, dO = four successive rng.standard_normal((B, H, L, d)) draws (f64)
+  Q, K, V, dO = four successive rng.standard_normal draws (f64) of shapes
+    (B, H, L, d), (B, H, Lk, d), (B, H, Lk, d), (B, H, L, d); Lk = L unless
+    the workload is a cross-attention one
   Q, K, V *= qkv_std;  dO *= do_std
   cast to float32 (round to nearest even); for bf16, round the f32 bits to
   bf16 (round to nearest even).
@@ -42,6 +48,11 @@ class Workload:
     key_len_lo: int = 0
     key_len_hi: int = 0
     seed: int = 0
+    Lk: int = 0            # key/value length; 0 means L (self-attention)
+
+    @property
+    def key_length(self):
+        return self.Lk or self.L
 
     @property
     def scale(self):
@@ -65,6 +76,10 @@ WORKLOADS = {
                 padded=True, key_len_lo=128, key_len_hi=512, seed=5),
     6: Workload("causal_8x8x1024_d64_accel", 8, 8, 1024, 64, True, "accelerated",
                 qkv_std=0.5, seed=6),
+    7: Workload("cross_4x8x1024x77_d64_f32", 4, 8, 1024, 64, False, "strict_f32",
+                seed=7, Lk=77),
+    8: Workload("full_2x6x1500_d64_f32", 2, 6, 1500, 64, False, "strict_f32",
+                seed=8),
 }
 
 
@@ -100,9 +115,10 @@ class AttnInputs:
 
 def make_inputs(B, H, L, d, *, causal, contract="strict_f32", seed=0,
                 qkv_std=1.0, do_std=1.0, key_len=None, key_len_range=None,
-                scale=None):
+                scale=None, Lk=None):
     """Draw one seeded input set following the recipe in the module doc.
 
+    L is the query length; Lk the key/value length (None: L).
     key_len: explicit per-batch key lengths (sequence of B ints), or
     key_len_range=(lo, hi) to draw them (inclusive) first from the stream.
     """
@@ -115,8 +131,9 @@ def make_inputs(B, H, L, d, *, causal, contract="strict_f32", seed=0,
         kl = rng.integers(lo, hi + 1, size=B).astype(np.int32)
     elif key_len is not None:
         kl = np.asarray(key_len, dtype=np.int32).reshape(B)
-    shape = (B, H, L, d)
-    draws = [rng.standard_normal(shape) for _ in range(4)]
+    Lk = L if Lk is None else int(Lk)
+    shapes = [(B, H, L, d), (B, H, Lk, d), (B, H, Lk, d), (B, H, L, d)]
+    draws = [rng.standard_normal(shape) for shape in shapes]
     Q, K, V = (x * qkv_std for x in draws[:3])
     dO = draws[3] * do_std
     arrs = [np.ascontiguousarray(x.astype(np.float32)) for x in (Q, K, V, dO)]
@@ -137,18 +154,21 @@ def workload_inputs(wid):
     w = WORKLOADS[wid]
     return make_inputs(w.B, w.H, w.L, w.d, causal=w.causal, contract=w.contract,
                        seed=w.seed, qkv_std=w.qkv_std, do_std=w.do_std,
-                       key_len_range=(w.key_len_lo, w.key_len_hi) if w.padded else None)
+                       key_len_range=(w.key_len_lo, w.key_len_hi) if w.padded else None,
+                       Lk=w.key_length)
 
 
-def unmasked_pairs(B, H, L, causal, key_len=None):
+def unmasked_pairs(B, H, L, causal, key_len=None, Lk=None):
     """Number of (query, key) pairs that attention must evaluate: the unit
-    the credited FLOP and byte counts are quoted per."""
+    the credited FLOP and byte counts are quoted per.  L queries, Lk keys
+    (None: L); the causal mask is aligned to the bottom-right corner."""
+    Lk = L if Lk is None else Lk
     total = 0
     for b in range(B):
-        n = L if key_len is None else max(0, min(int(key_len[b]), L))
+        n = Lk if key_len is None else max(0, min(int(key_len[b]), Lk))
         if causal:
-            # rows i see keys j <= i and j < n
-            per_head = sum(min(i + 1, n) for i in range(L))
+            # rows i see keys j <= i + Lk - L and j < n
+            per_head = sum(max(0, min(i + Lk - L + 1, n)) for i in range(L))
         else:
             per_head = L * n
         total += H * per_head
