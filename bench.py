@@ -79,6 +79,10 @@ def kernel_work(name, w, pairs, rows, key_len=None):
     d, es = w.d, (4 if w.contract == "strict_f32" else 2)
     if name.startswith("attn_fwd"):
         return 4.0 * d * pairs, "flop", "mfma"
+    if name.startswith("attn_dkdvreduce"):
+        # reads S dK and S dV partials, writes dK and dV (all f32)
+        n = w.B * w.H * w.key_length * d
+        return 4.0 * 2 * n * (query_splits(w) + 1), "byte", "hbm"
     if name.startswith("attn_dkdvq"):
         return 10.0 * d * pairs, "flop", "mfma"       # S recompute, dV, dP, dK, dQ
     if name.startswith("attn_dkdv"):
@@ -100,11 +104,24 @@ def kernel_peak(name):
     return LOWP_MFMA_PEAK if ("_bf16_" in name or "_accel_" in name) else F32_MFMA_PEAK
 
 
+def fused_key_rows(w):
+    return 128 if (w.causal and -(-w.key_length // 128) * w.B * w.H >= 512) else 64
+
+
+def query_splits(w):
+    """Workgroups over which the fused backward splits each key tile's query
+    tiles (the rule the library's workspace query documents)."""
+    grid = -(-w.key_length // fused_key_rows(w)) * w.B * w.H
+    if grid >= 512:
+        return 1
+    return max(1, min(-(-1024 // grid), -(-w.L // 32) // 4))
+
+
 def partial_rows(w, key_len):
     """(key tile, query row) pairs the fused dQ reduction reads (key tiles of
     128 keys when causal with >= 512 such tiles, else 64)."""
     Lk = w.key_length
-    key_rows = 128 if (w.causal and -(-Lk // 128) * w.B * w.H >= 512) else 64
+    key_rows = fused_key_rows(w)
     total = 0
     kls = [Lk] * w.B if key_len is None else [int(n) for n in key_len]
     for n in kls:

@@ -98,8 +98,12 @@ mg_status_t mg_attn_fwd(const void *Q, const void *K, const void *V,
  * for strict_f32 and accelerated with d <= 64 when they fit in 1 GiB, one f32
  * dQ partial per (key tile, query row): ceil(L/T) * B*H*L*d floats with key
  * tiles of T = 128 keys when causal and ceil(L/128)*B*H >= 512, else T = 64.
- * The partials let the dK/dV kernel produce dQ without a second recompute.  Returns 0 when the
- * arguments are invalid.
+ * The partials let the dK/dV kernel produce dQ without a second recompute.
+ * When ceil(L/T)*B*H < 512 (too few key tiles to fill the GPU), the query
+ * tiles of each key tile are split over S workgroups and 2*S*B*H*L*d more
+ * f32 hold their dK and dV partials (S = min(ceil(1024 / (ceil(L/T)*B*H)),
+ * floor(ceil(L/32) / 4)), no partials when S <= 1), each region starting on
+ * a 256-byte boundary.  Returns 0 when the arguments are invalid.
  */
 size_t mg_attn_bwd_workspace_bytes(int B, int H, int L, int d, int causal,
                                    mg_contract_t contract);
@@ -138,7 +142,8 @@ mg_status_t mg_attn_bwd(const void *Q, const void *K, const void *V,
  * which call them.  Arguments, contracts, ownership, asynchrony and errors
  * are otherwise as there; the workspace holds D and, for strict_f32 and
  * accelerated with d <= 64 when they fit in 1 GiB, ceil(Lk/T) * B*H*Lq*d
- * f32 dQ partials (T as above, decided from Lk).
+ * f32 dQ partials and 2*S*B*H*Lk*d f32 dK/dV partials (T and S as above,
+ * with Lk for the key length and ceil(Lq/32) query tiles).
  */
 mg_status_t mg_attn_fwd_cross(const void *Q, const void *K, const void *V,
                               void *O, float *LSE,

@@ -37,6 +37,7 @@
 // Masking: an element's offset inside its tile is compared against one
 // per-lane threshold (key length, causal diagonal); the forward kernel skips
 // the comparison on tiles that hold no masked element.
+#include <algorithm>
 #include <climits>
 
 #include "device_common.h"
@@ -505,8 +506,8 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
                     const float *__restrict__ V, const float *__restrict__ dO,
                     const float *__restrict__ LSE, const float *__restrict__ Dws,
                     float *__restrict__ dK, float *__restrict__ dV, float *__restrict__ dQp,
-                    const int32_t *__restrict__ key_len, int H, int Lq, int Lk, int causal, float scale,
-                    float scale_log2, int BH) {
+                    float *__restrict__ dKVp, const int32_t *__restrict__ key_len, int H, int Lq,
+                    int Lk, int causal, float scale, float scale_log2, int BH, int nsplit) {
     constexpr int DQ = D / 4;
     constexpr int NC = D / 16;
     constexpr int BR = 16 * NIB;
@@ -525,7 +526,8 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
     const int rank = blockIdx.x / BH;
     const int head = blockIdx.x - rank * BH;
-    const int kt = rank;
+    const int kt = rank / nsplit;          // key tile
+    const int split = rank - kt * nsplit;  // share of its query tiles
     const int b = head / H;
     const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
     const float *Qh = Q + qoff;
@@ -543,9 +545,12 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
     const int klen = key_limit(key_len, b, Lk);
     const int nq = (Lq + BR - 1) / BR;
-    // first query tile holding a row that sees key k0
-    const int qstart = causal ? min(nq, max(0, k0 - diag) / BR) : 0;
-    const int qstop = (k0 < klen) ? nq : qstart;
+    // first query tile holding a row that sees key k0, and the end of the
+    // range; split `split` of `nsplit` takes a contiguous share of it
+    const int qfirst = causal ? min(nq, max(0, k0 - diag) / BR) : 0;
+    const int qlast = (k0 < klen) ? nq : qfirst;
+    const int qstart = qfirst + (int)((long)(qlast - qfirst) * split / nsplit);
+    const int qstop = qfirst + (int)((long)(qlast - qfirst) * (split + 1) / nsplit);
 
     const Tile tile;
 
@@ -726,16 +731,37 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     }
     if (qstart < qstop) store_dq(qstop - 1);
 
+    // One split writes dK and dV directly; several write partials laid out
+    // [dK, dV][split][B*H][Lk][d] (every split writes its rows, zeros for an
+    // empty share) for attn_dkdv_reduce_f32.
     if (kj < Lk) {
         const bool keep = kj < klen;
-        float *dkrow = dK + hoff + (size_t)kj * D;
-        float *dvrow = dV + hoff + (size_t)kj * D;
+        const size_t row = hoff + (size_t)kj * D;
+        const size_t part = (size_t)BH * Lk * D;
+        float *dkrow = (nsplit == 1) ? dK + row : dKVp + (size_t)split * part + row;
+        float *dvrow = (nsplit == 1) ? dV + row : dKVp + (size_t)(nsplit + split) * part + row;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
             *reinterpret_cast<f32x4 *>(dkrow + 16 * c + 4 * g) = keep ? dkacc[c] * scale : zero4();
             *reinterpret_cast<f32x4 *>(dvrow + 16 * c + 4 * g) = keep ? dvacc[c] : zero4();
         }
     }
+}
+
+// dK and dV from the per-split partials of attn_dkdvq_f32, added in
+// increasing split order (a fixed order).  n4 = B*H*Lk*d / 4.
+__global__ __launch_bounds__(256) void attn_dkdv_reduce_f32(const float *__restrict__ dKVp,
+                                                            float *__restrict__ dK,
+                                                            float *__restrict__ dV,
+                                                            int nsplit, long n4) {
+    const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= 2 * n4) return;
+    const int t = idx >= n4;           // 0: dK, 1: dV
+    const long e4 = idx - t * n4;
+    const f32x4 *src = reinterpret_cast<const f32x4 *>(dKVp) + (long)t * nsplit * n4 + e4;
+    f32x4 sum = zero4();
+    for (int s = 0; s < nsplit; ++s) sum += src[(long)s * n4];
+    reinterpret_cast<f32x4 *>(t ? dV : dK)[e4] = sum;
 }
 
 // dQ[i] = scale * sum over key tiles kt that hold an allowed key for row i of
@@ -969,17 +995,40 @@ int fused_dq_key_rows(const AttnProblem &p) {
     return wide_key_tiles(p) ? DkdvqCausalCfg::ROWS : DkdvCfg::ROWS;
 }
 
+// Few keys (a short context, few heads) leave the key-stationary grid far
+// smaller than the chip: below MG_DKDV_SPLIT_BELOW workgroups, each key
+// tile's query tiles are split over up to ceil(MG_DKDV_SPLIT_TARGET / grid)
+// workgroups, keeping at least MG_DKDV_SPLIT_MIN_TILES query tiles each.
+#ifndef MG_DKDV_SPLIT_BELOW
+#define MG_DKDV_SPLIT_BELOW 512
+#endif
+#ifndef MG_DKDV_SPLIT_TARGET
+#define MG_DKDV_SPLIT_TARGET 1024
+#endif
+#ifndef MG_DKDV_SPLIT_MIN_TILES
+#define MG_DKDV_SPLIT_MIN_TILES 4
+#endif
+int fused_dq_query_splits(const AttnProblem &p) {
+    const long grid = (long)cdiv(p.Lk, fused_dq_key_rows(p)) * p.B * p.H;
+    if (grid >= MG_DKDV_SPLIT_BELOW) return 1;
+    const int br = 16 * (wide_key_tiles(p) ? MG_DKDVQ_CAUSAL_NIB : MG_DKDV_NIB);
+    const long by_grid = (MG_DKDV_SPLIT_TARGET + grid - 1) / grid;
+    const long by_tiles = cdiv(p.Lq, br) / MG_DKDV_SPLIT_MIN_TILES;
+    return (int)std::max(1L, std::min(by_grid, by_tiles));
+}
+
 template <class C, int NIB>
 static hipError_t launch_dkdvq(const AttnProblem &p, const float *Q, const float *K,
                                const float *V, const float *dO, const float *LSE,
                                const float *Dws, float *dK, float *dV, float *dQp,
-                               hipStream_t s) {
+                               float *dKVp, hipStream_t s) {
     const int BH = p.B * p.H;
-    const dim3 grid(cdiv(p.Lk, C::ROWS) * BH), block(C::NT);
+    const int ns = fused_dq_query_splits(p);
+    const dim3 grid(cdiv(p.Lk, C::ROWS) * ns * BH), block(C::NT);
     const float sl2 = p.scale * kLog2e;
     switch (p.d) {
-    case 32: attn_dkdvq_f32<32, NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
-    case 64: attn_dkdvq_f32<64, NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
+    case 32: attn_dkdvq_f32<32, NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, dKVp, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH, ns); break;
+    case 64: attn_dkdvq_f32<64, NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, dKVp, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH, ns); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -988,10 +1037,19 @@ static hipError_t launch_dkdvq(const AttnProblem &p, const float *Q, const float
 hipError_t launch_bwd_dkdvq_f32(const AttnProblem &p, const float *Q, const float *K,
                                 const float *V, const float *dO, const float *LSE,
                                 const float *Dws, float *dK, float *dV, float *dQp,
-                                hipStream_t s) {
+                                float *dKVp, hipStream_t s) {
+    if (fused_dq_query_splits(p) > 1 && dKVp == nullptr) return hipErrorInvalidValue;
     return wide_key_tiles(p)
-        ? launch_dkdvq<DkdvqCausalCfg, MG_DKDVQ_CAUSAL_NIB>(p, Q, K, V, dO, LSE, Dws, dK, dV, dQp, s)
-        : launch_dkdvq<DkdvCfg, MG_DKDV_NIB>(p, Q, K, V, dO, LSE, Dws, dK, dV, dQp, s);
+        ? launch_dkdvq<DkdvqCausalCfg, MG_DKDVQ_CAUSAL_NIB>(p, Q, K, V, dO, LSE, Dws, dK, dV, dQp, dKVp, s)
+        : launch_dkdvq<DkdvCfg, MG_DKDV_NIB>(p, Q, K, V, dO, LSE, Dws, dK, dV, dQp, dKVp, s);
+}
+
+hipError_t launch_bwd_dkdv_reduce_f32(const AttnProblem &p, const float *dKVp, float *dK,
+                                      float *dV, hipStream_t s) {
+    const long n4 = (long)p.B * p.H * p.Lk * p.d / 4;
+    const dim3 grid((unsigned)((2 * n4 + 255) / 256)), block(256);
+    attn_dkdv_reduce_f32<<<grid, block, 0, s>>>(dKVp, dK, dV, fused_dq_query_splits(p), n4);
+    return hipGetLastError();
 }
 
 hipError_t launch_bwd_dq_reduce_f32(const AttnProblem &p, const float *dQp, float *dQ,

@@ -50,13 +50,20 @@ hipError_t launch_bwd_dkdv_bf16(const AttnProblem &p, const uint16_t *Q,
 
 // Backward steps 2+3 fused (strict f32, d <= 64): dK, dV as above plus one
 // f32 dQ partial per (key tile, query row) written to dQp, laid out
-// [key tile][B*H][L][d]; then dQ = scale * sum of a row's partials.  The
-// key-tile height (64 or 128) depends on the problem.
+// [key tile][B*H][Lq][d]; then dQ = scale * sum of a row's partials.  The
+// key-tile height (64 or 128) depends on the problem.  When the key tiles
+// alone give too small a grid, each key tile's query tiles are split over
+// fused_dq_query_splits(p) workgroups, which write dK/dV partials to dKVp
+// ([dK, dV][split][B*H][Lk][d] f32; unused, may be null, with one split)
+// for launch_bwd_dkdv_reduce_f32 to add.
 int fused_dq_key_rows(const AttnProblem &p);
+int fused_dq_query_splits(const AttnProblem &p);
 hipError_t launch_bwd_dkdvq_f32(const AttnProblem &p, const float *Q, const float *K,
                                 const float *V, const float *dO, const float *LSE,
                                 const float *Dws, float *dK, float *dV, float *dQp,
-                                hipStream_t s);
+                                float *dKVp, hipStream_t s);
+hipError_t launch_bwd_dkdv_reduce_f32(const AttnProblem &p, const float *dKVp, float *dK,
+                                      float *dV, hipStream_t s);
 hipError_t launch_bwd_dq_reduce_f32(const AttnProblem &p, const float *dQp, float *dQ,
                                     hipStream_t s);
 

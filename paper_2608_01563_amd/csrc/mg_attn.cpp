@@ -203,13 +203,25 @@ bool use_fused_dq(int B, int H, int Lq, int Lk, int d, int causal, mg_contract_t
            dq_partial_bytes(B, H, Lq, Lk, d, causal) <= kFusedPartialLimit;
 }
 
-// Layout: D (f32 per query row) first, then the dQ partials when fused.
+// dK/dV partials of a fused backward whose query tiles are split (zero
+// bytes with one split).
+size_t dkdv_partial_bytes(int B, int H, int Lq, int Lk, int d, int causal) {
+    const mg::AttnProblem p{B, H, Lq, Lk, d, causal ? 1 : 0, 1.0f, nullptr};
+    const int ns = mg::fused_dq_query_splits(p);
+    return ns > 1 ? (size_t)2 * ns * B * H * Lk * d * sizeof(float) : 0;
+}
+
+// Layout: D (f32 per query row) first; when fused, the dQ partials, then
+// (256-byte aligned) the dK/dV partials of a split backward.
 size_t workspace_bytes(int B, int H, int Lq, int Lk, int d, int causal,
                        mg_contract_t contract) {
     contract = backward_contract(contract);
     size_t n = round256((size_t)B * H * Lq * sizeof(float));
-    if (use_fused_dq(B, H, Lq, Lk, d, causal, contract))
+    if (use_fused_dq(B, H, Lq, Lk, d, causal, contract)) {
         n += dq_partial_bytes(B, H, Lq, Lk, d, causal);
+        const size_t kv = dkdv_partial_bytes(B, H, Lq, Lk, d, causal);
+        if (kv > 0) n = round256(n) + kv;
+    }
     return n;
 }
 
@@ -275,11 +287,19 @@ mg_status_t mg_attn_bwd_cross(const void *Q, const void *K, const void *V, const
         MG_TRY(run_kernel(kernel_name("attn_rowdot", contract, d), stream,
                           [&] { return mg::launch_bwd_rowdot_f32(p, o, go, Dws, stream); }));
         if (use_fused_dq(B, H, Lq, Lk, d, causal, contract)) {
-            float *dQp = (float *)((char *)workspace + round256((size_t)B * H * Lq * sizeof(float)));
+            char *base = (char *)workspace;
+            float *dQp = (float *)(base + round256((size_t)B * H * Lq * sizeof(float)));
+            float *dKVp = dkdv_partial_bytes(B, H, Lq, Lk, d, causal) == 0 ? nullptr
+                : (float *)((char *)dQp + round256(dq_partial_bytes(B, H, Lq, Lk, d, causal)));
             MG_TRY(run_kernel(kernel_name("attn_dkdvq", contract, d), stream, [&] {
                 return mg::launch_bwd_dkdvq_f32(p, q, k, v, go, LSE, Dws, (float *)dK,
-                                                (float *)dV, dQp, stream);
+                                                (float *)dV, dQp, dKVp, stream);
             }));
+            if (dKVp != nullptr)
+                MG_TRY(run_kernel(kernel_name("attn_dkdvreduce", contract, d), stream, [&] {
+                    return mg::launch_bwd_dkdv_reduce_f32(p, dKVp, (float *)dK, (float *)dV,
+                                                          stream);
+                }));
             MG_TRY(run_kernel(kernel_name("attn_dqreduce", contract, d), stream, [&] {
                 return mg::launch_bwd_dq_reduce_f32(p, dQp, (float *)dQ, stream);
             }));

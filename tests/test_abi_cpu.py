@@ -60,8 +60,10 @@ def test_workspace_query(lib):
     # partials above 1 GiB fall back to the separate dQ kernel (D only)
     assert mg.mg_attn_bwd_workspace_bytes(8, 8, 8192, 64, 0, 0) == 8 * 8 * 8192 * 4
     assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 32, 0, 0) == 256 + 3 * 32 * 4
-    # causal but too few 128-key tiles: 64-key tiles (B4 H4 L256 -> 4 tiles)
-    assert mg.mg_attn_bwd_workspace_bytes(4, 4, 256, 64, 1, 0) == 4096 * 4 + 4 * 4096 * 64 * 4
+    # causal but too few 128-key tiles: 64-key tiles (B4 H4 L256 -> 4 tiles);
+    # 64 workgroups split each key tile's 8 query tiles in S = min(16, 8/4) = 2
+    assert mg.mg_attn_bwd_workspace_bytes(4, 4, 256, 64, 1, 0) == \
+        4096 * 4 + 4 * 4096 * 64 * 4 + 2 * 2 * 16 * 256 * 64 * 4
     assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 48, 0, 0) == 0     # unsupported d
     assert mg.mg_attn_bwd_workspace_bytes(0, 1, 3, 32, 0, 0) == 0     # bad size
     assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 32, 0, 7) == 0     # bad contract
@@ -76,12 +78,14 @@ def test_cross_workspace_query(lib):
     # ceil(Lk / key_rows) * B*H*Lq*d f32, key tiles decided from Lk
     B, H, Lq, Lk, d = 4, 8, 1024, 77, 64
     rows = B * H * Lq
+    # 2 key tiles x 32 heads = 64 workgroups: S = min(1024/64, (1024/32)/4) = 8
     assert mg.mg_attn_bwd_cross_workspace_bytes(B, H, Lq, Lk, d, 0, 0) == \
-        rows * 4 + 2 * rows * d * 4
+        rows * 4 + 2 * rows * d * 4 + 2 * 8 * B * H * Lk * d * 4
     assert mg.mg_attn_bwd_cross_workspace_bytes(B, H, Lq, Lk, d, 0, 1) == rows * 4
     assert mg.mg_attn_bwd_cross_workspace_bytes(B, H, Lq, Lk, d, 0, 2) == \
         mg.mg_attn_bwd_cross_workspace_bytes(B, H, Lq, Lk, d, 0, 0)
-    # 50 action queries onto 66 keys: D rounded up to 256 bytes
+    # 50 action queries onto 66 keys: D rounded up to 256 bytes; two query
+    # tiles are too few to split
     assert mg.mg_attn_bwd_cross_workspace_bytes(1, 1, 50, 66, 32, 1, 0) == 256 + 2 * 50 * 32 * 4
     # causal, Lk = 1024 with 8*8 heads -> 512 tiles of 128 keys over Lq = 300 rows
     assert mg.mg_attn_bwd_cross_workspace_bytes(8, 8, 300, 1024, 64, 1, 0) == \
