@@ -1,4 +1,4 @@
-"""ctypes binding of libmgattn.so: argument marshalling only.
+"""ctypes binding of libmg.so: argument marshalling only.
 
 Every function here checks the torch tensors it is given (device, dtype,
 shape, contiguity), passes their device pointers and the current HIP stream
@@ -11,8 +11,9 @@ import os
 import threading
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libmgattn.so")
+LIB_PATH = os.path.join(HERE, "libmg.so")
 HEADER_PATH = os.path.join(os.path.dirname(HERE), "include", "mg_attn.h")
+CONV_HEADER_PATH = os.path.join(os.path.dirname(HERE), "include", "mg_conv.h")
 
 STRICT_F32 = 0
 FAST_BF16 = 1
@@ -34,6 +35,12 @@ class MgError(RuntimeError):
         super().__init__("%s: %s" % (STATUS_NAMES.get(status, status), detail))
 
 
+class ConvShape(ctypes.Structure):
+    """mg_conv2d_shape_t of mg_conv.h."""
+    _fields_ = [(n, ctypes.c_int) for n in
+                ("N", "H", "W", "C", "K", "R", "S", "stride_h", "stride_w", "pad_h", "pad_w")]
+
+
 def _declare(lib):
     vp, c_int, c_float, c_size = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
     lib.mg_attn_fwd.argtypes = [vp, vp, vp, vp, vp, vp, c_int, c_int, c_int, c_int, c_int,
@@ -53,6 +60,13 @@ def _declare(lib):
     lib.mg_attn_bwd_cross.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, c_int, c_int,
                                       c_int, c_int, c_int, c_int, c_float, c_int, vp, c_size, vp]
     lib.mg_attn_bwd_cross.restype = c_int
+    shp = ctypes.POINTER(ConvShape)
+    lib.mg_conv2d_bwd_data.argtypes = [vp, vp, vp, shp, c_int, vp]
+    lib.mg_conv2d_bwd_data.restype = c_int
+    lib.mg_conv2d_bwd_filter_workspace_bytes.argtypes = [shp, c_int]
+    lib.mg_conv2d_bwd_filter_workspace_bytes.restype = c_size
+    lib.mg_conv2d_bwd_filter.argtypes = [vp, vp, vp, shp, c_int, vp, c_size, vp]
+    lib.mg_conv2d_bwd_filter.restype = c_int
     lib.mg_status_string.argtypes = [c_int]
     lib.mg_status_string.restype = ctypes.c_char_p
     lib.mg_last_error_detail.argtypes = []
@@ -69,14 +83,14 @@ def _declare(lib):
 
 
 def load_library(path=LIB_PATH):
-    """Load libmgattn.so (after torch, so both share one HIP runtime)."""
+    """Load libmg.so (after torch, so both share one HIP runtime)."""
     global _lib
     with _lock:
         if _lib is None:
             import torch  # noqa: F401  (brings in the HIP runtime the library binds to)
             if not os.path.exists(path):
                 raise RuntimeError(
-                    "libmgattn.so is not built (%s); run `python -m "
+                    "libmg.so is not built (%s); run `python -m "
                     "paper_2608_01563_amd.build` or __graft_entry__.build()" % path)
             _lib = _declare(ctypes.CDLL(path))
         return _lib
@@ -238,6 +252,68 @@ def mg_attn_bwd_cross(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len=None, *, causal, 
                                  _stream_handle(stream)))
 
 
+def conv_shape(X_shape, W_shape, stride=(1, 1), pad=(0, 0)):
+    """ConvShape from X [N,H,W,C], W [K,R,S,C], stride and padding (h, w)."""
+    N, H, Wd, C = (int(v) for v in X_shape)
+    K, R, S, C2 = (int(v) for v in W_shape)
+    if C2 != C:
+        raise ValueError("X has %d channels, the filter %d" % (C, C2))
+    return ConvShape(N, H, Wd, C, K, R, S, int(stride[0]), int(stride[1]), int(pad[0]),
+                     int(pad[1]))
+
+
+def conv_out_hw(shape):
+    return ((shape.H + 2 * shape.pad_h - shape.R) // shape.stride_h + 1,
+            (shape.W + 2 * shape.pad_w - shape.S) // shape.stride_w + 1)
+
+
+def _check_f32(named):
+    import torch
+    for name, t, want in named:
+        if not t.is_cuda or t.dtype != torch.float32 or not t.is_contiguous():
+            raise ValueError("%s must be a contiguous float32 GPU tensor" % name)
+        if tuple(t.shape) != tuple(want):
+            raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(want)))
+
+
+def mg_conv2d_bwd_data(dY, W, dX, *, stride=(1, 1), pad=(0, 0), contract=STRICT_F32,
+                       stream=None):
+    """Data gradient into caller-provided dX [N,H,W,C] (channels-last)."""
+    lib = load_library()
+    shape = conv_shape(dX.shape, W.shape, stride, pad)
+    P, Q = conv_out_hw(shape)
+    _check_f32((("dY", dY, (shape.N, P, Q, shape.K)), ("W", W, tuple(W.shape)),
+                ("dX", dX, tuple(dX.shape))))
+    _check(lib.mg_conv2d_bwd_data(_ptr(dY), _ptr(W), _ptr(dX), ctypes.byref(shape),
+                                  _contract_id(contract), _stream_handle(stream)))
+
+
+def mg_conv2d_bwd_filter_workspace_bytes(X_shape, W_shape, stride=(1, 1), pad=(0, 0),
+                                         contract=STRICT_F32):
+    shape = conv_shape(X_shape, W_shape, stride, pad)
+    return int(load_library().mg_conv2d_bwd_filter_workspace_bytes(ctypes.byref(shape),
+                                                                   _contract_id(contract)))
+
+
+def mg_conv2d_bwd_filter(X, dY, dW, *, stride=(1, 1), pad=(0, 0), contract=STRICT_F32,
+                         workspace=None, stream=None):
+    """Filter gradient into caller-provided dW [K,R,S,C].  `workspace` as for
+    mg_attn_bwd (allocated here with torch when None and needed)."""
+    import torch
+    lib = load_library()
+    shape = conv_shape(X.shape, dW.shape, stride, pad)
+    P, Q = conv_out_hw(shape)
+    _check_f32((("X", X, tuple(X.shape)), ("dY", dY, (shape.N, P, Q, shape.K)),
+                ("dW", dW, tuple(dW.shape))))
+    need = mg_conv2d_bwd_filter_workspace_bytes(X.shape, dW.shape, stride, pad, contract)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib.mg_conv2d_bwd_filter(_ptr(X), _ptr(dY), _ptr(dW), ctypes.byref(shape),
+                                    _contract_id(contract), _ptr(workspace), nbytes,
+                                    _stream_handle(stream)))
+
+
 def mg_status_string(status):
     return load_library().mg_status_string(int(status)).decode()
 
@@ -292,3 +368,17 @@ def attention_backward(Q, K, V, O, LSE, dO, *, causal, scale, key_len=None, cont
     mg_attn_bwd_cross(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len, causal=causal, scale=scale,
                       contract=c, workspace=workspace, stream=stream)
     return dQ, dK, dV
+
+
+def conv2d_backward(X, W, dY, *, stride=(1, 1), pad=(0, 0), contract=STRICT_F32, stream=None,
+                    need_input_grad=True):
+    """Allocate with torch and run both convolution derivatives; returns
+    (dX or None, dW).  Layouts: X [N,H,W,C], W [K,R,S,C], dY [N,P,Q,K]."""
+    import torch
+    dX = None
+    if need_input_grad:
+        dX = torch.empty_like(X)
+        mg_conv2d_bwd_data(dY, W, dX, stride=stride, pad=pad, contract=contract, stream=stream)
+    dW = torch.empty_like(W)
+    mg_conv2d_bwd_filter(X, dY, dW, stride=stride, pad=pad, contract=contract, stream=stream)
+    return dX, dW

@@ -1,4 +1,5 @@
-"""Build libmgattn.so (the C-ABI attention library) in-tree for gfx950.
+"""Build libmg.so (the C-ABI attention and convolution-derivative library)
+in-tree for gfx950.
 
     python -m paper_2608_01563_amd.build [-v]
 
@@ -18,7 +19,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(HERE, "_build")
-LIB_PATH = os.path.join(HERE, "libmgattn.so")
+LIB_PATH = os.path.join(HERE, "libmg.so")
 ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
 ARCH = "gfx950"
@@ -54,9 +55,12 @@ def _compile(src, verbose):
 
 
 def build(verbose=False):
-    """Compile every source under csrc/ and link libmgattn.so; returns its path."""
+    """Compile every source under csrc/ and csrc/conv/ and link libmg.so; returns
+    its path."""
     os.makedirs(BUILD_DIR, exist_ok=True)
-    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")))
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")) + glob.glob(os.path.join(CSRC, "*.cpp")) +
+                  glob.glob(os.path.join(CSRC, "conv", "*.hip")) +
+                  glob.glob(os.path.join(CSRC, "conv", "*.cpp")))
     with cf.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
         objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
     tmp = LIB_PATH + ".tmp%d" % os.getpid()

@@ -8,36 +8,19 @@
 
 #include <algorithm>
 #include <cmath>
-#include <cstdarg>
 #include <cstdint>
 #include <cstdio>
-#include <initializer_list>
-#include <map>
-#include <mutex>
 #include <string>
-#include <vector>
 
+#include "host_runtime.h"
 #include "launch.h"
 
 namespace {
 
-thread_local std::string g_detail;
-
-mg_status_t fail(mg_status_t st, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
-mg_status_t fail(mg_status_t st, const char *fmt, ...) {
-    char buf[512];
-    va_list ap;
-    va_start(ap, fmt);
-    vsnprintf(buf, sizeof buf, fmt, ap);
-    va_end(ap);
-    g_detail = buf;
-    return st;
-}
-
-mg_status_t ok() {
-    g_detail.clear();
-    return MG_OK;
-}
+using mg::host::fail;
+using mg::host::ok;
+using mg::host::round256;
+using mg::host::run_kernel;
 
 constexpr int64_t kMaxElems = INT32_MAX;
 
@@ -59,127 +42,21 @@ mg_status_t check_shape(int B, int H, int Lq, int Lk, int d, float scale,
     return MG_OK;
 }
 
-struct NamedPtr {
-    const void *ptr;
-    const char *name;
-};
-
-// Required tensor pointers: non-null and 16-byte aligned (checked for all of
-// them first, without touching the runtime), then device-accessible.
-mg_status_t check_tensors(std::initializer_list<NamedPtr> ptrs) {
-    for (const NamedPtr &p : ptrs) {
-        if (p.ptr == nullptr) return fail(MG_ERR_INVALID_ARGUMENT, "%s is NULL", p.name);
-        if (reinterpret_cast<uintptr_t>(p.ptr) % 16 != 0)
-            return fail(MG_ERR_MISALIGNED, "%s is not 16-byte aligned", p.name);
-    }
-    for (const NamedPtr &p : ptrs) {
-        hipPointerAttribute_t attr;
-        hipError_t e = hipPointerGetAttributes(&attr, p.ptr);
-        if (e != hipSuccess) {
-            (void)hipGetLastError();   // keep the lookup error out of the caller's state
-            return fail(MG_ERR_INVALID_ARGUMENT, "%s is not a device pointer (%s)", p.name,
-                        hipGetErrorString(e));
-        }
-        if (attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged)
-            return fail(MG_ERR_INVALID_ARGUMENT, "%s is not device memory", p.name);
-    }
-    return MG_OK;
+mg_status_t check_tensors(std::initializer_list<mg::host::NamedPtr> ptrs) {
+    return mg::host::check_device_ptrs(ptrs, 16);
 }
 
 mg_status_t check_key_len(const int32_t *key_len) {
-    if (key_len == nullptr) return MG_OK;
-    if (reinterpret_cast<uintptr_t>(key_len) % 4 != 0)
-        return fail(MG_ERR_MISALIGNED, "key_len is not 4-byte aligned");
-    hipPointerAttribute_t attr;
-    hipError_t e = hipPointerGetAttributes(&attr, key_len);
-    if (e != hipSuccess) {
-        (void)hipGetLastError();
-        return fail(MG_ERR_INVALID_ARGUMENT, "key_len is not a device pointer (%s)",
-                    hipGetErrorString(e));
-    }
-    if (attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged)
-        return fail(MG_ERR_INVALID_ARGUMENT, "key_len is not device memory");
-    return MG_OK;
-}
-
-#define MG_TRY(expr)                         \
-    do {                                     \
-        mg_status_t st_ = (expr);            \
-        if (st_ != MG_OK) return st_;        \
-    } while (0)
-
-// ------------------------------------------------------------- profiling --
-struct ProfRecord {
-    const char *name;
-    hipEvent_t start, stop;
-};
-
-struct Profiler {
-    std::mutex mu;
-    bool enabled = false;
-    std::vector<hipEvent_t> pool;
-    std::vector<ProfRecord> pending;
-    std::map<std::string, std::pair<int64_t, double>> totals;
-    std::vector<const char *> order;   // names in first-seen order (static storage)
-
-    hipError_t take(hipEvent_t *ev) {
-        if (!pool.empty()) {
-            *ev = pool.back();
-            pool.pop_back();
-            return hipSuccess;
-        }
-        return hipEventCreate(ev);
-    }
-};
-
-Profiler &prof() {
-    static Profiler p;
-    return p;
-}
-
-// Launch one kernel, bracketed by events when profiling is enabled.
-template <typename F>
-mg_status_t run_kernel(const char *name, hipStream_t stream, F &&launch) {
-    Profiler &p = prof();
-    ProfRecord rec{name, nullptr, nullptr};
-    bool timed = false;
-    {
-        std::lock_guard<std::mutex> g(p.mu);
-        if (p.enabled) {
-            if (p.take(&rec.start) != hipSuccess || p.take(&rec.stop) != hipSuccess)
-                return fail(MG_ERR_HIP, "hipEventCreate failed for %s", name);
-            timed = true;
-        }
-    }
-    if (timed && hipEventRecord(rec.start, stream) != hipSuccess)
-        return fail(MG_ERR_HIP, "hipEventRecord failed before %s", name);
-    hipError_t e = launch();
-    if (e != hipSuccess)
-        return fail(MG_ERR_HIP, "launch of %s failed: %s", name, hipGetErrorString(e));
-    if (timed) {
-        if (hipEventRecord(rec.stop, stream) != hipSuccess)
-            return fail(MG_ERR_HIP, "hipEventRecord failed after %s", name);
-        std::lock_guard<std::mutex> g(p.mu);
-        p.pending.push_back(rec);
-    }
-    return MG_OK;
+    return mg::host::check_optional_device_ptr(key_len, "key_len", 4);
 }
 
 const char *kernel_name(const char *stage, mg_contract_t c, int d) {
-    // Static storage: one name per (stage, contract, d).
-    static std::mutex mu;
-    static std::map<std::string, std::string> names;
-    char buf[96];
     const char *suffix = c == MG_CONTRACT_STRICT_F32 ? "f32"
                          : c == MG_CONTRACT_FAST_BF16 ? "bf16" : "accel";
+    char buf[96];
     snprintf(buf, sizeof buf, "%s_%s_d%d", stage, suffix, d);
-    std::lock_guard<std::mutex> g(mu);
-    auto it = names.find(buf);
-    if (it == names.end()) it = names.emplace(buf, buf).first;
-    return it->second.c_str();
+    return mg::host::intern_name(buf);
 }
-
-size_t round256(size_t n) { return (n + 255) / 256 * 256; }
 
 // The accelerated contract's backward is the strict-f32 backward (its
 // tensors are f32 and its backward matrices stay f32).
@@ -258,9 +135,9 @@ mg_status_t mg_attn_fwd_cross(const void *Q, const void *K, const void *V, void 
 
 size_t mg_attn_bwd_cross_workspace_bytes(int B, int H, int Lq, int Lk, int d, int causal,
                                          mg_contract_t contract) {
-    std::string saved = g_detail;
+    const std::string saved = mg::host::saved_detail();
     mg_status_t st = check_shape(B, H, Lq, Lk, d, 1.0f, contract);
-    g_detail = saved;
+    mg::host::restore_detail(saved);
     if (st != MG_OK) return 0;
     return workspace_bytes(B, H, Lq, Lk, d, causal, contract);
 }
@@ -348,66 +225,6 @@ mg_status_t mg_attn_bwd(const void *Q, const void *K, const void *V, const void 
                         size_t ws_bytes, hipStream_t stream) {
     return mg_attn_bwd_cross(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len, B, H, L, L, d, causal,
                              scale, contract, workspace, ws_bytes, stream);
-}
-
-const char *mg_status_string(mg_status_t s) {
-    switch (s) {
-    case MG_OK: return "MG_OK";
-    case MG_ERR_INVALID_ARGUMENT: return "MG_ERR_INVALID_ARGUMENT";
-    case MG_ERR_UNSUPPORTED: return "MG_ERR_UNSUPPORTED";
-    case MG_ERR_MISALIGNED: return "MG_ERR_MISALIGNED";
-    case MG_ERR_WORKSPACE: return "MG_ERR_WORKSPACE";
-    case MG_ERR_HIP: return "MG_ERR_HIP";
-    }
-    return "MG_ERR_UNKNOWN";
-}
-
-const char *mg_last_error_detail(void) { return g_detail.c_str(); }
-
-mg_status_t mg_profile_enable(int enable) {
-    Profiler &p = prof();
-    std::lock_guard<std::mutex> g(p.mu);
-    p.enabled = enable != 0;
-    return ok();
-}
-
-int mg_profile_collect(const char **names, int64_t *launches, double *total_ms,
-                       int max_entries) {
-    Profiler &p = prof();
-    std::lock_guard<std::mutex> g(p.mu);
-    for (const ProfRecord &r : p.pending) {
-        float ms = 0.f;
-        if (hipEventSynchronize(r.stop) != hipSuccess ||
-            hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess) {
-            fail(MG_ERR_HIP, "event wait failed for %s", r.name);
-            return -1;
-        }
-        auto it = p.totals.find(r.name);
-        if (it == p.totals.end()) {
-            it = p.totals.emplace(r.name, std::make_pair((int64_t)0, 0.0)).first;
-            p.order.push_back(r.name);
-        }
-        it->second.first += 1;
-        it->second.second += ms;
-        p.pool.push_back(r.start);
-        p.pool.push_back(r.stop);
-    }
-    p.pending.clear();
-    const int n = (int)p.order.size();
-    for (int i = 0; i < n && i < max_entries; ++i) {
-        const auto &t = p.totals[p.order[i]];
-        if (names) names[i] = p.order[i];
-        if (launches) launches[i] = t.first;
-        if (total_ms) total_ms[i] = t.second;
-    }
-    return n;
-}
-
-void mg_profile_reset(void) {
-    Profiler &p = prof();
-    std::lock_guard<std::mutex> g(p.mu);
-    p.totals.clear();
-    p.order.clear();
 }
 
 }  // extern "C"

@@ -13,23 +13,27 @@ from paper_2608_01563_amd import _binding
 
 
 def header_functions():
-    with open(mg.HEADER_PATH) as f:
-        text = f.read()
-    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(mg_[a-z_0-9]+)\s*\(", text)))
+    names = set()
+    for path in (mg.HEADER_PATH, mg.CONV_HEADER_PATH):
+        with open(path) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        names.update(re.findall(r"\b(mg_[a-z_0-9]+)\s*\(", text))
+    return sorted(names)
 
 
 @pytest.fixture(scope="module")
 def lib():
     if not os.path.exists(mg.LIB_PATH):
-        pytest.fail("libmgattn.so is not built; run __graft_entry__.build()")
+        pytest.fail("libmg.so is not built; run __graft_entry__.build()")
     return mg.load_library()
 
 
 def test_header_declares_the_boundary():
     names = header_functions()
     for required in ("mg_attn_fwd", "mg_attn_bwd", "mg_attn_bwd_workspace_bytes",
-                     "mg_status_string", "mg_last_error_detail"):
+                     "mg_status_string", "mg_last_error_detail", "mg_conv2d_bwd_data",
+                     "mg_conv2d_bwd_filter", "mg_conv2d_bwd_filter_workspace_bytes"):
         assert required in names
 
 
@@ -160,3 +164,58 @@ def test_host_memory_is_refused(lib):
     ptrs = [(ctypes.addressof(b) + 15) // 16 * 16 for b in bufs]
     assert _fwd(lib, ptrs) == 1
     assert "device" in mg.mg_last_error_detail()
+
+
+# ---- convolution derivatives (include/mg_conv.h)
+
+def _shape(N=1, H=8, W=8, C=4, K=8, R=3, S=3, sh=1, sw=1, ph=1, pw=1):
+    return _binding.ConvShape(N, H, W, C, K, R, S, sh, sw, ph, pw)
+
+
+def test_conv_workspace_query(lib):
+    # ResNet-50's first layer at batch 4: 3 output tiles (64 x 147 of dW) over
+    # 4*112*112 positions -> min(ceil(1024/3), 3136/16) = 196 splits
+    s = _shape(4, 224, 224, 3, 64, 7, 7, 2, 2, 3, 3)
+    assert lib.mg_conv2d_bwd_filter_workspace_bytes(ctypes.byref(s), 0) == 196 * 64 * 147 * 4
+    # a 3x3 512->512 layer at 7x7: 8 x 72 = 576 tiles fill the GPU: no workspace
+    s = _shape(4, 7, 7, 512, 512, 3, 3, 1, 1, 1, 1)
+    assert lib.mg_conv2d_bwd_filter_workspace_bytes(ctypes.byref(s), 0) == 0
+    # accelerated = strict; bf16, bad sizes and a filter larger than the
+    # padded input give 0
+    s = _shape(4, 56, 56, 64, 64, 1, 1, 1, 1, 0, 0)
+    assert lib.mg_conv2d_bwd_filter_workspace_bytes(ctypes.byref(s), 2) == \
+        lib.mg_conv2d_bwd_filter_workspace_bytes(ctypes.byref(s), 0) > 0
+    assert lib.mg_conv2d_bwd_filter_workspace_bytes(ctypes.byref(s), 1) == 0
+    assert lib.mg_conv2d_bwd_filter_workspace_bytes(ctypes.byref(_shape(C=0)), 0) == 0
+    assert lib.mg_conv2d_bwd_filter_workspace_bytes(
+        ctypes.byref(_shape(H=2, W=2, R=5, S=5, ph=1, pw=1)), 0) == 0
+
+
+@pytest.mark.parametrize("kwargs,status", [
+    (dict(N=0), 1), (dict(C=-1), 1), (dict(R=0), 1), (dict(sh=0), 1), (dict(pw=-1), 1),
+    (dict(H=2, R=5, ph=1), 1),                                   # no output row
+    (dict(N=64, H=512, W=512, C=64), 1),                         # X above 2^31-1 bytes
+])
+def test_conv_rejects_bad_shapes_before_any_device_call(lib, kwargs, status):
+    vp = ctypes.c_void_p
+    s = _shape(**kwargs)
+    assert lib.mg_conv2d_bwd_data(vp(0x1000), vp(0x2000), vp(0x3000), ctypes.byref(s), 0,
+                                  None) == status
+    assert mg.mg_last_error_detail() != ""
+
+
+def test_conv_contracts_and_pointers(lib):
+    vp = ctypes.c_void_p
+    s = _shape()
+    assert lib.mg_conv2d_bwd_data(vp(0x1000), vp(0x2000), vp(0x3000), ctypes.byref(s), 1,
+                                  None) == 2                     # no bf16 contract
+    assert lib.mg_conv2d_bwd_data(vp(0x1000), vp(0x2000), vp(0x3000), ctypes.byref(s), 7,
+                                  None) == 1
+    assert lib.mg_conv2d_bwd_data(vp(0x1000), None, vp(0x3000), ctypes.byref(s), 0,
+                                  None) == 1
+    assert lib.mg_conv2d_bwd_data(vp(0x1004), vp(0x2000), vp(0x3000), ctypes.byref(s), 0,
+                                  None) == 3
+    assert lib.mg_conv2d_bwd_data(vp(0x1000), vp(0x2000), vp(0x3000), None, 0, None) == 1
+    big = _shape(4, 224, 224, 3, 64, 7, 7, 2, 2, 3, 3)
+    assert lib.mg_conv2d_bwd_filter(vp(0x1000), vp(0x2000), vp(0x3000), ctypes.byref(big), 0,
+                                    None, 0, None) == 4          # workspace needed

@@ -1,0 +1,126 @@
+"""GPU parity of the convolution derivatives (through the C ABI) against the
+f64 convolution oracle on the same seeded inputs.
+
+Tolerance: normwise, max|gpu - oracle| / max|oracle| <= 1e-4 per output
+tensor.  Both derivatives are f32 sums of products with f32 accumulation; a
+sum of n products of unit-scale values carries a rounding error of about
+sqrt(n) * 2^-24 relative to its typical size (n up to 50176 here, about
+1.3e-5), and the normwise metric divides by the largest output, so 1e-4
+leaves a margin of several times over the measured errors.
+
+Small shapes are compared element by element; the ResNet-50 layer shapes
+(batch 4, 224x224) are run at full size and compared on sampled outputs that
+the oracle computes one by one.
+"""
+import numpy as np
+import pytest
+
+from gpu_util import normwise_error, say
+from workloads.conv import layer_inputs, make_conv_inputs, resnet50_layers
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-4
+
+# (N, H, W, C, K, R, S, stride, pad): odd sizes, channel counts off every
+# vector width, per-axis strides and pads, filters larger than the tile of a
+# dimension, single pixels and single channels
+SMALL = [
+    (2, 9, 7, 3, 5, 3, 3, (1, 1), (1, 1)),
+    (1, 13, 11, 3, 64, 7, 7, (2, 2), (3, 3)),
+    (2, 8, 8, 16, 24, 1, 1, (1, 1), (0, 0)),
+    (2, 9, 9, 16, 20, 1, 1, (2, 2), (0, 0)),
+    (1, 10, 12, 8, 12, 3, 3, (2, 2), (1, 1)),
+    (3, 5, 6, 68, 70, 3, 3, (1, 1), (1, 1)),
+    (1, 7, 9, 5, 7, 3, 2, (2, 1), (1, 0)),
+    (2, 1, 1, 4, 8, 1, 1, (1, 1), (0, 0)),
+    (1, 6, 6, 1, 1, 3, 3, (1, 1), (2, 2)),
+    (2, 17, 15, 32, 130, 3, 3, (1, 1), (1, 1)),
+    (1, 4, 4, 132, 36, 4, 4, (1, 1), (0, 0)),
+    (4, 12, 12, 64, 64, 3, 3, (1, 1), (1, 1)),
+]
+
+
+def run_gpu(x, need_input_grad=True):
+    import torch
+    import paper_2608_01563_amd as mg
+    X, W, dY = (torch.from_numpy(a.copy()).cuda() for a in (x.X, x.W, x.dY))
+    dX, dW = mg.conv2d_backward(X, W, dY, stride=x.stride, pad=x.pad,
+                                need_input_grad=need_input_grad)
+    torch.cuda.synchronize()
+    host = lambda t: None if t is None else t.cpu().numpy().astype(np.float64)
+    return host(dX), host(dW)
+
+
+@pytest.mark.parametrize("shape", SMALL)
+def test_small_shapes(gpu_lib, shape):
+    from oracle.conv import oracle_conv2d_bwd_data, oracle_conv2d_bwd_filter
+    N, H, W, C, K, R, S, stride, pad = shape
+    say("conv small N%d H%d W%d C%d K%d R%d S%d stride%s pad%s" % (N, H, W, C, K, R, S, stride,
+                                                                    pad))
+    x = make_conv_inputs(N, H, W, C, K, R, S, stride, pad, seed=H * 131 + C * 7 + K)
+    dX, dW = run_gpu(x)
+    rX = oracle_conv2d_bwd_data(x.dY, x.W, x.X.shape, stride, pad)
+    rW = oracle_conv2d_bwd_filter(x.X, x.dY, x.W.shape, stride, pad)
+    eX, eW = normwise_error(dX, rX), normwise_error(dW, rW)
+    assert eX <= TOL and eW <= TOL, (eX, eW)
+    # positions that no output reads (stride > filter) get exact zeros
+    assert np.all(dX[rX == 0.0] == 0.0)
+
+
+def test_repeatable_bit_for_bit(gpu_lib):
+    x = make_conv_inputs(4, 28, 28, 64, 64, 3, 3, 1, 1, seed=3)
+    a, b = run_gpu(x), run_gpu(x)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])
+
+
+LAYERS = resnet50_layers()
+# one layer of every distinct shape
+DISTINCT = {}
+for _layer in LAYERS:
+    DISTINCT.setdefault((_layer.H, _layer.C, _layer.K, _layer.R, _layer.stride), _layer)
+
+
+@pytest.mark.parametrize("layer", list(DISTINCT.values()), ids=lambda l: l.name)
+def test_resnet50_layer_sampled(gpu_lib, layer):
+    """Full-size ResNet-50 layer (batch 4): 256 sampled elements of dX and
+    of dW against the oracle's one-by-one sums, plus finiteness everywhere."""
+    from oracle.conv import oracle_conv2d_bwd_data_at, oracle_conv2d_bwd_filter_at
+    say("resnet50 %s: N%d H%d C%d K%d R%d stride %d" % (layer.name, layer.N, layer.H, layer.C,
+                                                       layer.K, layer.R, layer.stride))
+    x = layer_inputs(layer, seed=len(layer.name) * 17 + layer.C)
+    dX, dW = run_gpu(x, need_input_grad=layer.input_grad)
+    rng = np.random.default_rng(layer.K + layer.H)
+    iw = rng.integers(0, dW.size, 256)
+    rW = oracle_conv2d_bwd_filter_at(x.X, x.dY, x.W.shape, iw, x.stride, x.pad)
+    eW = np.max(np.abs(dW.reshape(-1)[iw] - rW)) / np.max(np.abs(dW))
+    assert np.all(np.isfinite(dW)) and eW <= TOL, eW
+    if layer.input_grad:
+        ix = rng.integers(0, dX.size, 256)
+        rX = oracle_conv2d_bwd_data_at(x.dY, x.W, x.X.shape, ix, x.stride, x.pad)
+        eX = np.max(np.abs(dX.reshape(-1)[ix] - rX)) / np.max(np.abs(dX))
+        assert np.all(np.isfinite(dX)) and eX <= TOL, eX
+
+
+def test_argument_errors(gpu_lib):
+    import torch
+    mg = gpu_lib
+    X = torch.zeros(1, 4, 4, 4, device="cuda")
+    W = torch.zeros(8, 3, 3, 4, device="cuda")
+    dY = torch.zeros(1, 2, 2, 8, device="cuda")
+    dW = torch.empty_like(W)
+    with pytest.raises(mg.MgError) as e:
+        mg.mg_conv2d_bwd_filter(X, dY, dW, contract="fast_bf16")
+    assert e.value.status == 2
+    with pytest.raises(ValueError):
+        mg.mg_conv2d_bwd_filter(X, dY[:, :1], dW)       # dY of the wrong shape
+    big = mg.mg_conv2d_bwd_filter_workspace_bytes((4, 224, 224, 3), (64, 7, 7, 3), (2, 2),
+                                                  (3, 3))
+    assert big > 0
+    Xb = torch.zeros(4, 224, 224, 3, device="cuda")
+    dYb = torch.zeros(4, 112, 112, 64, device="cuda")
+    dWb = torch.empty(64, 7, 7, 3, device="cuda")
+    small = torch.empty(big - 4, dtype=torch.uint8, device="cuda")
+    with pytest.raises(mg.MgError) as e:
+        mg.mg_conv2d_bwd_filter(Xb, dYb, dWb, stride=(2, 2), pad=(3, 3), workspace=small)
+    assert e.value.status == 4
