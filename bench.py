@@ -48,6 +48,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", type=int, default=3,
                     help="workload id (3 = causal B8 H8 L1024 d64 strict f32)")
+    ap.add_argument("--conv", action="store_true",
+                    help="time the convolution derivatives of one ResNet-50 backward step "
+                         "(batch 4, 224x224) instead of attention")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="repeat the oracle sample until this much CPU wall time (>= 3 runs)")
@@ -59,13 +62,19 @@ def parse():
     return ap.parse_args()
 
 
-def kernel_source_digest():
-    """sha256 over the names and contents of every file the library is built
-    from (kernels, headers, host code): a counter record taken on any other
-    source is stale."""
+def kernel_source_digest(conv=False):
+    """sha256 over the names and contents of the files a kernel family is
+    built from (attention: every file directly under csrc/; convolution:
+    csrc/conv/ plus the shared device and host headers): a counter record
+    taken on any other source is stale."""
     h = hashlib.sha256()
     base = os.path.join(ROOT, KERNEL_SOURCE_DIR)
-    for name in sorted(os.listdir(base)):
+    if conv:
+        names = ["conv/" + n for n in sorted(os.listdir(os.path.join(base, "conv")))]
+        names += ["device_common.h", "host_runtime.h", "host_runtime.cpp"]
+    else:
+        names = sorted(os.listdir(base))
+    for name in names:
         path = os.path.join(base, name)
         if os.path.isfile(path):
             h.update(name.encode() + b"\0")
@@ -132,16 +141,16 @@ def partial_rows(w, key_len):
     return total * w.H
 
 
-def traffic_for(kernel, w):
-    """HBM bytes per launch of `kernel` on workload `w` from the committed
+def traffic_for(kernel, workload_name, conv=False):
+    """HBM bytes per launch of `kernel` on a workload from the committed
     FETCH_SIZE / WRITE_SIZE counter runs (scaled by a plain copy of known
     size), or None if absent or taken on a different kernel source."""
-    path = os.path.join(ROOT, COUNTER_FILE.format(workload=w.name))
+    path = os.path.join(ROOT, COUNTER_FILE.format(workload=workload_name))
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("source_sha256") != kernel_source_digest():
+    if rec.get("source_sha256") != kernel_source_digest(conv):
         return None
     return rec.get("kernels", {}).get(kernel, {}).get("bytes_per_launch")
 
@@ -153,6 +162,8 @@ def main():
               "(B*H heads shard across GPUs with no exchange, see the design notes)"
               % args.gpus, file=sys.stderr)
         sys.exit(2)
+    if args.conv:
+        return conv_main(args)
 
     import numpy as np
     import torch
@@ -272,7 +283,7 @@ def main():
             ach, peak, u = amount / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
         out["roofline"] = {"kernel": dom, "bound": bound, "achieved": round(ach, 3),
                            "peak": peak, "unit": u, "frac": round(ach / peak, 4),
-                           "traffic": traffic_for(dom, w),
+                           "traffic": traffic_for(dom, w.name),
                            "algorithmic_per_launch": amount}
         out["bwd_credited_tflops"] = round(
             10.0 * w.d * pairs / (sum(kernels[k][1] / kernels[k][0] for k in kernels
@@ -333,6 +344,240 @@ def cpu_baseline(args, w, x, pairs, gpu_outputs):
     parity["tolerance"] = TOLERANCE[w.contract]
     parity["pass"] = all(v <= parity["tolerance"] for k, v in parity.items()
                          if k in ("O", "LSE", "dQ", "dK", "dV"))
+    return base, parity
+
+
+# ------------------------------------------------- convolution derivatives --
+CONV_WORKLOAD = "resnet50_conv_bwd_b4_224_f32"
+CONV_METRIC = ("ResNet-50 convolution derivatives TFLOP/s (data + filter gradients of all "
+               "53 layers, batch 4, 224x224, strict f32)")
+
+
+def conv_main(args):
+    """One step = the data gradient (every layer but the first) and the
+    filter gradient of each of ResNet-50's 53 convolutions, in backward
+    order, on resident inputs.  The step's launches are captured once into a
+    HIP graph and replayed (105 host calls per step would otherwise leave
+    the GPU waiting on the host); every replay's results are checked against
+    the eager step's.  Credited work: 2*N*P*Q*K*R*S*C flop per derivative."""
+    import numpy as np
+    import torch
+    import paper_2608_01563_amd as mg
+    from workloads.conv import layer_inputs, resnet50_layers
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    layers = resnet50_layers()
+    bufs = []
+    for i, L in enumerate(layers):
+        x = layer_inputs(L, seed=i)
+        X, W, dY = (torch.from_numpy(a.copy()).to(dev) for a in (x.X, x.W, x.dY))
+        dX = torch.empty_like(X) if L.input_grad else None
+        dW = torch.empty_like(W)
+        need = mg.mg_conv2d_bwd_filter_workspace_bytes(X.shape, W.shape, x.stride, x.pad)
+        need_x = mg.mg_conv2d_bwd_data_workspace_bytes(X.shape, W.shape, x.stride, x.pad)
+        need_b = mg.mg_conv2d_bwd_workspace_bytes(X.shape, W.shape, x.stride, x.pad)
+        ws = torch.empty(max(need, need_x, need_b, 256), dtype=torch.uint8, device=dev)
+        bufs.append((L, x, X, W, dY, dX, dW, ws, need, need_x))
+
+    def step():
+        # both derivatives in one call per layer; the first layer's input
+        # (the image) takes no gradient
+        for L, x, X, W, dY, dX, dW, ws, _, _ in reversed(bufs):
+            if dX is not None:
+                mg.mg_conv2d_bwd(X, W, dY, dX, dW, stride=x.stride, pad=x.pad, workspace=ws)
+            else:
+                mg.mg_conv2d_bwd_filter(X, dY, dW, stride=x.stride, pad=x.pad, workspace=ws)
+
+    def outputs():
+        return [(b[5].clone() if b[5] is not None else None, b[6].clone()) for b in bufs]
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    eager = outputs()
+
+    # eager step time (host launch bound) for reference
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    eager_ms = (time.perf_counter() - t0) * 1e3 / args.steps
+
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, capture_error_mode="relaxed"):
+        step()
+    torch.cuda.synchronize()
+    for b in bufs:                      # clear, so replays must rewrite every output
+        if b[5] is not None:
+            b[5].fill_(float("nan"))
+        b[6].fill_(float("nan"))
+    mismatches = 0
+    for _ in range(3):
+        graph.replay()
+        torch.cuda.synchronize()
+        mismatches += sum(int(not torch.equal(a[1], b[6])) +
+                          int(a[0] is not None and not torch.equal(a[0], b[5]))
+                          for a, b in zip(eager, bufs))
+    if mismatches:
+        raise RuntimeError("graph replay differs from the eager step (%d tensors)" % mismatches)
+
+    stream = torch.cuda.current_stream()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    stops = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        starts[k].record(stream)
+        graph.replay()
+        stops[k].record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
+    samples = sorted(a.elapsed_time(b) for a, b in zip(starts, stops))
+
+    flops = sum(L.flops() * (2 if L.input_grad else 1) for L in layers)
+    value = flops / (ms_per_step * 1e-3) / 1e12
+
+    # per-kernel durations: eager steps with the library's per-launch events
+    kernels = {}
+    if not args.no_kernel_events:
+        mg.mg_profile_reset()
+        mg.mg_profile_enable(True)
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        mg.mg_profile_enable(False)
+        kernels = mg.mg_profile_collect()
+    work = {"conv_bwd_f32": (sum(2 * L.flops() for L in layers if L.input_grad), "flop"),
+            "conv_bwd_reduce_f32": (sum(b[8] + b[9] + 4.0 * b[0].K * b[0].R * b[0].S * b[0].C *
+                                        (b[8] > 0) + 4.0 * b[0].N * b[0].H * b[0].W * b[0].C *
+                                        (b[9] > 0) for b in bufs if b[0].input_grad and
+                                        b[8] + b[9] > 0), "byte"),
+            "conv_dgrad_f32": (sum(L.flops() for L in layers if L.input_grad), "flop"),
+            "conv_wgrad_f32": (sum(L.flops() for L in layers if not L.input_grad), "flop"),
+            # each reads every split's partials and writes the output once
+            "conv_wgrad_reduce_f32": (sum(b[8] + 4.0 * b[0].K * b[0].R * b[0].S * b[0].C
+                                          for b in bufs if b[8] > 0 and not b[0].input_grad),
+                                      "byte"),
+            "conv_dgrad_reduce_f32": (sum(b[9] + 4.0 * b[0].N * b[0].H * b[0].W * b[0].C
+                                          for b in bufs if b[9] > 0 and b[0].input_grad),
+                                      "byte")}
+    out = {
+        "metric": CONV_METRIC,
+        "value": round(value, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": CONV_WORKLOAD, "layers": len(layers), "batch": 4,
+                   "image": 224, "layout": "NHWC / KRSC", "credited_gflop_per_step": flops / 1e9,
+                   "launch": "HIP graph of the whole step"},
+        "step_ms": {"median": round(float(np.median(samples)), 4),
+                    "min": round(samples[0], 4), "max": round(samples[-1], 4)},
+        "eager_ms_per_step": round(eager_ms, 4),
+        "pct_of_mfma_peak": round(100.0 * value / F32_MFMA_PEAK, 2),
+    }
+    if kernels:
+        per = {}
+        for name, (n, total) in kernels.items():
+            amount, unit = work[name]
+            per_step_ms = total / args.steps
+            rate = amount / (per_step_ms * 1e-3) / (1e12 if unit == "flop" else 1e9)
+            per[name] = {"launches_per_step": n // args.steps, "ms_per_step": round(per_step_ms, 4),
+                         "achieved": round(rate, 3),
+                         "unit": "TFLOP/s" if unit == "flop" else "GB/s"}
+        out["kernels"] = per
+        dom = max(kernels, key=lambda k: kernels[k][1])
+        n, total = kernels[dom]
+        amount, unit = work[dom]
+        per_launch = amount * args.steps / n
+        avg_s = total / n * 1e-3
+        if unit == "flop":
+            ach, peak, u, bound = per_launch / avg_s / 1e12, F32_MFMA_PEAK, "TFLOP/s", "mfma"
+        else:
+            ach, peak, u, bound = per_launch / avg_s / 1e9, HBM_PEAK_GBS, "GB/s", "hbm"
+        out["roofline"] = {"kernel": dom, "bound": bound, "achieved": round(ach, 3),
+                           "peak": peak, "unit": u, "frac": round(ach / peak, 4),
+                           "traffic": traffic_for(dom, CONV_WORKLOAD, conv=True),
+                           "algorithmic_per_launch": per_launch,
+                           "note": "averages over the step's launches of this kernel "
+                                   "(one per layer, shapes differ)"}
+        out["layers_ms"] = conv_layer_times(mg, bufs, torch)
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"], out["parity"] = conv_cpu_baseline(args, layers, bufs)
+    if args.copy_calibration_mib > 0:
+        nf = args.copy_calibration_mib * (1 << 20) // 4
+        src = torch.ones(nf, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_calibration_bytes"] = nf * 4
+    print(json.dumps(out), flush=True)
+
+
+def conv_layer_times(mg, bufs, torch, reps=5):
+    """Per-layer kernel time (ms) of the data and filter gradients, from the
+    library's per-launch events over `reps` eager runs of each layer."""
+    res = {}
+    for L, x, X, W, dY, dX, dW, ws, _, _ in bufs:
+        mg.mg_profile_reset()
+        mg.mg_profile_enable(True)
+        for _ in range(reps):
+            if dX is not None:
+                mg.mg_conv2d_bwd(X, W, dY, dX, dW, stride=x.stride, pad=x.pad, workspace=ws)
+            else:
+                mg.mg_conv2d_bwd_filter(X, dY, dW, stride=x.stride, pad=x.pad, workspace=ws)
+        torch.cuda.synchronize()
+        mg.mg_profile_enable(False)
+        ks = mg.mg_profile_collect()
+        res[L.name] = {k.replace("conv_", "").replace("_f32", ""): round(v[1] / v[0], 4)
+                       for k, v in ks.items()}
+    return res
+
+
+def conv_cpu_baseline(args, layers, bufs):
+    """The f64 oracle on the host's cores over a bounded sample: the two
+    derivatives of one mid-network layer (layer3.1.conv2, 3x3 256->256 at
+    14x14), repeated until about --cpu-seconds; plus sampled parity of the
+    timed run's outputs for that layer and for the first layer."""
+    import numpy as np
+    from oracle import oracle_num_threads
+    from oracle.conv import (oracle_conv2d_bwd_data, oracle_conv2d_bwd_filter,
+                             oracle_conv2d_bwd_filter_at)
+    idx = [i for i, L in enumerate(layers) if L.name == "layer3.1.conv2"][0]
+    L, x = bufs[idx][0], bufs[idx][1]
+    times = []
+    while len(times) < 3 or (sum(times) < args.cpu_seconds and len(times) < 100):
+        t0 = time.perf_counter()
+        rX = oracle_conv2d_bwd_data(x.dY, x.W, x.X.shape, x.stride, x.pad)
+        rW = oracle_conv2d_bwd_filter(x.X, x.dY, x.W.shape, x.stride, x.pad)
+        times.append(time.perf_counter() - t0)
+    total = float(sum(times))
+    value = 2 * L.flops() * len(times) / total / 1e12
+    base = {"value": round(value, 6), "unit": "TFLOP/s", "cores": oracle_num_threads(),
+            "kind": "oracle",
+            "sample": "both derivatives of %s (3x3, 256->256, 14x14, batch 4), run %d times "
+                      "back to back (%.1f s of CPU wall time)" % (L.name, len(times), total)}
+    parity = {}
+    gX = bufs[idx][5].cpu().numpy().astype(np.float64)
+    gW = bufs[idx][6].cpu().numpy().astype(np.float64)
+    parity[L.name + ".dX"] = float(np.max(np.abs(gX - rX)) / np.max(np.abs(rX)))
+    parity[L.name + ".dW"] = float(np.max(np.abs(gW - rW)) / np.max(np.abs(rW)))
+    L0, x0 = bufs[0][0], bufs[0][1]
+    g0 = bufs[0][6].cpu().numpy().astype(np.float64).reshape(-1)
+    iw = np.random.default_rng(0).integers(0, g0.size, 512)
+    r0 = oracle_conv2d_bwd_filter_at(x0.X, x0.dY, x0.W.shape, iw, x0.stride, x0.pad)
+    parity[L0.name + ".dW_sampled"] = float(np.max(np.abs(g0[iw] - r0)) / np.max(np.abs(g0)))
+    parity["tolerance"] = 1e-4
+    parity["pass"] = all(v <= 1e-4 for k, v in parity.items() if k not in ("tolerance",))
     return base, parity
 
 

@@ -53,34 +53,56 @@ typedef struct mg_conv2d_shape {
 } mg_conv2d_shape_t;
 
 /*
- * Data gradient dX [N][H][W][C] from dY [N][P][Q][K] and W [K][R][S][C].
- * MG_ERR_INVALID_ARGUMENT for sizes < 1, negative padding, no output
- * position (P < 1 or Q < 1), or any tensor above 2^31-1 bytes.
+ * Workspace.  Each derivative is one implicit GEMM; when its 64x64 output
+ * tiles number fewer than 512, the sum behind each output element is split
+ * over S = min(ceil(1024 / tiles), floor(ceil(terms / 32) / 4)) workgroups
+ * (terms = R*S*K for the data gradient, N*P*Q for the filter gradient), which
+ * write f32 partial outputs that a second kernel adds in split order.  The
+ * workspace holds those partials: S * (output elements) floats when S > 1,
+ * else nothing.  The *_workspace_bytes queries return that size (0 also for
+ * invalid arguments); `workspace` is caller-owned device memory of at least
+ * that many bytes, may be NULL when the size is 0, and its contents on entry
+ * are ignored.
  */
-mg_status_t mg_conv2d_bwd_data(const float *dY, const float *W, float *dX,
-                               const mg_conv2d_shape_t *shape, mg_contract_t contract,
-                               hipStream_t stream);
-
-/*
- * Bytes of device workspace mg_conv2d_bwd_filter needs: zero when the
- * filter's output tiles alone fill the GPU, else the f32 partial sums of
- * the pixel-range splits (splits * K*R*S*C floats).  Returns 0 also for
- * invalid arguments.
- */
+size_t mg_conv2d_bwd_data_workspace_bytes(const mg_conv2d_shape_t *shape,
+                                          mg_contract_t contract);
 size_t mg_conv2d_bwd_filter_workspace_bytes(const mg_conv2d_shape_t *shape,
                                             mg_contract_t contract);
 
 /*
+ * Data gradient dX [N][H][W][C] from dY [N][P][Q][K] and W [K][R][S][C].
+ * MG_ERR_INVALID_ARGUMENT for sizes < 1, negative padding, no output
+ * position (P < 1 or Q < 1), or any tensor above 2^31-1 bytes;
+ * MG_ERR_WORKSPACE for a missing or short workspace.
+ */
+mg_status_t mg_conv2d_bwd_data(const float *dY, const float *W, float *dX,
+                               const mg_conv2d_shape_t *shape, mg_contract_t contract,
+                               void *workspace, size_t workspace_bytes,
+                               hipStream_t stream);
+
+/*
  * Filter gradient dW [K][R][S][C] from X [N][H][W][C] and dY [N][P][Q][K].
- * `workspace` (caller-owned device memory of at least
- * mg_conv2d_bwd_filter_workspace_bytes(...) bytes, may be NULL when that is
- * zero) holds the partial sums when the sum over the N*P*Q output positions
- * is split over workgroups; its contents on entry are ignored.
+ * Errors as for the data gradient.
  */
 mg_status_t mg_conv2d_bwd_filter(const float *X, const float *dY, float *dW,
                                  const mg_conv2d_shape_t *shape, mg_contract_t contract,
                                  void *workspace, size_t workspace_bytes,
                                  hipStream_t stream);
+
+/*
+ * Both derivatives in one call (what a training step needs for every layer
+ * whose input takes a gradient): the two implicit GEMMs run as one launch,
+ * so each fills the GPU the other leaves idle, and their split sums are
+ * added by one more launch.  Results are bit for bit those of
+ * mg_conv2d_bwd_data and mg_conv2d_bwd_filter.  The workspace holds the data
+ * gradient's partials, then, from the next 256-byte boundary, the filter
+ * gradient's (mg_conv2d_bwd_workspace_bytes returns the total).
+ */
+size_t mg_conv2d_bwd_workspace_bytes(const mg_conv2d_shape_t *shape, mg_contract_t contract);
+
+mg_status_t mg_conv2d_bwd(const float *X, const float *W, const float *dY, float *dX,
+                          float *dW, const mg_conv2d_shape_t *shape, mg_contract_t contract,
+                          void *workspace, size_t workspace_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -24,9 +24,12 @@ from ._binding import (  # noqa: F401
     mg_attn_bwd_workspace_bytes,
     mg_attn_fwd,
     mg_attn_fwd_cross,
+    mg_conv2d_bwd,
     mg_conv2d_bwd_data,
+    mg_conv2d_bwd_data_workspace_bytes,
     mg_conv2d_bwd_filter,
     mg_conv2d_bwd_filter_workspace_bytes,
+    mg_conv2d_bwd_workspace_bytes,
     mg_last_error_detail,
     mg_profile_collect,
     mg_profile_enable,

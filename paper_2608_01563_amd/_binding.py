@@ -61,12 +61,18 @@ def _declare(lib):
                                       c_int, c_int, c_int, c_int, c_float, c_int, vp, c_size, vp]
     lib.mg_attn_bwd_cross.restype = c_int
     shp = ctypes.POINTER(ConvShape)
-    lib.mg_conv2d_bwd_data.argtypes = [vp, vp, vp, shp, c_int, vp]
+    lib.mg_conv2d_bwd_data_workspace_bytes.argtypes = [shp, c_int]
+    lib.mg_conv2d_bwd_data_workspace_bytes.restype = c_size
+    lib.mg_conv2d_bwd_data.argtypes = [vp, vp, vp, shp, c_int, vp, c_size, vp]
     lib.mg_conv2d_bwd_data.restype = c_int
     lib.mg_conv2d_bwd_filter_workspace_bytes.argtypes = [shp, c_int]
     lib.mg_conv2d_bwd_filter_workspace_bytes.restype = c_size
     lib.mg_conv2d_bwd_filter.argtypes = [vp, vp, vp, shp, c_int, vp, c_size, vp]
     lib.mg_conv2d_bwd_filter.restype = c_int
+    lib.mg_conv2d_bwd_workspace_bytes.argtypes = [shp, c_int]
+    lib.mg_conv2d_bwd_workspace_bytes.restype = c_size
+    lib.mg_conv2d_bwd.argtypes = [vp, vp, vp, vp, vp, shp, c_int, vp, c_size, vp]
+    lib.mg_conv2d_bwd.restype = c_int
     lib.mg_status_string.argtypes = [c_int]
     lib.mg_status_string.restype = ctypes.c_char_p
     lib.mg_last_error_detail.argtypes = []
@@ -276,16 +282,31 @@ def _check_f32(named):
             raise ValueError("%s has shape %s, expected %s" % (name, tuple(t.shape), tuple(want)))
 
 
+def mg_conv2d_bwd_data_workspace_bytes(X_shape, W_shape, stride=(1, 1), pad=(0, 0),
+                                       contract=STRICT_F32):
+    shape = conv_shape(X_shape, W_shape, stride, pad)
+    return int(load_library().mg_conv2d_bwd_data_workspace_bytes(ctypes.byref(shape),
+                                                                 _contract_id(contract)))
+
+
 def mg_conv2d_bwd_data(dY, W, dX, *, stride=(1, 1), pad=(0, 0), contract=STRICT_F32,
-                       stream=None):
-    """Data gradient into caller-provided dX [N,H,W,C] (channels-last)."""
+                       workspace=None, stream=None):
+    """Data gradient into caller-provided dX [N,H,W,C] (channels-last).
+    `workspace` as for mg_attn_bwd (allocated here with torch when None and
+    needed)."""
+    import torch
     lib = load_library()
     shape = conv_shape(dX.shape, W.shape, stride, pad)
     P, Q = conv_out_hw(shape)
     _check_f32((("dY", dY, (shape.N, P, Q, shape.K)), ("W", W, tuple(W.shape)),
                 ("dX", dX, tuple(dX.shape))))
+    need = mg_conv2d_bwd_data_workspace_bytes(dX.shape, W.shape, stride, pad, contract)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dX.device)
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib.mg_conv2d_bwd_data(_ptr(dY), _ptr(W), _ptr(dX), ctypes.byref(shape),
-                                  _contract_id(contract), _stream_handle(stream)))
+                                  _contract_id(contract), _ptr(workspace), nbytes,
+                                  _stream_handle(stream)))
 
 
 def mg_conv2d_bwd_filter_workspace_bytes(X_shape, W_shape, stride=(1, 1), pad=(0, 0),
@@ -312,6 +333,32 @@ def mg_conv2d_bwd_filter(X, dY, dW, *, stride=(1, 1), pad=(0, 0), contract=STRIC
     _check(lib.mg_conv2d_bwd_filter(_ptr(X), _ptr(dY), _ptr(dW), ctypes.byref(shape),
                                     _contract_id(contract), _ptr(workspace), nbytes,
                                     _stream_handle(stream)))
+
+
+def mg_conv2d_bwd_workspace_bytes(X_shape, W_shape, stride=(1, 1), pad=(0, 0),
+                                  contract=STRICT_F32):
+    shape = conv_shape(X_shape, W_shape, stride, pad)
+    return int(load_library().mg_conv2d_bwd_workspace_bytes(ctypes.byref(shape),
+                                                            _contract_id(contract)))
+
+
+def mg_conv2d_bwd(X, W, dY, dX, dW, *, stride=(1, 1), pad=(0, 0), contract=STRICT_F32,
+                  workspace=None, stream=None):
+    """Both derivatives in one call into caller-provided dX and dW."""
+    import torch
+    lib = load_library()
+    shape = conv_shape(X.shape, W.shape, stride, pad)
+    P, Q = conv_out_hw(shape)
+    _check_f32((("X", X, tuple(X.shape)), ("W", W, tuple(W.shape)),
+                ("dY", dY, (shape.N, P, Q, shape.K)), ("dX", dX, tuple(X.shape)),
+                ("dW", dW, tuple(W.shape))))
+    need = mg_conv2d_bwd_workspace_bytes(X.shape, W.shape, stride, pad, contract)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib.mg_conv2d_bwd(_ptr(X), _ptr(W), _ptr(dY), _ptr(dX), _ptr(dW),
+                             ctypes.byref(shape), _contract_id(contract), _ptr(workspace),
+                             nbytes, _stream_handle(stream)))
 
 
 def mg_status_string(status):
@@ -375,10 +422,11 @@ def conv2d_backward(X, W, dY, *, stride=(1, 1), pad=(0, 0), contract=STRICT_F32,
     """Allocate with torch and run both convolution derivatives; returns
     (dX or None, dW).  Layouts: X [N,H,W,C], W [K,R,S,C], dY [N,P,Q,K]."""
     import torch
-    dX = None
-    if need_input_grad:
-        dX = torch.empty_like(X)
-        mg_conv2d_bwd_data(dY, W, dX, stride=stride, pad=pad, contract=contract, stream=stream)
     dW = torch.empty_like(W)
-    mg_conv2d_bwd_filter(X, dY, dW, stride=stride, pad=pad, contract=contract, stream=stream)
+    if not need_input_grad:
+        mg_conv2d_bwd_filter(X, dY, dW, stride=stride, pad=pad, contract=contract,
+                             stream=stream)
+        return None, dW
+    dX = torch.empty_like(X)
+    mg_conv2d_bwd(X, W, dY, dX, dW, stride=stride, pad=pad, contract=contract, stream=stream)
     return dX, dW

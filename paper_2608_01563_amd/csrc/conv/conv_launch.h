@@ -13,19 +13,37 @@ struct ConvProblem {
     int P, Q;
 };
 
-// Data gradient dX = implicit GEMM over (n, h, w) x c, summing (r, s, k).
-hipError_t launch_conv_dgrad_f32(const ConvProblem &p, const float *dY, const float *Wt,
-                                 float *dX, hipStream_t s);
+// Division of 0 <= n < 2^31 by a fixed d >= 1 without a divide:
+// n / d == (mulhi(n, mul) + n) >> shift with shift = ceil(log2 d) and
+// mul = floor(2^32 (2^shift - d) / d) + 1 (the round-up method of Granlund
+// and Montgomery, 1994).
+struct FastDiv {
+    unsigned mul, shift;
+};
+FastDiv make_fastdiv(unsigned d);
 
-// Filter gradient dW = implicit GEMM over k x (r, s, c), summing (n, p, q).
-// When the output tiles alone leave the GPU mostly idle, the sum over
-// output positions is split over conv_wgrad_splits(p) workgroups per tile;
-// they write f32 partials [split][K*R*S*C] to `partials`, which
-// launch_conv_wgrad_reduce_f32 adds in split order.
+// Both derivatives are implicit GEMMs: the data gradient over (n, h, w) x c
+// summing (r, s, k), the filter gradient over k x (r, s, c) summing
+// (n, p, q).  When the output tiles alone leave the GPU mostly idle, the sum
+// is split over conv_*_splits(p) workgroups per tile; they write f32
+// partials [split][output elements] to `partials`, which
+// launch_conv_split_reduce_f32 adds in split order into the output.
+int conv_dgrad_splits(const ConvProblem &p);
 int conv_wgrad_splits(const ConvProblem &p);
+hipError_t launch_conv_dgrad_f32(const ConvProblem &p, const float *dY, const float *Wt,
+                                 float *dX, float *partials, hipStream_t s);
 hipError_t launch_conv_wgrad_f32(const ConvProblem &p, const float *X, const float *dY,
                                  float *dW, float *partials, hipStream_t s);
-hipError_t launch_conv_wgrad_reduce_f32(const ConvProblem &p, const float *partials, float *dW,
-                                        hipStream_t s);
+hipError_t launch_conv_split_reduce_f32(const float *partials, int nsplit, int total,
+                                        float *out, hipStream_t s);
+
+// Both derivatives in one launch (the data gradient's tiles first), and both
+// split reductions in one launch.
+hipError_t launch_conv_bwd_f32(const ConvProblem &p, const float *X, const float *Wt,
+                               const float *dY, float *dX, float *dW, float *dpart,
+                               float *wpart, hipStream_t s);
+hipError_t launch_conv_split_reduce2_f32(const float *part_a, int nsplit_a, int total_a,
+                                         float *out_a, const float *part_b, int nsplit_b,
+                                         int total_b, float *out_b, hipStream_t s);
 
 }  // namespace mg

@@ -174,12 +174,27 @@ def _shape(N=1, H=8, W=8, C=4, K=8, R=3, S=3, sh=1, sw=1, ph=1, pw=1):
 
 def test_conv_workspace_query(lib):
     # ResNet-50's first layer at batch 4: 3 output tiles (64 x 147 of dW) over
-    # 4*112*112 positions -> min(ceil(1024/3), 3136/16) = 196 splits
+    # 4*112*112 positions in 1568 32-deep steps -> min(ceil(1024/3), 1568/4) = 342 splits
     s = _shape(4, 224, 224, 3, 64, 7, 7, 2, 2, 3, 3)
-    assert lib.mg_conv2d_bwd_filter_workspace_bytes(ctypes.byref(s), 0) == 196 * 64 * 147 * 4
-    # a 3x3 512->512 layer at 7x7: 8 x 72 = 576 tiles fill the GPU: no workspace
+    assert lib.mg_conv2d_bwd_filter_workspace_bytes(ctypes.byref(s), 0) == 342 * 64 * 147 * 4
+    # a 3x3 512->512 layer at 7x7: the filter gradient's 8 x 72 = 576 tiles fill
+    # the GPU (no workspace); its data gradient has 4 x 8 = 32 tiles over 144
+    # steps -> min(32, 144/4) = 32 splits of the 196 x 512 output
     s = _shape(4, 7, 7, 512, 512, 3, 3, 1, 1, 1, 1)
     assert lib.mg_conv2d_bwd_filter_workspace_bytes(ctypes.byref(s), 0) == 0
+    assert lib.mg_conv2d_bwd_data_workspace_bytes(ctypes.byref(s), 0) == 32 * 196 * 512 * 4
+    # both at once: the data gradient's partials, 256-byte aligned, then the
+    # filter gradient's
+    s3 = _shape(4, 14, 14, 256, 256, 3, 3, 1, 1, 1, 1)
+    d = lib.mg_conv2d_bwd_data_workspace_bytes(ctypes.byref(s3), 0)
+    w = lib.mg_conv2d_bwd_filter_workspace_bytes(ctypes.byref(s3), 0)
+    assert d > 0 and w > 0
+    assert lib.mg_conv2d_bwd_workspace_bytes(ctypes.byref(s3), 0) == (d + 255) // 256 * 256 + w
+    assert lib.mg_conv2d_bwd_workspace_bytes(ctypes.byref(s), 0) == \
+        lib.mg_conv2d_bwd_data_workspace_bytes(ctypes.byref(s), 0)     # filter: no split
+    # 56x56 at batch 4 with 256 channels: 196 x 4 = 784 tiles, no split
+    s = _shape(4, 56, 56, 256, 64, 1, 1, 1, 1, 0, 0)
+    assert lib.mg_conv2d_bwd_data_workspace_bytes(ctypes.byref(s), 0) == 0
     # accelerated = strict; bf16, bad sizes and a filter larger than the
     # padded input give 0
     s = _shape(4, 56, 56, 64, 64, 1, 1, 1, 1, 0, 0)
@@ -200,22 +215,33 @@ def test_conv_rejects_bad_shapes_before_any_device_call(lib, kwargs, status):
     vp = ctypes.c_void_p
     s = _shape(**kwargs)
     assert lib.mg_conv2d_bwd_data(vp(0x1000), vp(0x2000), vp(0x3000), ctypes.byref(s), 0,
-                                  None) == status
+                                  None, 0, None) == status
     assert mg.mg_last_error_detail() != ""
 
 
 def test_conv_contracts_and_pointers(lib):
     vp = ctypes.c_void_p
     s = _shape()
-    assert lib.mg_conv2d_bwd_data(vp(0x1000), vp(0x2000), vp(0x3000), ctypes.byref(s), 1,
-                                  None) == 2                     # no bf16 contract
-    assert lib.mg_conv2d_bwd_data(vp(0x1000), vp(0x2000), vp(0x3000), ctypes.byref(s), 7,
-                                  None) == 1
-    assert lib.mg_conv2d_bwd_data(vp(0x1000), None, vp(0x3000), ctypes.byref(s), 0,
-                                  None) == 1
-    assert lib.mg_conv2d_bwd_data(vp(0x1004), vp(0x2000), vp(0x3000), ctypes.byref(s), 0,
-                                  None) == 3
-    assert lib.mg_conv2d_bwd_data(vp(0x1000), vp(0x2000), vp(0x3000), None, 0, None) == 1
+    call = lambda a, b, c, shp, k: lib.mg_conv2d_bwd_data(a, b, c, shp, k, None, 0, None)
+    assert call(vp(0x1000), vp(0x2000), vp(0x3000), ctypes.byref(s), 1) == 2   # no bf16
+    assert call(vp(0x1000), vp(0x2000), vp(0x3000), ctypes.byref(s), 7) == 1
+    assert call(vp(0x1000), None, vp(0x3000), ctypes.byref(s), 0) == 1
+    assert call(vp(0x1004), vp(0x2000), vp(0x3000), ctypes.byref(s), 0) == 3
+    assert call(vp(0x1000), vp(0x2000), vp(0x3000), None, 0) == 1
+    s7 = _shape(4, 7, 7, 512, 512, 3, 3, 1, 1, 1, 1)
+    assert call(vp(0x1000), vp(0x2000), vp(0x3000), ctypes.byref(s7), 0) == 4  # workspace
     big = _shape(4, 224, 224, 3, 64, 7, 7, 2, 2, 3, 3)
     assert lib.mg_conv2d_bwd_filter(vp(0x1000), vp(0x2000), vp(0x3000), ctypes.byref(big), 0,
                                     None, 0, None) == 4          # workspace needed
+
+
+def test_conv_fused_entry_point_checks(lib):
+    vp = ctypes.c_void_p
+    s = _shape()
+    args = [vp(0x1000), vp(0x2000), vp(0x3000), vp(0x4000), vp(0x5000)]
+    assert lib.mg_conv2d_bwd(*args, ctypes.byref(s), 1, None, 0, None) == 2
+    args[3] = None
+    assert lib.mg_conv2d_bwd(*args, ctypes.byref(s), 0, None, 0, None) == 1
+    big = _shape(4, 7, 7, 512, 512, 3, 3, 1, 1, 1, 1)
+    args[3] = vp(0x4000)
+    assert lib.mg_conv2d_bwd(*args, ctypes.byref(big), 0, None, 0, None) == 4

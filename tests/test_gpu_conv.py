@@ -68,6 +68,28 @@ def test_small_shapes(gpu_lib, shape):
     assert np.all(dX[rX == 0.0] == 0.0)
 
 
+@pytest.mark.parametrize("shape", [SMALL[1], SMALL[4], SMALL[9], (4, 7, 7, 128, 128, 3, 3, 1, 1),
+                                   (4, 14, 14, 64, 256, 1, 1, 2, 0)])
+def test_fused_equals_separate_calls(gpu_lib, shape):
+    """mg_conv2d_bwd (both derivatives in one launch) gives exactly the
+    results of mg_conv2d_bwd_data and mg_conv2d_bwd_filter."""
+    import torch
+    mg = gpu_lib
+    N, H, W, C, K, R, S, stride, pad = shape
+    stride = (stride, stride) if isinstance(stride, int) else stride
+    pad = (pad, pad) if isinstance(pad, int) else pad
+    say("conv fused vs separate N%d H%d C%d K%d R%d stride%s" % (N, H, C, K, R, stride))
+    x = make_conv_inputs(N, H, W, C, K, R, S, stride, pad, seed=11)
+    X, Wt, dY = (torch.from_numpy(a.copy()).cuda() for a in (x.X, x.W, x.dY))
+    dX1, dW1 = torch.empty_like(X), torch.empty_like(Wt)
+    mg.mg_conv2d_bwd_data(dY, Wt, dX1, stride=stride, pad=pad)
+    mg.mg_conv2d_bwd_filter(X, dY, dW1, stride=stride, pad=pad)
+    dX2, dW2 = torch.empty_like(X), torch.empty_like(Wt)
+    mg.mg_conv2d_bwd(X, Wt, dY, dX2, dW2, stride=stride, pad=pad)
+    torch.cuda.synchronize()
+    assert torch.equal(dX1, dX2) and torch.equal(dW1, dW2)
+
+
 def test_repeatable_bit_for_bit(gpu_lib):
     x = make_conv_inputs(4, 28, 28, 64, 64, 3, 3, 1, 1, seed=3)
     a, b = run_gpu(x), run_gpu(x)
