@@ -55,8 +55,11 @@ typedef struct mg_conv2d_shape {
 /*
  * Workspace.  Each derivative is one implicit GEMM; when its 64x64 output
  * tiles number fewer than 512, the sum behind each output element is split
- * over S = min(ceil(1024 / tiles), floor(ceil(terms / 32) / 4)) workgroups
- * (terms = R*S*K for the data gradient, N*P*Q for the filter gradient), which
+ * over S = min(ceil(1024 / tiles), floor(ceil(terms / 16) / 8)) workgroups
+ * (terms = N*P*Q for the filter gradient; for the data gradient, whose
+ * pixels split into stride-parity classes that each sum only the filter taps
+ * reaching them, tiles are counted over all classes and terms = the largest
+ * class's taps times K), which
  * write f32 partial outputs that a second kernel adds in split order.  The
  * workspace holds those partials: S * (output elements) floats when S > 1,
  * else nothing.  The *_workspace_bytes queries return that size (0 also for

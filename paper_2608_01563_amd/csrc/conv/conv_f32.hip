@@ -15,7 +15,7 @@
 //
 // Both run 64x64 output tiles on 256 threads: each of the four waves owns a
 // 32x32 quarter as 2x2 blocks of 16x16 accumulators, and the reduction
-// advances BK (32) at a time through double-buffered LDS tiles (one barrier
+// advances BK (16) at a time through double-buffered LDS tiles (one barrier
 // per step; the global loads of steps t+1 and t+2 are in flight, in two
 // register sets, during the products of step t).  Operands reach LDS through raw buffer loads whose offset is
 // pushed past the end of the buffer for a padded or out-of-range element,
@@ -23,6 +23,9 @@
 // dimension and the positions a strided data gradient skips all become
 // zeros without a branch.  Every output element is one fixed-order sum
 // (within a workgroup, then across splits in split order): no atomics.
+#include <algorithm>
+#include <vector>
+
 #include "../device_common.h"
 #include "conv_launch.h"
 
@@ -30,7 +33,7 @@ namespace mg {
 namespace {
 
 #ifndef MG_CONV_BK
-#define MG_CONV_BK 32
+#define MG_CONV_BK 16
 #endif
 constexpr int BM = 64;          // output rows per workgroup
 constexpr int BN = 64;          // output columns per workgroup
@@ -38,9 +41,14 @@ constexpr int BK = MG_CONV_BK;  // reduction step (16 or 32)
 constexpr int NSUB = BK / 16;   // staged rows per thread and operand in one step
 constexpr int NT = 256;         // four waves
 constexpr int LDR = 64 + 16;    // reduction-major tiles: rows 80 floats (16 banks) apart
-constexpr int LDM = BK + 4;     // the data gradient's pixel-major A tile: 20 or 36 floats
-                                // per row, both conflict-free for the operand reads
+constexpr int LDM = BK + 4;     // the data gradient's pixel-major A tile: 20 (or 36)
+                                // floats per row, conflict-free for the operand reads
 static_assert(BK == 16 || BK == 32, "reduction step");
+// Waves per SIMD the register allocator must allow (measured best of 4, 6
+// and 8 at a 16-deep step; 4 also fits 40 KB workgroups at a 32-deep one).
+#ifndef MG_CONV_OCC
+#define MG_CONV_OCC 4
+#endif
 constexpr int kOOB = 0x7ffffff0;   // byte offset past every buffer: reads as zero
 
 __device__ __forceinline__ int fdiv(int n, FastDiv f) {
@@ -103,11 +111,25 @@ struct WgradJob {
     float *out;        // dW (one split) or the partials [split][K][R*S*C]
     int tiles_j, nsplit, nsteps, blocks;
 };
-// Work of one data-gradient launch: grid (m tile, c tile, split), split fastest.
+// Data-gradient work of one stride-parity class.  With strides (sh, sw) the
+// input pixels split into sh*sw classes h = a + sh*i, w = b + sw*j, and the
+// only filter taps that reach a pixel of class (a, b) are r = r0 + sh*tr,
+// s = s0 + sw*ts with r0 = (a + ph) mod sh, s0 = (b + pw) mod sw; such a tap
+// reads output position p = i + da - tr, q = j + db - ts.  Each class is a
+// dense GEMM over (n, i, j) x c summing only its (tr, ts, k): no tap that
+// skips the pixel is ever multiplied (stride 1 is one class with every tap).
+// Grid of a class: (m tile, c tile, split), split fastest.
 struct DgradJob {
     const float *dY, *Wt;
-    float *out;        // dX (one split) or the partials [split][N*H*W][C]
+    float *out;        // dX (one split) or the partials [split][N*H*W][C], dX layout
     int tiles_c, nsplit, blocks;
+    int a, b, Hc, Wc, r0, s0, Rc, Sc, da, db;
+    FastDiv HWc, Wc_, Sc_;
+};
+constexpr int kMaxClasses = 16;   // strides up to 4 x 4 in one launch
+struct DgradJobs {
+    DgradJob c[kMaxClasses];
+    int n;
 };
 
 // ------------------------------------------------------- filter gradient --
@@ -247,7 +269,8 @@ __device__ __forceinline__ void wgrad_tile(int bid, WgradLds &L, const WgradJob 
 }
 
 template <int VA, int VB>
-__global__ __launch_bounds__(NT) void conv_wgrad_f32(WgradJob job, ConvProblem p, ConvDivs dv) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(MG_CONV_OCC, 8)))
+void conv_wgrad_f32(WgradJob job, ConvProblem p, ConvDivs dv) {
     __shared__ ConvLds lds;
     wgrad_tile<VA, VB>(blockIdx.x, lds.w, job, p, dv);
 }
@@ -301,8 +324,9 @@ __global__ __launch_bounds__(256) void conv_split_reduce_f32(ReduceJob a, Reduce
 }
 
 // --------------------------------------------------------- data gradient --
-// Block `bid` of the job: split `split` of `nsplit` sums the reduction steps
-// [st0, st1) of (r, s, k) for one 64x64 tile of dX.
+// Block `bid` of a class job: split `split` of `nsplit` sums the reduction
+// steps [st0, st1) of the class's (tr, ts, k) for one 64x64 tile of its
+// pixels x channels.
 template <int VA, int VB>
 __device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob &job,
                                            const ConvProblem &p, const ConvDivs &dv) {
@@ -313,9 +337,10 @@ __device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob 
     float *__restrict__ out = job.out;
     const int tiles_c = job.tiles_c, nsplit = job.nsplit;
 
-    const int M = p.N * p.H * p.W;
-    const int RSK = p.R * p.S * p.K;
-    const int nsteps = (RSK + BK - 1) / BK;
+    const int HWc = job.Hc * job.Wc;
+    const int Mc = p.N * HWc;
+    const int RSKc = job.Rc * job.Sc * p.K;
+    const int nsteps = (RSKc + BK - 1) / BK;
     const int split = bid % nsplit;
     bid /= nsplit;
     const int m0 = (bid / tiles_c) * BM;
@@ -332,42 +357,43 @@ __device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob 
     const auto rdy = buffer_rsrc(dY, p.N * p.P * p.Q * p.K * 4);
     const auto rw = buffer_rsrc(Wt, p.K * p.R * p.S * p.C * 4);
 
-    // A staging: pixel row ar (fixed), reduction columns 4*jq + 16u .. +3 of
-    // a step; B staging: reduction rows jr + 16u of a step, channel columns.
+    // A staging: class pixel row ar (fixed), reduction columns 4*jq + 16u ..
+    // +3 of a step; B staging: reduction rows jr + 16u of a step, channel columns.
     const int ar = tid >> 2, jq = tid & 3;
     const int m = m0 + ar;
-    const bool mok = m < M;
-    const int n = fdiv(m, dv.HW), hw = m - n * (p.H * p.W);
-    const int h = fdiv(hw, dv.W), wpix = hw - h * p.W;
+    const bool mok = m < Mc;
+    const int n = fdiv(m, job.HWc), ij = m - n * HWc;
+    const int i = fdiv(ij, job.Wc_), jw = ij - i * job.Wc;
     const int jr = tid >> 4, cc = tid & 15;
     int cb[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) cb[e] = (VB == 4) ? c0 + 4 * cc + e : c0 + cc + 16 * e;
 
-    const int nP = n * p.P, hph = h + p.ph, wpw = wpix + p.pw;
-    const int RS = p.R * p.S;
-    // K % BK == 0: every step lies within one tap (r, s), known to the whole
-    // workgroup; otherwise each staged element finds its own tap.
+    const int nP = n * p.P, pi = i + job.da, qj = jw + job.db;   // p = pi - tr, q = qj - ts
+    // K % BK == 0: every step lies within one tap (tr, ts), known to the
+    // whole workgroup; otherwise each staged element finds its own tap.
     const bool tap_uniform = p.K % BK == 0;
 
-    // dY offset of reduction index (tap t = r*S + s, channel k) for this
-    // thread's pixel, or kOOB when no output position (p, q) reads it.
-    auto dy_offset = [&](int r, int s, int k) {
-        const int hp = hph - r, wq = wpw - s;   // = p*sh, q*sw
-        const int pp = fdiv(hp < 0 ? 0 : hp, dv.sh), qq = fdiv(wq < 0 ? 0 : wq, dv.sw);
-        const bool ok = mok && hp >= 0 && wq >= 0 && pp * p.sh == hp && qq * p.sw == wq &&
-                        pp < p.P && qq < p.Q;
+    // dY offset of (tap (tr, ts), channel k) for this thread's pixel, or kOOB
+    // when the tap's output position lies outside dY.
+    auto dy_offset = [&](int tr, int ts, int k) {
+        const int pp = pi - tr, qq = qj - ts;
+        const bool ok = mok && (unsigned)pp < (unsigned)p.P && (unsigned)qq < (unsigned)p.Q;
         return ok ? (((nP + pp) * p.Q + qq) * p.K + k) * 4 : kOOB;
+    };
+    // first float of W[k][r][s][:] for tap (tr, ts)
+    auto w_row = [&](int k, int tr, int ts) {
+        return ((k * p.R + job.r0 + p.sh * tr) * p.S + job.s0 + p.sw * ts) * p.C;
     };
 
     auto load = [&](int st, f32x4 (&ra)[NSUB], f32x4 (&rb)[NSUB]) {
         const int j0 = st * BK;
-        int t0 = 0, kb = 0, r0 = 0, s0 = 0;
+        int kb = 0, tr0 = 0, ts0 = 0;
         if (tap_uniform) {
-            t0 = fdiv(j0, dv.K);
+            const int t0 = fdiv(j0, dv.K);
             kb = j0 - t0 * p.K;
-            r0 = fdiv(t0, dv.S);
-            s0 = t0 - r0 * p.S;
+            tr0 = fdiv(t0, job.Sc_);
+            ts0 = t0 - tr0 * job.Sc;
         }
 #pragma unroll
         for (int u = 0; u < NSUB; ++u) {
@@ -376,14 +402,14 @@ __device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob 
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
                     const int dk = 16 * u + 4 * jq + e;
-                    oa[e] = j0 + dk < RSK ? dy_offset(r0, s0, kb + dk) : kOOB;
+                    oa[e] = j0 + dk < RSKc ? dy_offset(tr0, ts0, kb + dk) : kOOB;
                     if (VA == 4) break;
                 }
-                // W[k][r][s][c] for reduction row k = kb + 16u + jr of tap t0
-                const int row = ((kb + 16 * u + jr) * RS + t0) * p.C;
+                // W[k][r][s][c] for reduction row k = kb + 16u + jr of the tap
+                const int row = w_row(kb + 16 * u + jr, tr0, ts0);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    ob[e] = (j0 + 16 * u + jr < RSK && cb[e] < p.C) ? (row + cb[e]) * 4 : kOOB;
+                    ob[e] = (j0 + 16 * u + jr < RSKc && cb[e] < p.C) ? (row + cb[e]) * 4 : kOOB;
                     if (VB == 4) break;
                 }
             } else {
@@ -392,16 +418,17 @@ __device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob 
                     // a 16-byte chunk (VA == 4, K % 4 == 0) never straddles two taps
                     const int j = j0 + 16 * u + 4 * jq + e;
                     const int t = fdiv(j, dv.K), k = j - t * p.K;
-                    const int r = fdiv(t, dv.S), s = t - r * p.S;
-                    oa[e] = j < RSK ? dy_offset(r, s, k) : kOOB;
+                    const int tr = fdiv(t, job.Sc_), ts = t - tr * job.Sc;
+                    oa[e] = j < RSKc ? dy_offset(tr, ts, k) : kOOB;
                     if (VA == 4) break;
                 }
                 const int j = j0 + 16 * u + jr;
                 const int t = fdiv(j, dv.K), k = j - t * p.K;
-                const int row = (k * RS + t) * p.C;   // ((k*R + r)*S + s) * C
+                const int tr = fdiv(t, job.Sc_), ts = t - tr * job.Sc;
+                const int row = w_row(k, tr, ts);
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    ob[e] = (j < RSK && cb[e] < p.C) ? (row + cb[e]) * 4 : kOOB;
+                    ob[e] = (j < RSKc && cb[e] < p.C) ? (row + cb[e]) * 4 : kOOB;
                     if (VB == 4) break;
                 }
             }
@@ -424,9 +451,9 @@ __device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob 
 
     f32x4 acc[2][2];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
-        for (int jb = 0; jb < 2; ++jb) acc[i][jb] = zero4();
+        for (int jb = 0; jb < 2; ++jb) acc[ii][jb] = zero4();
 
     // Two register sets keep the loads of the next two steps in flight while
     // the current step, already in LDS, is multiplied.
@@ -441,7 +468,7 @@ __device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob 
         const int cur = (st - st0) & 1;
         if (st + 2 < st1) load(st + 2, fa, fb);
         mma_step(acc,
-                 [&](int kk, int i) { return As[cur][32 * wm + 16 * i + il][4 * kk + g]; },
+                 [&](int kk, int ii) { return As[cur][32 * wm + 16 * ii + il][4 * kk + g]; },
                  [&](int kk, int jb) { return Bs[cur][4 * kk + g][32 * wn + 16 * jb + il]; });
         if (st + 1 < st1) store(cur ^ 1, na, nb);
         __syncthreads();
@@ -451,35 +478,59 @@ __device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob 
         if (st + 1 < st1) body(st + 1, ra0, rb0, ra1, rb1);
     }
 
-    float *dst = out + (size_t)split * M * p.C;   // split 0 of 1 is dX itself
+    // rows of this lane's accumulators back to dX pixels (n, a + sh*i, b + sw*j)
+    float *dst = out + (size_t)split * p.N * p.H * p.W * p.C;   // split 0 of 1 is dX
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
-        for (int jb = 0; jb < 2; ++jb)
+        for (int r = 0; r < 4; ++r) {
+            const int mo = m0 + 32 * wm + 16 * ii + 4 * g + r;
+            if (mo >= Mc) continue;
+            const int on = fdiv(mo, job.HWc), oij = mo - on * HWc;
+            const int oi = fdiv(oij, job.Wc_), oj = oij - oi * job.Wc;
+            const size_t pix = ((size_t)on * p.H + job.a + p.sh * oi) * p.W + job.b + p.sw * oj;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int mo = m0 + 32 * wm + 16 * i + 4 * g + r;
+            for (int jb = 0; jb < 2; ++jb) {
                 const int c = c0 + 32 * wn + 16 * jb + il;
-                if (mo < M && c < p.C) dst[(size_t)mo * p.C + c] = acc[i][jb][r];
+                if (c < p.C) dst[pix * p.C + c] = acc[ii][jb][r];
             }
+        }
+}
+
+// Which class job a block belongs to (job counts and sizes are uniform).
+__device__ __forceinline__ int find_class(const DgradJobs &jobs, int &bid) {
+    int c = 0;
+    while (c + 1 < jobs.n && bid >= jobs.c[c].blocks) {
+        bid -= jobs.c[c].blocks;
+        ++c;
+    }
+    return c;
 }
 
 template <int VA, int VB>
-__global__ __launch_bounds__(NT) void conv_dgrad_f32(DgradJob job, ConvProblem p, ConvDivs dv) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(MG_CONV_OCC, 8)))
+void conv_dgrad_f32(DgradJobs jobs, ConvProblem p,
+                                                     ConvDivs dv) {
     __shared__ ConvLds lds;
-    dgrad_tile<VA, VB>(blockIdx.x, lds.d, job, p, dv);
+    int bid = blockIdx.x;
+    const int c = find_class(jobs, bid);
+    dgrad_tile<VA, VB>(bid, lds.d, jobs.c[c], p, dv);
 }
 
-// Both derivatives of one convolution in one launch: the first d.blocks
-// workgroups run the data gradient, the rest the filter gradient.
+// Both derivatives of one convolution in one launch: the first `dblocks`
+// workgroups run the data gradient's class jobs, the rest the filter gradient.
 template <int VA, int VB>
-__global__ __launch_bounds__(NT) void conv_bwd_f32(DgradJob d, WgradJob w, ConvProblem p,
-                                                   ConvDivs dv) {
+__global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(MG_CONV_OCC, 8)))
+void conv_bwd_f32(DgradJobs d, int dblocks, WgradJob w,
+                                                   ConvProblem p, ConvDivs dv) {
     __shared__ ConvLds lds;
-    if ((int)blockIdx.x < d.blocks)
-        dgrad_tile<VA, VB>(blockIdx.x, lds.d, d, p, dv);
-    else
-        wgrad_tile<VA, VB>(blockIdx.x - d.blocks, lds.w, w, p, dv);
+    int bid = blockIdx.x;
+    if (bid < dblocks) {
+        const int c = find_class(d, bid);
+        dgrad_tile<VA, VB>(bid, lds.d, d.c[c], p, dv);
+    } else {
+        wgrad_tile<VA, VB>(bid - dblocks, lds.w, w, p, dv);
+    }
 }
 
 int cdiv(int a, int b) { return (a + b - 1) / b; }
@@ -524,9 +575,46 @@ int conv_wgrad_splits(const ConvProblem &p) {
                       cdiv(p.N * p.P * p.Q, BK));
 }
 
+namespace {
+
+// The stride-parity classes of the data gradient (see DgradJob), without
+// the pointers and split; classes without pixels are left out.
+std::vector<DgradJob> dgrad_classes(const ConvProblem &p) {
+    std::vector<DgradJob> cls;
+    for (int a = 0; a < p.sh; ++a)
+        for (int b = 0; b < p.sw; ++b) {
+            DgradJob j{};
+            j.a = a;
+            j.b = b;
+            j.Hc = a < p.H ? cdiv(p.H - a, p.sh) : 0;
+            j.Wc = b < p.W ? cdiv(p.W - b, p.sw) : 0;
+            if (j.Hc == 0 || j.Wc == 0) continue;
+            j.r0 = (a + p.ph) % p.sh;
+            j.s0 = (b + p.pw) % p.sw;
+            j.Rc = j.r0 < p.R ? cdiv(p.R - j.r0, p.sh) : 0;
+            j.Sc = j.s0 < p.S ? cdiv(p.S - j.s0, p.sw) : 0;
+            j.da = (a + p.ph - j.r0) / p.sh;
+            j.db = (b + p.pw - j.s0) / p.sw;
+            j.HWc = make_fastdiv(j.Hc * j.Wc);
+            j.Wc_ = make_fastdiv(j.Wc);
+            j.Sc_ = make_fastdiv(j.Sc > 0 ? j.Sc : 1);
+            j.tiles_c = cdiv(p.C, BN);
+            cls.push_back(j);
+        }
+    return cls;
+}
+
+}  // namespace
+
+// One split count for every class: from the classes' total tiles and the
+// longest class reduction.
 int conv_dgrad_splits(const ConvProblem &p) {
-    return splits_for((long)cdiv(p.N * p.H * p.W, BM) * cdiv(p.C, BN),
-                      cdiv(p.R * p.S * p.K, BK));
+    long tiles = 0, steps = 0;
+    for (const DgradJob &j : dgrad_classes(p)) {
+        tiles += (long)cdiv(p.N * j.Hc * j.Wc, BM) * j.tiles_c;
+        steps = std::max<long>(steps, cdiv(j.Rc * j.Sc * p.K, BK));
+    }
+    return splits_for(tiles, steps);
 }
 
 namespace {
@@ -539,12 +627,28 @@ WgradJob wgrad_job(const ConvProblem &p, const float *X, const float *dY, float 
                     cdiv(p.K, BM) * tiles_j * ns};
 }
 
-DgradJob dgrad_job(const ConvProblem &p, const float *dY, const float *Wt, float *dX,
-                   float *partials) {
+// The data gradient's class jobs, in launches of at most kMaxClasses.
+std::vector<DgradJobs> dgrad_jobs(const ConvProblem &p, const float *dY, const float *Wt,
+                                  float *dX, float *partials) {
     const int ns = conv_dgrad_splits(p);
-    const int tiles_c = cdiv(p.C, BN);
-    return DgradJob{dY, Wt, ns > 1 ? partials : dX, tiles_c, ns,
-                    cdiv(p.N * p.H * p.W, BM) * tiles_c * ns};
+    std::vector<DgradJobs> launches;
+    for (DgradJob j : dgrad_classes(p)) {
+        j.dY = dY;
+        j.Wt = Wt;
+        j.out = ns > 1 ? partials : dX;
+        j.nsplit = ns;
+        j.blocks = cdiv(p.N * j.Hc * j.Wc, BM) * j.tiles_c * ns;
+        if (launches.empty() || launches.back().n == kMaxClasses) launches.push_back(DgradJobs{});
+        DgradJobs &l = launches.back();
+        l.c[l.n++] = j;
+    }
+    return launches;
+}
+
+int total_blocks(const DgradJobs &d) {
+    int b = 0;
+    for (int i = 0; i < d.n; ++i) b += d.c[i].blocks;
+    return b;
 }
 
 ReduceJob reduce_job(const float *partials, int nsplit, int total, float *out) {
@@ -577,17 +681,18 @@ struct LaunchW {
 };
 template <int VA, int VB>
 struct LaunchD {
-    static hipError_t run(const DgradJob &j, const ConvProblem &p, const ConvDivs &dv,
+    static hipError_t run(const DgradJobs &j, const ConvProblem &p, const ConvDivs &dv,
                           hipStream_t s) {
-        conv_dgrad_f32<VA, VB><<<dim3(j.blocks), dim3(NT), 0, s>>>(j, p, dv);
+        conv_dgrad_f32<VA, VB><<<dim3(total_blocks(j)), dim3(NT), 0, s>>>(j, p, dv);
         return hipGetLastError();
     }
 };
 template <int VA, int VB>
 struct LaunchDW {
-    static hipError_t run(const DgradJob &d, const WgradJob &w, const ConvProblem &p,
+    static hipError_t run(const DgradJobs &d, const WgradJob &w, const ConvProblem &p,
                           const ConvDivs &dv, hipStream_t s) {
-        conv_bwd_f32<VA, VB><<<dim3(d.blocks + w.blocks), dim3(NT), 0, s>>>(d, w, p, dv);
+        const int db = total_blocks(d);
+        conv_bwd_f32<VA, VB><<<dim3(db + w.blocks), dim3(NT), 0, s>>>(d, db, w, p, dv);
         return hipGetLastError();
     }
 };
@@ -608,19 +713,28 @@ hipError_t launch_conv_wgrad_f32(const ConvProblem &p, const float *X, const flo
 
 hipError_t launch_conv_dgrad_f32(const ConvProblem &p, const float *dY, const float *Wt,
                                  float *dX, float *partials, hipStream_t s) {
-    const DgradJob j = dgrad_job(p, dY, Wt, dX, partials);
-    if (j.nsplit > 1 && partials == nullptr) return hipErrorInvalidValue;
-    return by_widths<LaunchD>(p, j, p, make_divs(p), s);
+    if (conv_dgrad_splits(p) > 1 && partials == nullptr) return hipErrorInvalidValue;
+    const ConvDivs dv = make_divs(p);
+    for (const DgradJobs &j : dgrad_jobs(p, dY, Wt, dX, partials)) {
+        const hipError_t e = by_widths<LaunchD>(p, j, p, dv, s);
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 hipError_t launch_conv_bwd_f32(const ConvProblem &p, const float *X, const float *Wt,
                                const float *dY, float *dX, float *dW, float *dpart,
                                float *wpart, hipStream_t s) {
-    const DgradJob d = dgrad_job(p, dY, Wt, dX, dpart);
     const WgradJob w = wgrad_job(p, X, dY, dW, wpart);
-    if ((d.nsplit > 1 && dpart == nullptr) || (w.nsplit > 1 && wpart == nullptr))
+    if ((conv_dgrad_splits(p) > 1 && dpart == nullptr) || (w.nsplit > 1 && wpart == nullptr))
         return hipErrorInvalidValue;
-    return by_widths<LaunchDW>(p, d, w, p, make_divs(p), s);
+    const ConvDivs dv = make_divs(p);
+    const std::vector<DgradJobs> d = dgrad_jobs(p, dY, Wt, dX, dpart);
+    // the filter gradient shares the first launch; strides beyond 4 x 4 add
+    // data-gradient-only launches for the remaining classes
+    hipError_t e = by_widths<LaunchDW>(p, d[0], w, p, dv, s);
+    for (size_t i = 1; i < d.size() && e == hipSuccess; ++i) e = by_widths<LaunchD>(p, d[i], p, dv, s);
+    return e;
 }
 
 hipError_t launch_conv_split_reduce_f32(const float *partials, int nsplit, int total,

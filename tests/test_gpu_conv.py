@@ -38,6 +38,11 @@ SMALL = [
     (2, 17, 15, 32, 130, 3, 3, (1, 1), (1, 1)),
     (1, 4, 4, 132, 36, 4, 4, (1, 1), (0, 0)),
     (4, 12, 12, 64, 64, 3, 3, (1, 1), (1, 1)),
+    # stride-parity classes: stride 3 (9 classes), stride 5 (25 classes, more
+    # than one launch holds), and an input shorter than its stride
+    (1, 11, 13, 8, 12, 3, 3, (3, 3), (1, 1)),
+    (1, 12, 12, 4, 8, 5, 5, (5, 5), (2, 2)),
+    (2, 1, 5, 4, 4, 1, 3, (2, 2), (0, 1)),
 ]
 
 
