@@ -55,7 +55,7 @@ typedef struct mg_conv2d_shape {
 /*
  * Workspace.  Each derivative is one implicit GEMM; when its 64x64 output
  * tiles number fewer than 512, the sum behind each output element is split
- * over S = min(ceil(1024 / tiles), floor(ceil(terms / 16) / 8)) workgroups
+ * over S = min(ceil(1024 / tiles), floor(ceil(terms / 16) / 16)) workgroups
  * (terms = N*P*Q for the filter gradient; for the data gradient, whose
  * pixels split into stride-parity classes that each sum only the filter taps
  * reaching them, tiles are counted over all classes and terms = the largest

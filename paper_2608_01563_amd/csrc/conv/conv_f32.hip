@@ -560,7 +560,7 @@ FastDiv make_fastdiv(unsigned d) {
 #define MG_CONV_SPLIT_TARGET 1024
 #endif
 #ifndef MG_CONV_SPLIT_TERMS
-#define MG_CONV_SPLIT_TERMS 128
+#define MG_CONV_SPLIT_TERMS 256
 #endif
 static int splits_for(long tiles, long steps) {
     if (tiles >= MG_CONV_SPLIT_BELOW) return 1;

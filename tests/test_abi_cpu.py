@@ -174,20 +174,20 @@ def _shape(N=1, H=8, W=8, C=4, K=8, R=3, S=3, sh=1, sw=1, ph=1, pw=1):
 
 def test_conv_workspace_query(lib):
     # ResNet-50's first layer at batch 4: 3 output tiles (64 x 147 of dW) over
-    # 4*112*112 positions in 3136 16-deep steps -> min(ceil(1024/3), 3136/8) = 342 splits
+    # 4*112*112 positions in 3136 16-deep steps -> min(ceil(1024/3), 3136/16) = 196 splits
     s = _shape(4, 224, 224, 3, 64, 7, 7, 2, 2, 3, 3)
-    assert lib.mg_conv2d_bwd_filter_workspace_bytes(ctypes.byref(s), 0) == 342 * 64 * 147 * 4
+    assert lib.mg_conv2d_bwd_filter_workspace_bytes(ctypes.byref(s), 0) == 196 * 64 * 147 * 4
     # a 3x3 512->512 layer at 7x7: the filter gradient's 8 x 72 = 576 tiles fill
     # the GPU (no workspace); its data gradient has 4 x 8 = 32 tiles over 288
-    # steps -> min(32, 288/8) = 32 splits of the 196 x 512 output
+    # steps -> min(32, 288/16) = 18 splits of the 196 x 512 output
     s = _shape(4, 7, 7, 512, 512, 3, 3, 1, 1, 1, 1)
     assert lib.mg_conv2d_bwd_filter_workspace_bytes(ctypes.byref(s), 0) == 0
-    assert lib.mg_conv2d_bwd_data_workspace_bytes(ctypes.byref(s), 0) == 32 * 196 * 512 * 4
+    assert lib.mg_conv2d_bwd_data_workspace_bytes(ctypes.byref(s), 0) == 18 * 196 * 512 * 4
     # a stride-2 3x3 layer: four parity classes (taps 2x2, 2x1, 1x2, 1x1) of
     # 7x7, 7x7, 7x7, 7x7 pixels at batch 4 -> 4 tiles each x 4 channel tiles
-    # = 64 tiles, the longest class sums 4 taps x 256 = 64 steps -> min(16, 8)
+    # = 64 tiles, the longest class sums 4 taps x 256 = 64 steps -> min(16, 4)
     s2 = _shape(4, 14, 14, 256, 256, 3, 3, 2, 2, 1, 1)
-    assert lib.mg_conv2d_bwd_data_workspace_bytes(ctypes.byref(s2), 0) == 8 * 4 * 14 * 14 * 256 * 4
+    assert lib.mg_conv2d_bwd_data_workspace_bytes(ctypes.byref(s2), 0) == 4 * 4 * 14 * 14 * 256 * 4
     # both at once: the data gradient's partials, 256-byte aligned, then the
     # filter gradient's
     s3 = _shape(4, 14, 14, 256, 256, 3, 3, 1, 1, 1, 1)
