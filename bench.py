@@ -212,7 +212,30 @@ def main():
         stops[k].record(stream)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    samples = sorted(a.elapsed_time(b) for a, b in zip(starts, stops))
+    samples_raw = [a.elapsed_time(b) for a, b in zip(starts, stops)]   # in timing order
+    samples = sorted(samples_raw)
+
+    # Separate series for the forward and the backward call (events around
+    # each call on the launch stream), `steps` samples each.
+    series = {"fwd_bwd": samples_raw}
+    for part in ("fwd", "bwd"):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+        for a, b in ev:
+            if part == "bwd":
+                mg.mg_attn_fwd_cross(Q, K, V, O, LSE, kl, causal=w.causal, scale=w.scale,
+                                     contract=w.contract, stream=stream)
+            a.record(stream)
+            if part == "fwd":
+                mg.mg_attn_fwd_cross(Q, K, V, O, LSE, kl, causal=w.causal, scale=w.scale,
+                                     contract=w.contract, stream=stream)
+            else:
+                mg.mg_attn_bwd_cross(Q, K, V, O, LSE, dO, dQ, dK, dV, kl, causal=w.causal,
+                                     scale=w.scale, contract=w.contract, workspace=ws,
+                                     stream=stream)
+            b.record(stream)
+        torch.cuda.synchronize()
+        series[part] = [a.elapsed_time(b) for a, b in ev]
 
     # Per-kernel durations: the same `steps` steps again, with the library
     # bracketing every kernel launch by HIP events on the launch stream.
@@ -259,6 +282,13 @@ def main():
                     "q3": round(float(np.percentile(samples, 75)), 4),
                     "min": round(samples[0], 4), "max": round(samples[-1], 4)},
         "pct_of_mfma_peak": round(100.0 * value / PEAK_TFLOPS[w.contract], 2),
+        "series_ms": {k: summarize(v) for k, v in series.items()},
+        "series_tflops": {
+            "fwd": round(4.0 * w.d * pairs / (np.median(series["fwd"]) * 1e-3) / 1e12, 3),
+            "bwd": round(10.0 * w.d * pairs / (np.median(series["bwd"]) * 1e-3) / 1e12, 3),
+            # the conservative count: 8d per pair, no credit for the score recompute
+            "bwd_8d": round(8.0 * w.d * pairs / (np.median(series["bwd"]) * 1e-3) / 1e12, 3)},
+        "env": environment(),
     }
     if events_ms_per_step is not None:
         out["ms_per_step_with_kernel_events"] = round(events_ms_per_step, 4)
@@ -301,6 +331,40 @@ def main():
         torch.cuda.synchronize()
         out["copy_calibration_bytes"] = n * 4
     print(json.dumps(out), flush=True)
+
+
+def summarize(samples):
+    """Median, quartiles, extremes and the raw samples (ms) of one series."""
+    import numpy as np
+    a = np.asarray(samples, dtype=np.float64)
+    return {"median": round(float(np.median(a)), 4),
+            "q1": round(float(np.percentile(a, 25)), 4),
+            "q3": round(float(np.percentile(a, 75)), 4),
+            "min": round(float(a.min()), 4), "max": round(float(a.max()), 4),
+            "samples": [round(float(v), 4) for v in samples]}
+
+
+def environment():
+    """GPU name, HIP/torch versions, the source revision and the GPU clocks
+    as the driver reports them (each null when unavailable)."""
+    import subprocess
+    import torch
+    env = {"gpu": torch.cuda.get_device_name(0), "hip": torch.version.hip,
+           "torch": torch.__version__, "git_revision": None, "clocks": None}
+    try:
+        r = subprocess.run(["git", "-C", ROOT, "rev-parse", "--short", "HEAD"],
+                           capture_output=True, text=True, timeout=10)
+        env["git_revision"] = r.stdout.strip() or None
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        r = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True,
+                           timeout=20)
+        lines = [l.strip() for l in r.stdout.splitlines() if "sclk" in l or "mclk" in l]
+        env["clocks"] = lines[:4] or None
+    except (OSError, subprocess.SubprocessError):
+        pass
+    return env
 
 
 def cpu_baseline(args, w, x, pairs, gpu_outputs):
@@ -434,7 +498,8 @@ def conv_main(args):
         stops[k].record(stream)
     torch.cuda.synchronize()
     ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
-    samples = sorted(a.elapsed_time(b) for a, b in zip(starts, stops))
+    samples_raw = [a.elapsed_time(b) for a, b in zip(starts, stops)]   # in timing order
+    samples = sorted(samples_raw)
 
     flops = sum(L.flops() * (2 if L.input_grad else 1) for L in layers)
     value = flops / (ms_per_step * 1e-3) / 1e12
@@ -483,6 +548,8 @@ def conv_main(args):
                     "min": round(samples[0], 4), "max": round(samples[-1], 4)},
         "eager_ms_per_step": round(eager_ms, 4),
         "pct_of_mfma_peak": round(100.0 * value / F32_MFMA_PEAK, 2),
+        "series_ms": {"step": summarize(samples_raw)},
+        "env": environment(),
     }
     if kernels:
         per = {}
