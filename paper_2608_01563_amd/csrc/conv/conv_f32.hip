@@ -9,20 +9,21 @@
 //       k = output channel, j = (r, s, c) flattened (the [K][R][S][C] order of
 //       dW), m = (n, p, q) flattened, Xg[m][j] = X[n][p*sh-ph+r][q*sw-pw+s][c]
 //   data gradient    dX[m][c]  = sum_j dYg[m][j] * W[j][c]
-//       m = (n, h, w) flattened, j = (r, s, k) flattened with k fastest,
-//       W[j][c] = W[k][r][s][c], dYg[m][j] = dY[n][p][q][k] for the output
-//       position (p, q) with p*sh-ph+r = h and q*sw-pw+s = w, 0 if none.
+//       per stride-parity class of pixels (see DgradJob): m = (n, i, j) of
+//       the class, j = (tr, ts, k) over the class's filter taps with k
+//       fastest, W[j][c] = W[k][r][s][c], dYg[m][j] = dY at the output
+//       position the tap reads, 0 outside dY.
 //
 // Both run 64x64 output tiles on 256 threads: each of the four waves owns a
 // 32x32 quarter as 2x2 blocks of 16x16 accumulators, and the reduction
 // advances BK (16) at a time through double-buffered LDS tiles (one barrier
 // per step; the global loads of steps t+1 and t+2 are in flight, in two
-// register sets, during the products of step t).  Operands reach LDS through raw buffer loads whose offset is
-// pushed past the end of the buffer for a padded or out-of-range element,
-// which reads as zero: the padding of the convolution, the tails of every
-// dimension and the positions a strided data gradient skips all become
-// zeros without a branch.  Every output element is one fixed-order sum
-// (within a workgroup, then across splits in split order): no atomics.
+// register sets, during the products of step t).  Operands reach LDS
+// through raw buffer loads whose offset is pushed past the end of the buffer
+// for a padded or out-of-range element, which reads as zero: the padding of
+// the convolution and the tails of every dimension become zeros without a
+// branch.  Every output element is one fixed-order sum (within a workgroup,
+// then across splits in a fixed order): no atomics.
 #include <algorithm>
 #include <vector>
 
@@ -35,12 +36,12 @@ namespace {
 #ifndef MG_CONV_BK
 #define MG_CONV_BK 16
 #endif
-constexpr int BM = 64;          // output rows per workgroup
-constexpr int BN = 64;          // output columns per workgroup
+constexpr int BM = 64;          // output rows per workgroup (columns: 64 or 128, TN)
 constexpr int BK = MG_CONV_BK;  // reduction step (16 or 32)
 constexpr int NSUB = BK / 16;   // staged rows per thread and operand in one step
 constexpr int NT = 256;         // four waves
-constexpr int LDR = 64 + 16;    // reduction-major tiles: rows 80 floats (16 banks) apart
+constexpr int LDR = 64 + 16;    // reduction-major 64-wide tiles: rows 80 floats (16 banks)
+                                // apart; 128-wide ones use 144 (also 16 banks)
 constexpr int LDM = BK + 4;     // the data gradient's pixel-major A tile: 20 (or 36)
                                 // floats per row, conflict-free for the operand reads
 static_assert(BK == 16 || BK == 32, "reduction step");
@@ -57,7 +58,7 @@ __device__ __forceinline__ int fdiv(int n, FastDiv f) {
 
 // Divisors the kernels use in their per-step index arithmetic.
 struct ConvDivs {
-    FastDiv PQ, Q, K, S, sh, sw, C, HW, W;
+    FastDiv PQ, Q, K, S, C;
 };
 
 __device__ __forceinline__ float buffer_load_f32(__amdgpu_buffer_rsrc_t r, int byte_offset) {
@@ -75,34 +76,51 @@ __device__ __forceinline__ f32x4 load_vec(__amdgpu_buffer_rsrc_t r, const int (&
     return v;
 }
 
-// 2x2 blocks of v_mfma_f32_16x16x4_f32 over one reduction step.
+// 2 x NJ blocks of v_mfma_f32_16x16x4_f32 over one reduction step.
 // a(kk, i) and b(kk, jb) return this lane's operand: A[row 16i + l%16][red 4kk + l/16]
-// and B[red 4kk + l/16][col 16jb + l%16] of the wave's 32x32 quarter.
-template <typename FA, typename FB>
-__device__ __forceinline__ void mma_step(f32x4 (&acc)[2][2], FA &&a, FB &&b) {
+// and B[red 4kk + l/16][col 16jb + l%16] of the wave's 32 x 16NJ part of the tile.
+template <int NJ, typename FA, typename FB>
+__device__ __forceinline__ void mma_step(f32x4 (&acc)[2][NJ], FA &&a, FB &&b) {
 #pragma unroll
     for (int kk = 0; kk < BK / 4; ++kk) {
         const float a0 = a(kk, 0), a1 = a(kk, 1);
-        const float b0 = b(kk, 0), b1 = b(kk, 1);
-        acc[0][0] = mfma16x16x4(a0, b0, acc[0][0]);
-        acc[0][1] = mfma16x16x4(a0, b1, acc[0][1]);
-        acc[1][0] = mfma16x16x4(a1, b0, acc[1][0]);
-        acc[1][1] = mfma16x16x4(a1, b1, acc[1][1]);
+        float bj[NJ];
+#pragma unroll
+        for (int jb = 0; jb < NJ; ++jb) bj[jb] = b(kk, jb);
+#pragma unroll
+        for (int jb = 0; jb < NJ; ++jb) {
+            acc[0][jb] = mfma16x16x4(a0, bj[jb], acc[0][jb]);
+            acc[1][jb] = mfma16x16x4(a1, bj[jb], acc[1][jb]);
+        }
     }
 }
 
+// Staged B columns of one thread: with 16-byte chunks (VB == 4), TN/64
+// chunks at columns 4*col + 64v; with 4-byte loads (VB == 1, TN == 64), four
+// floats at columns col + 16e.
+template <int VB, int TN>
+struct BCols {
+    static_assert(TN == 64 || (TN == 128 && VB == 4), "tile width");
+    static constexpr int NV = VB == 4 ? TN / 64 : 1;   // f32x4 registers per row
+    static constexpr int NE = VB == 4 ? TN / 64 : 4;   // separately addressed elements
+    __device__ static int col(int c, int e) { return VB == 4 ? 4 * c + 64 * e : c + 16 * e; }
+};
+
 // LDS of one workgroup: the two derivatives' double-buffered tiles share it.
+template <int TN>
 struct WgradLds {
-    float As[2][BK][LDR];   // dY tile, [m][k]
-    float Bs[2][BK][LDR];   // X gather, [m][j]
+    float As[2][BK][LDR];      // dY tile, [m][k]
+    float Bs[2][BK][TN + 16];  // X gather, [m][j]
 };
+template <int TN>
 struct DgradLds {
-    float As[2][BM][LDM];   // dY gather, [m][j]
-    float Bs[2][BK][LDR];   // W rows, [j][c]
+    float As[2][BM][LDM];      // dY gather, [m][j]
+    float Bs[2][BK][TN + 16];  // W rows, [j][c]
 };
+template <int TN>
 union __attribute__((aligned(16))) ConvLds {
-    WgradLds w;
-    DgradLds d;
+    WgradLds<TN> w;
+    DgradLds<TN> d;
 };
 
 // Work of one filter-gradient launch: grid (k tile, j tile, split), split fastest.
@@ -135,9 +153,11 @@ struct DgradJobs {
 // ------------------------------------------------------- filter gradient --
 // Block `bid` of the job: split `split` of `nsplit` sums the reduction steps
 // [st0, st1) of the N*P*Q positions for one 64x64 tile of dW.
-template <int VA, int VB>
-__device__ __forceinline__ void wgrad_tile(int bid, WgradLds &L, const WgradJob &job,
+template <int VA, int VB, int TN>
+__device__ __forceinline__ void wgrad_tile(int bid, WgradLds<TN> &L, const WgradJob &job,
                                            const ConvProblem &p, const ConvDivs &dv) {
+    using BC = BCols<VB, TN>;
+    constexpr int NJ = TN / 32;   // 16-column blocks per wave
     auto &As = L.As;
     auto &Bs = L.Bs;
     const float *__restrict__ X = job.X;
@@ -151,7 +171,7 @@ __device__ __forceinline__ void wgrad_tile(int bid, WgradLds &L, const WgradJob 
     const int split = bid % nsplit;
     bid /= nsplit;
     const int k0 = (bid / tiles_j) * BM;
-    const int j0 = (bid % tiles_j) * BN;
+    const int j0 = (bid % tiles_j) * TN;
     const int st0 = (int)((long)nsteps * split / nsplit);
     const int st1 = (int)((long)nsteps * (split + 1) / nsplit);
 
@@ -168,14 +188,17 @@ __device__ __forceinline__ void wgrad_tile(int bid, WgradLds &L, const WgradJob 
 
     // Columns this thread stages: k for A, j = (r, s, c) for B (fixed for
     // the whole reduction).
-    int ka4[4], br[4], bsx[4], boff[4];   // byte offsets (ka4, boff) and taps
-    bool kok[4], bok[4];
+    int ka4[4], br[BC::NE], bsx[BC::NE], boff[BC::NE];   // byte offsets (ka4, boff), taps
+    bool kok[4], bok[BC::NE];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
         const int ka = (VA == 4) ? k0 + 4 * lcol : k0 + lcol + 16 * e;
         ka4[e] = 4 * ka;
         kok[e] = ka < p.K;
-        const int j = (VB == 4) ? j0 + 4 * lcol : j0 + lcol + 16 * e;
+    }
+#pragma unroll
+    for (int e = 0; e < BC::NE; ++e) {
+        const int j = j0 + BC::col(lcol, e);
         const int rs = fdiv(j, dv.C), c = j - rs * p.C;
         br[e] = fdiv(rs, dv.S);
         bsx[e] = rs - br[e] * p.S;
@@ -184,7 +207,8 @@ __device__ __forceinline__ void wgrad_tile(int bid, WgradLds &L, const WgradJob 
     }
 
     // Step st stages reduction rows st*BK + lrow + 16u, u < NSUB.
-    auto load = [&](int st, f32x4 (&ra)[NSUB], f32x4 (&rb)[NSUB]) {
+    using Regs = f32x4[NSUB][1 + BC::NV];   // [u][0]: A (dY), [u][1 + v]: B (X)
+    auto load = [&](int st, Regs &rg) {
 #pragma unroll
         for (int u = 0; u < NSUB; ++u) {
             const int m = st * BK + lrow + 16 * u;
@@ -193,86 +217,96 @@ __device__ __forceinline__ void wgrad_tile(int bid, WgradLds &L, const WgradJob 
             const int pp = fdiv(pq, dv.Q), qq = pq - pp * p.Q;
             const int hb = pp * p.sh - p.ph, wb = qq * p.sw - p.pw;
             const int xbase = ((n * p.H + hb) * p.W + wb) * p.C;
-            int oa[4], ob[4];
+            int oa[4], ob[BC::NE];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 oa[e] = (mok && kok[e]) ? m * (4 * p.K) + ka4[e] : kOOB;
+                if (VA == 4) break;
+            }
+#pragma unroll
+            for (int e = 0; e < BC::NE; ++e) {
                 const int h = hb + br[e], wi = wb + bsx[e];
                 const bool ok = mok && bok[e] && (unsigned)h < (unsigned)p.H &&
                                 (unsigned)wi < (unsigned)p.W;
                 ob[e] = ok ? xbase * 4 + boff[e] : kOOB;
-                if (VA == 4 && VB == 4) break;
             }
-            ra[u] = load_vec<VA>(rdy, oa);
-            rb[u] = load_vec<VB>(rx, ob);
+            rg[u][0] = load_vec<VA>(rdy, oa);
+            if (VB == 4) {
+#pragma unroll
+                for (int v = 0; v < BC::NV; ++v) rg[u][1 + v] = buffer_load_f32x4(rx, ob[v]);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) rg[u][1][e] = buffer_load_f32(rx, ob[e]);
+            }
         }
     };
-    auto store = [&](int buf, const f32x4 (&ra)[NSUB], const f32x4 (&rb)[NSUB]) {
+    auto store = [&](int buf, const Regs &rg) {
 #pragma unroll
         for (int u = 0; u < NSUB; ++u) {
             const int row = lrow + 16 * u;
             if (VA == 4) {
-                *reinterpret_cast<f32x4 *>(&As[buf][row][4 * lcol]) = ra[u];
+                *reinterpret_cast<f32x4 *>(&As[buf][row][4 * lcol]) = rg[u][0];
             } else {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) As[buf][row][lcol + 16 * e] = ra[u][e];
+                for (int e = 0; e < 4; ++e) As[buf][row][lcol + 16 * e] = rg[u][0][e];
             }
             if (VB == 4) {
-                *reinterpret_cast<f32x4 *>(&Bs[buf][row][4 * lcol]) = rb[u];
+#pragma unroll
+                for (int v = 0; v < BC::NV; ++v)
+                    *reinterpret_cast<f32x4 *>(&Bs[buf][row][BC::col(lcol, v)]) = rg[u][1 + v];
             } else {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) Bs[buf][row][lcol + 16 * e] = rb[u][e];
+                for (int e = 0; e < 4; ++e) Bs[buf][row][BC::col(lcol, e)] = rg[u][1][e];
             }
         }
     };
 
-    f32x4 acc[2][2];
+    f32x4 acc[2][NJ];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int jb = 0; jb < 2; ++jb) acc[i][jb] = zero4();
+        for (int jb = 0; jb < NJ; ++jb) acc[i][jb] = zero4();
 
     // Two register sets keep the loads of the next two steps in flight while
     // the current step, already in LDS, is multiplied.
-    f32x4 ra0[NSUB], rb0[NSUB], ra1[NSUB], rb1[NSUB];
-    if (st0 < st1) load(st0, ra0, rb0);
-    if (st0 + 1 < st1) load(st0 + 1, ra1, rb1);
-    if (st0 < st1) store(0, ra0, rb0);
+    Regs r0, r1;
+    if (st0 < st1) load(st0, r0);
+    if (st0 + 1 < st1) load(st0 + 1, r1);
+    if (st0 < st1) store(0, r0);
     __syncthreads();
-    // step st: `na`/`nb` hold step st+1 (in flight), `fa`/`fb` are free
-    auto body = [&](int st, f32x4 (&na)[NSUB], f32x4 (&nb)[NSUB], f32x4 (&fa)[NSUB],
-                    f32x4 (&fb)[NSUB]) {
+    // step st: `nx` holds step st+1 (in flight), `fr` is free
+    auto body = [&](int st, Regs &nx, Regs &fr) {
         const int cur = (st - st0) & 1;
-        if (st + 2 < st1) load(st + 2, fa, fb);
-        mma_step(acc,
-                 [&](int kk, int i) { return As[cur][4 * kk + g][32 * wm + 16 * i + il]; },
-                 [&](int kk, int jb) { return Bs[cur][4 * kk + g][32 * wn + 16 * jb + il]; });
-        if (st + 1 < st1) store(cur ^ 1, na, nb);
+        if (st + 2 < st1) load(st + 2, fr);
+        mma_step<NJ>(acc,
+                     [&](int kk, int i) { return As[cur][4 * kk + g][32 * wm + 16 * i + il]; },
+                     [&](int kk, int jb) { return Bs[cur][4 * kk + g][(TN / 2) * wn + 16 * jb + il]; });
+        if (st + 1 < st1) store(cur ^ 1, nx);
         __syncthreads();
     };
     for (int st = st0; st < st1; st += 2) {
-        body(st, ra1, rb1, ra0, rb0);
-        if (st + 1 < st1) body(st + 1, ra0, rb0, ra1, rb1);
+        body(st, r1, r0);
+        if (st + 1 < st1) body(st + 1, r0, r1);
     }
 
     float *dst = out + (size_t)split * p.K * RSC;   // split 0 of 1 is dW itself
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int jb = 0; jb < 2; ++jb)
+        for (int jb = 0; jb < NJ; ++jb)
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int k = k0 + 32 * wm + 16 * i + 4 * g + r;
-                const int j = j0 + 32 * wn + 16 * jb + il;
+                const int j = j0 + (TN / 2) * wn + 16 * jb + il;
                 if (k < p.K && j < RSC) dst[(size_t)k * RSC + j] = acc[i][jb][r];
             }
 }
 
-template <int VA, int VB>
+template <int VA, int VB, int TN>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(MG_CONV_OCC, 8)))
 void conv_wgrad_f32(WgradJob job, ConvProblem p, ConvDivs dv) {
-    __shared__ ConvLds lds;
-    wgrad_tile<VA, VB>(blockIdx.x, lds.w, job, p, dv);
+    __shared__ ConvLds<TN> lds;
+    wgrad_tile<VA, VB, TN>(blockIdx.x, lds.w, job, p, dv);
 }
 
 // out[i] = sum over splits of part[split][i].  A group of G consecutive lanes
@@ -327,9 +361,11 @@ __global__ __launch_bounds__(256) void conv_split_reduce_f32(ReduceJob a, Reduce
 // Block `bid` of a class job: split `split` of `nsplit` sums the reduction
 // steps [st0, st1) of the class's (tr, ts, k) for one 64x64 tile of its
 // pixels x channels.
-template <int VA, int VB>
-__device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob &job,
+template <int VA, int VB, int TN>
+__device__ __forceinline__ void dgrad_tile(int bid, DgradLds<TN> &L, const DgradJob &job,
                                            const ConvProblem &p, const ConvDivs &dv) {
+    using BC = BCols<VB, TN>;
+    constexpr int NJ = TN / 32;   // 16-column blocks per wave
     auto &As = L.As;
     auto &Bs = L.Bs;
     const float *__restrict__ dY = job.dY;
@@ -344,7 +380,7 @@ __device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob 
     const int split = bid % nsplit;
     bid /= nsplit;
     const int m0 = (bid / tiles_c) * BM;
-    const int c0 = (bid % tiles_c) * BN;
+    const int c0 = (bid % tiles_c) * TN;
     const int st0 = (int)((long)nsteps * split / nsplit);
     const int st1 = (int)((long)nsteps * (split + 1) / nsplit);
 
@@ -365,9 +401,9 @@ __device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob 
     const int n = fdiv(m, job.HWc), ij = m - n * HWc;
     const int i = fdiv(ij, job.Wc_), jw = ij - i * job.Wc;
     const int jr = tid >> 4, cc = tid & 15;
-    int cb[4];
+    int cb[BC::NE];   // channel columns this thread stages
 #pragma unroll
-    for (int e = 0; e < 4; ++e) cb[e] = (VB == 4) ? c0 + 4 * cc + e : c0 + cc + 16 * e;
+    for (int e = 0; e < BC::NE; ++e) cb[e] = c0 + BC::col(cc, e);
 
     const int nP = n * p.P, pi = i + job.da, qj = jw + job.db;   // p = pi - tr, q = qj - ts
     // K % BK == 0: every step lies within one tap (tr, ts), known to the
@@ -386,7 +422,8 @@ __device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob 
         return ((k * p.R + job.r0 + p.sh * tr) * p.S + job.s0 + p.sw * ts) * p.C;
     };
 
-    auto load = [&](int st, f32x4 (&ra)[NSUB], f32x4 (&rb)[NSUB]) {
+    using Regs = f32x4[NSUB][1 + BC::NV];   // [u][0]: A (dY), [u][1 + v]: B (W)
+    auto load = [&](int st, Regs &rg) {
         const int j0 = st * BK;
         int kb = 0, tr0 = 0, ts0 = 0;
         if (tap_uniform) {
@@ -397,7 +434,7 @@ __device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob 
         }
 #pragma unroll
         for (int u = 0; u < NSUB; ++u) {
-            int oa[4], ob[4];
+            int oa[4], ob[BC::NE];
             if (tap_uniform) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
@@ -408,10 +445,8 @@ __device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob 
                 // W[k][r][s][c] for reduction row k = kb + 16u + jr of the tap
                 const int row = w_row(kb + 16 * u + jr, tr0, ts0);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
+                for (int e = 0; e < BC::NE; ++e)
                     ob[e] = (j0 + 16 * u + jr < RSKc && cb[e] < p.C) ? (row + cb[e]) * 4 : kOOB;
-                    if (VB == 4) break;
-                }
             } else {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
@@ -427,55 +462,60 @@ __device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob 
                 const int tr = fdiv(t, job.Sc_), ts = t - tr * job.Sc;
                 const int row = w_row(k, tr, ts);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
+                for (int e = 0; e < BC::NE; ++e)
                     ob[e] = (j < RSKc && cb[e] < p.C) ? (row + cb[e]) * 4 : kOOB;
-                    if (VB == 4) break;
-                }
             }
-            ra[u] = load_vec<VA>(rdy, oa);
-            rb[u] = load_vec<VB>(rw, ob);
-        }
-    };
-    auto store = [&](int buf, const f32x4 (&ra)[NSUB], const f32x4 (&rb)[NSUB]) {
-#pragma unroll
-        for (int u = 0; u < NSUB; ++u) {
-            *reinterpret_cast<f32x4 *>(&As[buf][ar][16 * u + 4 * jq]) = ra[u];
+            rg[u][0] = load_vec<VA>(rdy, oa);
             if (VB == 4) {
-                *reinterpret_cast<f32x4 *>(&Bs[buf][jr + 16 * u][4 * cc]) = rb[u];
+#pragma unroll
+                for (int v = 0; v < BC::NV; ++v) rg[u][1 + v] = buffer_load_f32x4(rw, ob[v]);
             } else {
 #pragma unroll
-                for (int e = 0; e < 4; ++e) Bs[buf][jr + 16 * u][cc + 16 * e] = rb[u][e];
+                for (int e = 0; e < 4; ++e) rg[u][1][e] = buffer_load_f32(rw, ob[e]);
+            }
+        }
+    };
+    auto store = [&](int buf, const Regs &rg) {
+#pragma unroll
+        for (int u = 0; u < NSUB; ++u) {
+            *reinterpret_cast<f32x4 *>(&As[buf][ar][16 * u + 4 * jq]) = rg[u][0];
+            if (VB == 4) {
+#pragma unroll
+                for (int v = 0; v < BC::NV; ++v)
+                    *reinterpret_cast<f32x4 *>(&Bs[buf][jr + 16 * u][BC::col(cc, v)]) = rg[u][1 + v];
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) Bs[buf][jr + 16 * u][BC::col(cc, e)] = rg[u][1][e];
             }
         }
     };
 
-    f32x4 acc[2][2];
+    f32x4 acc[2][NJ];
 #pragma unroll
     for (int ii = 0; ii < 2; ++ii)
 #pragma unroll
-        for (int jb = 0; jb < 2; ++jb) acc[ii][jb] = zero4();
+        for (int jb = 0; jb < NJ; ++jb) acc[ii][jb] = zero4();
 
     // Two register sets keep the loads of the next two steps in flight while
     // the current step, already in LDS, is multiplied.
-    f32x4 ra0[NSUB], rb0[NSUB], ra1[NSUB], rb1[NSUB];
-    if (st0 < st1) load(st0, ra0, rb0);
-    if (st0 + 1 < st1) load(st0 + 1, ra1, rb1);
-    if (st0 < st1) store(0, ra0, rb0);
+    Regs r0, r1;
+    if (st0 < st1) load(st0, r0);
+    if (st0 + 1 < st1) load(st0 + 1, r1);
+    if (st0 < st1) store(0, r0);
     __syncthreads();
-    // step st: `na`/`nb` hold step st+1 (in flight), `fa`/`fb` are free
-    auto body = [&](int st, f32x4 (&na)[NSUB], f32x4 (&nb)[NSUB], f32x4 (&fa)[NSUB],
-                    f32x4 (&fb)[NSUB]) {
+    // step st: `nx` holds step st+1 (in flight), `fr` is free
+    auto body = [&](int st, Regs &nx, Regs &fr) {
         const int cur = (st - st0) & 1;
-        if (st + 2 < st1) load(st + 2, fa, fb);
-        mma_step(acc,
-                 [&](int kk, int ii) { return As[cur][32 * wm + 16 * ii + il][4 * kk + g]; },
-                 [&](int kk, int jb) { return Bs[cur][4 * kk + g][32 * wn + 16 * jb + il]; });
-        if (st + 1 < st1) store(cur ^ 1, na, nb);
+        if (st + 2 < st1) load(st + 2, fr);
+        mma_step<NJ>(acc,
+                     [&](int kk, int ii) { return As[cur][32 * wm + 16 * ii + il][4 * kk + g]; },
+                     [&](int kk, int jb) { return Bs[cur][4 * kk + g][(TN / 2) * wn + 16 * jb + il]; });
+        if (st + 1 < st1) store(cur ^ 1, nx);
         __syncthreads();
     };
     for (int st = st0; st < st1; st += 2) {
-        body(st, ra1, rb1, ra0, rb0);
-        if (st + 1 < st1) body(st + 1, ra0, rb0, ra1, rb1);
+        body(st, r1, r0);
+        if (st + 1 < st1) body(st + 1, r0, r1);
     }
 
     // rows of this lane's accumulators back to dX pixels (n, a + sh*i, b + sw*j)
@@ -490,8 +530,8 @@ __device__ __forceinline__ void dgrad_tile(int bid, DgradLds &L, const DgradJob 
             const int oi = fdiv(oij, job.Wc_), oj = oij - oi * job.Wc;
             const size_t pix = ((size_t)on * p.H + job.a + p.sh * oi) * p.W + job.b + p.sw * oj;
 #pragma unroll
-            for (int jb = 0; jb < 2; ++jb) {
-                const int c = c0 + 32 * wn + 16 * jb + il;
+            for (int jb = 0; jb < NJ; ++jb) {
+                const int c = c0 + (TN / 2) * wn + 16 * jb + il;
                 if (c < p.C) dst[pix * p.C + c] = acc[ii][jb][r];
             }
         }
@@ -507,29 +547,27 @@ __device__ __forceinline__ int find_class(const DgradJobs &jobs, int &bid) {
     return c;
 }
 
-template <int VA, int VB>
+template <int VA, int VB, int TN>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(MG_CONV_OCC, 8)))
-void conv_dgrad_f32(DgradJobs jobs, ConvProblem p,
-                                                     ConvDivs dv) {
-    __shared__ ConvLds lds;
+void conv_dgrad_f32(DgradJobs jobs, ConvProblem p, ConvDivs dv) {
+    __shared__ ConvLds<TN> lds;
     int bid = blockIdx.x;
     const int c = find_class(jobs, bid);
-    dgrad_tile<VA, VB>(bid, lds.d, jobs.c[c], p, dv);
+    dgrad_tile<VA, VB, TN>(bid, lds.d, jobs.c[c], p, dv);
 }
 
 // Both derivatives of one convolution in one launch: the first `dblocks`
 // workgroups run the data gradient's class jobs, the rest the filter gradient.
-template <int VA, int VB>
+template <int VA, int VB, int TN>
 __global__ __launch_bounds__(NT) __attribute__((amdgpu_waves_per_eu(MG_CONV_OCC, 8)))
-void conv_bwd_f32(DgradJobs d, int dblocks, WgradJob w,
-                                                   ConvProblem p, ConvDivs dv) {
-    __shared__ ConvLds lds;
+void conv_bwd_f32(DgradJobs d, int dblocks, WgradJob w, ConvProblem p, ConvDivs dv) {
+    __shared__ ConvLds<TN> lds;
     int bid = blockIdx.x;
     if (bid < dblocks) {
         const int c = find_class(d, bid);
-        dgrad_tile<VA, VB>(bid, lds.d, d.c[c], p, dv);
+        dgrad_tile<VA, VB, TN>(bid, lds.d, d.c[c], p, dv);
     } else {
-        wgrad_tile<VA, VB>(bid - dblocks, lds.w, w, p, dv);
+        wgrad_tile<VA, VB, TN>(bid - dblocks, lds.w, w, p, dv);
     }
 }
 
@@ -537,8 +575,7 @@ int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 ConvDivs make_divs(const ConvProblem &p) {
     return ConvDivs{make_fastdiv(p.P * p.Q), make_fastdiv(p.Q), make_fastdiv(p.K),
-                    make_fastdiv(p.S), make_fastdiv(p.sh), make_fastdiv(p.sw),
-                    make_fastdiv(p.C), make_fastdiv(p.H * p.W), make_fastdiv(p.W)};
+                    make_fastdiv(p.S), make_fastdiv(p.C)};
 }
 
 }  // namespace
@@ -570,8 +607,20 @@ static int splits_for(long tiles, long steps) {
     return s < 1 ? 1 : (int)s;
 }
 
+// Output tile width: 64 columns.  A build option (MG_CONV_WIDE=1) selects
+// 128 columns, with half the operand loads per product, when the channel
+// vectors allow 16-byte loads and there are that many channels; on the
+// ResNet-50 step it measured 6 % slower (fewer tiles, more splits, five
+// waves per SIMD instead of seven).
+#ifndef MG_CONV_WIDE
+#define MG_CONV_WIDE 0
+#endif
+int conv_tile_n(const ConvProblem &p) {
+    return (MG_CONV_WIDE && p.C % 4 == 0 && p.C >= 128) ? 128 : 64;
+}
+
 int conv_wgrad_splits(const ConvProblem &p) {
-    return splits_for((long)cdiv(p.K, BM) * cdiv(p.R * p.S * p.C, BN),
+    return splits_for((long)cdiv(p.K, BM) * cdiv(p.R * p.S * p.C, conv_tile_n(p)),
                       cdiv(p.N * p.P * p.Q, BK));
 }
 
@@ -598,7 +647,7 @@ std::vector<DgradJob> dgrad_classes(const ConvProblem &p) {
             j.HWc = make_fastdiv(j.Hc * j.Wc);
             j.Wc_ = make_fastdiv(j.Wc);
             j.Sc_ = make_fastdiv(j.Sc > 0 ? j.Sc : 1);
-            j.tiles_c = cdiv(p.C, BN);
+            j.tiles_c = cdiv(p.C, conv_tile_n(p));
             cls.push_back(j);
         }
     return cls;
@@ -622,7 +671,7 @@ namespace {
 WgradJob wgrad_job(const ConvProblem &p, const float *X, const float *dY, float *dW,
                    float *partials) {
     const int ns = conv_wgrad_splits(p);
-    const int tiles_j = cdiv(p.R * p.S * p.C, BN);
+    const int tiles_j = cdiv(p.R * p.S * p.C, conv_tile_n(p));
     return WgradJob{X, dY, ns > 1 ? partials : dW, tiles_j, ns, cdiv(p.N * p.P * p.Q, BK),
                     cdiv(p.K, BM) * tiles_j * ns};
 }
@@ -660,39 +709,46 @@ ReduceJob reduce_job(const float *partials, int nsplit, int total, float *out) {
     return ReduceJob{partials, out, nsplit, total, G, vec, (int)((groups * G + 255) / 256)};
 }
 
-// The kernel instance for the operands' vector widths: 16-byte loads along
-// k (K % 4 == 0) and along c (C % 4 == 0), else 4-byte loads.
-template <template <int, int> class Launch, typename... Args>
+// The kernel instance for the operands' vector widths (16-byte loads along
+// k when K % 4 == 0 and along c when C % 4 == 0, else 4-byte loads) and the
+// output tile width.
+template <template <int, int, int> class Launch, typename... Args>
 hipError_t by_widths(const ConvProblem &p, Args &&...args) {
     const bool va = p.K % 4 == 0, vb = p.C % 4 == 0;
-    if (va && vb) return Launch<4, 4>::run(args...);
-    if (va) return Launch<4, 1>::run(args...);
-    if (vb) return Launch<1, 4>::run(args...);
-    return Launch<1, 1>::run(args...);
+#if MG_CONV_WIDE
+    if (conv_tile_n(p) == 128) {
+        if (va) return Launch<4, 4, 128>::run(args...);
+        return Launch<1, 4, 128>::run(args...);
+    }
+#endif
+    if (va && vb) return Launch<4, 4, 64>::run(args...);
+    if (va) return Launch<4, 1, 64>::run(args...);
+    if (vb) return Launch<1, 4, 64>::run(args...);
+    return Launch<1, 1, 64>::run(args...);
 }
 
-template <int VA, int VB>
+template <int VA, int VB, int TN>
 struct LaunchW {
     static hipError_t run(const WgradJob &j, const ConvProblem &p, const ConvDivs &dv,
                           hipStream_t s) {
-        conv_wgrad_f32<VA, VB><<<dim3(j.blocks), dim3(NT), 0, s>>>(j, p, dv);
+        conv_wgrad_f32<VA, VB, TN><<<dim3(j.blocks), dim3(NT), 0, s>>>(j, p, dv);
         return hipGetLastError();
     }
 };
-template <int VA, int VB>
+template <int VA, int VB, int TN>
 struct LaunchD {
     static hipError_t run(const DgradJobs &j, const ConvProblem &p, const ConvDivs &dv,
                           hipStream_t s) {
-        conv_dgrad_f32<VA, VB><<<dim3(total_blocks(j)), dim3(NT), 0, s>>>(j, p, dv);
+        conv_dgrad_f32<VA, VB, TN><<<dim3(total_blocks(j)), dim3(NT), 0, s>>>(j, p, dv);
         return hipGetLastError();
     }
 };
-template <int VA, int VB>
+template <int VA, int VB, int TN>
 struct LaunchDW {
     static hipError_t run(const DgradJobs &d, const WgradJob &w, const ConvProblem &p,
                           const ConvDivs &dv, hipStream_t s) {
         const int db = total_blocks(d);
-        conv_bwd_f32<VA, VB><<<dim3(db + w.blocks), dim3(NT), 0, s>>>(d, db, w, p, dv);
+        conv_bwd_f32<VA, VB, TN><<<dim3(db + w.blocks), dim3(NT), 0, s>>>(d, db, w, p, dv);
         return hipGetLastError();
     }
 };

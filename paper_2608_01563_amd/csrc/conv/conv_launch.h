@@ -28,6 +28,7 @@ FastDiv make_fastdiv(unsigned d);
 // is split over conv_*_splits(p) workgroups per tile; they write f32
 // partials [split][output elements] to `partials`, which
 // launch_conv_split_reduce_f32 adds in split order into the output.
+int conv_tile_n(const ConvProblem &p);   // output tile width, 64 or 128
 int conv_dgrad_splits(const ConvProblem &p);
 int conv_wgrad_splits(const ConvProblem &p);
 hipError_t launch_conv_dgrad_f32(const ConvProblem &p, const float *dY, const float *Wt,
