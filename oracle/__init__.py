@@ -26,6 +26,7 @@ from .conv import (  # noqa: F401
     build_conv_oracle,
     conv_out_size,
     oracle_conv2d_fwd,
+    oracle_conv2d_fwd_at,
     oracle_conv2d_bwd_data,
     oracle_conv2d_bwd_data_at,
     oracle_conv2d_bwd_filter,

@@ -38,7 +38,8 @@ def _bind(lib):
     for name in ("oracle_conv2d_fwd", "oracle_conv2d_bwd_data", "oracle_conv2d_bwd_filter"):
         getattr(lib, name).argtypes = [dp, dp, *shape, dp]
         getattr(lib, name).restype = ci
-    for name in ("oracle_conv2d_bwd_data_at", "oracle_conv2d_bwd_filter_at"):
+    for name in ("oracle_conv2d_fwd_at", "oracle_conv2d_bwd_data_at",
+                 "oracle_conv2d_bwd_filter_at"):
         getattr(lib, name).argtypes = [dp, dp, *shape, lp, ci, dp]
         getattr(lib, name).restype = ci
     return lib
@@ -115,6 +116,19 @@ def oracle_conv2d_bwd_filter(X, dY, W_shape, stride=(1, 1), pad=(0, 0), lib=None
     if lib.oracle_conv2d_bwd_filter(_p(X), _p(dY), *dims, _p(dW)) != 0:
         raise ValueError("invalid convolution shape")
     return dW
+
+
+def oracle_conv2d_fwd_at(X, Wt, flat_idx, stride=(1, 1), pad=(0, 0), lib=None):
+    """Elements `flat_idx` (flat indices into Y [N,P,Q,K]) of the forward."""
+    lib = lib or load_conv_oracle()
+    X, Wt = _f64(X), _f64(Wt)
+    dims = _dims(X.shape, Wt.shape, stride, pad)
+    idx = np.ascontiguousarray(np.asarray(flat_idx, dtype=np.int64))
+    out = np.full(idx.shape, np.nan)
+    if lib.oracle_conv2d_fwd_at(_p(X), _p(Wt), *dims, _p(idx, ctypes.c_int64), int(idx.size),
+                                _p(out)) != 0:
+        raise ValueError("invalid shape or index")
+    return out
 
 
 def oracle_conv2d_bwd_data_at(dY, Wt, X_shape, flat_idx, stride=(1, 1), pad=(0, 0), lib=None):

@@ -163,7 +163,28 @@ int oracle_conv2d_bwd_filter(const double *X, const double *dY, int N, int H, in
 }
 
 /* The same sums at selected flat output indices only (for checks of full-size
- * problems): out[j] is element idx[j] of dX (data) or of dW (filter). */
+ * problems): out[j] is element idx[j] of Y (forward), dX (data) or dW (filter). */
+int oracle_conv2d_fwd_at(const double *X, const double *Wt, int N, int H, int W, int C, int K,
+                         int R, int S, int sh, int sw, int ph, int pw, const int64_t *idx,
+                         int nidx, double *out) {
+    if (bad_shape(N, H, W, C, K, R, S, sh, sw, ph, pw)) return 1;
+    const int P = out_len(H, ph, R, sh), Q = out_len(W, pw, S, sw);
+    const int64_t total = (int64_t)N * P * Q * K;
+    for (int j = 0; j < nidx; ++j)
+        if (idx[j] < 0 || idx[j] >= total) return 2;
+#pragma omp parallel for schedule(dynamic, 4)
+    for (int j = 0; j < nidx; ++j) {
+        const int64_t i = idx[j];
+        const int k = (int)(i % K);
+        const int64_t pix = i / K;
+        const int q = (int)(pix % Q);
+        const int p = (int)((pix / Q) % P);
+        const int n = (int)(pix / ((int64_t)Q * P));
+        out[j] = fwd_at(X, Wt, H, W, C, R, S, sh, sw, ph, pw, n, p, q, k);
+    }
+    return 0;
+}
+
 int oracle_conv2d_bwd_data_at(const double *dY, const double *Wt, int N, int H, int W, int C,
                               int K, int R, int S, int sh, int sw, int ph, int pw,
                               const int64_t *idx, int nidx, double *out) {

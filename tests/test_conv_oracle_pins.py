@@ -11,7 +11,7 @@ import pytest
 
 from oracle.conv import (conv_out_size, oracle_conv2d_bwd_data, oracle_conv2d_bwd_data_at,
                          oracle_conv2d_bwd_filter, oracle_conv2d_bwd_filter_at,
-                         oracle_conv2d_fwd)
+                         oracle_conv2d_fwd, oracle_conv2d_fwd_at)
 
 # (N, H, W, C, K, R, S, stride, pad): strides and pads that differ per axis,
 # non-square filters, one channel, odd sizes
@@ -177,6 +177,9 @@ def test_sampled_elements_equal_the_full_gradients(shape):
     iw = rng.integers(0, dW.size, 40)
     np.testing.assert_array_equal(oracle_conv2d_bwd_data_at(dY, Wt, X.shape, ix, stride, pad),
                                   dX.reshape(-1)[ix])
+    Y = oracle_conv2d_fwd(X, Wt, stride, pad)
+    iy = rng.integers(0, Y.size, 40)
+    np.testing.assert_array_equal(oracle_conv2d_fwd_at(X, Wt, iy, stride, pad), Y.reshape(-1)[iy])
     np.testing.assert_array_equal(oracle_conv2d_bwd_filter_at(X, dY, Wt.shape, iw, stride, pad),
                                   dW.reshape(-1)[iw])
 
