@@ -93,7 +93,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
 void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
                     const float *__restrict__ V, float *__restrict__ O, float *__restrict__ LSE,
                     const int32_t *__restrict__ key_len, int H, int Lq, int Lk, int causal,
-                    float scale_log2, int n_qtiles, int BH) {
+                    float scale_log2, int n_qtiles, int BH, int layer) {
     constexpr int NS = D / 16;    // 16-deep contraction steps over d
     constexpr int NCB = D / 32;   // 32-column blocks of d
     constexpr int NKB = kKeys / 32;
@@ -102,8 +102,9 @@ void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
     __shared__ __attribute__((aligned(16))) uint16_t Kr[kKeys][LD];
     __shared__ __attribute__((aligned(16))) uint16_t Vr[kKeys][LD];
 
-    const int rank = blockIdx.x / BH;
-    const int head = blockIdx.x - rank * BH;
+    const int slot = blockIdx.x / BH;
+    const int head = blockIdx.x - slot * BH;
+    const int rank = serpentine_rank(slot, n_qtiles, layer);
     const int qt = causal ? (n_qtiles - 1 - rank) : rank;
     const int b = head / H;
     const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
@@ -264,12 +265,13 @@ hipError_t launch_fwd_accel(const AttnProblem &p, const float *Q, const float *K
     const int nqt = cdiv(p.Lq, kRows);
     const dim3 grid(nqt * BH), block(kThreads);
     const float sl2 = p.scale * kLog2e;
-#define MG_FWD_ACCEL(DD)                                                                     \
-    (p.scale > 0.f                                                                          \
-         ? (attn_fwd_accel<DD, true><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, \
-                                                            p.Lq, p.Lk, p.causal, sl2, nqt, BH))     \
-         : (attn_fwd_accel<DD, false><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len,     \
-                                                             p.H, p.Lq, p.Lk, p.causal, sl2, nqt, BH)))
+    auto go = [&](auto kern) {
+        const int ly = causal_rank_layer((const void *)kern, kThreads, grid.x, BH, p.causal);
+        kern<<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal, sl2,
+                                    nqt, BH, ly);
+    };
+#define MG_FWD_ACCEL(DD) \
+    (p.scale > 0.f ? go(attn_fwd_accel<DD, true>) : go(attn_fwd_accel<DD, false>))
     switch (p.d) {
     case 32: MG_FWD_ACCEL(32); break;
     case 64: MG_FWD_ACCEL(64); break;

@@ -62,7 +62,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8))
 void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
                    const uint16_t *__restrict__ V, uint16_t *__restrict__ O,
                    float *__restrict__ LSE, const int32_t *__restrict__ key_len, int H, int Lq, int Lk,
-                   int causal, float scale_log2, int n_qtiles, int BH) {
+                   int causal, float scale_log2, int n_qtiles, int BH, int layer) {
     constexpr int NS = D / 16;    // 16-deep contraction steps over d
     constexpr int NCB = D / 32;   // 32-column blocks of d
     constexpr int NKB = kStream / 32;
@@ -76,8 +76,9 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
     auto kdst = reinterpret_cast<float (*)[LD / 2]>(&Kr[0][0]);
     auto vdst = reinterpret_cast<float (*)[LD / 2]>(&Vr[0][0]);
 
-    const int rank = blockIdx.x / BH;
-    const int head = blockIdx.x - rank * BH;
+    const int slot = blockIdx.x / BH;
+    const int head = blockIdx.x - slot * BH;
+    const int rank = serpentine_rank(slot, n_qtiles, layer);
     const int qt = causal ? (n_qtiles - 1 - rank) : rank;
     const int b = head / H;
     const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
@@ -255,7 +256,7 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
                     const float *__restrict__ LSE, const float *__restrict__ Dws,
                     uint16_t *__restrict__ dK, uint16_t *__restrict__ dV,
                     const int32_t *__restrict__ key_len, int H, int Lq, int Lk, int causal, float scale,
-                    float scale_log2, int BH) {
+                    float scale_log2, int BH, int layer) {
     constexpr int NS = D / 32;
     constexpr int NC = D / 16;
     constexpr int LD = Bf16Ld<D>::value;
@@ -268,9 +269,9 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
     __shared__ __attribute__((aligned(16))) float lse2s[2][kStream];
     __shared__ __attribute__((aligned(16))) float Ds[2][kStream];
 
-    const int rank = blockIdx.x / BH;
-    const int head = blockIdx.x - rank * BH;
-    const int kt = rank;
+    const int slot = blockIdx.x / BH;
+    const int head = blockIdx.x - slot * BH;
+    const int kt = serpentine_rank(slot, (Lk + kStatRows - 1) / kStatRows, layer);
     const int b = head / H;
     const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
     const int diag = Lk - Lq;   // causal: row i sees keys j <= i + diag
@@ -411,7 +412,7 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
                   const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
                   const float *__restrict__ LSE, const float *__restrict__ Dws,
                   uint16_t *__restrict__ dQ, const int32_t *__restrict__ key_len, int H, int Lq, int Lk,
-                  int causal, float scale, float scale_log2, int n_qtiles, int BH) {
+                  int causal, float scale, float scale_log2, int n_qtiles, int BH, int layer) {
     constexpr int NS = D / 16;
     constexpr int NCB = D / 32;
     constexpr int NKB = KS / 32;
@@ -422,8 +423,9 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
     __shared__ __attribute__((aligned(16))) uint16_t Kr[2][KS][LD];
     __shared__ __attribute__((aligned(16))) uint16_t Vr[2][KS][LD];
 
-    const int rank = blockIdx.x / BH;
-    const int head = blockIdx.x - rank * BH;
+    const int slot = blockIdx.x / BH;
+    const int head = blockIdx.x - slot * BH;
+    const int rank = serpentine_rank(slot, n_qtiles, layer);
     const int qt = causal ? (n_qtiles - 1 - rank) : rank;
     const int b = head / H;
     const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
@@ -530,12 +532,13 @@ hipError_t launch_fwd_bf16(const AttnProblem &p, const uint16_t *Q, const uint16
     const int nqt = cdiv(p.Lq, kFwdRows);
     const dim3 grid(nqt * BH), block(kThreads);
     const float sl2 = p.scale * kLog2e;
-#define MG_FWD_BF16(DD)                                                                     \
-    (p.scale > 0.f                                                                         \
-         ? (attn_fwd_bf16<DD, true><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H,  \
-                                                          p.Lq, p.Lk, p.causal, sl2, nqt, BH), 0) \
-         : (attn_fwd_bf16<DD, false><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, \
-                                                           p.Lq, p.Lk, p.causal, sl2, nqt, BH), 0))
+    auto go = [&](auto kern) {
+        const int ly = causal_rank_layer((const void *)kern, kThreads, grid.x, BH, p.causal);
+        kern<<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal, sl2,
+                                    nqt, BH, ly);
+    };
+#define MG_FWD_BF16(DD) \
+    (p.scale > 0.f ? go(attn_fwd_bf16<DD, true>) : go(attn_fwd_bf16<DD, false>))
     switch (p.d) {
     case 32: MG_FWD_BF16(32); break;
     case 64: MG_FWD_BF16(64); break;
@@ -565,10 +568,15 @@ hipError_t launch_bwd_dkdv_bf16(const AttnProblem &p, const uint16_t *Q, const u
     const int BH = p.B * p.H;
     const dim3 grid(cdiv(p.Lk, kStatRows) * BH), block(kThreads);
     const float sl2 = p.scale * kLog2e;
+    auto go = [&](auto kern) {
+        const int ly = causal_rank_layer((const void *)kern, kThreads, grid.x, BH, p.causal);
+        kern<<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.Lq, p.Lk,
+                                    p.causal, p.scale, sl2, BH, ly);
+    };
     switch (p.d) {
-    case 32: attn_dkdv_bf16<32><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
-    case 64: attn_dkdv_bf16<64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
-    case 128: attn_dkdv_bf16<128><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
+    case 32: go(attn_dkdv_bf16<32>); break;
+    case 64: go(attn_dkdv_bf16<64>); break;
+    case 128: go(attn_dkdv_bf16<128>); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -581,10 +589,15 @@ hipError_t launch_bwd_dq_bf16(const AttnProblem &p, const uint16_t *Q, const uin
     const int nqt = cdiv(p.Lq, kFwdRows);
     const dim3 grid(nqt * BH), block(kThreads);
     const float sl2 = p.scale * kLog2e;
+    auto go = [&](auto kern) {
+        const int ly = causal_rank_layer((const void *)kern, kThreads, grid.x, BH, p.causal);
+        kern<<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk,
+                                    p.causal, p.scale, sl2, nqt, BH, ly);
+    };
     switch (p.d) {
-    case 32: attn_dq_bf16<32, 64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, nqt, BH); break;
-    case 64: attn_dq_bf16<64, 64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, nqt, BH); break;
-    case 128: attn_dq_bf16<128, 64><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, nqt, BH); break;
+    case 32: go(attn_dq_bf16<32, 64>); break;
+    case 64: go(attn_dq_bf16<64, 64>); break;
+    case 128: go(attn_dq_bf16<128, 64>); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

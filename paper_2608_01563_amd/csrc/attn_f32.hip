@@ -29,10 +29,14 @@
 // issued before the current one is consumed and written to LDS after it.
 //
 // Workgroup order: the 1-D grid is numbered rank-major over heads
-// (id = rank * B*H + head) with rank 0 the tile that has the most work under
-// a causal mask, so the longest tiles start first; with B*H a multiple of 8
-// every tile of a head lands on the same XCD (workgroups are dealt to the
-// eight XCDs round-robin), so a head's K/V or Q/dO stay in one L2.
+// (id = slot * B*H + head) with rank 0 the tile that has the most work under
+// a causal mask.  When the grid is larger than what the chip holds at once,
+// slot = rank, so the longest tiles start first and the dispatcher hands the
+// short ones to whichever CU frees up; when every workgroup is resident at
+// once, layers of slots alternate direction (serpentine_rank) so that each
+// CU holds a mix of long and short tiles.  With B*H a multiple of 8 every
+// tile of a head lands on the same XCD (workgroups are dealt to the eight
+// XCDs round-robin), so a head's K/V or Q/dO stay in one L2.
 //
 // Masking: an element's offset inside its tile is compared against one
 // per-lane threshold (key length, causal diagonal); the forward kernel skips
@@ -108,7 +112,7 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::templa
 void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
                   const float *__restrict__ V, float *__restrict__ O, float *__restrict__ LSE,
                   const int32_t *__restrict__ key_len, int H, int Lq, int Lk, int causal,
-                  float scale_log2, int n_qtiles, int BH) {
+                  float scale_log2, int n_qtiles, int BH, int layer) {
     constexpr int KS = kFwdStream;
     constexpr int DQ = D / 4;    // contraction values per lane in one S chain
     constexpr int NC = D / 16;   // 16-column blocks of the head dimension
@@ -119,8 +123,9 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
     __shared__ __attribute__((aligned(16))) float Ks[KS * D];
     __shared__ __attribute__((aligned(16))) float Vs[KS * D];
 
-    const int rank = blockIdx.x / BH;
-    const int head = blockIdx.x - rank * BH;
+    const int slot = blockIdx.x / BH;
+    const int head = blockIdx.x - slot * BH;
+    const int rank = serpentine_rank(slot, n_qtiles, layer);
     const int qt = causal ? (n_qtiles - 1 - rank) : rank;
     const int b = head / H;
     const float *Qh = Q + (size_t)head * Lq * D;
@@ -319,7 +324,7 @@ void attn_dkdv_f32(const float *__restrict__ Q, const float *__restrict__ K,
                    const float *__restrict__ LSE, const float *__restrict__ Dws,
                    float *__restrict__ dK, float *__restrict__ dV,
                    const int32_t *__restrict__ key_len, int H, int Lq, int Lk, int causal, float scale,
-                   float scale_log2, int BH) {
+                   float scale_log2, int BH, int layer) {
     constexpr int DQ = D / 4;
     constexpr int NC = D / 16;
     constexpr int BR = 16 * NIB;
@@ -330,9 +335,10 @@ void attn_dkdv_f32(const float *__restrict__ Q, const float *__restrict__ K,
     __shared__ __attribute__((aligned(16))) float lse2s[C::NBUF][BR];
     __shared__ __attribute__((aligned(16))) float Ds[C::NBUF][BR];
 
-    const int rank = blockIdx.x / BH;
-    const int head = blockIdx.x - rank * BH;
-    const int kt = rank;   // low key tiles see the most queries under a causal mask
+    const int slot = blockIdx.x / BH;
+    const int head = blockIdx.x - slot * BH;
+    // low key tiles see the most queries under a causal mask
+    const int kt = serpentine_rank(slot, (Lk + C::ROWS - 1) / C::ROWS, layer);
     const int b = head / H;
     const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
     const float *Qh = Q + qoff;
@@ -507,7 +513,8 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
                     const float *__restrict__ LSE, const float *__restrict__ Dws,
                     float *__restrict__ dK, float *__restrict__ dV, float *__restrict__ dQp,
                     float *__restrict__ dKVp, const int32_t *__restrict__ key_len, int H, int Lq,
-                    int Lk, int causal, float scale, float scale_log2, int BH, int nsplit) {
+                    int Lk, int causal, float scale, float scale_log2, int BH, int nsplit,
+                    int nranks, int layer) {
     constexpr int DQ = D / 4;
     constexpr int NC = D / 16;
     constexpr int BR = 16 * NIB;
@@ -524,8 +531,9 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     __shared__ __attribute__((aligned(16))) float Kt[D][KR + 4];    // key tile, transposed
     __shared__ __attribute__((aligned(16))) float dSs[BR][KR + 4];  // dS of the query tile
 
-    const int rank = blockIdx.x / BH;
-    const int head = blockIdx.x - rank * BH;
+    const int slot = blockIdx.x / BH;
+    const int head = blockIdx.x - slot * BH;
+    const int rank = serpentine_rank(slot, nranks, layer);
     const int kt = rank / nsplit;          // key tile
     const int split = rank - kt * nsplit;  // share of its query tiles
     const int b = head / H;
@@ -802,7 +810,7 @@ void attn_dq_f32(const float *__restrict__ Q, const float *__restrict__ K,
                  const float *__restrict__ V, const float *__restrict__ dO,
                  const float *__restrict__ LSE, const float *__restrict__ Dws,
                  float *__restrict__ dQ, const int32_t *__restrict__ key_len, int H, int Lq,
-                 int Lk, int causal, float scale, float scale_log2, int n_qtiles, int BH) {
+                 int Lk, int causal, float scale, float scale_log2, int n_qtiles, int BH, int layer) {
     constexpr int DQ = D / 4;
     constexpr int NC = D / 16;
     using Stager = F32TileStager<kStream, D, C::NT>;
@@ -810,8 +818,9 @@ void attn_dq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     __shared__ __attribute__((aligned(16))) float Ks[C::NBUF][kStream][LD];
     __shared__ __attribute__((aligned(16))) float Vs[C::NBUF][kStream][LD];
 
-    const int rank = blockIdx.x / BH;
-    const int head = blockIdx.x - rank * BH;
+    const int slot = blockIdx.x / BH;
+    const int head = blockIdx.x - slot * BH;
+    const int rank = serpentine_rank(slot, n_qtiles, layer);
     const int qt = causal ? (n_qtiles - 1 - rank) : rank;
     const int b = head / H;
     const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
@@ -947,10 +956,15 @@ hipError_t launch_fwd_f32(const AttnProblem &p, const float *Q, const float *K,
     const int nqt = cdiv(p.Lq, C::ROWS);
     const dim3 grid(nqt * BH), block(C::NT);
     const float sl2 = p.scale * kLog2e;
+    auto go = [&](auto kern) {
+        const int ly = causal_rank_layer((const void *)kern, C::NT, grid.x, BH, p.causal);
+        kern<<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal, sl2,
+                                    nqt, BH, ly);
+    };
     switch (p.d) {
-    case 32: attn_fwd_f32<32, C><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal, sl2, nqt, BH); break;
-    case 64: attn_fwd_f32<64, C><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal, sl2, nqt, BH); break;
-    case 128: attn_fwd_f32<128, C><<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal, sl2, nqt, BH); break;
+    case 32: go(attn_fwd_f32<32, C>); break;
+    case 64: go(attn_fwd_f32<64, C>); break;
+    case 128: go(attn_fwd_f32<128, C>); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -976,10 +990,15 @@ hipError_t launch_bwd_dkdv_f32(const AttnProblem &p, const float *Q, const float
     const int BH = p.B * p.H;
     const dim3 grid(cdiv(p.Lk, C::ROWS) * BH), block(C::NT);
     const float sl2 = p.scale * kLog2e;
+    auto go = [&](auto kern) {
+        const int ly = causal_rank_layer((const void *)kern, C::NT, grid.x, BH, p.causal);
+        kern<<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.Lq, p.Lk,
+                                    p.causal, p.scale, sl2, BH, ly);
+    };
     switch (p.d) {
-    case 32: attn_dkdv_f32<32, MG_DKDV_NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
-    case 64: attn_dkdv_f32<64, MG_DKDV_NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
-    case 128: attn_dkdv_f32<128, 2, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH); break;
+    case 32: go(attn_dkdv_f32<32, MG_DKDV_NIB, C>); break;
+    case 64: go(attn_dkdv_f32<64, MG_DKDV_NIB, C>); break;
+    case 128: go(attn_dkdv_f32<128, 2, C>); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -1024,11 +1043,17 @@ static hipError_t launch_dkdvq(const AttnProblem &p, const float *Q, const float
                                float *dKVp, hipStream_t s) {
     const int BH = p.B * p.H;
     const int ns = fused_dq_query_splits(p);
-    const dim3 grid(cdiv(p.Lk, C::ROWS) * ns * BH), block(C::NT);
+    const int nr = cdiv(p.Lk, C::ROWS) * ns;   // ranks: key tile x split
+    const dim3 grid(nr * BH), block(C::NT);
     const float sl2 = p.scale * kLog2e;
+    auto go = [&](auto kern) {
+        const int ly = causal_rank_layer((const void *)kern, C::NT, grid.x, BH, p.causal);
+        kern<<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, dKVp, p.key_len, p.H,
+                                    p.Lq, p.Lk, p.causal, p.scale, sl2, BH, ns, nr, ly);
+    };
     switch (p.d) {
-    case 32: attn_dkdvq_f32<32, NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, dKVp, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH, ns); break;
-    case 64: attn_dkdvq_f32<64, NIB, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, dKVp, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH, ns); break;
+    case 32: go(attn_dkdvq_f32<32, NIB, C>); break;
+    case 64: go(attn_dkdvq_f32<64, NIB, C>); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
@@ -1074,10 +1099,15 @@ hipError_t launch_bwd_dq_f32(const AttnProblem &p, const float *Q, const float *
     const int nqt = cdiv(p.Lq, C::ROWS);
     const dim3 grid(nqt * BH), block(C::NT);
     const float sl2 = p.scale * kLog2e;
+    auto go = [&](auto kern) {
+        const int ly = causal_rank_layer((const void *)kern, C::NT, grid.x, BH, p.causal);
+        kern<<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk,
+                                    p.causal, p.scale, sl2, nqt, BH, ly);
+    };
     switch (p.d) {
-    case 32: attn_dq_f32<32, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, nqt, BH); break;
-    case 64: attn_dq_f32<64, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, nqt, BH); break;
-    case 128: attn_dq_f32<128, C><<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, nqt, BH); break;
+    case 32: go(attn_dq_f32<32, C>); break;
+    case 64: go(attn_dq_f32<64, C>); break;
+    case 128: go(attn_dq_f32<128, C>); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -131,6 +131,20 @@ __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt(0x0F70 | (N & 15) | ((N >> 4) << 14));
 }
 
+// Rank of the tile a workgroup takes.  Workgroups are dealt to the chip's
+// compute units in layers (one workgroup slot on every CU per layer of
+// `layer` ranks, `layer` * B*H workgroups); reversing the rank order in every
+// other layer puts a heavy causal tile and a light one on the same CU.
+// layer <= 0 keeps the plain order.
+__device__ __forceinline__ int serpentine_rank(int rho, int nranks, int layer) {
+    if (layer <= 0) return rho;
+    const int s = rho / layer;
+    if ((s & 1) == 0) return rho;
+    const int base = s * layer;
+    const int len = min(layer, nranks - base);
+    return base + len - 1 - (rho - base);
+}
+
 // Clamp a per-batch key length to [0, L]; L when no padding is given.
 __device__ __forceinline__ int key_limit(const int32_t *key_len, int b, int L) {
     if (key_len == nullptr) return L;

@@ -1,10 +1,15 @@
 // host_runtime.cpp -- the shared host plumbing of host_runtime.h and the
 // library-wide C entry points that report on it (status strings, the last
-// error detail, per-launch event timing).
+// error detail, per-launch event timing), plus the launch-order query of
+// launch.h (causal_rank_layer).
 #include "host_runtime.h"
+#include "launch.h"
 
 #include <cstdarg>
 #include <cstdio>
+#include <map>
+#include <mutex>
+#include <tuple>
 
 namespace mg {
 namespace host {
@@ -86,6 +91,43 @@ Profiler &profiler() {
 }
 
 }  // namespace host
+}  // namespace mg
+
+namespace mg {
+
+int causal_rank_layer(const void *kernel, int block, long grid, int BH, int causal) {
+    if (!causal || BH <= 0) return 0;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    // (kernel, block, device) -> (CUs, resident workgroups per CU)
+    static std::mutex mu;
+    static std::map<std::tuple<const void *, int, int>, std::pair<int, int>> cache;
+    std::pair<int, int> res;
+    {
+        std::lock_guard<std::mutex> g(mu);
+        auto key = std::make_tuple(kernel, block, dev);
+        auto it = cache.find(key);
+        if (it == cache.end()) {
+            int cus = 0, per_cu = 0;
+            if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) !=
+                    hipSuccess ||
+                hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, block, 0) !=
+                    hipSuccess) {
+                (void)hipGetLastError();
+                cus = per_cu = 0;
+            }
+            it = cache.emplace(key, std::make_pair(cus, per_cu)).first;
+        }
+        res = it->second;
+    }
+    const int cus = res.first, per_cu = res.second;
+    if (cus <= 0 || per_cu <= 0 || grid > (long)cus * per_cu || cus % BH != 0) return 0;
+    return cus / BH;
+}
+
 }  // namespace mg
 
 using namespace mg::host;

@@ -21,6 +21,16 @@ struct AttnProblem {
     const int32_t *key_len;  // device [B] or nullptr
 };
 
+// Rank-order layer of a causal tile grid (the `layer` argument of
+// serpentine_rank in device_common.h).  When all `grid` workgroups of
+// `kernel` (`block` threads each, no dynamic LDS) are resident on the current
+// device at once and its CU count is a multiple of the head count BH, the
+// dispatcher places workgroup i on CU i mod CUs, so layers of CUs/BH ranks
+// that alternate direction give every CU a mix of heavy and light causal
+// tiles.  Otherwise 0: heavy tiles first, and the dispatcher hands the light
+// ones to whichever CU frees up first.  Non-causal grids get 0.
+int causal_rank_layer(const void *kernel, int block, long grid, int BH, int causal);
+
 // Forward, strict f32: O, LSE from Q, K, V.
 hipError_t launch_fwd_f32(const AttnProblem &p, const float *Q, const float *K,
                           const float *V, float *O, float *LSE, hipStream_t s);
