@@ -63,7 +63,7 @@
 #define MG_DKDV_CFG 4, 3, false
 #endif
 #ifndef MG_DKDVQ_CAUSAL_CFG
-#define MG_DKDVQ_CAUSAL_CFG 8, 3, false   // 128-key tiles: half the dQ partials
+#define MG_DKDVQ_CAUSAL_CFG 8, 4, false   // 128-key tiles: half the dQ partials
 #endif
 #ifndef MG_DQ_CFG
 #define MG_DQ_CFG 8, 0, false
@@ -501,8 +501,10 @@ void attn_dkdv_f32(const float *__restrict__ Q, const float *__restrict__ K,
 // attn_dq_reduce_f32 adds the partials of a row in key-tile order: no atomics,
 // bitwise-reproducible, and no second recompute of S and dP.
 //
-// The Q and dO tiles reach LDS by row-wise direct-to-LDS loads (no staging
-// registers, padded rows as in the kernel above).  With two LDS buffers (C::NBUF == 2) the next tile is fetched
+// The Q and dO tiles, and the LSE and D values of their rows, reach LDS by
+// row-wise direct-to-LDS loads (no staging registers, padded rows as in the
+// kernel above); dQ partials leave through raw buffer stores whose
+// descriptor ends at row Lq.  With two LDS buffers (C::NBUF == 2) the next tile is fetched
 // during the whole current iteration; with one, during the dQ product.  A
 // tile's dQ partials are stored at the start of the next iteration, so the
 // wait for the next tile never waits on a just-issued store.
@@ -526,7 +528,7 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     using Tile = RowDirectTile<BR, D, C::NW, LD>;
     __shared__ __attribute__((aligned(16))) float Qs[NB][BR][LD];
     __shared__ __attribute__((aligned(16))) float dOs[NB][BR][LD];
-    __shared__ __attribute__((aligned(16))) float lse2s[NB][BR];
+    __shared__ __attribute__((aligned(16))) float lse2s[NB][BR];    // LSE (natural log)
     __shared__ __attribute__((aligned(16))) float Ds[NB][BR];
     __shared__ __attribute__((aligned(16))) float Kt[D][KR + 4];    // key tile, transposed
     __shared__ __attribute__((aligned(16))) float dSs[BR][KR + 4];  // dS of the query tile
@@ -562,20 +564,20 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
     const Tile tile;
 
-    float lse_pre = 0.f, d_pre = 0.f;
-    auto fetch = [&](int qt, int buf) {   // direct loads of Q, dO; LSE, D to registers
+    // Direct-to-LDS loads of the Q and dO rows of query tile qt, and of their
+    // LSE (wave 0) and D (the last wave) values; rows past Lq arrive as zeros.
+    auto fetch = [&](int qt, int buf) {
         tile.issue(Qs[buf], Qh, qt * BR, Lq, w, lane);
         tile.issue(dOs[buf], dOh, qt * BR, Lq, w, lane);
-        if (tid < BR) {
-            const int row = qt * BR + tid;
-            lse_pre = (row < Lq) ? LSE[(size_t)head * Lq + row] : 0.f;
-            d_pre = (row < Lq) ? Dws[(size_t)head * Lq + row] : 0.f;
-        }
-    };
-    auto publish = [&](int buf) {   // LSE (base 2) and D of the fetched rows
-        if (tid < BR) {
-            lse2s[buf][tid] = lse_pre * kLog2e;
-            Ds[buf][tid] = d_pre;
+        if (w == 0 || w == C::NW - 1) {
+            const int row0 = qt * BR;
+            const int rows = min(max(Lq - row0, 0), BR);
+            const float *src = (w == 0 ? LSE : Dws) + (size_t)head * Lq + row0;
+            const auto rsrc = buffer_rsrc(src, rows * 4);
+            float *dst = (w == 0) ? lse2s[buf] : Ds[buf];
+            if (lane < BR)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                    rsrc, (__attribute__((address_space(3))) void *)dst, 4, lane * 4, 0, 0, 0);
         }
     };
     if (qstart < qstop) fetch(qstart, 0);
@@ -623,24 +625,25 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
         return (NBLK % C::NW == 0) ? w * PER_WAVE + bb : w + bb * C::NW;
     };
     f32x4 dqacc[PER_WAVE];   // partials of the previous query tile, not yet stored
+    // Raw buffer stores through a descriptor that covers the tile's rows below
+    // Lq: stores of rows past Lq fall outside it and are dropped.
+    float *dQp_head = dQp + ((size_t)kt * BH + head) * Lq * D;
     auto store_dq = [&](int qt) {
+        const int row0 = qt * BR;
+        const auto rsrc = buffer_rsrc(dQp_head + (size_t)row0 * D, min(Lq - row0, BR) * D * 4);
 #pragma unroll
         for (int bb = 0; bb < PER_WAVE; ++bb) {
             const int blk = dq_block(bb);
             if (NBLK % C::NW != 0 && blk >= NBLK) break;
             const int ib = blk / NC;
             const int c = blk - ib * NC;
-            const int row = qt * BR + 16 * ib + il;
-            if (row < Lq)
-                *reinterpret_cast<f32x4 *>(dQp + ((size_t)kt * BH + head) * Lq * D +
-                                           (size_t)row * D + 16 * c + 4 * g) = dqacc[bb];
+            __builtin_amdgcn_raw_buffer_store_b128(
+                __builtin_bit_cast(u32x4, dqacc[bb]), rsrc,
+                ((16 * ib + il) * D + 16 * c + 4 * g) * 4, 0, 0);
         }
     };
 
-    if (qstart < qstop) {
-        wait_vmcnt<0>();
-        publish(0);
-    }
+    if (qstart < qstop) wait_vmcnt<0>();
     __syncthreads();   // first tile, its LSE/D and Kt visible
 
     for (int qt = qstart; qt < qstop; ++qt) {
@@ -659,28 +662,39 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
                 sacc[ib] = zero4();
                 pacc[ib] = zero4();
             }
+            // S = Q K^T, then dP = dO V^T: one product at a time keeps one
+            // set of A operands live, so the kernel fits in 128 VGPRs (four
+            // waves per SIMD, two 8-wave workgroups per CU).
 #pragma unroll
             for (int s4 = 0; s4 < DQ / 4; ++s4) {
-                f32x4 aq[NIB], ao[NIB];
+                f32x4 aq[NIB];
 #pragma unroll
-                for (int ib = 0; ib < NIB; ++ib) {
+                for (int ib = 0; ib < NIB; ++ib)
                     aq[ib] = *reinterpret_cast<const f32x4 *>(&Qs[cb][16 * ib + il][g * DQ + 4 * s4]);
-                    ao[ib] = *reinterpret_cast<const f32x4 *>(&dOs[cb][16 * ib + il][g * DQ + 4 * s4]);
-                }
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
 #pragma unroll
-                    for (int ib = 0; ib < NIB; ++ib) {
+                    for (int ib = 0; ib < NIB; ++ib)
                         sacc[ib] = mfma16x16x4(aq[ib][e], kreg[4 * s4 + e], sacc[ib]);
+            }
+#pragma unroll
+            for (int s4 = 0; s4 < DQ / 4; ++s4) {
+                f32x4 ao[NIB];
+#pragma unroll
+                for (int ib = 0; ib < NIB; ++ib)
+                    ao[ib] = *reinterpret_cast<const f32x4 *>(&dOs[cb][16 * ib + il][g * DQ + 4 * s4]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+#pragma unroll
+                    for (int ib = 0; ib < NIB; ++ib)
                         pacc[ib] = mfma16x16x4(ao[ib][e], vreg[4 * s4 + e], pacc[ib]);
-                    }
             }
 
             const int ibase = qt * BR + 4 * g;
             const int thr = kthr - ibase;
 #pragma unroll
             for (int ib = 0; ib < NIB; ++ib) {
-                const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lse2s[cb][16 * ib + 4 * g]);
+                const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lse2s[cb][16 * ib + 4 * g]) * kLog2e;
                 const f32x4 dd = *reinterpret_cast<const f32x4 *>(&Ds[cb][16 * ib + 4 * g]);
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
@@ -731,10 +745,7 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
             dqacc[bb] = acc;
         }
 
-        if (qt + 1 < qstop) {
-            wait_vmcnt<0>();   // next Q/dO tile landed, its LSE/D in registers
-            publish(NB == 2 ? (cb ^ 1) : 0);
-        }
+        if (qt + 1 < qstop) wait_vmcnt<0>();   // next Q/dO tile and its LSE/D landed
         __syncthreads();   // next tile visible; dS and this tile's buffer free
     }
     if (qstart < qstop) store_dq(qstop - 1);
