@@ -46,6 +46,11 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup-ms", type=float, default=250.0,
+                    help="after the W warmup steps, keep running untimed steps until this "
+                         "much wall time has passed: the GPU raises its clocks over the "
+                         "first ~30 ms of sustained load, and a timed region that starts "
+                         "earlier measures the ramp, not the kernels")
     ap.add_argument("--workload", type=int, default=3,
                     help="workload id (3 = causal B8 H8 L1024 d64 strict f32)")
     ap.add_argument("--conv", action="store_true",
@@ -197,9 +202,7 @@ def main():
         mg.mg_attn_bwd_cross(Q, K, V, O, LSE, dO, dQ, dK, dV, kl, causal=w.causal,
                              scale=w.scale, contract=w.contract, workspace=ws, stream=stream)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    warm = warm_up(step, args, torch)
 
     # Timed region: exactly `steps` steps between device synchronizations.
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
@@ -267,6 +270,8 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "warmup_steps_run": warm[0],
+        "warmup_ms": round(warm[1], 1),
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -344,6 +349,24 @@ def summarize(samples):
             "samples": [round(float(v), 4) for v in samples]}
 
 
+def warm_up(step, args, torch):
+    """Run the W requested warmup steps, then more untimed steps until
+    --warmup-ms of wall time has passed (the GPU's clock ramp under sustained
+    load), synchronizing every few steps.  Returns (steps run, ms)."""
+    t0 = time.perf_counter()
+    n = 0
+    for _ in range(args.warmup):
+        step()
+        n += 1
+    torch.cuda.synchronize()
+    while (time.perf_counter() - t0) * 1e3 < args.warmup_ms and n < 100000:
+        for _ in range(8):
+            step()
+            n += 1
+        torch.cuda.synchronize()
+    return n, (time.perf_counter() - t0) * 1e3
+
+
 def environment():
     """GPU name, HIP/torch versions, the source revision and the GPU clocks
     as the driver reports them (each null when unavailable)."""
@@ -357,6 +380,10 @@ def environment():
         env["git_revision"] = r.stdout.strip() or None
     except (OSError, subprocess.SubprocessError):
         pass
+    if under_profiler():
+        # rocm-smi is a script started through `env`; with the profiler's
+        # library preloaded, that hop would initialise the GPU and then exec
+        return env
     try:
         r = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True,
                            timeout=20)
@@ -365,6 +392,15 @@ def environment():
     except (OSError, subprocess.SubprocessError):
         pass
     return env
+
+
+def under_profiler():
+    """True when a rocprofiler library is mapped into this process."""
+    try:
+        with open("/proc/self/maps") as f:
+            return "rocprofiler" in f.read()
+    except OSError:
+        return False
 
 
 def cpu_baseline(args, w, x, pairs, gpu_outputs):
@@ -456,9 +492,7 @@ def conv_main(args):
     def outputs():
         return [(b[5].clone() if b[5] is not None else None, b[6].clone()) for b in bufs]
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
+    warm = warm_up(step, args, torch)
     eager = outputs()
 
     # eager step time (host launch bound) for reference
@@ -535,6 +569,8 @@ def conv_main(args):
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
+        "warmup_steps_run": warm[0],
+        "warmup_ms": round(warm[1], 1),
         "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True,
         "scaling": "weak",
