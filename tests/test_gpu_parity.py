@@ -264,6 +264,24 @@ def test_wide_key_tiles_ragged(gpu_lib, d, padded):
     assert max(errs.values()) <= TOL["strict_f32"], errs
 
 
+@pytest.mark.parametrize("contract,d", [("fast_bf16", 128), ("fast_bf16", 64),
+                                        ("accelerated", 64)])
+def test_resident_causal_grid_ragged(gpu_lib, contract, d):
+    """B*H = 64 heads of a ragged causal L = 1000: the forward grids (and the
+    bf16 dQ grid) fit on the chip at once, so their tiles are dealt in
+    alternating-direction layers of 256 / (B*H) ranks; every tile must still
+    be computed once."""
+    B, H, L = 4, 16, 1000
+    say("resident causal grid %s B%d H%d L%d d%d" % (contract, B, H, L, d))
+    x = make_inputs(B, H, L, d, causal=True, contract=contract, seed=91 + d)
+    if contract == "accelerated":
+        accel_check(x)
+        return
+    errs = compare(run_gpu(x), oracle_reference(x), contract)
+    say("  errors %s" % {k: "%.2e" % v for k, v in errs.items()})
+    assert max(errs.values()) <= TOL[contract], errs
+
+
 # ---- accelerated contract: f32 tensors, f16 forward matrix inputs, strict backward
 
 ACCEL_SMALL = [(L, d, mode) for L in (1, 17, 65, 200) for d in (32, 64, 128)
