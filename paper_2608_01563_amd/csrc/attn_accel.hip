@@ -191,16 +191,26 @@ void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
 #pragma unroll
             for (int v = 0; v < 16; v += 2) mx = fmaxf(mx, fmaxf(sacc[kb][v], sacc[kb][v + 1]));
         mx = max_xor32(mx);
-        const float m_new = fmaxf(m_run, mx);
-        const float m2 = (m_new == -INFINITY) ? 0.f : (POS_SCALE ? m_new * scale_log2 : m_new);
-        if (__any(m_new != m_run)) {
+        // The running maximum is only an offset: the probabilities are
+        // exp2(s - m) for any m at or below the true row maximum, so O and l
+        // are rescaled only when some row's maximum grew by more than kSlack
+        // (base 2); otherwise the stale m stays and this tile's probabilities
+        // are at most 2^kSlack (no overflow, the same relative rounding).
+        const float grow2 = POS_SCALE ? (mx - m_run) * scale_log2 : mx - m_run;
+        if (__any(grow2 > kSlack)) {
+            const float m_new = fmaxf(m_run, mx);
             const float m2_old = POS_SCALE ? m_run * scale_log2 : m_run;
-            const float alpha = exp2_fast(m2_old - m2);
+            const float m2_new =
+                (m_new == -INFINITY) ? 0.f : (POS_SCALE ? m_new * scale_log2 : m_new);
+            const float alpha = exp2_fast(m2_old - m2_new);
             l_run *= alpha;
 #pragma unroll
             for (int cb = 0; cb < NCB; ++cb) oacc[cb] *= alpha;
+            m_run = m_new;
         }
-        m_run = m_new;
+        // exponent offset in base-2 units; a row with nothing allowed yet
+        // keeps all-zero probabilities
+        const float m2 = (m_run == -INFINITY) ? 0.f : (POS_SCALE ? m_run * scale_log2 : m_run);
         float psum = 0.f;
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb)

@@ -31,6 +31,9 @@ typedef uint16_t u16x8 __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr float kLog2e = 1.4426950408889634f;
+// Online-softmax slack (base 2): a forward may keep a running maximum up to
+// this far below the true one, so probabilities stay at most 2^kSlack.
+constexpr float kSlack = 8.f;
 constexpr float kLn2 = 0.69314718055994531f;
 
 __device__ __forceinline__ f32x4 mfma16x16x4(float a, float b, f32x4 c) {
