@@ -59,6 +59,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="repeat the oracle sample until this much CPU wall time (>= 3 runs)")
+    ap.add_argument("--no-mfma-probe", action="store_true",
+                    help="do not measure the sustained MFMA throughput for the roofline")
     ap.add_argument("--no-kernel-events", action="store_true",
                     help="do not bracket kernels with events (no roofline)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
@@ -69,7 +71,8 @@ def parse():
 
 def kernel_source_digest(conv=False):
     """sha256 over the names and contents of the files a kernel family is
-    built from (attention: every file directly under csrc/; convolution:
+    built from (attention: every file directly under csrc/ except the MFMA
+    probe; convolution:
     csrc/conv/ plus the shared device and host headers): a counter record
     taken on any other source is stale."""
     h = hashlib.sha256()
@@ -78,7 +81,8 @@ def kernel_source_digest(conv=False):
         names = ["conv/" + n for n in sorted(os.listdir(os.path.join(base, "conv")))]
         names += ["device_common.h", "host_runtime.h", "host_runtime.cpp"]
     else:
-        names = sorted(os.listdir(base))
+        # the MFMA probe is a measuring tool, not attention code
+        names = sorted(n for n in os.listdir(base) if n != "mfma_probe.hip")
     for name in names:
         path = os.path.join(base, name)
         if os.path.isfile(path):
@@ -111,6 +115,14 @@ def kernel_work(name, w, pairs, rows, key_len=None):
         n = w.B * w.H * w.L * d
         return 2.0 * n * es + 4.0 * rows, "byte", "hbm"
     raise KeyError(name)
+
+
+MFMA_PROBE_ITERS = {"f32": 20000, "bf16": 40000, "f16": 40000}   # ~15-20 ms each
+
+
+def mfma_kind(name):
+    """Matrix type a kernel multiplies in (the probe kind)."""
+    return "bf16" if "_bf16_" in name else ("f16" if "_accel_" in name else "f32")
 
 
 def kernel_peak(name):
@@ -320,6 +332,14 @@ def main():
                            "peak": peak, "unit": u, "frac": round(ach / peak, 4),
                            "traffic": traffic_for(dom, w.name),
                            "algorithmic_per_launch": amount}
+        if unit == "flop" and not args.no_mfma_probe:
+            # the same fraction against what the matrix cores sustain at the
+            # running clock (the library's MFMA probe, no memory traffic)
+            kind = mfma_kind(dom)
+            measured = mg.mg_mfma_peak(kind, MFMA_PROBE_ITERS[kind])
+            out["roofline"]["measured_peak"] = round(measured, 2)
+            out["roofline"]["measured_peak_kind"] = kind
+            out["roofline"]["frac_of_measured"] = round(ach / measured, 4)
         out["bwd_credited_tflops"] = round(
             10.0 * w.d * pairs / (sum(kernels[k][1] / kernels[k][0] for k in kernels
                                       if not k.startswith("attn_fwd")) * 1e-3) / 1e12, 3)

@@ -186,6 +186,20 @@ int mg_profile_collect(const char **names, int64_t *launches, double *total_ms,
                        int max_entries);
 void mg_profile_reset(void);
 
+/*
+ * Sustained matrix-core throughput of the current device, for reading the
+ * roofline fractions against what the chip delivers at its running clock
+ * (the published dense peaks assume 2.4 GHz).  Runs a kernel of independent
+ * MFMA accumulator chains (no memory traffic, eight waves per SIMD, on
+ * every CU) for `iters` steps on `stream`, after a warm-up launch of
+ * iters/8 steps, and WAITS for it (unlike every other call here); *tflops
+ * receives the achieved dense TFLOP/s.  kind: 0 = f32
+ * (v_mfma_f32_16x16x4_f32, eight chains per wave), 1 = bf16 and 2 = f16
+ * (v_mfma_f32_32x32x16_{bf16,f16}, four chains per wave).  iters in
+ * [1, 2^24].  Allocates nothing; events are created and destroyed inside.
+ */
+mg_status_t mg_mfma_peak(int kind, int iters, double *tflops, hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -83,6 +83,8 @@ def _declare(lib):
                                        ctypes.POINTER(ctypes.c_int64),
                                        ctypes.POINTER(ctypes.c_double), c_int]
     lib.mg_profile_collect.restype = c_int
+    lib.mg_mfma_peak.argtypes = [c_int, c_int, ctypes.POINTER(ctypes.c_double), vp]
+    lib.mg_mfma_peak.restype = c_int
     lib.mg_profile_reset.argtypes = []
     lib.mg_profile_reset.restype = None
     return lib
@@ -375,6 +377,19 @@ def mg_profile_enable(enable=True):
 
 def mg_profile_reset():
     load_library().mg_profile_reset()
+
+
+MFMA_KINDS = {"f32": 0, "bf16": 1, "f16": 2}
+
+
+def mg_mfma_peak(kind="f32", iters=20000, stream=None):
+    """Sustained dense TFLOP/s of the device's matrix cores for `kind`
+    ("f32", "bf16" or "f16"), measured by the library's probe kernel; waits
+    for the probe to finish."""
+    out = ctypes.c_double(0.0)
+    _check(load_library().mg_mfma_peak(MFMA_KINDS[kind], int(iters), ctypes.byref(out),
+                                       _stream_handle(stream)))
+    return out.value
 
 
 def mg_profile_collect(max_entries=32):

@@ -250,3 +250,13 @@ def test_conv_fused_entry_point_checks(lib):
     big = _shape(4, 7, 7, 512, 512, 3, 3, 1, 1, 1, 1)
     args[3] = vp(0x4000)
     assert lib.mg_conv2d_bwd(*args, ctypes.byref(big), 0, None, 0, None) == 4
+
+
+def test_mfma_probe_rejects_bad_arguments_before_any_device_call(lib):
+    out = ctypes.c_double(0.0)
+    assert lib.mg_mfma_peak(3, 100, ctypes.byref(out), None) == 1
+    assert lib.mg_mfma_peak(-1, 100, ctypes.byref(out), None) == 1
+    assert lib.mg_mfma_peak(0, 0, ctypes.byref(out), None) == 1
+    assert lib.mg_mfma_peak(0, (1 << 24) + 1, ctypes.byref(out), None) == 1
+    assert lib.mg_mfma_peak(1, 100, None, None) == 1
+    assert mg.mg_last_error_detail() != ""
