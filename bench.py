@@ -651,6 +651,11 @@ def conv_main(args):
                            "algorithmic_per_launch": per_launch,
                            "note": "averages over the step's launches of this kernel "
                                    "(one per layer, shapes differ)"}
+        if unit == "flop" and not args.no_mfma_probe:
+            measured = mg.mg_mfma_peak("f32", MFMA_PROBE_ITERS["f32"])
+            out["roofline"]["measured_peak"] = round(measured, 2)
+            out["roofline"]["measured_peak_kind"] = "f32"
+            out["roofline"]["frac_of_measured"] = round(ach / measured, 4)
         out["layers_ms"] = conv_layer_times(mg, bufs, torch)
     if not args.no_cpu_baseline:
         out["cpu_baseline"], out["parity"] = conv_cpu_baseline(args, layers, bufs)
