@@ -99,6 +99,80 @@ using DkdvCfg = Cfg<MG_DKDV_CFG>;
 using DkdvqCausalCfg = Cfg<MG_DKDVQ_CAUSAL_CFG>;
 using DqCfg = Cfg<MG_DQ_CFG>;
 
+// ---------------------------------- work-first order for key-padded grids
+// In a non-causal problem with key padding, the key tiles at or past a
+// batch's key length have no query work (their workgroups only write zero
+// dK/dV rows).  Numbered in plain slot-major order such idle workgroups sit
+// between the working ones and leave CU slots empty while working tiles wait,
+// which measured 20-40 % slower than the same number of working tiles
+// dispatched back to back.  Here every XCD x takes the heads h = x (mod 8)
+// (workgroups are dealt to the eight XCDs round-robin, so block 8k + x runs
+// on XCD x and a head's tiles share one L2), and its k-th block takes the
+// k-th working (slot, head) of those heads in slot-major order, then the
+// idle ones.  Needs B*H a multiple of 8 and at most 64 heads per XCD; the
+// launcher checks both.  All lanes return the same slot and head.
+__device__ __forceinline__ int nth_set_bit(uint64_t mask, int n) {
+    for (int t = 0; t < n; ++t) mask &= mask - 1;   // drop the n lowest set bits
+    return __builtin_ctzll(mask);
+}
+
+__device__ __forceinline__ void work_first_tile(int id, int nslots, int nsplit, int key_rows,
+                                                int BH, int H, int Lk,
+                                                const int32_t *__restrict__ key_len, int &slot,
+                                                int &head) {
+    const int lane = threadIdx.x & 63;
+    const int x = id & 7, k = id >> 3;
+    const int G = BH >> 3;                // heads of this XCD's group
+    const bool valid = lane < G;
+    const int klen = valid ? key_limit(key_len, (x + 8 * lane) / H, Lk) : 0;
+    int before = 0;
+    for (int pass = 0; pass < 2; ++pass) {   // working tiles, then idle ones
+        for (int s = 0; s < nslots; ++s) {
+            const bool works = (s / nsplit) * key_rows < klen;
+            const uint64_t m = __ballot(valid && works == (pass == 0));
+            const int c = __popcll(m);
+            if (k < before + c) {
+                slot = s;
+                head = x + 8 * nth_set_bit(m, k - before);
+                return;
+            }
+            before += c;
+        }
+    }
+    slot = 0;   // not reached: the grid holds exactly nslots * B*H blocks
+    head = x;
+}
+
+// The forward's version: every query tile of a non-causal key-padded head
+// costs ceil(key length / key_rows) key tiles, so the k-th block of XCD x
+// takes its heads' (slot, head) pairs by decreasing cost (head by head within
+// one cost), and the short ones fill in at the end (a longest-first list
+// schedule per XCD).  Same requirements as work_first_tile.
+__device__ __forceinline__ void heavy_first_tile(int id, int nslots, int key_rows, int BH, int H,
+                                                 int Lk, const int32_t *__restrict__ key_len,
+                                                 int &slot, int &head) {
+    const int lane = threadIdx.x & 63;
+    const int x = id & 7, k = id >> 3;
+    const int G = BH >> 3;
+    const bool valid = lane < G;
+    const int klen = valid ? key_limit(key_len, (x + 8 * lane) / H, Lk) : 0;
+    const int cost = (klen + key_rows - 1) / key_rows;
+    int before = 0;
+    for (int v = (Lk + key_rows - 1) / key_rows; v >= 0; --v) {
+        const uint64_t m = __ballot(valid && cost == v);
+        const int c = __popcll(m) * nslots;
+        if (k < before + c) {
+            const int j = k - before;
+            head = x + 8 * nth_set_bit(m, j / nslots);
+            slot = j % nslots;
+            return;
+        }
+        before += c;
+    }
+    slot = 0;   // not reached
+    head = x;
+}
+
 // ---------------------------------------------------------------- forward --
 // Query tile of C::ROWS rows stationary (16 per wave); 64-key K and V tiles
 // stream through LDS by direct-to-LDS loads.  The next K tile is fetched
@@ -112,7 +186,7 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::templa
 void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
                   const float *__restrict__ V, float *__restrict__ O, float *__restrict__ LSE,
                   const int32_t *__restrict__ key_len, int H, int Lq, int Lk, int causal,
-                  float scale_log2, int n_qtiles, int BH, int layer) {
+                  float scale_log2, int n_qtiles, int BH, int layer, int work_first) {
     constexpr int KS = kFwdStream;
     constexpr int DQ = D / 4;    // contraction values per lane in one S chain
     constexpr int NC = D / 16;   // 16-column blocks of the head dimension
@@ -123,8 +197,13 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
     __shared__ __attribute__((aligned(16))) float Ks[KS * D];
     __shared__ __attribute__((aligned(16))) float Vs[KS * D];
 
-    const int slot = blockIdx.x / BH;
-    const int head = blockIdx.x - slot * BH;
+    int slot, head;
+    if (work_first) {
+        heavy_first_tile(blockIdx.x, n_qtiles, KS, BH, H, Lk, key_len, slot, head);
+    } else {
+        slot = blockIdx.x / BH;
+        head = blockIdx.x - slot * BH;
+    }
     const int rank = serpentine_rank(slot, n_qtiles, layer);
     const int qt = causal ? (n_qtiles - 1 - rank) : rank;
     const int b = head / H;
@@ -516,7 +595,7 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
                     float *__restrict__ dK, float *__restrict__ dV, float *__restrict__ dQp,
                     float *__restrict__ dKVp, const int32_t *__restrict__ key_len, int H, int Lq,
                     int Lk, int causal, float scale, float scale_log2, int BH, int nsplit,
-                    int nranks, int layer) {
+                    int nranks, int layer, int work_first) {
     constexpr int DQ = D / 4;
     constexpr int NC = D / 16;
     constexpr int BR = 16 * NIB;
@@ -533,8 +612,13 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     __shared__ __attribute__((aligned(16))) float Kt[D][KR + 4];    // key tile, transposed
     __shared__ __attribute__((aligned(16))) float dSs[BR][KR + 4];  // dS of the query tile
 
-    const int slot = blockIdx.x / BH;
-    const int head = blockIdx.x - slot * BH;
+    int slot, head;
+    if (work_first) {
+        work_first_tile(blockIdx.x, nranks, nsplit, C::ROWS, BH, H, Lk, key_len, slot, head);
+    } else {
+        slot = blockIdx.x / BH;
+        head = blockIdx.x - slot * BH;
+    }
     const int rank = serpentine_rank(slot, nranks, layer);
     const int kt = rank / nsplit;          // key tile
     const int split = rank - kt * nsplit;  // share of its query tiles
@@ -957,6 +1041,14 @@ void attn_dq_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
+// Key-padded non-causal grids take the XCD-grouped work orders
+// (heavy_first_tile, work_first_tile) when the heads split evenly over the
+// eight XCDs, at most 64 per XCD.
+inline int padded_work_order(const AttnProblem &p) {
+    const int BH = p.B * p.H;
+    return (p.key_len != nullptr && !p.causal && BH % 8 == 0 && BH <= 512) ? 1 : 0;
+}
+
 }  // namespace
 
 // ---------------------------------------------------------------- launchers
@@ -970,7 +1062,7 @@ hipError_t launch_fwd_f32(const AttnProblem &p, const float *Q, const float *K,
     auto go = [&](auto kern) {
         const int ly = causal_rank_layer((const void *)kern, C::NT, grid.x, BH, p.causal);
         kern<<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal, sl2,
-                                    nqt, BH, ly);
+                                    nqt, BH, ly, padded_work_order(p));
     };
     switch (p.d) {
     case 32: go(attn_fwd_f32<32, C>); break;
@@ -1060,7 +1152,8 @@ static hipError_t launch_dkdvq(const AttnProblem &p, const float *Q, const float
     auto go = [&](auto kern) {
         const int ly = causal_rank_layer((const void *)kern, C::NT, grid.x, BH, p.causal);
         kern<<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, dKVp, p.key_len, p.H,
-                                    p.Lq, p.Lk, p.causal, p.scale, sl2, BH, ns, nr, ly);
+                                    p.Lq, p.Lk, p.causal, p.scale, sl2, BH, ns, nr, ly,
+                                    padded_work_order(p));
     };
     switch (p.d) {
     case 32: go(attn_dkdvq_f32<32, NIB, C>); break;
