@@ -1043,10 +1043,12 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 // Key-padded non-causal grids take the XCD-grouped work orders
 // (heavy_first_tile, work_first_tile) when the heads split evenly over the
-// eight XCDs, at most 64 per XCD.
+// eight XCDs, at most 64 per XCD, and the per-workgroup search (one ballot
+// per key tile) stays short: at most 1024 key tiles.
 inline int padded_work_order(const AttnProblem &p) {
     const int BH = p.B * p.H;
-    return (p.key_len != nullptr && !p.causal && BH % 8 == 0 && BH <= 512) ? 1 : 0;
+    return (p.key_len != nullptr && !p.causal && BH % 8 == 0 && BH <= 512 &&
+            p.Lk <= 1024 * 64) ? 1 : 0;
 }
 
 }  // namespace
