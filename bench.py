@@ -147,7 +147,8 @@ def query_splits(w):
     grid = -(-w.key_length // fused_key_rows(w)) * w.B * w.H
     if grid >= 512:
         return 1
-    return max(1, min(-(-1024 // grid), -(-w.L // 32) // 4))
+    nqt = -(-w.L // 32)
+    return max(1, min(-(-1024 // grid), nqt // (2 if nqt <= 8 else 4)))
 
 
 def partial_rows(w, key_len):

@@ -102,8 +102,9 @@ mg_status_t mg_attn_fwd(const void *Q, const void *K, const void *V,
  * When ceil(L/T)*B*H < 512 (too few key tiles to fill the GPU), the query
  * tiles of each key tile are split over S workgroups and 2*S*B*H*L*d more
  * f32 hold their dK and dV partials (S = min(ceil(1024 / (ceil(L/T)*B*H)),
- * floor(ceil(L/32) / 4)), no partials when S <= 1), each region starting on
- * a 256-byte boundary.  Returns 0 when the arguments are invalid.
+ * floor(n / m)) with n = ceil(L/32) query tiles and m = 2 when n <= 8, else
+ * m = 4; no partials when S <= 1), each region starting on a 256-byte
+ * boundary.  Returns 0 when the arguments are invalid.
  */
 size_t mg_attn_bwd_workspace_bytes(int B, int H, int L, int d, int causal,
                                    mg_contract_t contract);

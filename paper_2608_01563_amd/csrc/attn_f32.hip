@@ -1137,7 +1137,10 @@ int fused_dq_query_splits(const AttnProblem &p) {
     if (grid >= MG_DKDV_SPLIT_BELOW) return 1;
     const int br = 16 * (wide_key_tiles(p) ? MG_DKDVQ_CAUSAL_NIB : MG_DKDV_NIB);
     const long by_grid = (MG_DKDV_SPLIT_TARGET + grid - 1) / grid;
-    const long by_tiles = cdiv(p.Lq, br) / MG_DKDV_SPLIT_MIN_TILES;
+    // short query sides (at most 8 tiles) split down to 2 tiles per share:
+    // each share is then latency-bound, and finer shares measured faster
+    const int nqt = cdiv(p.Lq, br);
+    const long by_tiles = nqt / (nqt <= 8 ? 2 : MG_DKDV_SPLIT_MIN_TILES);
     return (int)std::max(1L, std::min(by_grid, by_tiles));
 }
 

@@ -65,9 +65,10 @@ def test_workspace_query(lib):
     assert mg.mg_attn_bwd_workspace_bytes(8, 8, 8192, 64, 0, 0) == 8 * 8 * 8192 * 4
     assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 32, 0, 0) == 256 + 3 * 32 * 4
     # causal but too few 128-key tiles: 64-key tiles (B4 H4 L256 -> 4 tiles);
-    # 64 workgroups split each key tile's 8 query tiles in S = min(16, 8/4) = 2
+    # 64 workgroups split each key tile's 8 query tiles (a short query side:
+    # shares down to 2 tiles) in S = min(16, 8/2) = 4
     assert mg.mg_attn_bwd_workspace_bytes(4, 4, 256, 64, 1, 0) == \
-        4096 * 4 + 4 * 4096 * 64 * 4 + 2 * 2 * 16 * 256 * 64 * 4
+        4096 * 4 + 4 * 4096 * 64 * 4 + 2 * 4 * 16 * 256 * 64 * 4
     assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 48, 0, 0) == 0     # unsupported d
     assert mg.mg_attn_bwd_workspace_bytes(0, 1, 3, 32, 0, 0) == 0     # bad size
     assert mg.mg_attn_bwd_workspace_bytes(1, 1, 3, 32, 0, 7) == 0     # bad contract
