@@ -43,6 +43,7 @@
 // the comparison on tiles that hold no masked element.
 #include <algorithm>
 #include <climits>
+#include <type_traits>
 
 #include "device_common.h"
 #include "launch.h"
@@ -812,22 +813,35 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
         if (NB == 1 && qt + 1 < qstop) fetch(qt + 1, 0);
 
         // dQ_part^T[16c + 4g + r][16ib + il] = sum_j K^T[16c + il'][j] dS^T[j][16ib + il]
+        // over the 16-key blocks that hold an allowed key for some row of the
+        // tile (the rest of dS is zero: past the key length, or past the
+        // tile's last row under a causal mask)
+        int qblocks = min(KR / 16, (klen - k0 + 15) / 16);
+        if (causal) qblocks = min(qblocks, max(0, qt * BR + BR - 1 + diag - k0) / 16 + 1);
+        // (full tiles keep a loop without exits, which the compiler schedules freely)
+        auto dq_product = [&](auto full) {
 #pragma unroll
-        for (int bb = 0; bb < PER_WAVE; ++bb) {
-            const int blk = dq_block(bb);
-            if (NBLK % C::NW != 0 && blk >= NBLK) break;
-            const int ib = blk / NC;
-            const int c = blk - ib * NC;
-            f32x4 acc = zero4();
+            for (int bb = 0; bb < PER_WAVE; ++bb) {
+                const int blk = dq_block(bb);
+                if (NBLK % C::NW != 0 && blk >= NBLK) break;
+                const int ib = blk / NC;
+                const int c = blk - ib * NC;
+                f32x4 acc = zero4();
 #pragma unroll
-            for (int q = 0; q < KR / 16; ++q) {
-                const f32x4 bv = *reinterpret_cast<const f32x4 *>(&dSs[16 * ib + il][16 * q + 4 * g]);
-                const f32x4 av = *reinterpret_cast<const f32x4 *>(&Kt[16 * c + il][16 * q + 4 * g]);
+                for (int q = 0; q < KR / 16; ++q) {
+                    if (!decltype(full)::value && q >= qblocks) break;
+                    const f32x4 bv = *reinterpret_cast<const f32x4 *>(&dSs[16 * ib + il][16 * q + 4 * g]);
+                    const f32x4 av = *reinterpret_cast<const f32x4 *>(&Kt[16 * c + il][16 * q + 4 * g]);
 #pragma unroll
-                for (int e = 0; e < 4; ++e) acc = mfma16x16x4(av[e], bv[e], acc);
+                    for (int e = 0; e < 4; ++e) acc = mfma16x16x4(av[e], bv[e], acc);
+                }
+                dqacc[bb] = acc;
             }
-            dqacc[bb] = acc;
-        }
+        };
+        if (qblocks == KR / 16)
+            dq_product(std::true_type{});
+        else
+            dq_product(std::false_type{});
 
         if (qt + 1 < qstop) wait_vmcnt<0>();   // next Q/dO tile and its LSE/D landed
         __syncthreads();   // next tile visible; dS and this tile's buffer free
