@@ -261,3 +261,26 @@ def test_mfma_probe_rejects_bad_arguments_before_any_device_call(lib):
     assert lib.mg_mfma_peak(0, (1 << 24) + 1, ctypes.byref(out), None) == 1
     assert lib.mg_mfma_peak(1, 100, None, None) == 1
     assert mg.mg_last_error_detail() != ""
+
+
+def test_error_detail_is_per_thread(lib):
+    """mg_last_error_detail describes the calling thread's last call only."""
+    import threading
+    seen = {}
+
+    def fresh():
+        seen["fresh"] = mg.mg_last_error_detail()
+
+    def failing():
+        assert _fwd(lib, GOOD, d=48) == 2
+        seen["own"] = mg.mg_last_error_detail()
+
+    assert _fwd(lib, GOOD, B=0) == 1
+    mine = mg.mg_last_error_detail()
+    for target in (fresh, failing):
+        t = threading.Thread(target=target)
+        t.start()
+        t.join()
+    assert seen["fresh"] == ""
+    assert seen["own"] != "" and seen["own"] != mine
+    assert mg.mg_last_error_detail() == mine   # untouched by the other threads
