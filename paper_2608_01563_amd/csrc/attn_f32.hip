@@ -6,6 +6,10 @@
 //
 //   attn_fwd_f32      query tile stationary, streams K/V tiles, online
 //                     softmax in base 2, writes O and LSE (natural log).
+//   attn_fwd_f32_ks2  the same for grids too small to spread evenly over
+//                     the CUs: 32-row query tiles, whose key tiles are split
+//                     between two halves of the workgroup; the halves merge
+//                     their (max, sum, O) states through LDS at the end.
 //   attn_rowdot_f32   D_i = sum_k dO_ik O_ik (HBM-bound row reduction).
 //   attn_dkdv_f32     key tile stationary: recomputes P from LSE, then
 //                     dV += P^T dO, dP = dO V^T, dS = P(dP - D), dK += dS^T Q.
@@ -80,6 +84,15 @@ namespace mg {
 namespace {
 
 constexpr int kStream = 64;   // streamed rows per step
+#ifndef MG_FWD_SPLIT_CFG
+#define MG_FWD_SPLIT_CFG 2, 3, false
+#endif
+#ifndef MG_FWD_SPLIT_KS
+#define MG_FWD_SPLIT_KS 32
+#endif
+#ifndef MG_FWD_SPLIT_BELOW
+#define MG_FWD_SPLIT_BELOW 512   // forward grids below this split their key tiles in two
+#endif
 #ifndef MG_FWD_KS
 #define MG_FWD_KS 64
 #endif
@@ -96,6 +109,7 @@ struct Cfg {
     static constexpr int NBUF = DB_ ? 2 : 1;   // LDS buffers for the streamed tile
 };
 using FwdCfg = Cfg<MG_FWD_CFG>;
+using FwdSplitCfg = Cfg<MG_FWD_SPLIT_CFG>;   // 32-row tiles, keys split in two
 using DkdvCfg = Cfg<MG_DKDV_CFG>;
 using DkdvqCausalCfg = Cfg<MG_DKDVQ_CAUSAL_CFG>;
 using DqCfg = Cfg<MG_DQ_CFG>;
@@ -182,21 +196,25 @@ __device__ __forceinline__ void heavy_first_tile(int id, int nslots, int key_row
 // registers:
 //   S(kt) from K | wait V(kt), barrier | fetch K(kt+1) | softmax, P V(kt)
 //   | wait K(kt+1), barrier | fetch V(kt+1)
-template <int D, class C>
-__global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::template occ<D>(), 8)))
-void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
+template <int D, class C, int KSPLIT>
+__device__ __forceinline__ void fwd_f32_body(const float *__restrict__ Q, const float *__restrict__ K,
                   const float *__restrict__ V, float *__restrict__ O, float *__restrict__ LSE,
                   const int32_t *__restrict__ key_len, int H, int Lq, int Lk, int causal,
                   float scale_log2, int n_qtiles, int BH, int layer, int work_first) {
-    constexpr int KS = kFwdStream;
+    // keys per streamed tile (the split form streams shorter tiles, so that
+    // four of its workgroups fit in one CU's LDS)
+    constexpr int KS = (KSPLIT > 1) ? MG_FWD_SPLIT_KS : kFwdStream;
     constexpr int DQ = D / 4;    // contraction values per lane in one S chain
     constexpr int NC = D / 16;   // 16-column blocks of the head dimension
     constexpr int NJB = KS / 16; // 16-key blocks per streamed tile
     using Tile = DirectTile<KS, D, C::NW>;
     static_assert(Tile::kEven, "the vmcnt waits below count kPerWave loads per fetch");
     constexpr int NL = Tile::kPerWave;   // vector-memory operations per tile fetch
-    __shared__ __attribute__((aligned(16))) float Ks[KS * D];
-    __shared__ __attribute__((aligned(16))) float Vs[KS * D];
+    static_assert(KSPLIT == 1 || (KSPLIT == 2 && C::NW * NC * 256 <= KS * D),
+                  "half 1's O must fit in its K tile");
+    __shared__ __attribute__((aligned(16))) float Ks[KSPLIT][KS * D];
+    __shared__ __attribute__((aligned(16))) float Vs[KSPLIT][KS * D];
+    __shared__ float xml[KSPLIT > 1 ? 2 * C::NW * 64 : 1];   // key split: m, l of half 1
 
     int slot, head;
     if (work_first) {
@@ -215,7 +233,9 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
-    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wg = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int hh = (KSPLIT > 1) ? wg / C::NW : 0;   // key half of this wave
+    const int w = (KSPLIT > 1) ? wg - hh * C::NW : wg;   // row wave within its half
     const int il = lane & 15;
     const int g = lane >> 4;
     const int q0 = qt * C::ROWS;
@@ -225,6 +245,14 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
     const int klen = key_limit(key_len, b, Lk);
     const int kend = causal ? min(klen, q0 + C::ROWS + diag) : klen;
     const int ntiles = (kend + KS - 1) / KS;
+    // Key split: half 0 takes the first ceil(n/2) key tiles, half 1 the
+    // rest; both run ceil(n/2) iterations so that every barrier is reached
+    // by all waves (half 1's surplus iteration only waits).
+    const int iters = (KSPLIT > 1) ? (ntiles + 1) / 2 : ntiles;
+    const int tbeg = hh * iters;
+    const int tend = (KSPLIT > 1 && hh == 0) ? iters : ntiles;
+    float *const Ksh = Ks[hh];
+    float *const Vsh = Vs[hh];
 
     Tile tile;
     tile.init(w, lane);
@@ -237,9 +265,9 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
     for (int r = 0; r < 4; ++r)
 #pragma unroll
         for (int c = 0; c < NC; ++c) voffs[r][c] = Tile::at(4 * g + r, 16 * c + il);
-    if (ntiles > 0) {
-        tile.issue(Ks, Kh, 0, Lk, w);
-        tile.issue(Vs, Vh, 0, Lk, w);
+    if (tbeg < tend) {
+        tile.issue(Ksh, Kh, tbeg * KS, Lk, w);
+        tile.issue(Vsh, Vh, tbeg * KS, Lk, w);
     }
 
     // B operand of S^T = K Q^T: lane holds Q[qi][g*DQ + s] times
@@ -261,7 +289,9 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
     wait_vmcnt<NL>();   // K(0) landed (V(0) may still be in flight)
     __syncthreads();
-    for (int kt = 0; kt < ntiles; ++kt) {
+    for (int it = 0; it < iters; ++it) {
+        const int kt = tbeg + it;
+        const bool act = (KSPLIT == 1) || kt < tend;   // uniform over the half
         // 16-key blocks of this tile that hold an allowed key for some row
         // of this wave (a prefix: keys past the key length, or past the
         // wave's last row under a causal mask, are masked for every row).
@@ -269,7 +299,7 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
         // masked below and their probabilities are exactly zero.
         const int jt = kt * KS;
         const int kcut = causal ? min(klen, qw0 + 16 + diag) : klen;
-        const int nlive = min(NJB, (kcut - jt + 15) / 16);
+        const int nlive = act ? min(NJB, (kcut - jt + 15) / 16) : 0;
 
         // S^T[16jb + 4g + r][qi] = sum_k K[j][k] Q[qi][k]
         f32x4 sacc[NJB];
@@ -281,7 +311,7 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
                 f32x4 a[NJB];
 #pragma unroll
                 for (int jb = 0; jb < NJB; ++jb)
-                    a[jb] = *reinterpret_cast<const f32x4 *>(&Ks[koff[s4] + 16 * jb * D]);
+                    a[jb] = *reinterpret_cast<const f32x4 *>(&Ksh[koff[s4] + 16 * jb * D]);
 #pragma unroll
                 for (int e = 0; e < 4; ++e)
 #pragma unroll
@@ -295,7 +325,7 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
 #pragma unroll
                 for (int s4 = 0; s4 < DQ / 4; ++s4) {
                     const f32x4 a =
-                        *reinterpret_cast<const f32x4 *>(&Ks[koff[s4] + 16 * jb * D]);
+                        *reinterpret_cast<const f32x4 *>(&Ksh[koff[s4] + 16 * jb * D]);
 #pragma unroll
                     for (int e = 0; e < 4; ++e)
                         sacc[jb] = mfma16x16x4(a[e], qreg[4 * s4 + e], sacc[jb]);
@@ -304,66 +334,93 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
         }
         wait_vmcnt<0>();   // V(kt) landed
         __syncthreads();   // every wave is done with K(kt) and sees V(kt)
-        if (kt + 1 < ntiles) tile.issue(Ks, Kh, (kt + 1) * KS, Lk, w);
+        if (kt + 1 < tend) tile.issue(Ksh, Kh, (kt + 1) * KS, Lk, w);
 
-        // Element (jb, r) holds key j0 + 16jb + r, allowed iff that offset is
-        // below a per-lane threshold (key length; the query row if causal).
-        // Only tiles that reach past the key length or past the wave's first
-        // query row (causal) hold masked elements.
-        if (jt + KS > klen || (causal && jt + KS - 1 > qw0 + diag)) {
-            const int j0 = jt + 4 * g;
-            const int thr = causal ? min(klen - j0, qi + diag - j0 + 1) : klen - j0;
-#pragma unroll
-            for (int jb = 0; jb < NJB; ++jb)
-#pragma unroll
-                for (int r = 0; r < 4; ++r)
-                    sacc[jb][r] = (16 * jb + r < thr) ? sacc[jb][r] : -INFINITY;
-        }
-        float mx = -INFINITY;
-#pragma unroll
-        for (int jb = 0; jb < NJB; ++jb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sacc[jb][r]);
-        mx = max_over_groups(mx);
-        const float m_new = fmaxf(m_run, mx);
-        const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-        // Rescaling by 2^(m_run - m_new) is a multiplication by one on every
-        // lane whose maximum did not move; skip it when that holds wave-wide.
-        if (__any(m_new != m_run)) {
-            const float alpha = exp2_fast(m_run - m_use);
-            l_run *= alpha;
-#pragma unroll
-            for (int c = 0; c < NC; ++c) oacc[c] *= alpha;
-        }
-        m_run = m_new;
-        float psum = 0.f;
-#pragma unroll
-        for (int jb = 0; jb < NJB; ++jb)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const float p = exp2_fast(sacc[jb][r] - m_use);
-                sacc[jb][r] = p;
-                psum += p;
+        if (act) {
+            // Element (jb, r) holds key j0 + 16jb + r, allowed iff that offset is
+            // below a per-lane threshold (key length; the query row if causal).
+            // Only tiles that reach past the key length or past the wave's first
+            // query row (causal) hold masked elements.
+            if (jt + KS > klen || (causal && jt + KS - 1 > qw0 + diag)) {
+                const int j0 = jt + 4 * g;
+                const int thr = causal ? min(klen - j0, qi + diag - j0 + 1) : klen - j0;
+    #pragma unroll
+                for (int jb = 0; jb < NJB; ++jb)
+    #pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        sacc[jb][r] = (16 * jb + r < thr) ? sacc[jb][r] : -INFINITY;
             }
-        l_run += psum;
+            float mx = -INFINITY;
+    #pragma unroll
+            for (int jb = 0; jb < NJB; ++jb)
+    #pragma unroll
+                for (int r = 0; r < 4; ++r) mx = fmaxf(mx, sacc[jb][r]);
+            mx = max_over_groups(mx);
+            const float m_new = fmaxf(m_run, mx);
+            const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
+            // Rescaling by 2^(m_run - m_new) is a multiplication by one on every
+            // lane whose maximum did not move; skip it when that holds wave-wide.
+            if (__any(m_new != m_run)) {
+                const float alpha = exp2_fast(m_run - m_use);
+                l_run *= alpha;
+    #pragma unroll
+                for (int c = 0; c < NC; ++c) oacc[c] *= alpha;
+            }
+            m_run = m_new;
+            float psum = 0.f;
+    #pragma unroll
+            for (int jb = 0; jb < NJB; ++jb)
+    #pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const float p = exp2_fast(sacc[jb][r] - m_use);
+                    sacc[jb][r] = p;
+                    psum += p;
+                }
+            l_run += psum;
 
-        // O^T[16c + 4g + r][qi] += sum_j V[j][16c + il'] P^T[j][qi]
-#pragma unroll
-        for (int jb = 0; jb < NJB; ++jb) {
-            if (jb >= nlive) break;
-#pragma unroll
-            for (int r = 0; r < 4; ++r)
-#pragma unroll
-                for (int c = 0; c < NC; ++c)
-                    oacc[c] = mfma16x16x4(Vs[voffs[r][c] + 16 * jb * D], sacc[jb][r], oacc[c]);
+            // O^T[16c + 4g + r][qi] += sum_j V[j][16c + il'] P^T[j][qi]
+    #pragma unroll
+            for (int jb = 0; jb < NJB; ++jb) {
+                if (jb >= nlive) break;
+    #pragma unroll
+                for (int r = 0; r < 4; ++r)
+    #pragma unroll
+                    for (int c = 0; c < NC; ++c)
+                        oacc[c] = mfma16x16x4(Vsh[voffs[r][c] + 16 * jb * D], sacc[jb][r], oacc[c]);
+            }
         }
 
         wait_vmcnt<0>();   // K(kt+1) landed
         __syncthreads();   // every wave is done with V(kt) and sees K(kt+1)
-        if (kt + 1 < ntiles) tile.issue(Vs, Vh, (kt + 1) * KS, Lk, w);
+        if (kt + 1 < tend) tile.issue(Vsh, Vh, (kt + 1) * KS, Lk, w);
     }
 
-    const float l = sum_over_groups(l_run);
+    float l = sum_over_groups(l_run);
+    if constexpr (KSPLIT > 1) {
+        // Half 1 hands its (m, l, O) to half 0 through its own K tile, which
+        // no wave reads any more; half 0 merges the two online-softmax states.
+        float *xo = Ks[1];
+        float *xm = xml, *xl = xml + C::NW * 64;
+        if (hh == 1) {
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+                *reinterpret_cast<f32x4 *>(&xo[((w * NC + c) * 64 + lane) * 4]) = oacc[c];
+            xm[w * 64 + lane] = m_run;
+            xl[w * 64 + lane] = l;
+        }
+        __syncthreads();
+        if (hh == 1) return;
+        const float m1 = xm[w * 64 + lane];
+        const float mm = fmaxf(m_run, m1);
+        const float mu = (mm == -INFINITY) ? 0.f : mm;
+        const float a0 = exp2_fast(m_run - mu), a1 = exp2_fast(m1 - mu);
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+            oacc[c] = oacc[c] * a0 +
+                      *reinterpret_cast<const f32x4 *>(&xo[((w * NC + c) * 64 + lane) * 4]) * a1;
+        l = l * a0 + xl[w * 64 + lane] * a1;
+        m_run = mm;
+    }
     if (qi < Lq) {
         const float inv = (l > 0.f) ? 1.f / l : 0.f;
         float *orow = O + ((size_t)head * Lq + qi) * D;
@@ -374,6 +431,28 @@ void attn_fwd_f32(const float *__restrict__ Q, const float *__restrict__ K,
             LSE[(size_t)head * Lq + qi] = (l > 0.f) ? (m_run + log2f(l)) * kLn2 : -INFINITY;
     }
 }
+
+// The kernels: one workgroup per (query tile, head); the _ks2 form splits
+// the key tiles over two halves of the workgroup (grids too small to fill
+// the chip).
+#define MG_FWD_F32_ARGS                                                                    \
+    const float *__restrict__ Q, const float *__restrict__ K, const float *__restrict__ V, \
+        float *__restrict__ O, float *__restrict__ LSE, const int32_t *__restrict__ key_len, \
+        int H, int Lq, int Lk, int causal, float scale_log2, int n_qtiles, int BH, int layer, \
+        int work_first
+template <int D, class C>
+__global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::template occ<D>(), 8)))
+void attn_fwd_f32(MG_FWD_F32_ARGS) {
+    fwd_f32_body<D, C, 1>(Q, K, V, O, LSE, key_len, H, Lq, Lk, causal, scale_log2, n_qtiles, BH,
+                          layer, work_first);
+}
+template <int D, class C>
+__global__ __launch_bounds__(2 * C::NT) __attribute__((amdgpu_waves_per_eu(C::template occ<D>(), 8)))
+void attn_fwd_f32_ks2(MG_FWD_F32_ARGS) {
+    fwd_f32_body<D, C, 2>(Q, K, V, O, LSE, key_len, H, Lq, Lk, causal, scale_log2, n_qtiles, BH,
+                          layer, work_first);
+}
+#undef MG_FWD_F32_ARGS
 
 // ------------------------------------------------- backward: D = rowsum(dO o O)
 template <int D>
@@ -1068,22 +1147,44 @@ inline int padded_work_order(const AttnProblem &p) {
 }  // namespace
 
 // ---------------------------------------------------------------- launchers
-hipError_t launch_fwd_f32(const AttnProblem &p, const float *Q, const float *K,
-                          const float *V, float *O, float *LSE, hipStream_t s) {
-    using C = FwdCfg;
+namespace {
+template <class C, class Kern>
+void launch_fwd_f32_as(Kern kern, int ksplit, const AttnProblem &p, const float *Q,
+                       const float *K, const float *V, float *O, float *LSE, hipStream_t s) {
     const int BH = p.B * p.H;
     const int nqt = cdiv(p.Lq, C::ROWS);
-    const dim3 grid(nqt * BH), block(C::NT);
-    const float sl2 = p.scale * kLog2e;
-    auto go = [&](auto kern) {
-        const int ly = causal_rank_layer((const void *)kern, C::NT, grid.x, BH, p.causal);
-        kern<<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal, sl2,
-                                    nqt, BH, ly, padded_work_order(p));
-    };
+    const dim3 grid(nqt * BH), block(C::NT * ksplit);
+    const int ly = causal_rank_layer((const void *)kern, block.x, grid.x, BH, p.causal);
+    kern<<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal,
+                                p.scale * kLog2e, nqt, BH, ly, padded_work_order(p));
+}
+}  // namespace
+
+hipError_t launch_fwd_f32(const AttnProblem &p, const float *Q, const float *K,
+                          const float *V, float *O, float *LSE, hipStream_t s) {
+    // Grids of fewer than MG_FWD_SPLIT_BELOW workgroups of 64 rows fall
+    // unevenly on the CUs (288 of them on 256 CUs put two on 32 CUs, which
+    // then set the kernel's time).  There the query tiles shrink to 32 rows
+    // and each workgroup splits its key tiles over two halves: four times
+    // the workgroups, each a quarter of the work (d <= 64, two or more key tiles).
+    const long grid = (long)cdiv(p.Lq, FwdCfg::ROWS) * p.B * p.H;
+    const bool split = p.d <= 64 && grid < MG_FWD_SPLIT_BELOW && p.Lk > kFwdStream;
     switch (p.d) {
-    case 32: go(attn_fwd_f32<32, C>); break;
-    case 64: go(attn_fwd_f32<64, C>); break;
-    case 128: go(attn_fwd_f32<128, C>); break;
+    case 32:
+        if (split)
+            launch_fwd_f32_as<FwdSplitCfg>(attn_fwd_f32_ks2<32, FwdSplitCfg>, 2, p, Q, K, V, O,
+                                           LSE, s);
+        else
+            launch_fwd_f32_as<FwdCfg>(attn_fwd_f32<32, FwdCfg>, 1, p, Q, K, V, O, LSE, s);
+        break;
+    case 64:
+        if (split)
+            launch_fwd_f32_as<FwdSplitCfg>(attn_fwd_f32_ks2<64, FwdSplitCfg>, 2, p, Q, K, V, O,
+                                           LSE, s);
+        else
+            launch_fwd_f32_as<FwdCfg>(attn_fwd_f32<64, FwdCfg>, 1, p, Q, K, V, O, LSE, s);
+        break;
+    case 128: launch_fwd_f32_as<FwdCfg>(attn_fwd_f32<128, FwdCfg>, 1, p, Q, K, V, O, LSE, s); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

@@ -264,6 +264,24 @@ def test_wide_key_tiles_ragged(gpu_lib, d, padded):
     assert max(errs.values()) <= TOL["strict_f32"], errs
 
 
+@pytest.mark.parametrize("d,padded,neg", [(32, False, False), (64, True, False),
+                                           (64, False, True)])
+def test_unsplit_forward_cross_ragged(gpu_lib, d, padded, neg):
+    """Strict forward grids of 512 or more 64-row workgroups keep the unsplit
+    kernel (smaller grids split their key tiles); B*H = 64 heads of Lq = 520
+    queries over Lk = 333 keys give 576 workgroups with ragged query and key
+    tails, a negative scale in one case."""
+    B, H, Lq, Lk = 8, 8, 520, 333
+    kl = [333, 300, 65, 64, 1, 0, 200, 333] if padded else None
+    scale = (-1.0 if neg else 1.0) / d ** 0.5
+    say("unsplit forward B%d H%d Lq%d Lk%d d%d padded=%s scale=%.3f" % (B, H, Lq, Lk, d,
+                                                                         padded, scale))
+    x = make_inputs(B, H, Lq, d, causal=False, seed=131 + d, key_len=kl, scale=scale, Lk=Lk)
+    errs = compare(run_gpu(x), oracle_reference(x), "strict_f32")
+    say("  errors %s" % {k: "%.2e" % v for k, v in errs.items()})
+    assert max(errs.values()) <= TOL["strict_f32"], errs
+
+
 @pytest.mark.parametrize("contract,d", [("fast_bf16", 128), ("fast_bf16", 64),
                                         ("accelerated", 64)])
 def test_resident_causal_grid_ragged(gpu_lib, contract, d):
