@@ -434,7 +434,10 @@ __device__ __forceinline__ void fwd_f32_body(const float *__restrict__ Q, const 
 
 // The kernels: one workgroup per (query tile, head); the _ks2 form splits
 // the key tiles over two halves of the workgroup (grids too small to fill
-// the chip).
+// the chip).  Two named kernels over one device body: as one kernel template
+// with the split as a third parameter, hipcc (ROCm 7.2) emitted the host
+// launch stub of only one of the two instances per head size, and the
+// library failed to link.
 #define MG_FWD_F32_ARGS                                                                    \
     const float *__restrict__ Q, const float *__restrict__ K, const float *__restrict__ V, \
         float *__restrict__ O, float *__restrict__ LSE, const int32_t *__restrict__ key_len, \
