@@ -104,10 +104,12 @@ def kernel_work(name, w, pairs, rows, key_len=None):
     d, es = w.d, (4 if w.contract == "strict_f32" else 2)
     if name.startswith("attn_fwd"):
         return 4.0 * d * pairs, "flop", "mfma"
-    if name.startswith("attn_dkdvreduce"):
-        # reads S dK and S dV partials, writes dK and dV (all f32)
+    if name.startswith("attn_bwdreduce"):
+        # query-split fused backward: reads S dK and S dV partials and writes
+        # dK and dV (all f32), and reduces the dQ partials as attn_dqreduce
         n = w.B * w.H * w.key_length * d
-        return 4.0 * 2 * n * (query_splits(w) + 1), "byte", "hbm"
+        dq = 4.0 * d * partial_rows(w, key_len) + 4.0 * w.B * w.H * w.L * d
+        return 4.0 * 2 * n * (query_splits(w) + 1) + dq, "byte", "hbm"
     if name.startswith("attn_dkdvq"):
         return 10.0 * d * pairs, "flop", "mfma"       # S recompute, dV, dP, dK, dQ
     if name.startswith("attn_dkdv"):

@@ -932,7 +932,7 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
     // One split writes dK and dV directly; several write partials laid out
     // [dK, dV][split][B*H][Lk][d] (every split writes its rows, zeros for an
-    // empty share) for attn_dkdv_reduce_f32.
+    // empty share) for attn_bwd_reduce_f32.
     if (kj < Lk) {
         const bool keep = kj < klen;
         const size_t row = hoff + (size_t)kj * D;
@@ -948,12 +948,11 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
 }
 
 // dK and dV from the per-split partials of attn_dkdvq_f32, added in
-// increasing split order (a fixed order).  n4 = B*H*Lk*d / 4.
-__global__ __launch_bounds__(256) void attn_dkdv_reduce_f32(const float *__restrict__ dKVp,
-                                                            float *__restrict__ dK,
-                                                            float *__restrict__ dV,
-                                                            int nsplit, long n4) {
-    const long idx = (long)blockIdx.x * 256 + threadIdx.x;
+// increasing split order (a fixed order).  n4 = B*H*Lk*d / 4; idx runs over
+// the 2*n4 16-byte chunks of dK then dV.
+__device__ __forceinline__ void dkdv_reduce_at(long idx, const float *__restrict__ dKVp,
+                                               float *__restrict__ dK, float *__restrict__ dV,
+                                               int nsplit, long n4) {
     if (idx >= 2 * n4) return;
     const int t = idx >= n4;           // 0: dK, 1: dV
     const long e4 = idx - t * n4;
@@ -967,14 +966,12 @@ __global__ __launch_bounds__(256) void attn_dkdv_reduce_f32(const float *__restr
 // dQ_part[kt][i], added in increasing kt (a fixed order).  Partials are laid
 // out [key tile][B*H][Lq][d].
 template <int D>
-__global__ __launch_bounds__(256) void attn_dq_reduce_f32(const float *__restrict__ dQp,
-                                                          float *__restrict__ dQ,
-                                                          const int32_t *__restrict__ key_len,
-                                                          int H, int Lq, int Lk, int causal,
-                                                          float scale,
-                                                          int BH, int key_rows) {
+__device__ __forceinline__ void dq_reduce_at(size_t idx, const float *__restrict__ dQp,
+                                             float *__restrict__ dQ,
+                                             const int32_t *__restrict__ key_len, int H, int Lq,
+                                             int Lk, int causal, float scale, int BH,
+                                             int key_rows) {
     constexpr int C4 = D / 4;
-    const size_t idx = (size_t)blockIdx.x * 256 + threadIdx.x;
     const size_t total = (size_t)BH * Lq * C4;
     if (idx >= total) return;
     const size_t rowg = idx / C4;              // head * Lq + i
@@ -991,6 +988,31 @@ __global__ __launch_bounds__(256) void attn_dq_reduce_f32(const float *__restric
     for (int kt = 0; kt < kmax; ++kt)
         sum += *reinterpret_cast<const f32x4 *>(src + (size_t)kt * stride);
     *reinterpret_cast<f32x4 *>(dQ + idx * 4) = sum * scale;
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void attn_dq_reduce_f32(const float *__restrict__ dQp,
+                                                          float *__restrict__ dQ,
+                                                          const int32_t *__restrict__ key_len,
+                                                          int H, int Lq, int Lk, int causal,
+                                                          float scale, int BH, int key_rows) {
+    dq_reduce_at<D>((size_t)blockIdx.x * 256 + threadIdx.x, dQp, dQ, key_len, H, Lq, Lk, causal,
+                    scale, BH, key_rows);
+}
+
+// Both reductions of a query-split fused backward in one launch: the first
+// nb_kv workgroups add the dK/dV partials, the rest the dQ partials.
+template <int D>
+__global__ __launch_bounds__(256) void attn_bwd_reduce_f32(
+    const float *__restrict__ dKVp, float *__restrict__ dK, float *__restrict__ dV, int nsplit,
+    long n4, unsigned nb_kv, const float *__restrict__ dQp, float *__restrict__ dQ,
+    const int32_t *__restrict__ key_len, int H, int Lq, int Lk, int causal, float scale, int BH,
+    int key_rows) {
+    if (blockIdx.x < nb_kv)
+        dkdv_reduce_at((long)blockIdx.x * 256 + threadIdx.x, dKVp, dK, dV, nsplit, n4);
+    else
+        dq_reduce_at<D>((size_t)(blockIdx.x - nb_kv) * 256 + threadIdx.x, dQp, dQ, key_len, H,
+                        Lq, Lk, causal, scale, BH, key_rows);
 }
 
 // ------------------------------------------------------------ backward: dQ
@@ -1296,11 +1318,19 @@ hipError_t launch_bwd_dkdvq_f32(const AttnProblem &p, const float *Q, const floa
         : launch_dkdvq<DkdvCfg, MG_DKDV_NIB>(p, Q, K, V, dO, LSE, Dws, dK, dV, dQp, dKVp, s);
 }
 
-hipError_t launch_bwd_dkdv_reduce_f32(const AttnProblem &p, const float *dKVp, float *dK,
-                                      float *dV, hipStream_t s) {
-    const long n4 = (long)p.B * p.H * p.Lk * p.d / 4;
-    const dim3 grid((unsigned)((2 * n4 + 255) / 256)), block(256);
-    attn_dkdv_reduce_f32<<<grid, block, 0, s>>>(dKVp, dK, dV, fused_dq_query_splits(p), n4);
+hipError_t launch_bwd_reduce_f32(const AttnProblem &p, const float *dKVp, float *dK,
+                                 float *dV, const float *dQp, float *dQ, hipStream_t s) {
+    const int BH = p.B * p.H;
+    const long n4 = (long)BH * p.Lk * p.d / 4;
+    const unsigned nb_kv = (unsigned)((2 * n4 + 255) / 256);
+    const size_t total = (size_t)BH * p.Lq * (p.d / 4);
+    const dim3 grid(nb_kv + (unsigned)((total + 255) / 256)), block(256);
+    const int ns = fused_dq_query_splits(p), kr = fused_dq_key_rows(p);
+    switch (p.d) {
+    case 32: attn_bwd_reduce_f32<32><<<grid, block, 0, s>>>(dKVp, dK, dV, ns, n4, nb_kv, dQp, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, BH, kr); break;
+    case 64: attn_bwd_reduce_f32<64><<<grid, block, 0, s>>>(dKVp, dK, dV, ns, n4, nb_kv, dQp, dQ, p.key_len, p.H, p.Lq, p.Lk, p.causal, p.scale, BH, kr); break;
+    default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }
 

@@ -65,15 +65,16 @@ hipError_t launch_bwd_dkdv_bf16(const AttnProblem &p, const uint16_t *Q,
 // alone give too small a grid, each key tile's query tiles are split over
 // fused_dq_query_splits(p) workgroups, which write dK/dV partials to dKVp
 // ([dK, dV][split][B*H][Lk][d] f32; unused, may be null, with one split)
-// for launch_bwd_dkdv_reduce_f32 to add.
+// for launch_bwd_reduce_f32 to add, together with the dQ partials, in one
+// launch (launch_bwd_dq_reduce_f32 alone when there is one split).
 int fused_dq_key_rows(const AttnProblem &p);
 int fused_dq_query_splits(const AttnProblem &p);
 hipError_t launch_bwd_dkdvq_f32(const AttnProblem &p, const float *Q, const float *K,
                                 const float *V, const float *dO, const float *LSE,
                                 const float *Dws, float *dK, float *dV, float *dQp,
                                 float *dKVp, hipStream_t s);
-hipError_t launch_bwd_dkdv_reduce_f32(const AttnProblem &p, const float *dKVp, float *dK,
-                                      float *dV, hipStream_t s);
+hipError_t launch_bwd_reduce_f32(const AttnProblem &p, const float *dKVp, float *dK,
+                                 float *dV, const float *dQp, float *dQ, hipStream_t s);
 hipError_t launch_bwd_dq_reduce_f32(const AttnProblem &p, const float *dQp, float *dQ,
                                     hipStream_t s);
 

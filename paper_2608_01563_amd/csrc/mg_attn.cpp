@@ -173,13 +173,14 @@ mg_status_t mg_attn_bwd_cross(const void *Q, const void *K, const void *V, const
                                                 (float *)dV, dQp, dKVp, stream);
             }));
             if (dKVp != nullptr)
-                MG_TRY(run_kernel(kernel_name("attn_dkdvreduce", contract, d), stream, [&] {
-                    return mg::launch_bwd_dkdv_reduce_f32(p, dKVp, (float *)dK, (float *)dV,
-                                                          stream);
+                MG_TRY(run_kernel(kernel_name("attn_bwdreduce", contract, d), stream, [&] {
+                    return mg::launch_bwd_reduce_f32(p, dKVp, (float *)dK, (float *)dV, dQp,
+                                                     (float *)dQ, stream);
                 }));
-            MG_TRY(run_kernel(kernel_name("attn_dqreduce", contract, d), stream, [&] {
-                return mg::launch_bwd_dq_reduce_f32(p, dQp, (float *)dQ, stream);
-            }));
+            else
+                MG_TRY(run_kernel(kernel_name("attn_dqreduce", contract, d), stream, [&] {
+                    return mg::launch_bwd_dq_reduce_f32(p, dQp, (float *)dQ, stream);
+                }));
             return ok();
         }
         MG_TRY(run_kernel(kernel_name("attn_dkdv", contract, d), stream, [&] {
