@@ -189,8 +189,9 @@ __device__ __forceinline__ void heavy_first_tile(int id, int nslots, int key_row
 }
 
 // ---------------------------------------------------------------- forward --
-// Query tile of C::ROWS rows stationary (16 per wave); 64-key K and V tiles
-// stream through LDS by direct-to-LDS loads.  The next K tile is fetched
+// Query tile of C::ROWS rows stationary (16 per wave); K and V tiles of KS
+// keys (64; 32 in the key-split form, one pair per half) stream through LDS
+// by direct-to-LDS loads.  The next K tile is fetched
 // while the softmax and P V of the current tile run, the next V tile while
 // the next S = K Q^T runs, so each iteration has two barriers and no staging
 // registers:
