@@ -411,38 +411,78 @@ def warm_up(step, args, torch):
 
 def environment():
     """GPU name, HIP/torch versions, the source revision and the GPU clocks
-    as the driver reports them (each null when unavailable)."""
-    import subprocess
+    (each null when unavailable).  Nothing here starts a child process: the
+    revision is read from .git when the tree has one, else it is the digest
+    of the kernel sources, and the clocks come from the driver's sysfs
+    files."""
     import torch
-    env = {"gpu": torch.cuda.get_device_name(0), "hip": torch.version.hip,
-           "torch": torch.__version__, "git_revision": None, "clocks": None}
-    try:
-        r = subprocess.run(["git", "-C", ROOT, "rev-parse", "--short", "HEAD"],
-                           capture_output=True, text=True, timeout=10)
-        env["git_revision"] = r.stdout.strip() or None
-    except (OSError, subprocess.SubprocessError):
-        pass
-    if under_profiler():
-        # rocm-smi is a script started through `env`; with the profiler's
-        # library preloaded, that hop would initialise the GPU and then exec
-        return env
-    try:
-        r = subprocess.run(["rocm-smi", "--showclocks"], capture_output=True, text=True,
-                           timeout=20)
-        lines = [l.strip() for l in r.stdout.splitlines() if "sclk" in l or "mclk" in l]
-        env["clocks"] = lines[:4] or None
-    except (OSError, subprocess.SubprocessError):
-        pass
-    return env
+    return {"gpu": torch.cuda.get_device_name(0), "hip": torch.version.hip,
+            "torch": torch.__version__, "git_revision": source_revision(),
+            "clocks": gpu_clocks(torch)}
 
 
-def under_profiler():
-    """True when a rocprofiler library is mapped into this process."""
+def source_revision():
+    """'git:<commit>' from .git/HEAD (a loose or packed ref, or a detached
+    commit), else 'src-sha256:<digest of the kernel sources>' for a copy of
+    the tree without its history."""
+    git = os.path.join(ROOT, ".git")
     try:
-        with open("/proc/self/maps") as f:
-            return "rocprofiler" in f.read()
+        with open(os.path.join(git, "HEAD")) as f:
+            head = f.read().strip()
+        if head.startswith("ref: "):
+            ref = head[5:]
+            path = os.path.join(git, ref)
+            if os.path.isfile(path):
+                with open(path) as f:
+                    return "git:" + f.read().strip()[:12]
+            with open(os.path.join(git, "packed-refs")) as f:
+                for line in f:
+                    parts = line.split()
+                    if len(parts) == 2 and parts[1] == ref:
+                        return "git:" + parts[0][:12]
+        elif head:
+            return "git:" + head[:12]
     except OSError:
-        return False
+        pass
+    return "src-sha256:" + kernel_source_digest()[:16]
+
+
+def gpu_clocks(torch):
+    """The amdgpu driver's clock levels (pp_dpm_sclk, pp_dpm_mclk,
+    pp_dpm_fclk: the active level ends in '*') for the card at device 0's
+    PCI address when torch reports it, else for every card listed; keyed by
+    PCI address.  None when no such file is readable."""
+    import glob
+    import re
+    want = None
+    try:
+        pr = torch.cuda.get_device_properties(0)
+        bus, dev = getattr(pr, "pci_bus_id", None), getattr(pr, "pci_device_id", None)
+        if bus is not None and dev is not None:
+            want = "%04x:%02x:%02x" % (getattr(pr, "pci_domain_id", 0) or 0, bus, dev)
+    except (RuntimeError, AttributeError, TypeError):
+        pass
+    out = {}
+    for card in sorted(glob.glob("/sys/class/drm/card*")):
+        if not re.search(r"card\d+$", card):
+            continue
+        dev_dir = os.path.join(card, "device")
+        addr = os.path.basename(os.path.realpath(dev_dir))
+        if want is not None and not addr.startswith(want):
+            continue
+        ent = {}
+        for name in ("sclk", "mclk", "fclk"):
+            try:
+                with open(os.path.join(dev_dir, "pp_dpm_" + name)) as f:
+                    levels = [l.strip() for l in f if l.strip()]
+            except OSError:
+                continue
+            active = [l for l in levels if l.endswith("*")]
+            ent[name] = active[0] if active else None
+            ent[name + "_levels"] = levels
+        if ent:
+            out[addr] = ent
+    return out or None
 
 
 def cpu_baseline(args, w, x, pairs, gpu_outputs):

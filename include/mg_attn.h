@@ -62,10 +62,18 @@
 extern "C" {
 #endif
 
+/*
+ * Both enums span the whole range of int (the two range markers are not
+ * values any call accepts): a caller may pass any int, and the library
+ * rejects an unknown contract with MG_ERR_INVALID_ARGUMENT instead of
+ * receiving a value its own type cannot hold.
+ */
 typedef enum {
     MG_CONTRACT_STRICT_F32 = 0,
     MG_CONTRACT_FAST_BF16 = 1,
-    MG_CONTRACT_ACCELERATED = 2
+    MG_CONTRACT_ACCELERATED = 2,
+    MG_CONTRACT_RANGE_MIN_ = (-0x7fffffff - 1),
+    MG_CONTRACT_RANGE_MAX_ = 0x7fffffff
 } mg_contract_t;
 
 typedef enum {
@@ -76,7 +84,9 @@ typedef enum {
     MG_ERR_UNSUPPORTED = 2,      /* head dimension d not in {32, 64, 128}   */
     MG_ERR_MISALIGNED = 3,       /* a tensor pointer not 16-byte aligned    */
     MG_ERR_WORKSPACE = 4,        /* backward workspace missing or too small */
-    MG_ERR_HIP = 5               /* a HIP runtime call or launch failed     */
+    MG_ERR_HIP = 5,              /* a HIP runtime call or launch failed     */
+    MG_STATUS_RANGE_MIN_ = (-0x7fffffff - 1),
+    MG_STATUS_RANGE_MAX_ = 0x7fffffff
 } mg_status_t;
 
 /*

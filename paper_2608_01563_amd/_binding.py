@@ -122,6 +122,26 @@ def _stream_handle(stream):
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def _alloc_stream(stream):
+    """Context in which torch allocates memory for work enqueued on `stream`.
+
+    The caching allocator ties a block to the stream current at allocation;
+    a block freed by Python is handed out again only to later allocations
+    on that stream, which are ordered after the kernels that use it.
+    Allocating a workspace or an output on another stream than the one the
+    kernels run on would let the next allocation there reuse the block while
+    those kernels still write to it."""
+    import contextlib
+    import torch
+    return contextlib.nullcontext() if stream is None else torch.cuda.stream(stream)
+
+
+def _empty_bytes(nbytes, device, stream):
+    import torch
+    with _alloc_stream(stream):
+        return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
 def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
@@ -196,7 +216,6 @@ def mg_attn_bwd(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len=None, *, causal, scale,
     """Backward pass into caller-provided dQ, dK, dV.  `workspace` is a GPU
     tensor of at least mg_attn_bwd_workspace_bytes(...) bytes; when None, one
     is allocated here with torch (the library itself never allocates)."""
-    import torch
     lib = load_library()
     c = _contract_id(contract)
     if Q.dim() != 4:
@@ -208,7 +227,7 @@ def mg_attn_bwd(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len=None, *, causal, scale,
     _check_key_len(key_len, B)
     need = mg_attn_bwd_workspace_bytes(B, H, L, d, causal, c)
     if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=Q.device)
+        workspace = _empty_bytes(need, Q.device, stream)
     nbytes = workspace.numel() * workspace.element_size()
     _check(lib.mg_attn_bwd(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(LSE), _ptr(dO), _ptr(dQ),
                            _ptr(dK), _ptr(dV), _ptr(key_len), B, H, L, d, int(bool(causal)),
@@ -242,7 +261,6 @@ def mg_attn_bwd_cross(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len=None, *, causal, 
     """Cross-attention backward: Q, O, dO, dQ [B,H,Lq,d]; K, V, dK, dV
     [B,H,Lk,d].  `workspace` as for mg_attn_bwd (sized by
     mg_attn_bwd_cross_workspace_bytes)."""
-    import torch
     lib = load_library()
     c = _contract_id(contract)
     B, H, Lq, Lk, d = _cross_shapes(Q, K)
@@ -252,7 +270,7 @@ def mg_attn_bwd_cross(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len=None, *, causal, 
     _check_key_len(key_len, B)
     need = mg_attn_bwd_cross_workspace_bytes(B, H, Lq, Lk, d, causal, c)
     if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=Q.device)
+        workspace = _empty_bytes(need, Q.device, stream)
     nbytes = workspace.numel() * workspace.element_size()
     _check(lib.mg_attn_bwd_cross(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(LSE), _ptr(dO),
                                  _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(key_len), B, H, Lq, Lk, d,
@@ -296,7 +314,6 @@ def mg_conv2d_bwd_data(dY, W, dX, *, stride=(1, 1), pad=(0, 0), contract=STRICT_
     """Data gradient into caller-provided dX [N,H,W,C] (channels-last).
     `workspace` as for mg_attn_bwd (allocated here with torch when None and
     needed)."""
-    import torch
     lib = load_library()
     shape = conv_shape(dX.shape, W.shape, stride, pad)
     P, Q = conv_out_hw(shape)
@@ -304,7 +321,7 @@ def mg_conv2d_bwd_data(dY, W, dX, *, stride=(1, 1), pad=(0, 0), contract=STRICT_
                 ("dX", dX, tuple(dX.shape))))
     need = mg_conv2d_bwd_data_workspace_bytes(dX.shape, W.shape, stride, pad, contract)
     if workspace is None and need > 0:
-        workspace = torch.empty(need, dtype=torch.uint8, device=dX.device)
+        workspace = _empty_bytes(need, dX.device, stream)
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib.mg_conv2d_bwd_data(_ptr(dY), _ptr(W), _ptr(dX), ctypes.byref(shape),
                                   _contract_id(contract), _ptr(workspace), nbytes,
@@ -322,7 +339,6 @@ def mg_conv2d_bwd_filter(X, dY, dW, *, stride=(1, 1), pad=(0, 0), contract=STRIC
                          workspace=None, stream=None):
     """Filter gradient into caller-provided dW [K,R,S,C].  `workspace` as for
     mg_attn_bwd (allocated here with torch when None and needed)."""
-    import torch
     lib = load_library()
     shape = conv_shape(X.shape, dW.shape, stride, pad)
     P, Q = conv_out_hw(shape)
@@ -330,7 +346,7 @@ def mg_conv2d_bwd_filter(X, dY, dW, *, stride=(1, 1), pad=(0, 0), contract=STRIC
                 ("dW", dW, tuple(dW.shape))))
     need = mg_conv2d_bwd_filter_workspace_bytes(X.shape, dW.shape, stride, pad, contract)
     if workspace is None and need > 0:
-        workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
+        workspace = _empty_bytes(need, X.device, stream)
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib.mg_conv2d_bwd_filter(_ptr(X), _ptr(dY), _ptr(dW), ctypes.byref(shape),
                                     _contract_id(contract), _ptr(workspace), nbytes,
@@ -347,7 +363,6 @@ def mg_conv2d_bwd_workspace_bytes(X_shape, W_shape, stride=(1, 1), pad=(0, 0),
 def mg_conv2d_bwd(X, W, dY, dX, dW, *, stride=(1, 1), pad=(0, 0), contract=STRICT_F32,
                   workspace=None, stream=None):
     """Both derivatives in one call into caller-provided dX and dW."""
-    import torch
     lib = load_library()
     shape = conv_shape(X.shape, W.shape, stride, pad)
     P, Q = conv_out_hw(shape)
@@ -356,7 +371,7 @@ def mg_conv2d_bwd(X, W, dY, dX, dW, *, stride=(1, 1), pad=(0, 0), contract=STRIC
                 ("dW", dW, tuple(W.shape))))
     need = mg_conv2d_bwd_workspace_bytes(X.shape, W.shape, stride, pad, contract)
     if workspace is None and need > 0:
-        workspace = torch.empty(need, dtype=torch.uint8, device=X.device)
+        workspace = _empty_bytes(need, X.device, stream)
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib.mg_conv2d_bwd(_ptr(X), _ptr(W), _ptr(dY), _ptr(dX), _ptr(dW),
                              ctypes.byref(shape), _contract_id(contract), _ptr(workspace),
@@ -412,8 +427,9 @@ def attention_forward(Q, K, V, *, causal, scale, key_len=None, contract=None, st
     import torch
     c = _contract_id(contract) if contract is not None else (
         FAST_BF16 if Q.dtype == torch.bfloat16 else STRICT_F32)
-    O = torch.empty_like(Q)
-    LSE = torch.empty(Q.shape[:3], dtype=torch.float32, device=Q.device)
+    with _alloc_stream(stream):
+        O = torch.empty_like(Q)
+        LSE = torch.empty(Q.shape[:3], dtype=torch.float32, device=Q.device)
     mg_attn_fwd_cross(Q, K, V, O, LSE, key_len, causal=causal, scale=scale, contract=c,
                       stream=stream)
     return O, LSE
@@ -426,7 +442,8 @@ def attention_backward(Q, K, V, O, LSE, dO, *, causal, scale, key_len=None, cont
     import torch
     c = _contract_id(contract) if contract is not None else (
         FAST_BF16 if Q.dtype == torch.bfloat16 else STRICT_F32)
-    dQ, dK, dV = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
+    with _alloc_stream(stream):
+        dQ, dK, dV = torch.empty_like(Q), torch.empty_like(K), torch.empty_like(V)
     mg_attn_bwd_cross(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len, causal=causal, scale=scale,
                       contract=c, workspace=workspace, stream=stream)
     return dQ, dK, dV
@@ -437,11 +454,12 @@ def conv2d_backward(X, W, dY, *, stride=(1, 1), pad=(0, 0), contract=STRICT_F32,
     """Allocate with torch and run both convolution derivatives; returns
     (dX or None, dW).  Layouts: X [N,H,W,C], W [K,R,S,C], dY [N,P,Q,K]."""
     import torch
-    dW = torch.empty_like(W)
+    with _alloc_stream(stream):
+        dW = torch.empty_like(W)
+        dX = torch.empty_like(X) if need_input_grad else None
     if not need_input_grad:
         mg_conv2d_bwd_filter(X, dY, dW, stride=stride, pad=pad, contract=contract,
                              stream=stream)
         return None, dW
-    dX = torch.empty_like(X)
     mg_conv2d_bwd(X, W, dY, dX, dW, stride=stride, pad=pad, contract=contract, stream=stream)
     return dX, dW

@@ -142,6 +142,7 @@ const char *mg_status_string(mg_status_t s) {
     case MG_ERR_MISALIGNED: return "MG_ERR_MISALIGNED";
     case MG_ERR_WORKSPACE: return "MG_ERR_WORKSPACE";
     case MG_ERR_HIP: return "MG_ERR_HIP";
+    default: break;
     }
     return "MG_ERR_UNKNOWN";
 }

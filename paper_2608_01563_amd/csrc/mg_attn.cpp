@@ -46,6 +46,15 @@ mg_status_t check_tensors(std::initializer_list<mg::host::NamedPtr> ptrs) {
     return mg::host::check_device_ptrs(ptrs, 16);
 }
 
+// key_len's alignment is a host-only check, so it runs with the other
+// pointers' null and alignment checks, before any pointer reaches the
+// runtime's device-memory query.
+mg_status_t check_key_len_alignment(const int32_t *key_len) {
+    if (key_len != nullptr && reinterpret_cast<uintptr_t>(key_len) % 4 != 0)
+        return fail(MG_ERR_MISALIGNED, "key_len is not 4-byte aligned");
+    return MG_OK;
+}
+
 mg_status_t check_key_len(const int32_t *key_len) {
     return mg::host::check_optional_device_ptr(key_len, "key_len", 4);
 }
@@ -111,6 +120,7 @@ mg_status_t mg_attn_fwd_cross(const void *Q, const void *K, const void *V, void 
                               int causal, float scale, mg_contract_t contract,
                               hipStream_t stream) {
     MG_TRY(check_shape(B, H, Lq, Lk, d, scale, contract));
+    MG_TRY(check_key_len_alignment(key_len));
     MG_TRY(check_tensors({{Q, "Q"}, {K, "K"}, {V, "V"}, {O, "O"}, {LSE, "LSE"}}));
     MG_TRY(check_key_len(key_len));
     const mg::AttnProblem p{B, H, Lq, Lk, d, causal ? 1 : 0, scale, key_len};
@@ -152,6 +162,7 @@ mg_status_t mg_attn_bwd_cross(const void *Q, const void *K, const void *V, const
     if (workspace == nullptr || ws_bytes < need)
         return fail(MG_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed",
                     workspace ? ws_bytes : (size_t)0, need);
+    MG_TRY(check_key_len_alignment(key_len));
     MG_TRY(check_tensors({{Q, "Q"}, {K, "K"}, {V, "V"}, {O, "O"}, {LSE, "LSE"}, {dO, "dO"},
                           {dQ, "dQ"}, {dK, "dK"}, {dV, "dV"}, {workspace, "workspace"}}));
     MG_TRY(check_key_len(key_len));

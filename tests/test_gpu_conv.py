@@ -108,24 +108,70 @@ for _layer in LAYERS:
     DISTINCT.setdefault((_layer.H, _layer.C, _layer.K, _layer.R, _layer.stride), _layer)
 
 
+def _edges(n, tile):
+    """Indices in [0, n) at the edges of `tile`-wide tiles: the first and
+    last index, both sides of the first two tile boundaries, and the first
+    and last index of the last (possibly partial) tile."""
+    last = (n - 1) // tile * tile
+    cand = {0, 1, tile - 1, tile, 2 * tile - 1, 2 * tile, last, last + 1, n - 2, n - 1}
+    return sorted(i for i in cand if 0 <= i < n)
+
+
+def boundary_samples(rows, cols, tiles_r=(64,), tiles_c=(64, 128)):
+    """Flat indices of a [rows][cols] output at the edges of its output
+    tiles (64 rows by 64 or 128 columns) and of the split reduction's vector
+    groups: the first and last 16 flat elements (the reduction's tail)."""
+    rs = sorted({i for t in tiles_r for i in _edges(rows, t)})
+    cs = sorted({i for t in tiles_c for i in _edges(cols, t)})
+    idx = {r * cols + c for r in rs for c in cs}
+    total = rows * cols
+    idx.update(range(min(16, total)))
+    idx.update(range(max(0, total - 16), total))
+    return np.array(sorted(idx), dtype=np.int64)
+
+
+def image_edge_samples(N, H, W, C):
+    """Flat indices of dX [N,H,W,C] at the image borders (first and last two
+    rows and columns of the first and last image, where the padding and
+    every stride-parity class of pixels meet) on the channel tile edges."""
+    cs = sorted({i for t in (64, 128) for i in _edges(C, t)})
+    ns = sorted({0, N - 1})
+    hs = sorted({h for h in (0, 1, H - 2, H - 1) if 0 <= h < H})
+    ws = sorted({w for w in (0, 1, W - 2, W - 1) if 0 <= w < W})
+    return np.array(sorted({((n * H + h) * W + w) * C + c for n in ns for h in hs for w in ws
+                            for c in cs}), dtype=np.int64)
+
+
+def sampled_error(got, flat_idx, ref_vals):
+    """max |got - oracle| over the samples / max |oracle| over the samples
+    (the denominator comes from the oracle only)."""
+    den = np.max(np.abs(ref_vals))
+    return np.max(np.abs(got.reshape(-1)[flat_idx] - ref_vals)) / den
+
+
 @pytest.mark.parametrize("layer", list(DISTINCT.values()), ids=lambda l: l.name)
 def test_resnet50_layer_sampled(gpu_lib, layer):
-    """Full-size ResNet-50 layer (batch 4): 256 sampled elements of dX and
-    of dW against the oracle's one-by-one sums, plus finiteness everywhere."""
+    """Full-size ResNet-50 layer (batch 4): 256 random elements of dX and of
+    dW plus every element at a tile edge or at the ends of the flat arrays,
+    against the oracle's one-by-one sums; finiteness everywhere."""
     from oracle.conv import oracle_conv2d_bwd_data_at, oracle_conv2d_bwd_filter_at
     say("resnet50 %s: N%d H%d C%d K%d R%d stride %d" % (layer.name, layer.N, layer.H, layer.C,
                                                        layer.K, layer.R, layer.stride))
     x = layer_inputs(layer, seed=len(layer.name) * 17 + layer.C)
     dX, dW = run_gpu(x, need_input_grad=layer.input_grad)
     rng = np.random.default_rng(layer.K + layer.H)
-    iw = rng.integers(0, dW.size, 256)
+    rsc = layer.R * layer.S * layer.C
+    iw = np.concatenate([rng.integers(0, dW.size, 256), boundary_samples(layer.K, rsc)])
     rW = oracle_conv2d_bwd_filter_at(x.X, x.dY, x.W.shape, iw, x.stride, x.pad)
-    eW = np.max(np.abs(dW.reshape(-1)[iw] - rW)) / np.max(np.abs(dW))
+    eW = sampled_error(dW, iw, rW)
     assert np.all(np.isfinite(dW)) and eW <= TOL, eW
     if layer.input_grad:
-        ix = rng.integers(0, dX.size, 256)
+        pixels = layer.N * layer.H * layer.W
+        ix = np.concatenate([rng.integers(0, dX.size, 256),
+                             boundary_samples(pixels, layer.C),
+                             image_edge_samples(layer.N, layer.H, layer.W, layer.C)])
         rX = oracle_conv2d_bwd_data_at(x.dY, x.W, x.X.shape, ix, x.stride, x.pad)
-        eX = np.max(np.abs(dX.reshape(-1)[ix] - rX)) / np.max(np.abs(dX))
+        eX = sampled_error(dX, ix, rX)
         assert np.all(np.isfinite(dX)) and eX <= TOL, eX
 
 

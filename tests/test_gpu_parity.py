@@ -177,21 +177,52 @@ def test_small_shapes_bf16(gpu_lib, L, d, mode):
     assert max(errs.values()) <= TOL["fast_bf16"], errs
 
 
-WORKLOAD4_HEADS = [(0, 0), (0, 5), (0, 10), (0, 15), (1, 2), (1, 7), (1, 11), (1, 14)]
-
-
-def test_workload4_sampled_heads_bf16(gpu_lib):
+@pytest.fixture(scope="module")
+def workload4():
+    """Workload 4's inputs and the oracle on every one of its 32 heads
+    (computed once for the end-to-end and the backward-isolation test)."""
     w = WORKLOADS[4]
-    say("workload 4 %s (oracle on %d of %d heads)" % (w.name, len(WORKLOAD4_HEADS), w.B * w.H))
+    say("workload 4 %s: oracle on all %d heads" % (w.name, w.B * w.H))
     x = workload_inputs(4)
+    return w, x, oracle_reference(x)
+
+
+def test_workload4_all_heads_bf16(gpu_lib, workload4):
+    w, x, ref = workload4
+    say("workload 4 %s end to end" % w.name)
     got = run_gpu(x)
-    ref = oracle_reference(x, heads=WORKLOAD4_HEADS)
-    errs = compare(got, ref, w.contract, heads=WORKLOAD4_HEADS)
+    errs = compare(got, ref, w.contract)
     say("  errors %s" % {k: "%.2e" % v for k, v in errs.items()})
     assert max(errs.values()) <= TOL[w.contract], errs
-    # every head (not only the sampled ones) is finite and written
-    for n in ("O", "dQ", "dK", "dV"):
-        assert np.all(np.isfinite(got[n]))
+    # the same gate head by head, so that one bad head cannot hide behind
+    # the others' larger maxima
+    for b in range(w.B):
+        for h in range(w.H):
+            e = compare(got, ref, w.contract, heads=[(b, h)])
+            assert max(e.values()) <= TOL[w.contract], (b, h, e)
+
+
+def test_workload4_backward_isolated_bf16(gpu_lib, workload4):
+    """The fast_bf16 backward alone: the oracle's O (rounded to bf16, nearest
+    even, as the contract stores it) and f32 LSE go into the GPU backward."""
+    w, x, ref = workload4
+    say("workload 4 backward isolation")
+    got = run_gpu(x, O_in=ref["O"], LSE_in=ref["LSE"])
+    errs = compare(got, ref, w.contract, names=("dQ", "dK", "dV"))
+    say("  errors %s" % {k: "%.2e" % v for k, v in errs.items()})
+    assert max(errs.values()) <= TOL[w.contract], errs
+
+
+@pytest.mark.parametrize("L,d,mode", [(200, 128, "padded"), (65, 64, "causal"),
+                                       (17, 32, "full")])
+def test_backward_isolated_bf16_ragged(gpu_lib, L, d, mode):
+    """fast_bf16 backward isolation on ragged tails and key padding."""
+    say("bf16 backward isolation L=%d d=%d %s" % (L, d, mode))
+    x = small_inputs(L, d, mode, contract="fast_bf16", seed=5)
+    ref = oracle_reference(x)
+    got = run_gpu(x, O_in=ref["O"], LSE_in=ref["LSE"])
+    errs = compare(got, ref, "fast_bf16", names=("dQ", "dK", "dV"))
+    assert max(errs.values()) <= TOL["fast_bf16"], errs
 
 
 def test_bitwise_pins_bf16(gpu_lib):

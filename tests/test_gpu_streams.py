@@ -128,3 +128,41 @@ def test_threads_each_with_a_stream_match_serial(gpu_lib):
     assert not errors, errors
     torch.cuda.synchronize()
     _check(problems, expected, "threads")
+
+
+def test_binding_temporaries_on_side_streams(gpu_lib):
+    """Workspaces and outputs that the binding allocates itself (no
+    workspace given) belong to the stream the kernels run on: freeing them
+    on return while those kernels still run, then allocating and filling
+    memory on the current stream, must leave every result intact."""
+    import torch
+    from workloads.conv import make_conv_inputs
+    mg = gpu_lib
+    say("streams: binding-allocated workspaces on side streams")
+    problems = [_Problem(gpu_lib, c) for c in CASES]
+    expected = _serial_reference(problems)
+    cx = make_conv_inputs(2, 20, 20, 64, 96, 3, 3, 1, 1, seed=75)
+    X, W, dY = (torch.from_numpy(a.copy()).cuda() for a in (cx.X, cx.W, cx.dY))
+    cref = mg.conv2d_backward(X, W, dY, stride=cx.stride, pad=cx.pad)
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream() for _ in problems]   # default priority
+    conv_stream = torch.cuda.Stream()
+    for rep in range(3):
+        results = []
+        for p, s in zip(problems, streams):
+            O, LSE = mg.attention_forward(p.Q, p.K, p.V, causal=p.causal, scale=p.x.scale,
+                                          key_len=p.kl, contract=p.contract, stream=s)
+            g = mg.attention_backward(p.Q, p.K, p.V, O, LSE, p.dO, causal=p.causal,
+                                      scale=p.x.scale, key_len=p.kl, contract=p.contract,
+                                      stream=s)
+            results.append((O, LSE) + tuple(g))
+            # the backward's workspace is already freed: memory taken and
+            # written on the current stream must not be that block
+            torch.full((1 << 22,), float("nan"), device="cuda")
+        cout = mg.conv2d_backward(X, W, dY, stride=cx.stride, pad=cx.pad, stream=conv_stream)
+        torch.full((1 << 22,), float("nan"), device="cuda")
+        torch.cuda.synchronize()
+        for i, (got, want) in enumerate(zip(results, expected)):
+            for name, a, b in zip(("O", "LSE", "dQ", "dK", "dV"), got, want):
+                assert torch.equal(a, b), ("rep %d" % rep, i, name)
+        assert torch.equal(cout[0], cref[0]) and torch.equal(cout[1], cref[1]), rep
