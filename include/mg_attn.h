@@ -174,6 +174,35 @@ mg_status_t mg_attn_bwd_cross(const void *Q, const void *K, const void *V,
                               void *workspace, size_t workspace_bytes,
                               hipStream_t stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * backward of mg_attn_bwd_cross with its workspace in a static device array
+ * of the library, MG_ATTN_NOALLOC_SCRATCH_BYTES bytes on each device it
+ * runs on, held until the process ends.  Same arguments, kernels, results
+ * and errors as mg_attn_bwd_cross without the workspace pair.  The call
+ * allocates nothing (no hipMalloc or hipFree, no allocating library call).
+ * When the caller-workspace layout (mg_attn_bwd_cross_workspace_bytes) fits
+ * in the array it is used as is, and results are bitwise those of
+ * mg_attn_bwd_cross; otherwise the workspace is D alone (B*H*Lq f32,
+ * rounded up to 256 bytes) and dQ comes from the separate query-stationary
+ * pass, which agrees with the partial-sum path within the contract's
+ * tolerance.  MG_ERR_WORKSPACE when even D does not fit
+ * (B*H*Lq > MG_ATTN_NOALLOC_SCRATCH_BYTES / 4).  The array is not cleared
+ * between calls and nothing in it needs to be: every call writes what it
+ * reads.  Every call on one device shares that device's array, so calls
+ * that overlap in time on one device (other streams, other threads) race
+ * and must be serialized by the caller.
+ */
+#define MG_ATTN_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+
+mg_status_t mg_attn_bwd_noalloc(const void *Q, const void *K, const void *V,
+                                const void *O, const float *LSE, const void *dO,
+                                void *dQ, void *dK, void *dV,
+                                const int32_t *key_len,
+                                int B, int H, int Lq, int Lk, int d, int causal, float scale,
+                                mg_contract_t contract, hipStream_t stream);
+
 /* Static, human-readable name of a status code. */
 const char *mg_status_string(mg_status_t status);
 

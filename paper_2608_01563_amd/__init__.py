@@ -21,6 +21,7 @@ from ._binding import (  # noqa: F401
     mg_attn_bwd,
     mg_attn_bwd_cross,
     mg_attn_bwd_cross_workspace_bytes,
+    mg_attn_bwd_noalloc,
     mg_attn_bwd_workspace_bytes,
     mg_attn_fwd,
     mg_attn_fwd_cross,

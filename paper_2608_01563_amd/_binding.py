@@ -60,6 +60,9 @@ def _declare(lib):
     lib.mg_attn_bwd_cross.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, c_int, c_int,
                                       c_int, c_int, c_int, c_int, c_float, c_int, vp, c_size, vp]
     lib.mg_attn_bwd_cross.restype = c_int
+    lib.mg_attn_bwd_noalloc.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, c_int, c_int,
+                                        c_int, c_int, c_int, c_int, c_float, c_int, vp]
+    lib.mg_attn_bwd_noalloc.restype = c_int
     shp = ctypes.POINTER(ConvShape)
     lib.mg_conv2d_bwd_data_workspace_bytes.argtypes = [shp, c_int]
     lib.mg_conv2d_bwd_data_workspace_bytes.restype = c_size
@@ -276,6 +279,23 @@ def mg_attn_bwd_cross(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len=None, *, causal, 
                                  _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(key_len), B, H, Lq, Lk, d,
                                  int(bool(causal)), float(scale), c, _ptr(workspace), nbytes,
                                  _stream_handle(stream)))
+
+
+def mg_attn_bwd_noalloc(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len=None, *, causal, scale,
+                        contract=STRICT_F32, stream=None):
+    """mg_attn_bwd_cross with the library's static scratch array as its
+    workspace: nothing is allocated, here or in the library."""
+    lib = load_library()
+    c = _contract_id(contract)
+    B, H, Lq, Lk, d = _cross_shapes(Q, K)
+    _check_tensors(c, Q.shape, (("Q", Q), ("O", O), ("dO", dO), ("dQ", dQ)))
+    _check_tensors(c, K.shape, (("K", K), ("V", V), ("dK", dK), ("dV", dV)))
+    _check_lse(LSE, Q.shape)
+    _check_key_len(key_len, B)
+    _check(lib.mg_attn_bwd_noalloc(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(LSE), _ptr(dO),
+                                   _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(key_len), B, H, Lq, Lk,
+                                   d, int(bool(causal)), float(scale), c,
+                                   _stream_handle(stream)))
 
 
 def conv_shape(X_shape, W_shape, stride=(1, 1), pad=(0, 0)):

@@ -12,6 +12,7 @@
 #include <cstdio>
 #include <string>
 
+#include "attn_bwd.h"
 #include "host_runtime.h"
 #include "launch.h"
 
@@ -84,9 +85,10 @@ size_t dq_partial_bytes(int B, int H, int Lq, int Lk, int d, int causal) {
     return (size_t)((Lk + kr - 1) / kr) * B * H * Lq * d * sizeof(float);
 }
 
-bool use_fused_dq(int B, int H, int Lq, int Lk, int d, int causal, mg_contract_t contract) {
+bool use_fused_dq(int B, int H, int Lq, int Lk, int d, int causal, mg_contract_t contract,
+                  size_t partial_limit) {
     return contract == MG_CONTRACT_STRICT_F32 && d <= 64 &&
-           dq_partial_bytes(B, H, Lq, Lk, d, causal) <= kFusedPartialLimit;
+           dq_partial_bytes(B, H, Lq, Lk, d, causal) <= partial_limit;
 }
 
 // dK/dV partials of a fused backward whose query tiles are split (zero
@@ -97,13 +99,17 @@ size_t dkdv_partial_bytes(int B, int H, int Lq, int Lk, int d, int causal) {
     return ns > 1 ? (size_t)2 * ns * B * H * Lk * d * sizeof(float) : 0;
 }
 
+}  // namespace
+
+namespace mg {
+
 // Layout: D (f32 per query row) first; when fused, the dQ partials, then
 // (256-byte aligned) the dK/dV partials of a split backward.
-size_t workspace_bytes(int B, int H, int Lq, int Lk, int d, int causal,
-                       mg_contract_t contract) {
+size_t attn_bwd_workspace(int B, int H, int Lq, int Lk, int d, int causal,
+                          mg_contract_t contract, size_t partial_limit) {
     contract = backward_contract(contract);
     size_t n = round256((size_t)B * H * Lq * sizeof(float));
-    if (use_fused_dq(B, H, Lq, Lk, d, causal, contract)) {
+    if (use_fused_dq(B, H, Lq, Lk, d, causal, contract, partial_limit)) {
         n += dq_partial_bytes(B, H, Lq, Lk, d, causal);
         const size_t kv = dkdv_partial_bytes(B, H, Lq, Lk, d, causal);
         if (kv > 0) n = round256(n) + kv;
@@ -111,61 +117,32 @@ size_t workspace_bytes(int B, int H, int Lq, int Lk, int d, int causal,
     return n;
 }
 
-}  // namespace
+size_t attn_bwd_partial_limit() { return kFusedPartialLimit; }
 
-extern "C" {
-
-mg_status_t mg_attn_fwd_cross(const void *Q, const void *K, const void *V, void *O, float *LSE,
-                              const int32_t *key_len, int B, int H, int Lq, int Lk, int d,
-                              int causal, float scale, mg_contract_t contract,
-                              hipStream_t stream) {
-    MG_TRY(check_shape(B, H, Lq, Lk, d, scale, contract));
+mg_status_t attn_bwd_check_args(const void *Q, const void *K, const void *V, const void *O,
+                                const float *LSE, const void *dO, void *dQ, void *dK,
+                                void *dV, const int32_t *key_len, const void *workspace) {
     MG_TRY(check_key_len_alignment(key_len));
-    MG_TRY(check_tensors({{Q, "Q"}, {K, "K"}, {V, "V"}, {O, "O"}, {LSE, "LSE"}}));
-    MG_TRY(check_key_len(key_len));
-    const mg::AttnProblem p{B, H, Lq, Lk, d, causal ? 1 : 0, scale, key_len};
-    if (contract == MG_CONTRACT_STRICT_F32) {
-        MG_TRY(run_kernel(kernel_name("attn_fwd", contract, d), stream, [&] {
-            return mg::launch_fwd_f32(p, (const float *)Q, (const float *)K, (const float *)V,
-                                      (float *)O, LSE, stream);
-        }));
-    } else if (contract == MG_CONTRACT_ACCELERATED) {
-        MG_TRY(run_kernel(kernel_name("attn_fwd", contract, d), stream, [&] {
-            return mg::launch_fwd_accel(p, (const float *)Q, (const float *)K, (const float *)V,
-                                        (float *)O, LSE, stream);
-        }));
-    } else {
-        MG_TRY(run_kernel(kernel_name("attn_fwd", contract, d), stream, [&] {
-            return mg::launch_fwd_bf16(p, (const uint16_t *)Q, (const uint16_t *)K,
-                                       (const uint16_t *)V, (uint16_t *)O, LSE, stream);
-        }));
-    }
-    return ok();
+    if (workspace != nullptr)
+        MG_TRY(check_tensors({{Q, "Q"}, {K, "K"}, {V, "V"}, {O, "O"}, {LSE, "LSE"},
+                              {dO, "dO"}, {dQ, "dQ"}, {dK, "dK"}, {dV, "dV"},
+                              {workspace, "workspace"}}));
+    else
+        MG_TRY(check_tensors({{Q, "Q"}, {K, "K"}, {V, "V"}, {O, "O"}, {LSE, "LSE"},
+                              {dO, "dO"}, {dQ, "dQ"}, {dK, "dK"}, {dV, "dV"}}));
+    return check_key_len(key_len);
 }
 
-size_t mg_attn_bwd_cross_workspace_bytes(int B, int H, int Lq, int Lk, int d, int causal,
-                                         mg_contract_t contract) {
-    const std::string saved = mg::host::saved_detail();
-    mg_status_t st = check_shape(B, H, Lq, Lk, d, 1.0f, contract);
-    mg::host::restore_detail(saved);
-    if (st != MG_OK) return 0;
-    return workspace_bytes(B, H, Lq, Lk, d, causal, contract);
+mg_status_t attn_bwd_check_shape(int B, int H, int Lq, int Lk, int d, float scale,
+                                 mg_contract_t contract) {
+    return check_shape(B, H, Lq, Lk, d, scale, contract);
 }
 
-mg_status_t mg_attn_bwd_cross(const void *Q, const void *K, const void *V, const void *O,
-                              const float *LSE, const void *dO, void *dQ, void *dK, void *dV,
-                              const int32_t *key_len, int B, int H, int Lq, int Lk, int d,
-                              int causal, float scale, mg_contract_t contract, void *workspace,
-                              size_t ws_bytes, hipStream_t stream) {
-    MG_TRY(check_shape(B, H, Lq, Lk, d, scale, contract));
-    const size_t need = workspace_bytes(B, H, Lq, Lk, d, causal, contract);
-    if (workspace == nullptr || ws_bytes < need)
-        return fail(MG_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed",
-                    workspace ? ws_bytes : (size_t)0, need);
-    MG_TRY(check_key_len_alignment(key_len));
-    MG_TRY(check_tensors({{Q, "Q"}, {K, "K"}, {V, "V"}, {O, "O"}, {LSE, "LSE"}, {dO, "dO"},
-                          {dQ, "dQ"}, {dK, "dK"}, {dV, "dV"}, {workspace, "workspace"}}));
-    MG_TRY(check_key_len(key_len));
+mg_status_t attn_bwd_enqueue(const void *Q, const void *K, const void *V, const void *O,
+                             const float *LSE, const void *dO, void *dQ, void *dK, void *dV,
+                             const int32_t *key_len, int B, int H, int Lq, int Lk, int d,
+                             int causal, float scale, mg_contract_t contract, void *workspace,
+                             size_t partial_limit, hipStream_t stream) {
     const mg::AttnProblem p{B, H, Lq, Lk, d, causal ? 1 : 0, scale, key_len};
     float *Dws = (float *)workspace;
     contract = backward_contract(contract);
@@ -174,7 +151,7 @@ mg_status_t mg_attn_bwd_cross(const void *Q, const void *K, const void *V, const
         const float *o = (const float *)O, *go = (const float *)dO;
         MG_TRY(run_kernel(kernel_name("attn_rowdot", contract, d), stream,
                           [&] { return mg::launch_bwd_rowdot_f32(p, o, go, Dws, stream); }));
-        if (use_fused_dq(B, H, Lq, Lk, d, causal, contract)) {
+        if (use_fused_dq(B, H, Lq, Lk, d, causal, contract, partial_limit)) {
             char *base = (char *)workspace;
             float *dQp = (float *)(base + round256((size_t)B * H * Lq * sizeof(float)));
             float *dKVp = dkdv_partial_bytes(B, H, Lq, Lk, d, causal) == 0 ? nullptr
@@ -216,6 +193,63 @@ mg_status_t mg_attn_bwd_cross(const void *Q, const void *K, const void *V, const
         }));
     }
     return ok();
+}
+
+}  // namespace mg
+
+extern "C" {
+
+mg_status_t mg_attn_fwd_cross(const void *Q, const void *K, const void *V, void *O, float *LSE,
+                              const int32_t *key_len, int B, int H, int Lq, int Lk, int d,
+                              int causal, float scale, mg_contract_t contract,
+                              hipStream_t stream) {
+    MG_TRY(check_shape(B, H, Lq, Lk, d, scale, contract));
+    MG_TRY(check_key_len_alignment(key_len));
+    MG_TRY(check_tensors({{Q, "Q"}, {K, "K"}, {V, "V"}, {O, "O"}, {LSE, "LSE"}}));
+    MG_TRY(check_key_len(key_len));
+    const mg::AttnProblem p{B, H, Lq, Lk, d, causal ? 1 : 0, scale, key_len};
+    if (contract == MG_CONTRACT_STRICT_F32) {
+        MG_TRY(run_kernel(kernel_name("attn_fwd", contract, d), stream, [&] {
+            return mg::launch_fwd_f32(p, (const float *)Q, (const float *)K, (const float *)V,
+                                      (float *)O, LSE, stream);
+        }));
+    } else if (contract == MG_CONTRACT_ACCELERATED) {
+        MG_TRY(run_kernel(kernel_name("attn_fwd", contract, d), stream, [&] {
+            return mg::launch_fwd_accel(p, (const float *)Q, (const float *)K, (const float *)V,
+                                        (float *)O, LSE, stream);
+        }));
+    } else {
+        MG_TRY(run_kernel(kernel_name("attn_fwd", contract, d), stream, [&] {
+            return mg::launch_fwd_bf16(p, (const uint16_t *)Q, (const uint16_t *)K,
+                                       (const uint16_t *)V, (uint16_t *)O, LSE, stream);
+        }));
+    }
+    return ok();
+}
+
+size_t mg_attn_bwd_cross_workspace_bytes(int B, int H, int Lq, int Lk, int d, int causal,
+                                         mg_contract_t contract) {
+    const std::string saved = mg::host::saved_detail();
+    mg_status_t st = check_shape(B, H, Lq, Lk, d, 1.0f, contract);
+    mg::host::restore_detail(saved);
+    if (st != MG_OK) return 0;
+    return mg::attn_bwd_workspace(B, H, Lq, Lk, d, causal, contract, kFusedPartialLimit);
+}
+
+mg_status_t mg_attn_bwd_cross(const void *Q, const void *K, const void *V, const void *O,
+                              const float *LSE, const void *dO, void *dQ, void *dK, void *dV,
+                              const int32_t *key_len, int B, int H, int Lq, int Lk, int d,
+                              int causal, float scale, mg_contract_t contract, void *workspace,
+                              size_t ws_bytes, hipStream_t stream) {
+    MG_TRY(check_shape(B, H, Lq, Lk, d, scale, contract));
+    const size_t need =
+        mg::attn_bwd_workspace(B, H, Lq, Lk, d, causal, contract, kFusedPartialLimit);
+    if (workspace == nullptr || ws_bytes < need)
+        return fail(MG_ERR_WORKSPACE, "workspace of %zu bytes given, %zu needed",
+                    workspace ? ws_bytes : (size_t)0, need);
+    MG_TRY(mg::attn_bwd_check_args(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len, workspace));
+    return mg::attn_bwd_enqueue(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len, B, H, Lq, Lk, d,
+                                causal, scale, contract, workspace, kFusedPartialLimit, stream);
 }
 
 mg_status_t mg_attn_fwd(const void *Q, const void *K, const void *V, void *O, float *LSE,

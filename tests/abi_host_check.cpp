@@ -100,6 +100,22 @@ void attention_checks() {
     EXPECT(need > 0);
     EXPECT(bwd(fake(0xa004), need, 0) == MG_ERR_MISALIGNED);
 
+    // the static-scratch backward: sizes first, then the rows D needs, then
+    // pointers; nothing here reaches the device
+    auto noalloc = [&](void *q, int Lq, int d, int contract) {
+        return mg_attn_bwd_noalloc(q, p9[1], p9[2], p9[3], static_cast<const float *>(p9[4]),
+                                   p9[5], p9[6], p9[7], p9[8], nullptr, 1, 1, Lq, 64, d, 1,
+                                   0.125f, static_cast<mg_contract_t>(contract), nullptr);
+    };
+    EXPECT(noalloc(p9[0], 8, 48, 0) == MG_ERR_UNSUPPORTED);
+    EXPECT(noalloc(p9[0], 8, 64, 4) == MG_ERR_INVALID_ARGUMENT);
+    const int too_many = (int)(MG_ATTN_NOALLOC_SCRATCH_BYTES / 4 + 1);
+    EXPECT(noalloc(p9[0], too_many, 32, 0) == MG_ERR_WORKSPACE);
+    EXPECT(std::strstr(mg_last_error_detail(), "scratch") != nullptr);
+    EXPECT(noalloc(p9[0], too_many, 32, 1) == MG_ERR_WORKSPACE);
+    EXPECT(noalloc(nullptr, 8, 64, 0) == MG_ERR_INVALID_ARGUMENT);
+    EXPECT(noalloc(fake(0x1008), 8, 64, 0) == MG_ERR_MISALIGNED);
+
     // workspace queries: D rounded to 256 bytes plus the dQ partials
     const size_t rows = 8 * 8 * 1024;
     EXPECT(mg_attn_bwd_workspace_bytes(8, 8, 1024, 64, 1, kStrict) ==
