@@ -257,6 +257,13 @@ __global__ __launch_bounds__(256) void attn_rowdot_bf16(const uint16_t *__restri
 // 16x16x32 products; query tiles of 64 rows stream through LDS row-major.
 // Masks as in the strict-f32 kernel: a causal threshold per lane, padded
 // keys overwritten with zeros at the end, rows past Lq inert.
+//
+// The two tile buffers are separate LDS arrays and the tile loop is unrolled
+// by two, so that every read names the buffer it reads at compile time: the
+// compiler can then tell the next tile's direct-to-LDS loads apart from the
+// current tile's operand reads and does not wait for the loads before the
+// reads (with one array indexed by a run-time buffer number it must assume
+// they may overlap, and the prefetch would stall every iteration).
 template <int D>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
 void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
@@ -267,15 +274,15 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
                     float scale_log2, int BH, int layer) {
     constexpr int NS = D / 32;
     constexpr int NC = D / 16;
-    constexpr int LD = Bf16Ld<D>::value;
+    constexpr int LD = Bf16LdKV<D>::value;
     // Q and dO rows move as D/2 floats into double-buffered padded LDS tiles
     // by direct-to-LDS loads: the next tile is fetched during the whole
     // current iteration, and one barrier per iteration suffices.
     using Tile = RowDirectTile<kStream, D / 2, kWaves, LD / 2>;
-    __shared__ __attribute__((aligned(16))) uint16_t Qr[2][kStream][LD];
-    __shared__ __attribute__((aligned(16))) uint16_t Or[2][kStream][LD];
-    __shared__ __attribute__((aligned(16))) float lse2s[2][kStream];
-    __shared__ __attribute__((aligned(16))) float Ds[2][kStream];
+    __shared__ __attribute__((aligned(16))) uint16_t Qr0[kStream][LD], Qr1[kStream][LD];
+    __shared__ __attribute__((aligned(16))) uint16_t Or0[kStream][LD], Or1[kStream][LD];
+    __shared__ __attribute__((aligned(16))) float lse0[kStream], lse1[kStream];   // LSE (natural log)
+    __shared__ __attribute__((aligned(16))) float Ds0[kStream], Ds1[kStream];
 
     const int slot = blockIdx.x / BH;
     const int head = blockIdx.x - slot * BH;
@@ -313,34 +320,30 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
     const Tile tile;
     const float *Qf = reinterpret_cast<const float *>(Q + qoff);
     const float *Of = reinterpret_cast<const float *>(dO + qoff);
-    float lse_pre = 0.f, d_pre = 0.f;
-    auto fetch = [&](int qt, int buf) {   // direct loads of Q, dO; LSE, D to registers
-        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Qr[buf][0][0]), Qf, qt * kStream, Lq, w,
-                   lane);
-        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Or[buf][0][0]), Of, qt * kStream, Lq, w,
-                   lane);
-        if (tid < kStream) {
-            const int row = qt * kStream + tid;
-            lse_pre = (row < Lq) ? LSE[(size_t)head * Lq + row] : 0.f;   // natural log
-            d_pre = (row < Lq) ? Dws[(size_t)head * Lq + row] : 0.f;
+    // Direct-to-LDS loads of the Q and dO rows of tile qt and of their LSE
+    // (natural log; wave 0) and D (the last wave) values; rows past Lq arrive
+    // as zeros.
+    auto fetch = [&](int qt, uint16_t (&Qn)[kStream][LD], uint16_t (&On)[kStream][LD],
+                     float (&ln)[kStream], float (&dn)[kStream]) {
+        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Qn[0][0]), Qf, qt * kStream, Lq, w, lane);
+        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&On[0][0]), Of, qt * kStream, Lq, w, lane);
+        if (w == 0 || w == kWaves - 1) {
+            const int row0 = qt * kStream;
+            const int rows = min(max(Lq - row0, 0), kStream);
+            const float *src = (w == 0 ? LSE : Dws) + (size_t)head * Lq + row0;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                buffer_rsrc(src, rows * 4),
+                (__attribute__((address_space(3))) void *)(w == 0 ? &ln[0] : &dn[0]), 4,
+                lane * 4, 0, 0, 0);
         }
     };
-    auto publish = [&](int buf) {   // LSE (base 2) and D of the fetched rows
-        if (tid < kStream) {
-            lse2s[buf][tid] = lse_pre * kLog2e;
-            Ds[buf][tid] = d_pre;
-        }
-    };
-    if (qstart < qstop) {
-        fetch(qstart, 0);
-        wait_vmcnt<0>();
-        publish(0);
-    }
-    __syncthreads();
 
-    for (int qt = qstart; qt < qstop; ++qt) {
-        const int cb = (qt - qstart) & 1;
-        if (qt + 1 < qstop) fetch(qt + 1, cb ^ 1);   // buffer cb^1 was freed by the last barrier
+    // One query tile from buffers (Qc, Oc, lc, dc) while tile qt + 1 loads
+    // into (Qn, On, ln, dn).
+    auto step = [&](int qt, uint16_t (&Qc)[kStream][LD], uint16_t (&Oc)[kStream][LD],
+                    float (&lc)[kStream], float (&dc)[kStream], uint16_t (&Qn)[kStream][LD],
+                    uint16_t (&On)[kStream][LD], float (&ln)[kStream], float (&dn)[kStream]) {
+        if (qt + 1 < qstop) fetch(qt + 1, Qn, On, ln, dn);   // freed by the last barrier
 
         f32x4 sacc[kBlk], pacc[kBlk];
 #pragma unroll
@@ -352,9 +355,9 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
         for (int s = 0; s < NS; ++s)
 #pragma unroll
             for (int ib = 0; ib < kBlk; ++ib) {
-                sacc[ib] = mfma16x16x32bf16(load_bf16x8(&Qr[cb][16 * ib + il][32 * s + 8 * g]),
+                sacc[ib] = mfma16x16x32bf16(load_bf16x8(&Qc[16 * ib + il][32 * s + 8 * g]),
                                             kreg[s], sacc[ib]);
-                pacc[ib] = mfma16x16x32bf16(load_bf16x8(&Or[cb][16 * ib + il][32 * s + 8 * g]),
+                pacc[ib] = mfma16x16x32bf16(load_bf16x8(&Oc[16 * ib + il][32 * s + 8 * g]),
                                             vreg[s], pacc[ib]);
             }
 
@@ -362,8 +365,8 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
         const int thr = causal ? kj - diag - ibase : -(1 << 30);
 #pragma unroll
         for (int ib = 0; ib < kBlk; ++ib) {
-            const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lse2s[cb][16 * ib + 4 * g]);
-            const f32x4 dd = *reinterpret_cast<const f32x4 *>(&Ds[cb][16 * ib + 4 * g]);
+            const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lc[16 * ib + 4 * g]) * kLog2e;
+            const f32x4 dd = *reinterpret_cast<const f32x4 *>(&dc[16 * ib + 4 * g]);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 float p = exp2_fast(fmaf(sacc[ib][r], scale_log2, -l2[r]));
@@ -381,18 +384,25 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
             const int r0 = 32 * t + 4 * g;
 #pragma unroll
             for (int c = 0; c < NC; ++c) {
-                dvacc[c] = mfma16x16x32bf16(
-                    load_tr_pair<LD>(Or[cb], r0, r0 + 16, 16 * c, jr, jc), pb, dvacc[c]);
-                dkacc[c] = mfma16x16x32bf16(
-                    load_tr_pair<LD>(Qr[cb], r0, r0 + 16, 16 * c, jr, jc), sb, dkacc[c]);
+                dvacc[c] = mfma16x16x32bf16(load_tr_pair<LD>(Oc, r0, r0 + 16, 16 * c, jr, jc),
+                                            pb, dvacc[c]);
+                dkacc[c] = mfma16x16x32bf16(load_tr_pair<LD>(Qc, r0, r0 + 16, 16 * c, jr, jc),
+                                            sb, dkacc[c]);
             }
         }
 
-        if (qt + 1 < qstop) {
-            wait_vmcnt<0>();   // next Q/dO tile landed, its LSE/D in registers
-            publish(cb ^ 1);
-        }
-        __syncthreads();   // next tile visible; buffer cb free
+        if (qt + 1 < qstop) wait_vmcnt<0>();   // next tile and its LSE, D landed
+        __syncthreads();   // next tile visible; buffers (Qc, Oc) free
+    };
+
+    if (qstart < qstop) {
+        fetch(qstart, Qr0, Or0, lse0, Ds0);
+        wait_vmcnt<0>();
+    }
+    __syncthreads();
+    for (int qt = qstart; qt < qstop; qt += 2) {
+        step(qt, Qr0, Or0, lse0, Ds0, Qr1, Or1, lse1, Ds1);
+        if (qt + 1 < qstop) step(qt + 1, Qr1, Or1, lse1, Ds1, Qr0, Or0, lse0, Ds0);
     }
 
     if (kj < Lk) {
@@ -413,7 +423,10 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
 // dQ^T += K^T dS^T with dS^T straight from registers and K^T from transpose
 // reads of the row-major K tile.  KS keys per streamed tile; K and V tiles
 // are double-buffered in LDS and arrive by direct-to-LDS row loads, so the
-// next tile is fetched during the whole current iteration.
+// next tile is fetched during the whole current iteration.  As in the dK/dV
+// kernel, the two buffers are separate arrays and the tile loop is unrolled
+// by two, so that the current tile's reads need not wait for the next
+// tile's loads.
 template <int D, int KS>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
 void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
@@ -428,8 +441,8 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
     // K and V rows move as D/2 floats into double-buffered padded LDS tiles:
     // the next tile is fetched during the whole current iteration.
     using Tile = RowDirectTile<KS, D / 2, kWaves, LD / 2>;
-    __shared__ __attribute__((aligned(16))) uint16_t Kr[2][KS][LD];
-    __shared__ __attribute__((aligned(16))) uint16_t Vr[2][KS][LD];
+    __shared__ __attribute__((aligned(16))) uint16_t Kr0[KS][LD], Kr1[KS][LD];
+    __shared__ __attribute__((aligned(16))) uint16_t Vr0[KS][LD], Vr1[KS][LD];
 
     const int slot = blockIdx.x / BH;
     const int head = blockIdx.x - slot * BH;
@@ -470,16 +483,14 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
     const Tile tile;
     const float *Kf = reinterpret_cast<const float *>(K + hoff);
     const float *Vf = reinterpret_cast<const float *>(V + hoff);
-    auto fetch = [&](int t, int buf) {
-        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Kr[buf][0][0]), Kf, t * KS, Lk, w, lane);
-        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Vr[buf][0][0]), Vf, t * KS, Lk, w, lane);
+    auto fetch = [&](int t, uint16_t (&Kn)[KS][LD], uint16_t (&Vn)[KS][LD]) {
+        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Kn[0][0]), Kf, t * KS, Lk, w, lane);
+        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Vn[0][0]), Vf, t * KS, Lk, w, lane);
     };
-    if (ntiles > 0) fetch(0, 0);
-    wait_vmcnt<0>();
-    __syncthreads();
-    for (int kt = 0; kt < ntiles; ++kt) {
-        const int cb = kt & 1;
-        if (kt + 1 < ntiles) fetch(kt + 1, cb ^ 1);   // buffer cb^1 was freed by the last barrier
+    // key tile kt from (Kc, Vc) while tile kt + 1 loads into (Kn, Vn)
+    auto step = [&](int kt, uint16_t (&Kc)[KS][LD], uint16_t (&Vc)[KS][LD],
+                    uint16_t (&Kn)[KS][LD], uint16_t (&Vn)[KS][LD]) {
+        if (kt + 1 < ntiles) fetch(kt + 1, Kn, Vn);   // freed by the last barrier
         const bool full = (kt + 1) * KS <= klen &&
                           (!causal || (kt + 1) * KS - 1 <= q0 + diag);
         const int j0 = kt * KS + 4 * h;
@@ -490,10 +501,10 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
             f32x16 sacc = zero16(), pacc = zero16();
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
-                sacc = mfma32x32x16bf16(load_bf16x8(&Kr[cb][32 * kb + c][16 * s + 8 * h]),
-                                        qreg[s], sacc);
-                pacc = mfma32x32x16bf16(load_bf16x8(&Vr[cb][32 * kb + c][16 * s + 8 * h]),
-                                        oreg[s], pacc);
+                sacc = mfma32x32x16bf16(load_bf16x8(&Kc[32 * kb + c][16 * s + 8 * h]), qreg[s],
+                                        sacc);
+                pacc = mfma32x32x16bf16(load_bf16x8(&Vc[32 * kb + c][16 * s + 8 * h]), oreg[s],
+                                        pacc);
             }
             // dS^T = P^T (dP^T - D), P^T = exp2(S^T * scale*log2e - LSE*log2e)
 #pragma unroll
@@ -509,12 +520,19 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
 #pragma unroll
                 for (int cb2 = 0; cb2 < NCB; ++cb2)
                     dqacc[cb2] = mfma32x32x16bf16(
-                        load_tr_pair<LD>(Kr[cb], r0, r0 + 8, 32 * cb2 + 16 * (c >> 4), jr, jc),
-                        sb, dqacc[cb2]);
+                        load_tr_pair<LD>(Kc, r0, r0 + 8, 32 * cb2 + 16 * (c >> 4), jr, jc), sb,
+                        dqacc[cb2]);
             }
         }
         wait_vmcnt<0>();   // next K/V tile landed
-        __syncthreads();   // it is visible; buffer cb is free
+        __syncthreads();   // it is visible; buffers (Kc, Vc) are free
+    };
+    if (ntiles > 0) fetch(0, Kr0, Vr0);
+    wait_vmcnt<0>();
+    __syncthreads();
+    for (int kt = 0; kt < ntiles; kt += 2) {
+        step(kt, Kr0, Vr0, Kr1, Vr1);
+        if (kt + 1 < ntiles) step(kt + 1, Kr1, Vr1, Kr0, Vr0);
     }
 
     if (qi < Lq) {

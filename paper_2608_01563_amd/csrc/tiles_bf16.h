@@ -26,6 +26,16 @@ template <> struct Bf16Ld<32> { static constexpr int value = 56; };
 template <> struct Bf16Ld<64> { static constexpr int value = 72; };
 template <> struct Bf16Ld<128> { static constexpr int value = 152; };
 
+// Row stride (u16) of the streamed tiles of the 16-key dK/dV kernel, whose
+// reads are 16 rows x 4 chunks (16-byte, 16x16x32 operands) and 4-row
+// transpose reads: a stride of 32 bytes modulo 64 serves both without
+// conflicts (the strides above serve the 32-row reads of the 32x32x16
+// kernels and conflict here).
+template <int D> struct Bf16LdKV;
+template <> struct Bf16LdKV<32> { static constexpr int value = 48; };
+template <> struct Bf16LdKV<64> { static constexpr int value = 80; };
+template <> struct Bf16LdKV<128> { static constexpr int value = 144; };
+
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 // Transpose read (see above): `p` is this lane's 8-byte chunk address.
