@@ -56,11 +56,11 @@ __device__ __forceinline__ f16x8 pack_f16_half(const f32x16 &a, int t) {
 }
 
 // An f32 [ROWS][D] tile staged through registers and written to LDS as f16
-// (row stride LD in 16-bit units).  Chunk f (4 floats) of the tile is row
+// (row stride LDD in 16-bit units, a parameter of the store).  Chunk f (4 floats) of the tile is row
 // f / (D/4), columns 4*(f % (D/4)); consecutive threads take consecutive
 // chunks, so global reads are coalesced and LDS writes contiguous per row.
 // Rows at or beyond L read as zeros (buffer descriptor over rows below L).
-template <int ROWS, int D, int NT, int LD>
+template <int ROWS, int D, int NT>
 struct F16ConvStager {
     static constexpr int kCpr = D / 4;
     static constexpr int kPer = ROWS * kCpr / NT;
@@ -74,7 +74,8 @@ struct F16ConvStager {
 #pragma unroll
         for (int u = 0; u < kPer; ++u) buf[u] = buffer_load_f32x4(rsrc, 16 * (tid + u * NT));
     }
-    __device__ __forceinline__ void store(uint16_t (*dst)[LD], int tid) const {
+    template <int LDD>
+    __device__ __forceinline__ void store(uint16_t (*dst)[LDD], int tid) const {
 #pragma unroll
         for (int u = 0; u < kPer; ++u) {
             const int f = tid + u * NT;
@@ -97,10 +98,11 @@ void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
     constexpr int NS = D / 16;    // 16-deep contraction steps over d
     constexpr int NCB = D / 32;   // 32-column blocks of d
     constexpr int NKB = kKeys / 32;
-    constexpr int LD = Bf16Ld<D>::value;   // 16-bit row stride (bank-conflict free)
-    using St = F16ConvStager<kKeys, D, kThreads, LD>;
+    constexpr int LD = Bf16Ld<D>::value;     // K rows: 16-byte reads of 32 rows
+    constexpr int LDV = Bf16LdTr<D>::value;  // V rows: transpose reads only
+    using St = F16ConvStager<kKeys, D, kThreads>;
     __shared__ __attribute__((aligned(16))) uint16_t Kr[kKeys][LD];
-    __shared__ __attribute__((aligned(16))) uint16_t Vr[kKeys][LD];
+    __shared__ __attribute__((aligned(16))) uint16_t Vr[kKeys][LDV];
 
     const int slot = blockIdx.x / BH;
     const int head = blockIdx.x - slot * BH;
@@ -233,7 +235,7 @@ void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
 #pragma unroll
                 for (int cb = 0; cb < NCB; ++cb)
                     oacc[cb] = mfma32x32x16f16(
-                        __builtin_bit_cast(f16x8, load_tr_pair<LD>(Vr, r0, r0 + 8,
+                        __builtin_bit_cast(f16x8, load_tr_pair<LDV>(Vr, r0, r0 + 8,
                                                                    32 * cb + 16 * (c >> 4), jr, jc)),
                         pb, oacc[cb]);
             }

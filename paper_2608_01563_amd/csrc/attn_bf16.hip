@@ -66,15 +66,18 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
     constexpr int NS = D / 16;    // 16-deep contraction steps over d
     constexpr int NCB = D / 32;   // 32-column blocks of d
     constexpr int NKB = kStream / 32;
-    constexpr int LD = Bf16Ld<D>::value;
-    // rows move as D/2 floats into LDS rows of LD/2 floats (the padded layout)
+    constexpr int LD = Bf16Ld<D>::value;     // K: 16-byte reads of 32 rows
+    constexpr int LDV = Bf16LdTr<D>::value;  // V: transpose reads only
+    // rows move as D/2 floats into LDS rows of LD/2 (LDV/2) floats
     using Tile = RowDirectTile<kStream, D / 2, kWaves, LD / 2>;
-    static_assert(Tile::kEven, "the vmcnt waits below count kPerWave loads per fetch");
+    using TileV = RowDirectTile<kStream, D / 2, kWaves, LDV / 2>;
+    static_assert(Tile::kEven && TileV::kPerWave == Tile::kPerWave,
+                  "the vmcnt waits below count kPerWave loads per fetch");
     constexpr int NL = Tile::kPerWave;
     __shared__ __attribute__((aligned(16))) uint16_t Kr[kStream][LD];
-    __shared__ __attribute__((aligned(16))) uint16_t Vr[kStream][LD];
+    __shared__ __attribute__((aligned(16))) uint16_t Vr[kStream][LDV];
     auto kdst = reinterpret_cast<float (*)[LD / 2]>(&Kr[0][0]);
-    auto vdst = reinterpret_cast<float (*)[LD / 2]>(&Vr[0][0]);
+    auto vdst = reinterpret_cast<float (*)[LDV / 2]>(&Vr[0][0]);
 
     const int slot = blockIdx.x / BH;
     const int head = blockIdx.x - slot * BH;
@@ -100,11 +103,12 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
     // K and V tiles: direct-to-LDS row loads; the next K tile is fetched
     // during P V, the next V tile during the next S = K Q^T.
     const Tile tile;
+    const TileV tilev;
     const float *Kf = reinterpret_cast<const float *>(K + hoff);
     const float *Vf = reinterpret_cast<const float *>(V + hoff);
     if (ntiles > 0) {
         tile.issue(kdst, Kf, 0, Lk, w, lane);
-        tile.issue(vdst, Vf, 0, Lk, w, lane);
+        tilev.issue(vdst, Vf, 0, Lk, w, lane);
     }
 
     // B operand of S^T = K Q^T: lane holds Q[qi][16s + 8h + e].
@@ -202,13 +206,13 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
 #pragma unroll
                 for (int cb = 0; cb < NCB; ++cb)
                     oacc[cb] = mfma32x32x16bf16(
-                        load_tr_pair<LD>(Vr, r0, r0 + 8, 32 * cb + 16 * (c >> 4), jr, jc), pb,
+                        load_tr_pair<LDV>(Vr, r0, r0 + 8, 32 * cb + 16 * (c >> 4), jr, jc), pb,
                         oacc[cb]);
             }
 
         wait_vmcnt<0>();   // K(kt+1) landed
         __syncthreads();   // every wave is done with V(kt) and sees K(kt+1)
-        if (kt + 1 < ntiles) tile.issue(vdst, Vf, (kt + 1) * kStream, Lk, w, lane);
+        if (kt + 1 < ntiles) tilev.issue(vdst, Vf, (kt + 1) * kStream, Lk, w, lane);
     }
 
     const float l = sum_xor32(l_run);

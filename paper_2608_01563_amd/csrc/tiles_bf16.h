@@ -26,6 +26,16 @@ template <> struct Bf16Ld<32> { static constexpr int value = 56; };
 template <> struct Bf16Ld<64> { static constexpr int value = 72; };
 template <> struct Bf16Ld<128> { static constexpr int value = 152; };
 
+// Row stride (u16) of a streamed tile that is only ever read by 4-row
+// transpose reads feeding 32x32x16 products (the V tile of the forward): a
+// stride of 0 bytes modulo 64 serves them without conflicts (the strides
+// above, which also serve 16-byte reads of 32 rows, cost such a read twice
+// the minimum).
+template <int D> struct Bf16LdTr;
+template <> struct Bf16LdTr<32> { static constexpr int value = 32; };
+template <> struct Bf16LdTr<64> { static constexpr int value = 96; };
+template <> struct Bf16LdTr<128> { static constexpr int value = 160; };
+
 // Row stride (u16) of the streamed tiles of the 16-key dK/dV kernel, whose
 // reads are 16 rows x 4 chunks (16-byte, 16x16x32 operands) and 4-row
 // transpose reads: a stride of 32 bytes modulo 64 serves both without
