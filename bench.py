@@ -63,6 +63,9 @@ def parse():
     ap.add_argument("--conv", action="store_true",
                     help="time the convolution derivatives of one ResNet-50 backward step "
                          "(batch 4, 224x224) instead of attention")
+    ap.add_argument("--lds-probe", action="store_true",
+                    help="print the LDS clocks per read of the kernels' access patterns for "
+                         "the row strides they use and the alternatives, then exit")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="repeat the oracle sample until this much CPU wall time (>= 3 runs)")
@@ -182,8 +185,48 @@ def traffic_for(kernel, workload_name, conv=False):
     return rec.get("kernels", {}).get(kernel, {}).get("bytes_per_launch")
 
 
+# The kernels' LDS read patterns (mg_lds_probe numbering) and the tiles that
+# use them, with the row stride each tile uses (bytes).
+LDS_PATTERNS = [
+    (0, "16x16x32 operand rows: bf16 dK/dV Q, dO tiles", {32: 96, 64: 160, 128: 288}),
+    (3, "16x16x32 transpose reads: bf16 dK/dV Q^T, dO^T", {32: 96, 64: 160, 128: 288}),
+    (2, "32x32x16 operand rows: bf16/accelerated forward K, bf16 dQ K and V",
+     {32: 112, 64: 144, 128: 304}),
+    (4, "32x32x16 transpose reads: forward V^T", {32: 64, 64: 192, 128: 320}),
+    (4, "32x32x16 transpose reads: bf16 dQ K^T (tile shared with its row reads)",
+     {32: 112, 64: 144, 128: 304}),
+    (1, "16x16x4 f32 operand groups: strict fused backward Q, dO tiles", {32: 144, 64: 272}),
+    (6, "f32 products over rows: strict fused backward dO, Q (4-byte reads)", {32: 144, 64: 272}),
+]
+
+
+def lds_probe_main():
+    """One JSON line: for each pattern and head dimension, the clocks per
+    read at the stride the kernel uses and at every stride of the same row
+    length padded by 0..240 bytes."""
+    import torch
+    import paper_2608_01563_amd as mg
+    torch.cuda.set_device(0)
+    mg.load_library()
+    out = {"metric": "LDS clocks per read instruction per CU (probe)",
+           "contiguous_16B": mg.mg_lds_probe(5, 256), "patterns": []}
+    for pattern, what, strides in LDS_PATTERNS:
+        for d, used in strides.items():
+            row = {"pattern": pattern, "tile": what, "d": d, "used": used, "by_stride": {}}
+            base = {32: 64, 64: 128, 128: 256}[d] if pattern not in (1, 6) else {32: 128, 64: 256}[d]
+            for pad in range(0, 256, 16):
+                rb = base + pad
+                if rb <= 480:
+                    row["by_stride"][rb] = round(mg.mg_lds_probe(pattern, rb), 2)
+            row["clocks_used"] = row["by_stride"].get(used, round(mg.mg_lds_probe(pattern, used), 2))
+            out["patterns"].append(row)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
+    if args.lds_probe:
+        return lds_probe_main()
     if args.gpus != 1:
         print("bench.py: this build runs on one GPU only; --gpus %d is not supported "
               "(B*H heads shard across GPUs with no exchange, see the design notes)"

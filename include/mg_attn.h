@@ -240,6 +240,29 @@ void mg_profile_reset(void);
  */
 mg_status_t mg_mfma_peak(int kind, int iters, double *tflops, hipStream_t stream);
 
+/*
+ * LDS read cost of one access pattern, for choosing the row strides of the
+ * kernels' LDS tiles (a measuring tool, like mg_mfma_peak; synchronous).
+ * Every wave of two 4-wave workgroups per CU issues `iters` x 8 reads of the
+ * pattern back to back; *clocks receives the shader clocks one read
+ * instruction costs a CU (its waves share the LDS), from the waves' own
+ * clock counters.  A 16-byte read of 64 lanes moves 1 KB, so 4 clocks is
+ * 256 bytes per clock, the conflict-free rate.  `row_bytes` (a multiple of
+ * 16 in [16, 480]) is the row stride of the tile the pattern reads; lane l:
+ *   0: 16-byte read, row l%16, chunk l/16        (16x16x32 operand rows)
+ *   1: 16-byte read, row l%16, byte 64*(l/16)    (16x16x4 f32 operand groups)
+ *   2: 16-byte read, row l%32, chunk l/32        (32x32x16 operand rows)
+ *   3: 8-byte transpose read, row 4*(l/16) + (l%16)/4, byte 8*(l%4)
+ *      (16x16x32 products over the tile's rows)
+ *   4: 8-byte transpose read, row 4*(l/32) + (l%16)/4,
+ *      byte 32*((l/16)%2) + 8*(l%4)               (32x32x16 products)
+ *   5: 16-byte read at byte 16*l                   (contiguous reference)
+ *   6: 4-byte read, row 4*(l/16), word l%16      (f32 products over rows)
+ * Allocates nothing.
+ */
+mg_status_t mg_lds_probe(int pattern, int row_bytes, int iters, double *clocks,
+                         hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -32,6 +32,7 @@ from ._binding import (  # noqa: F401
     mg_conv2d_bwd_filter_workspace_bytes,
     mg_conv2d_bwd_workspace_bytes,
     mg_last_error_detail,
+    mg_lds_probe,
     mg_mfma_peak,
     mg_profile_collect,
     mg_profile_enable,

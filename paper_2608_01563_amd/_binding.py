@@ -88,6 +88,8 @@ def _declare(lib):
     lib.mg_profile_collect.restype = c_int
     lib.mg_mfma_peak.argtypes = [c_int, c_int, ctypes.POINTER(ctypes.c_double), vp]
     lib.mg_mfma_peak.restype = c_int
+    lib.mg_lds_probe.argtypes = [c_int, c_int, c_int, ctypes.POINTER(ctypes.c_double), vp]
+    lib.mg_lds_probe.restype = c_int
     lib.mg_profile_reset.argtypes = []
     lib.mg_profile_reset.restype = None
     return lib
@@ -424,6 +426,15 @@ def mg_mfma_peak(kind="f32", iters=20000, stream=None):
     out = ctypes.c_double(0.0)
     _check(load_library().mg_mfma_peak(MFMA_KINDS[kind], int(iters), ctypes.byref(out),
                                        _stream_handle(stream)))
+    return out.value
+
+
+def mg_lds_probe(pattern, row_bytes, iters=4000, stream=None):
+    """LDS clocks per read instruction per CU for one of the kernels' access
+    patterns (0-6, see mg_attn.h) on rows of `row_bytes` bytes; waits."""
+    out = ctypes.c_double(0.0)
+    _check(load_library().mg_lds_probe(int(pattern), int(row_bytes), int(iters),
+                                       ctypes.byref(out), _stream_handle(stream)))
     return out.value
 
 

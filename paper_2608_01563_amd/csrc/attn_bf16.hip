@@ -278,15 +278,17 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
                     float scale_log2, int BH, int layer) {
     constexpr int NS = D / 32;
     constexpr int NC = D / 16;
+    constexpr int QR = kStream;      // query rows per streamed tile
+    constexpr int QB = QR / 16;      // 16-row blocks per tile
     constexpr int LD = Bf16LdKV<D>::value;
     // Q and dO rows move as D/2 floats into double-buffered padded LDS tiles
     // by direct-to-LDS loads: the next tile is fetched during the whole
     // current iteration, and one barrier per iteration suffices.
-    using Tile = RowDirectTile<kStream, D / 2, kWaves, LD / 2>;
-    __shared__ __attribute__((aligned(16))) uint16_t Qr0[kStream][LD], Qr1[kStream][LD];
-    __shared__ __attribute__((aligned(16))) uint16_t Or0[kStream][LD], Or1[kStream][LD];
-    __shared__ __attribute__((aligned(16))) float lse0[kStream], lse1[kStream];   // LSE (natural log)
-    __shared__ __attribute__((aligned(16))) float Ds0[kStream], Ds1[kStream];
+    using Tile = RowDirectTile<QR, D / 2, kWaves, LD / 2>;
+    __shared__ __attribute__((aligned(16))) uint16_t Qr0[QR][LD], Qr1[QR][LD];
+    __shared__ __attribute__((aligned(16))) uint16_t Or0[QR][LD], Or1[QR][LD];
+    __shared__ __attribute__((aligned(16))) float lse0[QR], lse1[QR];   // LSE (natural log)
+    __shared__ __attribute__((aligned(16))) float Ds0[QR], Ds1[QR];
 
     const int slot = blockIdx.x / BH;
     const int head = blockIdx.x - slot * BH;
@@ -305,9 +307,9 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
     const int kj = k0 + 16 * w + il;
 
     const int klen = key_limit(key_len, b, Lk);
-    const int nq = (Lq + kStream - 1) / kStream;
+    const int nq = (Lq + QR - 1) / QR;
     // first query tile holding a row that sees key k0
-    const int qstart = causal ? min(nq, max(0, k0 - diag) / kStream) : 0;
+    const int qstart = causal ? min(nq, max(0, k0 - diag) / QR) : 0;
     const int qstop = (k0 < klen) ? nq : qstart;
 
     bf16x8 kreg[NS], vreg[NS];
@@ -327,15 +329,16 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
     // Direct-to-LDS loads of the Q and dO rows of tile qt and of their LSE
     // (natural log; wave 0) and D (the last wave) values; rows past Lq arrive
     // as zeros.
-    auto fetch = [&](int qt, uint16_t (&Qn)[kStream][LD], uint16_t (&On)[kStream][LD],
-                     float (&ln)[kStream], float (&dn)[kStream]) {
-        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Qn[0][0]), Qf, qt * kStream, Lq, w, lane);
-        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&On[0][0]), Of, qt * kStream, Lq, w, lane);
+    auto fetch = [&](int qt, uint16_t (&Qn)[QR][LD], uint16_t (&On)[QR][LD],
+                     float (&ln)[QR], float (&dn)[QR]) {
+        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Qn[0][0]), Qf, qt * QR, Lq, w, lane);
+        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&On[0][0]), Of, qt * QR, Lq, w, lane);
         if (w == 0 || w == kWaves - 1) {
-            const int row0 = qt * kStream;
-            const int rows = min(max(Lq - row0, 0), kStream);
+            const int row0 = qt * QR;
+            const int rows = min(max(Lq - row0, 0), QR);
             const float *src = (w == 0 ? LSE : Dws) + (size_t)head * Lq + row0;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+            if (lane < QR)
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(
                 buffer_rsrc(src, rows * 4),
                 (__attribute__((address_space(3))) void *)(w == 0 ? &ln[0] : &dn[0]), 4,
                 lane * 4, 0, 0, 0);
@@ -344,31 +347,31 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
 
     // One query tile from buffers (Qc, Oc, lc, dc) while tile qt + 1 loads
     // into (Qn, On, ln, dn).
-    auto step = [&](int qt, uint16_t (&Qc)[kStream][LD], uint16_t (&Oc)[kStream][LD],
-                    float (&lc)[kStream], float (&dc)[kStream], uint16_t (&Qn)[kStream][LD],
-                    uint16_t (&On)[kStream][LD], float (&ln)[kStream], float (&dn)[kStream]) {
+    auto step = [&](int qt, uint16_t (&Qc)[QR][LD], uint16_t (&Oc)[QR][LD],
+                    float (&lc)[QR], float (&dc)[QR], uint16_t (&Qn)[QR][LD],
+                    uint16_t (&On)[QR][LD], float (&ln)[QR], float (&dn)[QR]) {
         if (qt + 1 < qstop) fetch(qt + 1, Qn, On, ln, dn);   // freed by the last barrier
 
-        f32x4 sacc[kBlk], pacc[kBlk];
+        f32x4 sacc[QB], pacc[QB];
 #pragma unroll
-        for (int ib = 0; ib < kBlk; ++ib) {
+        for (int ib = 0; ib < QB; ++ib) {
             sacc[ib] = zero4();
             pacc[ib] = zero4();
         }
 #pragma unroll
         for (int s = 0; s < NS; ++s)
 #pragma unroll
-            for (int ib = 0; ib < kBlk; ++ib) {
+            for (int ib = 0; ib < QB; ++ib) {
                 sacc[ib] = mfma16x16x32bf16(load_bf16x8(&Qc[16 * ib + il][32 * s + 8 * g]),
                                             kreg[s], sacc[ib]);
                 pacc[ib] = mfma16x16x32bf16(load_bf16x8(&Oc[16 * ib + il][32 * s + 8 * g]),
                                             vreg[s], pacc[ib]);
             }
 
-        const int ibase = qt * kStream + 4 * g;
+        const int ibase = qt * QR + 4 * g;
         const int thr = causal ? kj - diag - ibase : -(1 << 30);
 #pragma unroll
-        for (int ib = 0; ib < kBlk; ++ib) {
+        for (int ib = 0; ib < QB; ++ib) {
             const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lc[16 * ib + 4 * g]) * kLog2e;
             const f32x4 dd = *reinterpret_cast<const f32x4 *>(&dc[16 * ib + 4 * g]);
 #pragma unroll
@@ -382,7 +385,7 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
 
         // dV^T[16c + .][kj] += dO^T[16c + il'][i] P[i][kj]; dK^T likewise with Q, dS
 #pragma unroll
-        for (int t = 0; t < kBlk / 2; ++t) {
+        for (int t = 0; t < QB / 2; ++t) {
             const bf16x8 pb = pack_bf16(sacc[2 * t], sacc[2 * t + 1]);
             const bf16x8 sb = pack_bf16(pacc[2 * t], pacc[2 * t + 1]);
             const int r0 = 32 * t + 4 * g;

@@ -198,6 +198,10 @@ void runtime_checks() {
     EXPECT(mg_mfma_peak(3, 100, &out, nullptr) == MG_ERR_INVALID_ARGUMENT);
     EXPECT(mg_mfma_peak(0, 0, &out, nullptr) == MG_ERR_INVALID_ARGUMENT);
     EXPECT(mg_mfma_peak(1, 100, nullptr, nullptr) == MG_ERR_INVALID_ARGUMENT);
+    EXPECT(mg_lds_probe(7, 256, 100, &out, nullptr) == MG_ERR_INVALID_ARGUMENT);
+    EXPECT(mg_lds_probe(0, 264, 100, &out, nullptr) == MG_ERR_INVALID_ARGUMENT);
+    EXPECT(mg_lds_probe(0, 256, 0, &out, nullptr) == MG_ERR_INVALID_ARGUMENT);
+    EXPECT(mg_lds_probe(0, 256, 100, nullptr, nullptr) == MG_ERR_INVALID_ARGUMENT);
     // the profiler with nothing recorded
     EXPECT(mg_profile_enable(1) == MG_OK);
     const char *names[4];

@@ -263,6 +263,15 @@ def test_mfma_probe_rejects_bad_arguments_before_any_device_call(lib):
     assert mg.mg_last_error_detail() != ""
 
 
+def test_lds_probe_rejects_bad_arguments_before_any_device_call(lib):
+    out = ctypes.c_double(0.0)
+    for args in ((7, 256, 100), (-1, 256, 100), (0, 8, 100), (0, 488, 100), (0, 264, 100),
+                 (0, 256, 0), (0, 256, (1 << 20) + 1)):
+        assert lib.mg_lds_probe(*args, ctypes.byref(out), None) == 1, args
+    assert lib.mg_lds_probe(0, 256, 100, None, None) == 1
+    assert mg.mg_last_error_detail() != ""
+
+
 def test_error_detail_is_per_thread(lib):
     """mg_last_error_detail describes the calling thread's last call only."""
     import threading
