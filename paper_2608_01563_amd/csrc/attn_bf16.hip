@@ -66,18 +66,11 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
     constexpr int NS = D / 16;    // 16-deep contraction steps over d
     constexpr int NCB = D / 32;   // 32-column blocks of d
     constexpr int NKB = kStream / 32;
-    constexpr int LD = Bf16Ld<D>::value;     // K: 16-byte reads of 32 rows
-    constexpr int LDV = Bf16LdTr<D>::value;  // V: transpose reads only
-    // rows move as D/2 floats into LDS rows of LD/2 (LDV/2) floats
-    using Tile = RowDirectTile<kStream, D / 2, kWaves, LD / 2>;
-    using TileV = RowDirectTile<kStream, D / 2, kWaves, LDV / 2>;
-    static_assert(Tile::kEven && TileV::kPerWave == Tile::kPerWave,
-                  "the vmcnt waits below count kPerWave loads per fetch");
-    constexpr int NL = Tile::kPerWave;
-    __shared__ __attribute__((aligned(16))) uint16_t Kr[kStream][LD];
-    __shared__ __attribute__((aligned(16))) uint16_t Vr[kStream][LDV];
-    auto kdst = reinterpret_cast<float (*)[LD / 2]>(&Kr[0][0]);
-    auto vdst = reinterpret_cast<float (*)[LDV / 2]>(&Vr[0][0]);
+    using Tile = Bf16Tile<kStream, D, kWaves, 2>;
+    constexpr int NL = Tile::kPerWave;   // loads per wave per tile (the vmcnt waits below)
+    constexpr int BLK = Tile::kBlock;
+    __shared__ __attribute__((aligned(16))) uint16_t Kr[Tile::kSize];
+    __shared__ __attribute__((aligned(16))) uint16_t Vr[Tile::kSize];
 
     const int slot = blockIdx.x / BH;
     const int head = blockIdx.x - slot * BH;
@@ -100,16 +93,20 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
     const int kend = causal ? min(klen, q0 + kFwdRows + diag) : klen;
     const int ntiles = (kend + kStream - 1) / kStream;
 
-    // K and V tiles: direct-to-LDS row loads; the next K tile is fetched
+    // K and V tiles: 16-byte direct-to-LDS loads; the next K tile is fetched
     // during P V, the next V tile during the next S = K Q^T.
-    const Tile tile;
-    const TileV tilev;
-    const float *Kf = reinterpret_cast<const float *>(K + hoff);
-    const float *Vf = reinterpret_cast<const float *>(V + hoff);
+    Tile tile;
+    tile.init(lane);
     if (ntiles > 0) {
-        tile.issue(kdst, Kf, 0, Lk, w, lane);
-        tilev.issue(vdst, Vf, 0, Lk, w, lane);
+        tile.issue(Kr, K + hoff, 0, Lk, w);
+        tile.issue(Vr, V + hoff, 0, Lk, w);
     }
+    // Lane bases of the tile reads.  K: row 32kb + c, chunk 2(s%2) + h of
+    // block s/2 (kc[s%2]); V^T: rows 32kb + 16t + 4h + jr (+8) of column
+    // 32cb + 16(c/16) + jc (vlo, vhi).
+    const int kc[2] = {Tile::at(c, 8 * h), Tile::at(c, 16 + 8 * h)};
+    const int vlo = Tile::at(4 * h + jr, 16 * (c >> 4) + jc);
+    const int vhi = Tile::at(4 * h + jr + 8, 16 * (c >> 4) + jc);
 
     // B operand of S^T = K Q^T: lane holds Q[qi][16s + 8h + e].
     bf16x8 qreg[NS];
@@ -135,12 +132,13 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
             sacc[kb] = zero16();
 #pragma unroll
             for (int s = 0; s < NS; ++s)
-                sacc[kb] = mfma32x32x16bf16(load_bf16x8(&Kr[32 * kb + c][16 * s + 8 * h]),
-                                            qreg[s], sacc[kb]);
+                sacc[kb] = mfma32x32x16bf16(
+                    load_bf16x8(Kr + kc[s & 1] + (s >> 1) * BLK + 32 * 32 * kb), qreg[s],
+                    sacc[kb]);
         }
         wait_vmcnt<0>();   // V(kt) landed
         __syncthreads();   // every wave is done with K(kt) and sees V(kt)
-        if (kt + 1 < ntiles) tile.issue(kdst, Kf, (kt + 1) * kStream, Lk, w, lane);
+        if (kt + 1 < ntiles) tile.issue(Kr, K + hoff, (kt + 1) * kStream, Lk, w);
         if (!POS_SCALE) {
 #pragma unroll
             for (int kb = 0; kb < NKB; ++kb) sacc[kb] *= scale_log2;
@@ -202,17 +200,17 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
                 const bf16x8 pb = pack_bf16_half(sacc[kb], t);
-                const int r0 = 32 * kb + 16 * t + 4 * h;
+                const int r0 = 32 * (32 * kb + 16 * t);
 #pragma unroll
                 for (int cb = 0; cb < NCB; ++cb)
                     oacc[cb] = mfma32x32x16bf16(
-                        load_tr_pair<LDV>(Vr, r0, r0 + 8, 32 * cb + 16 * (c >> 4), jr, jc), pb,
+                        load_tr_pair_at(Vr + vlo + cb * BLK + r0, Vr + vhi + cb * BLK + r0), pb,
                         oacc[cb]);
             }
 
         wait_vmcnt<0>();   // K(kt+1) landed
         __syncthreads();   // every wave is done with V(kt) and sees K(kt+1)
-        if (kt + 1 < ntiles) tilev.issue(vdst, Vf, (kt + 1) * kStream, Lk, w, lane);
+        if (kt + 1 < ntiles) tile.issue(Vr, V + hoff, (kt + 1) * kStream, Lk, w);
     }
 
     const float l = sum_xor32(l_run);
@@ -280,13 +278,13 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
     constexpr int NC = D / 16;
     constexpr int QR = kStream;      // query rows per streamed tile
     constexpr int QB = QR / 16;      // 16-row blocks per tile
-    constexpr int LD = Bf16LdKV<D>::value;
-    // Q and dO rows move as D/2 floats into double-buffered padded LDS tiles
-    // by direct-to-LDS loads: the next tile is fetched during the whole
-    // current iteration, and one barrier per iteration suffices.
-    using Tile = RowDirectTile<QR, D / 2, kWaves, LD / 2>;
-    __shared__ __attribute__((aligned(16))) uint16_t Qr0[QR][LD], Qr1[QR][LD];
-    __shared__ __attribute__((aligned(16))) uint16_t Or0[QR][LD], Or1[QR][LD];
+    // Q and dO tiles are double-buffered and arrive by 16-byte direct-to-LDS
+    // loads: the next tile is fetched during the whole current iteration,
+    // and one barrier per iteration suffices.
+    using Tile = Bf16Tile<QR, D, kWaves, 1>;
+    constexpr int BLK = Tile::kBlock;
+    __shared__ __attribute__((aligned(16))) uint16_t Qr0[Tile::kSize], Qr1[Tile::kSize];
+    __shared__ __attribute__((aligned(16))) uint16_t Or0[Tile::kSize], Or1[Tile::kSize];
     __shared__ __attribute__((aligned(16))) float lse0[QR], lse1[QR];   // LSE (natural log)
     __shared__ __attribute__((aligned(16))) float Ds0[QR], Ds1[QR];
 
@@ -323,16 +321,20 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
         dvacc[c] = zero4();
     }
 
-    const Tile tile;
-    const float *Qf = reinterpret_cast<const float *>(Q + qoff);
-    const float *Of = reinterpret_cast<const float *>(dO + qoff);
+    Tile tile;
+    tile.init(lane);
+    // Lane bases of the tile reads.  Q, dO rows: row 16ib + il, chunk g of
+    // block s (qa); Q^T, dO^T: rows 32t + 4g + jr (+16) of column 16c + jc
+    // (qb[c%2], block c/2).
+    const int qa = Tile::at(il, 8 * g);
+    const int qb[2] = {Tile::at(4 * g + jr, jc), Tile::at(4 * g + jr, 16 + jc)};
     // Direct-to-LDS loads of the Q and dO rows of tile qt and of their LSE
     // (natural log; wave 0) and D (the last wave) values; rows past Lq arrive
     // as zeros.
-    auto fetch = [&](int qt, uint16_t (&Qn)[QR][LD], uint16_t (&On)[QR][LD],
-                     float (&ln)[QR], float (&dn)[QR]) {
-        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Qn[0][0]), Qf, qt * QR, Lq, w, lane);
-        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&On[0][0]), Of, qt * QR, Lq, w, lane);
+    using Buf = uint16_t[Tile::kSize];
+    auto fetch = [&](int qt, Buf &Qn, Buf &On, float (&ln)[QR], float (&dn)[QR]) {
+        tile.issue(Qn, Q + qoff, qt * QR, Lq, w);
+        tile.issue(On, dO + qoff, qt * QR, Lq, w);
         if (w == 0 || w == kWaves - 1) {
             const int row0 = qt * QR;
             const int rows = min(max(Lq - row0, 0), QR);
@@ -347,9 +349,8 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
 
     // One query tile from buffers (Qc, Oc, lc, dc) while tile qt + 1 loads
     // into (Qn, On, ln, dn).
-    auto step = [&](int qt, uint16_t (&Qc)[QR][LD], uint16_t (&Oc)[QR][LD],
-                    float (&lc)[QR], float (&dc)[QR], uint16_t (&Qn)[QR][LD],
-                    uint16_t (&On)[QR][LD], float (&ln)[QR], float (&dn)[QR]) {
+    auto step = [&](int qt, Buf &Qc, Buf &Oc, float (&lc)[QR], float (&dc)[QR], Buf &Qn,
+                    Buf &On, float (&ln)[QR], float (&dn)[QR]) {
         if (qt + 1 < qstop) fetch(qt + 1, Qn, On, ln, dn);   // freed by the last barrier
 
         f32x4 sacc[QB], pacc[QB];
@@ -362,9 +363,9 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
         for (int s = 0; s < NS; ++s)
 #pragma unroll
             for (int ib = 0; ib < QB; ++ib) {
-                sacc[ib] = mfma16x16x32bf16(load_bf16x8(&Qc[16 * ib + il][32 * s + 8 * g]),
+                sacc[ib] = mfma16x16x32bf16(load_bf16x8(Qc + qa + s * BLK + 16 * 32 * ib),
                                             kreg[s], sacc[ib]);
-                pacc[ib] = mfma16x16x32bf16(load_bf16x8(&Oc[16 * ib + il][32 * s + 8 * g]),
+                pacc[ib] = mfma16x16x32bf16(load_bf16x8(Oc + qa + s * BLK + 16 * 32 * ib),
                                             vreg[s], pacc[ib]);
             }
 
@@ -388,13 +389,14 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
         for (int t = 0; t < QB / 2; ++t) {
             const bf16x8 pb = pack_bf16(sacc[2 * t], sacc[2 * t + 1]);
             const bf16x8 sb = pack_bf16(pacc[2 * t], pacc[2 * t + 1]);
-            const int r0 = 32 * t + 4 * g;
+            const int r0 = 32 * 32 * t;
 #pragma unroll
             for (int c = 0; c < NC; ++c) {
-                dvacc[c] = mfma16x16x32bf16(load_tr_pair<LD>(Oc, r0, r0 + 16, 16 * c, jr, jc),
-                                            pb, dvacc[c]);
-                dkacc[c] = mfma16x16x32bf16(load_tr_pair<LD>(Qc, r0, r0 + 16, 16 * c, jr, jc),
-                                            sb, dkacc[c]);
+                const int o = qb[c & 1] + (c >> 1) * BLK + r0;
+                dvacc[c] = mfma16x16x32bf16(load_tr_pair_at(Oc + o, Oc + o + 16 * 32), pb,
+                                            dvacc[c]);
+                dkacc[c] = mfma16x16x32bf16(load_tr_pair_at(Qc + o, Qc + o + 16 * 32), sb,
+                                            dkacc[c]);
             }
         }
 
@@ -444,12 +446,12 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
     constexpr int NS = D / 16;
     constexpr int NCB = D / 32;
     constexpr int NKB = KS / 32;
-    constexpr int LD = Bf16Ld<D>::value;
-    // K and V rows move as D/2 floats into double-buffered padded LDS tiles:
-    // the next tile is fetched during the whole current iteration.
-    using Tile = RowDirectTile<KS, D / 2, kWaves, LD / 2>;
-    __shared__ __attribute__((aligned(16))) uint16_t Kr0[KS][LD], Kr1[KS][LD];
-    __shared__ __attribute__((aligned(16))) uint16_t Vr0[KS][LD], Vr1[KS][LD];
+    // K and V tiles are double-buffered and arrive by 16-byte direct-to-LDS
+    // loads: the next tile is fetched during the whole current iteration.
+    using Tile = Bf16Tile<KS, D, kWaves, 2>;
+    constexpr int BLK = Tile::kBlock;
+    __shared__ __attribute__((aligned(16))) uint16_t Kr0[Tile::kSize], Kr1[Tile::kSize];
+    __shared__ __attribute__((aligned(16))) uint16_t Vr0[Tile::kSize], Vr1[Tile::kSize];
 
     const int slot = blockIdx.x / BH;
     const int head = blockIdx.x - slot * BH;
@@ -487,16 +489,21 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb) dqacc[cb] = zero16();
 
-    const Tile tile;
-    const float *Kf = reinterpret_cast<const float *>(K + hoff);
-    const float *Vf = reinterpret_cast<const float *>(V + hoff);
-    auto fetch = [&](int t, uint16_t (&Kn)[KS][LD], uint16_t (&Vn)[KS][LD]) {
-        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Kn[0][0]), Kf, t * KS, Lk, w, lane);
-        tile.issue(reinterpret_cast<float (*)[LD / 2]>(&Vn[0][0]), Vf, t * KS, Lk, w, lane);
+    Tile tile;
+    tile.init(lane);
+    // Lane bases of the tile reads.  K, V rows: row 32kb + c, chunk
+    // 2(s%2) + h of block s/2 (kc[s%2]); K^T: rows 32kb + 16t + 4h + jr (+8)
+    // of column 32cb + 16(c/16) + jc (klo, khi).
+    const int kc[2] = {Tile::at(c, 8 * h), Tile::at(c, 16 + 8 * h)};
+    const int klo = Tile::at(4 * h + jr, 16 * (c >> 4) + jc);
+    const int khi = Tile::at(4 * h + jr + 8, 16 * (c >> 4) + jc);
+    using Buf = uint16_t[Tile::kSize];
+    auto fetch = [&](int t, Buf &Kn, Buf &Vn) {
+        tile.issue(Kn, K + hoff, t * KS, Lk, w);
+        tile.issue(Vn, V + hoff, t * KS, Lk, w);
     };
     // key tile kt from (Kc, Vc) while tile kt + 1 loads into (Kn, Vn)
-    auto step = [&](int kt, uint16_t (&Kc)[KS][LD], uint16_t (&Vc)[KS][LD],
-                    uint16_t (&Kn)[KS][LD], uint16_t (&Vn)[KS][LD]) {
+    auto step = [&](int kt, Buf &Kc, Buf &Vc, Buf &Kn, Buf &Vn) {
         if (kt + 1 < ntiles) fetch(kt + 1, Kn, Vn);   // freed by the last barrier
         const bool full = (kt + 1) * KS <= klen &&
                           (!causal || (kt + 1) * KS - 1 <= q0 + diag);
@@ -508,10 +515,9 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
             f32x16 sacc = zero16(), pacc = zero16();
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
-                sacc = mfma32x32x16bf16(load_bf16x8(&Kc[32 * kb + c][16 * s + 8 * h]), qreg[s],
-                                        sacc);
-                pacc = mfma32x32x16bf16(load_bf16x8(&Vc[32 * kb + c][16 * s + 8 * h]), oreg[s],
-                                        pacc);
+                const int o = kc[s & 1] + (s >> 1) * BLK + 32 * 32 * kb;
+                sacc = mfma32x32x16bf16(load_bf16x8(Kc + o), qreg[s], sacc);
+                pacc = mfma32x32x16bf16(load_bf16x8(Vc + o), oreg[s], pacc);
             }
             // dS^T = P^T (dP^T - D), P^T = exp2(S^T * scale*log2e - LSE*log2e)
 #pragma unroll
@@ -523,12 +529,12 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
                 const bf16x8 sb = pack_bf16_half(pacc, t);
-                const int r0 = 32 * kb + 16 * t + 4 * h;
+                const int r0 = 32 * (32 * kb + 16 * t);
 #pragma unroll
                 for (int cb2 = 0; cb2 < NCB; ++cb2)
                     dqacc[cb2] = mfma32x32x16bf16(
-                        load_tr_pair<LD>(Kc, r0, r0 + 8, 32 * cb2 + 16 * (c >> 4), jr, jc), sb,
-                        dqacc[cb2]);
+                        load_tr_pair_at(Kc + klo + cb2 * BLK + r0, Kc + khi + cb2 * BLK + r0),
+                        sb, dqacc[cb2]);
             }
         }
         wait_vmcnt<0>();   // next K/V tile landed
