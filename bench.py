@@ -188,22 +188,29 @@ def traffic_for(kernel, workload_name, conv=False):
 # The kernels' LDS read patterns (mg_lds_probe numbering) and the tiles that
 # use them, with the row stride each tile uses (bytes).
 LDS_PATTERNS = [
-    (0, "16x16x32 operand rows: bf16 dK/dV Q, dO tiles", {32: 96, 64: 160, 128: 288}),
-    (3, "16x16x32 transpose reads: bf16 dK/dV Q^T, dO^T", {32: 96, 64: 160, 128: 288}),
-    (2, "32x32x16 operand rows: bf16/accelerated forward K, bf16 dQ K and V",
-     {32: 112, 64: 144, 128: 304}),
-    (4, "32x32x16 transpose reads: forward V^T", {32: 64, 64: 192, 128: 320}),
-    (4, "32x32x16 transpose reads: bf16 dQ K^T (tile shared with its row reads)",
-     {32: 112, 64: 144, 128: 304}),
+    (2, "32x32x16 operand rows: accelerated forward K", {32: 112, 64: 144, 128: 304}),
+    (4, "32x32x16 transpose reads: accelerated forward V^T", {32: 64, 64: 192, 128: 320}),
     (1, "16x16x4 f32 operand groups: strict fused backward Q, dO tiles", {32: 144, 64: 272}),
     (6, "f32 products over rows: strict fused backward dO, Q (4-byte reads)", {32: 144, 64: 272}),
+    (0, "16x16x32 operand rows on padded rows (reference for pattern 7)", {128: 288}),
+    (3, "16x16x32 transpose reads on padded rows (reference for pattern 8)", {128: 288}),
+]
+# The bf16 kernels' swizzled column-block tiles (pattern, what), each beside
+# the same reads on unswizzled blocks (pattern + 5).
+LDS_BLOCK_PATTERNS = [
+    (7, "bf16 dK/dV Q, dO rows (16x16x32 operands)"),
+    (8, "bf16 dK/dV Q^T, dO^T (16x16x32 transpose reads)"),
+    (9, "bf16 forward K, dQ K and V rows (32x32x16 operands)"),
+    (10, "bf16 dQ K^T (32x32x16 transpose reads)"),
+    (11, "bf16 forward V^T (32x32x16 transpose reads, 64-column blocks)"),
 ]
 
 
 def lds_probe_main():
-    """One JSON line: for each pattern and head dimension, the clocks per
-    read at the stride the kernel uses and at every stride of the same row
-    length padded by 0..240 bytes."""
+    """One JSON line: for each padded-row pattern and head dimension, the
+    clocks per read at the stride the kernel uses and at every stride of the
+    same row length padded by 0..240 bytes; for the bf16 kernels' column-block
+    tiles, the clocks per read with and without their chunk swizzle."""
     import torch
     import paper_2608_01563_amd as mg
     torch.cuda.set_device(0)
@@ -220,6 +227,13 @@ def lds_probe_main():
                     row["by_stride"][rb] = round(mg.mg_lds_probe(pattern, rb), 2)
             row["clocks_used"] = row["by_stride"].get(used, round(mg.mg_lds_probe(pattern, used), 2))
             out["patterns"].append(row)
+    out["block_layouts"] = []
+    for pattern, what in LDS_BLOCK_PATTERNS:
+        rb = 128 if pattern == 11 else 64
+        out["block_layouts"].append({
+            "pattern": pattern, "tile": what, "row_bytes": rb,
+            "clocks_swizzled": round(mg.mg_lds_probe(pattern, rb), 2),
+            "clocks_unswizzled": round(mg.mg_lds_probe(pattern + 5, rb), 2)})
     print(json.dumps(out), flush=True)
 
 

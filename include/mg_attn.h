@@ -258,6 +258,21 @@ mg_status_t mg_mfma_peak(int kind, int iters, double *tflops, hipStream_t stream
  *      byte 32*((l/16)%2) + 8*(l%4)               (32x32x16 products)
  *   5: 16-byte read at byte 16*l                   (contiguous reference)
  *   6: 4-byte read, row 4*(l/16), word l%16      (f32 products over rows)
+ * Patterns 7..11 read the bf16 kernels' tiles themselves: [64][128] bf16
+ * stored as column blocks of 32 (64-byte rows) or 64 columns (128-byte
+ * rows), whose 16-byte chunks are permuted per row (chunk j of row r at
+ * j ^ swz(r)); `row_bytes` must be that block row (128 for 11 and 16, else
+ * 64):
+ *   7: 16-byte read, row l%16, columns 8*(l/16)..+7, swz = (r/2)%4
+ *      (dK/dV Q and dO tiles)
+ *   8: transpose read of the same tile, row 4*(l/16) + (l%16)/4, columns
+ *      4*(l%4)..+3
+ *   9: 16-byte read, row l%32, columns 8*(l/32)..+7, swz = (r/4)%4
+ *      (forward K, dQ K and V)
+ *  10: transpose read of that tile, row 4*(l/32) + (l%16)/4, columns
+ *      16*((l/16)%2) + 4*(l%4)..+3                (dQ K^T)
+ *  11: as 10 on 64-column blocks, swz = 4*((r/2)%2) (forward V^T)
+ *  12..16: patterns 7..11 with no chunk permutation (swz = 0).
  * Allocates nothing.
  */
 mg_status_t mg_lds_probe(int pattern, int row_bytes, int iters, double *clocks,

@@ -16,6 +16,8 @@
 // operand (a column of the row-major tile) comes from transpose reads.
 //   16x16x32 (dK/dV): rows 32t + 16*(e/4) + 4g + e%4, g = lane/16
 //   32x32x16 (forward, dQ): rows 16t + 8*(e/4) + 4h + e%4, h = lane/32
+#include <type_traits>
+
 #include "device_common.h"
 #include "launch.h"
 #include "tiles_bf16.h"
@@ -66,11 +68,17 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
     constexpr int NS = D / 16;    // 16-deep contraction steps over d
     constexpr int NCB = D / 32;   // 32-column blocks of d
     constexpr int NKB = kStream / 32;
-    using Tile = Bf16Tile<kStream, D, kWaves, 2>;
+    // K: 16-byte reads of 32 rows x 2 chunks (32-column blocks, swizzle
+    // (r/4) % 4); V: transpose reads only, which 64-column blocks (swizzle
+    // 4((r/2) % 2)) serve as well, loaded in 128-byte pieces.
+    using Tile = Bf16Tile<kStream, D, kWaves, 32, 2, 3, 1>;
+    constexpr int VW = (D >= 64) ? 64 : 32;
+    using TileV = std::conditional_t<VW == 64, Bf16Tile<kStream, D, kWaves, 64, 1, 1, 4>, Tile>;
     constexpr int NL = Tile::kPerWave;   // loads per wave per tile (the vmcnt waits below)
-    constexpr int BLK = Tile::kBlock;
+    static_assert(TileV::kPerWave == NL, "K and V loads per wave");
+    constexpr int BLK = Tile::kBlock, BLKV = TileV::kBlock;
     __shared__ __attribute__((aligned(16))) uint16_t Kr[Tile::kSize];
-    __shared__ __attribute__((aligned(16))) uint16_t Vr[Tile::kSize];
+    __shared__ __attribute__((aligned(16))) uint16_t Vr[TileV::kSize];
 
     const int slot = blockIdx.x / BH;
     const int head = blockIdx.x - slot * BH;
@@ -97,16 +105,23 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
     // during P V, the next V tile during the next S = K Q^T.
     Tile tile;
     tile.init(lane);
+    TileV tilev;
+    tilev.init(lane);
     if (ntiles > 0) {
         tile.issue(Kr, K + hoff, 0, Lk, w);
-        tile.issue(Vr, V + hoff, 0, Lk, w);
+        tilev.issue(Vr, V + hoff, 0, Lk, w);
     }
     // Lane bases of the tile reads.  K: row 32kb + c, chunk 2(s%2) + h of
     // block s/2 (kc[s%2]); V^T: rows 32kb + 16t + 4h + jr (+8) of column
-    // 32cb + 16(c/16) + jc (vlo, vhi).
+    // 32cb + 16(c/16) + jc (vlo, vhi; one pair per 32 columns of a block).
     const int kc[2] = {Tile::at(c, 8 * h), Tile::at(c, 16 + 8 * h)};
-    const int vlo = Tile::at(4 * h + jr, 16 * (c >> 4) + jc);
-    const int vhi = Tile::at(4 * h + jr + 8, 16 * (c >> 4) + jc);
+    constexpr int NV = VW / 32;
+    int vlo[NV], vhi[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        vlo[i] = TileV::at(4 * h + jr, 32 * i + 16 * (c >> 4) + jc);
+        vhi[i] = TileV::at(4 * h + jr + 8, 32 * i + 16 * (c >> 4) + jc);
+    }
 
     // B operand of S^T = K Q^T: lane holds Q[qi][16s + 8h + e].
     bf16x8 qreg[NS];
@@ -200,17 +215,19 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
                 const bf16x8 pb = pack_bf16_half(sacc[kb], t);
-                const int r0 = 32 * (32 * kb + 16 * t);
+                const int r0 = VW * (32 * kb + 16 * t);
 #pragma unroll
-                for (int cb = 0; cb < NCB; ++cb)
+                for (int cb = 0; cb < NCB; ++cb) {
+                    const int o = (cb / NV) * BLKV + r0;
                     oacc[cb] = mfma32x32x16bf16(
-                        load_tr_pair_at(Vr + vlo + cb * BLK + r0, Vr + vhi + cb * BLK + r0), pb,
+                        load_tr_pair_at(Vr + vlo[cb % NV] + o, Vr + vhi[cb % NV] + o), pb,
                         oacc[cb]);
+                }
             }
 
         wait_vmcnt<0>();   // K(kt+1) landed
         __syncthreads();   // every wave is done with V(kt) and sees K(kt+1)
-        if (kt + 1 < ntiles) tile.issue(Vr, V + hoff, (kt + 1) * kStream, Lk, w);
+        if (kt + 1 < ntiles) tilev.issue(Vr, V + hoff, (kt + 1) * kStream, Lk, w);
     }
 
     const float l = sum_xor32(l_run);
@@ -281,7 +298,8 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
     // Q and dO tiles are double-buffered and arrive by 16-byte direct-to-LDS
     // loads: the next tile is fetched during the whole current iteration,
     // and one barrier per iteration suffices.
-    using Tile = Bf16Tile<QR, D, kWaves, 1>;
+    constexpr int TW = 32;   // column block width of the tiles
+    using Tile = Bf16Tile<QR, D, kWaves, TW, 1, 3, 1>;
     constexpr int BLK = Tile::kBlock;
     __shared__ __attribute__((aligned(16))) uint16_t Qr0[Tile::kSize], Qr1[Tile::kSize];
     __shared__ __attribute__((aligned(16))) uint16_t Or0[Tile::kSize], Or1[Tile::kSize];
@@ -323,11 +341,16 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
 
     Tile tile;
     tile.init(lane);
-    // Lane bases of the tile reads.  Q, dO rows: row 16ib + il, chunk g of
-    // block s (qa); Q^T, dO^T: rows 32t + 4g + jr (+16) of column 16c + jc
-    // (qb[c%2], block c/2).
-    const int qa = Tile::at(il, 8 * g);
-    const int qb[2] = {Tile::at(4 * g + jr, jc), Tile::at(4 * g + jr, 16 + jc)};
+    // Lane bases of the tile reads (TW-column blocks).  Q, dO rows: row
+    // 16ib + il, columns 32s + 8g (qa[s % (TW/32)], block 32s/TW); Q^T, dO^T:
+    // rows 32t + 4g + jr (+16) of columns 16c + jc (qb[c % (TW/16)], block
+    // 16c/TW).
+    constexpr int NA = TW / 32, NB = TW / 16;
+    int qa[NA], qb[NB];
+#pragma unroll
+    for (int i = 0; i < NA; ++i) qa[i] = Tile::at(il, 32 * i + 8 * g);
+#pragma unroll
+    for (int i = 0; i < NB; ++i) qb[i] = Tile::at(4 * g + jr, 16 * i + jc);
     // Direct-to-LDS loads of the Q and dO rows of tile qt and of their LSE
     // (natural log; wave 0) and D (the last wave) values; rows past Lq arrive
     // as zeros.
@@ -363,10 +386,9 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
         for (int s = 0; s < NS; ++s)
 #pragma unroll
             for (int ib = 0; ib < QB; ++ib) {
-                sacc[ib] = mfma16x16x32bf16(load_bf16x8(Qc + qa + s * BLK + 16 * 32 * ib),
-                                            kreg[s], sacc[ib]);
-                pacc[ib] = mfma16x16x32bf16(load_bf16x8(Oc + qa + s * BLK + 16 * 32 * ib),
-                                            vreg[s], pacc[ib]);
+                const int o = qa[s % NA] + (s / NA) * BLK + 16 * TW * ib;
+                sacc[ib] = mfma16x16x32bf16(load_bf16x8(Qc + o), kreg[s], sacc[ib]);
+                pacc[ib] = mfma16x16x32bf16(load_bf16x8(Oc + o), vreg[s], pacc[ib]);
             }
 
         const int ibase = qt * QR + 4 * g;
@@ -389,13 +411,13 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
         for (int t = 0; t < QB / 2; ++t) {
             const bf16x8 pb = pack_bf16(sacc[2 * t], sacc[2 * t + 1]);
             const bf16x8 sb = pack_bf16(pacc[2 * t], pacc[2 * t + 1]);
-            const int r0 = 32 * 32 * t;
+            const int r0 = 32 * TW * t;
 #pragma unroll
             for (int c = 0; c < NC; ++c) {
-                const int o = qb[c & 1] + (c >> 1) * BLK + r0;
-                dvacc[c] = mfma16x16x32bf16(load_tr_pair_at(Oc + o, Oc + o + 16 * 32), pb,
+                const int o = qb[c % NB] + (c / NB) * BLK + r0;
+                dvacc[c] = mfma16x16x32bf16(load_tr_pair_at(Oc + o, Oc + o + 16 * TW), pb,
                                             dvacc[c]);
-                dkacc[c] = mfma16x16x32bf16(load_tr_pair_at(Qc + o, Qc + o + 16 * 32), sb,
+                dkacc[c] = mfma16x16x32bf16(load_tr_pair_at(Qc + o, Qc + o + 16 * TW), sb,
                                             dkacc[c]);
             }
         }
@@ -448,7 +470,7 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
     constexpr int NKB = KS / 32;
     // K and V tiles are double-buffered and arrive by 16-byte direct-to-LDS
     // loads: the next tile is fetched during the whole current iteration.
-    using Tile = Bf16Tile<KS, D, kWaves, 2>;
+    using Tile = Bf16Tile<KS, D, kWaves, 32, 2, 3, 1>;
     constexpr int BLK = Tile::kBlock;
     __shared__ __attribute__((aligned(16))) uint16_t Kr0[Tile::kSize], Kr1[Tile::kSize];
     __shared__ __attribute__((aligned(16))) uint16_t Vr0[Tile::kSize], Vr1[Tile::kSize];

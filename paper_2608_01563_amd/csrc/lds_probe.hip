@@ -13,6 +13,7 @@
 
 #include "device_common.h"
 #include "host_runtime.h"
+#include "tiles_bf16.h"
 
 namespace mg {
 
@@ -30,9 +31,45 @@ constexpr int kProbeWgThreads = 256;
 constexpr int kProbeWords = 16384;   // 64 KB of LDS per workgroup
 constexpr int kReadsPerStep = 8;
 
+// The bf16 kernels' tile layouts ([64 rows][128 columns] in column blocks),
+// and the same blocks without the chunk swizzle.
+using KvTile = Bf16Tile<64, 128, 4, 32, 1, 3, 1>;      // dK/dV: Q, dO
+using RowTile = Bf16Tile<64, 128, 4, 32, 2, 3, 1>;     // forward K, dQ K and V
+using TrTile = Bf16Tile<64, 128, 4, 64, 1, 1, 4>;      // forward V
+using Plain32 = Bf16Tile<64, 128, 4, 32, 0, 0, 0>;
+using Plain64 = Bf16Tile<64, 128, 4, 64, 0, 0, 0>;
+
+// Row and column that lane l reads in the block-layout patterns (7..16).
+__host__ __device__ inline int block_row(int p, int l) {
+    switch ((p - 7) % 5) {
+    case 0: return l & 15;                                 // 16 rows x 4 chunks
+    case 1: return 4 * (l >> 4) + ((l & 15) >> 2);          // 16-row transpose
+    case 2: return l & 31;                                 // 32 rows x 2 chunks
+    default: return 4 * (l >> 5) + ((l & 15) >> 2);         // 32x32 transpose
+    }
+}
+__host__ __device__ inline int block_col(int p, int l) {
+    switch ((p - 7) % 5) {
+    case 0: return 8 * (l >> 4);
+    case 1: return 4 * (l & 3);
+    case 2: return 8 * (l >> 5);
+    default: return 16 * ((l >> 4) & 1) + 4 * (l & 3);
+    }
+}
+
 // Byte offset of lane `l`'s read in pattern `p` for rows of `rb` bytes.
 __host__ __device__ inline int probe_offset(int p, int l, int rb) {
     const int il = l & 15, g = l >> 4, jr = il >> 2, jc = 4 * (il & 3);
+    if (p >= 7) {
+        const int r = block_row(p, l), e = block_col(p, l);
+        switch (p) {
+        case 7: case 8: return 2 * KvTile::at(r, e);
+        case 9: case 10: return 2 * RowTile::at(r, e);
+        case 11: return 2 * TrTile::at(r, e);
+        case 16: return 2 * Plain64::at(r, e);
+        default: return 2 * Plain32::at(r, e);
+        }
+    }
     switch (p) {
     case 0: return il * rb + 16 * g;                               // 16 rows x 4 adjacent chunks
     case 1: return il * rb + 64 * g;                               // 16 rows x 4 chunks 64 B apart
@@ -46,7 +83,14 @@ __host__ __device__ inline int probe_offset(int p, int l, int rb) {
 }
 
 // 0: 16-byte reads, 1: 8-byte transpose reads, 2: 4-byte reads
-__host__ __device__ constexpr int probe_kind(int p) { return (p == 3 || p == 4) ? 1 : (p == 6 ? 2 : 0); }
+__host__ __device__ constexpr int probe_kind(int p) {
+    return (p == 3 || p == 4 || p == 8 || p == 10 || p == 11 || p == 13 || p == 15 || p == 16)
+               ? 1
+               : (p == 6 ? 2 : 0);
+}
+
+// Row length (bytes) of the block-layout patterns' tiles.
+__host__ __device__ constexpr int block_row_bytes(int p) { return (p == 11 || p == 16) ? 128 : 64; }
 
 typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 
@@ -109,6 +153,9 @@ __global__ __launch_bounds__(kProbeWgThreads) void lds_probe(int pattern, int rb
 constexpr int kMaxRowBytes = 480;
 static_assert(31 * kMaxRowBytes + 16 + 3 * 4096 + 25600 + 16 <= 4 * kProbeWords,
               "probe reads must stay inside the LDS array");
+// The block-layout tiles are 16 KB.
+static_assert(2 * KvTile::kSize + 3 * 4096 + 25600 <= 4 * kProbeWords,
+              "block-layout reads must stay inside the LDS array");
 
 }  // namespace
 }  // namespace mg
@@ -118,8 +165,11 @@ using namespace mg::host;
 
 extern "C" mg_status_t mg_lds_probe(int pattern, int row_bytes, int iters, double *clocks,
                                     hipStream_t stream) {
-    if (pattern < 0 || pattern > 6)
-        return fail(MG_ERR_INVALID_ARGUMENT, "pattern %d outside [0, 6]", pattern);
+    if (pattern < 0 || pattern > 16)
+        return fail(MG_ERR_INVALID_ARGUMENT, "pattern %d outside [0, 16]", pattern);
+    if (pattern >= 7 && row_bytes != block_row_bytes(pattern))
+        return fail(MG_ERR_INVALID_ARGUMENT, "pattern %d reads %d-byte block rows, not %d",
+                    pattern, block_row_bytes(pattern), row_bytes);
     if (row_bytes < 16 || row_bytes > kMaxRowBytes || row_bytes % 16 != 0)
         return fail(MG_ERR_INVALID_ARGUMENT,
                     "row_bytes %d must be a multiple of 16 in [16, %d]", row_bytes, kMaxRowBytes);

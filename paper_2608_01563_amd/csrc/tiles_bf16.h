@@ -46,46 +46,52 @@ template <> struct Bf16LdKV<32> { static constexpr int value = 48; };
 template <> struct Bf16LdKV<64> { static constexpr int value = 80; };
 template <> struct Bf16LdKV<128> { static constexpr int value = 144; };
 
-// A [ROWS][D] bf16 tile stored as D/32 column blocks of [ROWS][32] (64-byte
-// rows), the four 16-byte chunks of row r permuted by j -> j ^ ((r >> SH) & 3).
-// It arrives by 16-byte direct-to-LDS loads: one load fills 1 KB, 16 rows of
-// one block, from 64-byte pieces of 16 global rows; a compute unit moves
-// more than twice the bytes per clock this way than with the 4-byte row
-// loads of tiles_direct.h.  The swizzle spreads the rows that one read instruction touches over
-// all 64 banks: SH = 2 serves the 32x32x16 kernels (16-byte reads of 32 rows
-// x 2 chunks and 4-row transpose reads of 8 rows x 64 bytes), SH = 1 the
-// 16x16x32 dK/dV kernel (16-byte reads of 16 rows x 4 chunks and transpose
-// reads of 16 rows x 32 bytes); all of them then run at the LDS's minimum
-// cycles per read.  Within a block, the chunk the swizzle moves depends only
-// on bits of the row that a lane's read pattern fixes, so every read is a
-// per-lane base (one or two per pattern) plus a compile-time offset.  Rows at or beyond L arrive as zeros.
-template <int ROWS, int D, int NW, int SH>
+// A [ROWS][D] bf16 tile stored as D/W column blocks of [ROWS][W] (rows of
+// 2W bytes), the 16-byte chunks of row r permuted by j -> j ^ swz(r) with
+// swz(r) = ((r >> SS) & SM) * SK.  It arrives by 16-byte direct-to-LDS
+// loads: one load fills 1 KB, 512/W rows of one block, from 2W-byte pieces
+// of as many global rows; a compute unit moves two to three times the bytes
+// per clock this way than with the 4-byte row loads of tiles_direct.h (more
+// with longer pieces).  The swizzle spreads the rows that one read
+// instruction touches over all 64 banks; the kernels pick, per tile, one
+// under which each of their read patterns runs at the LDS's minimum cycles
+// per instruction (measured: 16-byte reads of 16 rows x 4 chunks or 32 rows
+// x 2 chunks, 4-row transpose reads of 16 rows x 32 bytes or 8 rows x 64
+// bytes).  The chunk a swizzle moves depends only on bits of the row that a
+// lane's read pattern fixes, so every read is one of a few per-lane bases
+// plus a compile-time offset, and a load's lane offsets are the same for
+// every load of the tile.  Rows at or beyond L arrive as zeros.
+template <int ROWS, int D, int NW, int W, int SS, int SM, int SK>
 struct Bf16Tile {
-    static_assert(ROWS % 16 == 0 && D % 32 == 0 && (SH == 1 || SH == 2), "tile shape");
-    static constexpr int kBlock = ROWS * 32;    // u16 per column block
+    static constexpr int kRowsPerLoad = 512 / W;
+    static_assert((W == 32 || W == 64) && D % W == 0 && ROWS % kRowsPerLoad == 0, "tile shape");
+    static_assert(SM * SK < W / 8 && (kRowsPerLoad >> SS) % (SM + 1) == 0,
+                  "the swizzle stays inside a row and repeats every load");
+    static constexpr int kBlock = ROWS * W;     // u16 per column block
     static constexpr int kSize = ROWS * D;      // u16 per tile
     static constexpr int kLoads = kSize / 512;  // 1 KB loads per tile
     static constexpr int kPerWave = kLoads / NW;
     static_assert(kLoads % NW == 0, "every wave issues the same number of loads");
 
-    __host__ __device__ static constexpr int swz(int r) { return (r >> SH) & 3; }
+    __host__ __device__ static constexpr int swz(int r) { return ((r >> SS) & SM) * SK; }
     // u16 offset of element (r, e) in the tile
     __host__ __device__ static constexpr int at(int r, int e) {
-        return (e >> 5) * kBlock + r * 32 + 8 * (((e >> 3) & 3) ^ swz(r)) + (e & 7);
+        return (e / W) * kBlock + r * W + 8 * (((e % W) >> 3) ^ swz(r)) + (e & 7);
     }
 
-    int voff;   // this lane's byte offset within a group of 16 global rows
+    int voff;   // this lane's byte offset within the rows of one load
 
     __device__ __forceinline__ void init(int lane) {
-        // LDS chunk `lane` of a load is row lane/4 of the group, chunk
-        // position lane%4, which holds logical chunk (lane%4) ^ swz(lane/4)
-        voff = (lane >> 2) * D * 2 + 16 * ((lane & 3) ^ swz(lane >> 2));
+        // LDS chunk `lane` of a load is row lane / (W/8) of the load, chunk
+        // position lane % (W/8), which holds logical chunk position ^ swz(row)
+        const int r = lane / (W / 8), j = lane % (W / 8);
+        voff = r * D * 2 + 16 * (j ^ swz(r));
     }
 
     // This wave's share of rows [row0, row0 + ROWS) of src (row-major, D
     // bf16 per row) into dst (kSize u16 of LDS); kPerWave loads, tracked by
-    // the wave's vmcnt.  The group offset goes into the vector offset, the
-    // one the buffer's range check sees.
+    // the wave's vmcnt.  A load's row and block offset goes into the vector
+    // offset, the one the buffer's range check sees.
     __device__ __forceinline__ void issue(uint16_t *dst, const uint16_t *__restrict__ src,
                                           int row0, int L, int w) const {
         const int rows = min(max(L - row0, 0), ROWS);
@@ -93,10 +99,10 @@ struct Bf16Tile {
 #pragma unroll
         for (int uu = 0; uu < kPerWave; ++uu) {
             const int u = uu * NW + w;
-            const int goff = ((16 * u) % ROWS) * D * 2 + 64 * ((16 * u) / ROWS);
+            const int r0 = (kRowsPerLoad * u) % ROWS, blk = (kRowsPerLoad * u) / ROWS;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rsrc, (__attribute__((address_space(3))) void *)(dst + 512 * u), 16, voff + goff,
-                0, 0, 0);
+                rsrc, (__attribute__((address_space(3))) void *)(dst + 512 * u), 16,
+                voff + r0 * D * 2 + 2 * W * blk, 0, 0, 0);
         }
     }
 };
