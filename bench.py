@@ -82,7 +82,7 @@ def parse():
 def kernel_source_digest(conv=False):
     """sha256 over the names and contents of the files a kernel family is
     built from (attention: every file directly under csrc/ except the MFMA
-    probe; convolution:
+    and LDS probes; convolution:
     csrc/conv/ plus the shared device and host headers): a counter record
     taken on any other source is stale."""
     h = hashlib.sha256()
@@ -91,8 +91,8 @@ def kernel_source_digest(conv=False):
         names = ["conv/" + n for n in sorted(os.listdir(os.path.join(base, "conv")))]
         names += ["device_common.h", "host_runtime.h", "host_runtime.cpp"]
     else:
-        # the MFMA probe is a measuring tool, not attention code
-        names = sorted(n for n in os.listdir(base) if n != "mfma_probe.hip")
+        # the MFMA and LDS probes are measuring tools, not attention code
+        names = sorted(n for n in os.listdir(base) if n not in ("mfma_probe.hip", "lds_probe.hip"))
     for name in names:
         path = os.path.join(base, name)
         if os.path.isfile(path):
@@ -204,6 +204,12 @@ LDS_BLOCK_PATTERNS = [
     (10, "bf16 dQ K^T (32x32x16 transpose reads)"),
     (11, "bf16 forward V^T (32x32x16 transpose reads, 64-column blocks)"),
 ]
+# The strict f32 forward's chunk-permuted d = 64 tiles (pattern, what, the
+# same read shape on unpermuted 256-byte rows: (pattern, row bytes)).
+LDS_F32_FWD_PATTERNS = [
+    (17, "f32 forward K (16x16x4 operand groups)", (1, 256)),
+    (18, "f32 forward V (4-byte reads over rows)", (6, 256)),
+]
 
 
 def lds_probe_main():
@@ -234,6 +240,11 @@ def lds_probe_main():
             "pattern": pattern, "tile": what, "row_bytes": rb,
             "clocks_swizzled": round(mg.mg_lds_probe(pattern, rb), 2),
             "clocks_unswizzled": round(mg.mg_lds_probe(pattern + 5, rb), 2)})
+    for pattern, what, (plain, prb) in LDS_F32_FWD_PATTERNS:
+        out["block_layouts"].append({
+            "pattern": pattern, "tile": what, "row_bytes": 256,
+            "clocks_swizzled": round(mg.mg_lds_probe(pattern, 256), 2),
+            "clocks_unswizzled": round(mg.mg_lds_probe(plain, prb), 2)})
     print(json.dumps(out), flush=True)
 
 

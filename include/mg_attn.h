@@ -273,6 +273,11 @@ mg_status_t mg_mfma_peak(int kind, int iters, double *tflops, hipStream_t stream
  *      16*((l/16)%2) + 4*(l%4)..+3                (dQ K^T)
  *  11: as 10 on 64-column blocks, swz = 4*((r/2)%2) (forward V^T)
  *  12..16: patterns 7..11 with no chunk permutation (swz = 0).
+ * Patterns 17 and 18 read the strict f32 forward's d = 64 tiles: 256-byte
+ * rows whose 16-byte chunk j of row r sits at j ^ (r % 16); `row_bytes` must
+ * be 256:
+ *  17: 16-byte read, row l%16, floats 16*(l/16)..+3  (K, 16x16x4 operands)
+ *  18: 4-byte read, row 4*(l/16), float l%16        (V, products over rows)
  * Allocates nothing.
  */
 mg_status_t mg_lds_probe(int pattern, int row_bytes, int iters, double *clocks,

@@ -14,6 +14,7 @@
 #include "device_common.h"
 #include "host_runtime.h"
 #include "tiles_bf16.h"
+#include "tiles_direct.h"
 
 namespace mg {
 
@@ -38,6 +39,9 @@ using RowTile = Bf16Tile<64, 128, 4, 32, 2, 3, 1>;     // forward K, dQ K and V
 using TrTile = Bf16Tile<64, 128, 4, 64, 1, 1, 4>;      // forward V
 using Plain32 = Bf16Tile<64, 128, 4, 32, 0, 0, 0>;
 using Plain64 = Bf16Tile<64, 128, 4, 64, 0, 0, 0>;
+// The strict f32 forward's K and V tiles at d = 64 (rows of 256 bytes, the
+// 16-byte chunks of row r permuted by j -> j ^ (r % 16)).
+using F32FwdTile = DirectTile<64, 64, 4>;
 
 // Row and column that lane l reads in the block-layout patterns (7..16).
 __host__ __device__ inline int block_row(int p, int l) {
@@ -60,6 +64,8 @@ __host__ __device__ inline int block_col(int p, int l) {
 // Byte offset of lane `l`'s read in pattern `p` for rows of `rb` bytes.
 __host__ __device__ inline int probe_offset(int p, int l, int rb) {
     const int il = l & 15, g = l >> 4, jr = il >> 2, jc = 4 * (il & 3);
+    if (p == 17) return 4 * F32FwdTile::at(il, 16 * g);     // K: row l%16, group l/16
+    if (p == 18) return 4 * F32FwdTile::at(4 * g, il);      // V: row 4(l/16), word l%16
     if (p >= 7) {
         const int r = block_row(p, l), e = block_col(p, l);
         switch (p) {
@@ -86,11 +92,13 @@ __host__ __device__ inline int probe_offset(int p, int l, int rb) {
 __host__ __device__ constexpr int probe_kind(int p) {
     return (p == 3 || p == 4 || p == 8 || p == 10 || p == 11 || p == 13 || p == 15 || p == 16)
                ? 1
-               : (p == 6 ? 2 : 0);
+               : ((p == 6 || p == 18) ? 2 : 0);
 }
 
-// Row length (bytes) of the block-layout patterns' tiles.
-__host__ __device__ constexpr int block_row_bytes(int p) { return (p == 11 || p == 16) ? 128 : 64; }
+// Row length (bytes) of the fixed-layout patterns' tiles (7..18).
+__host__ __device__ constexpr int block_row_bytes(int p) {
+    return p >= 17 ? 256 : ((p == 11 || p == 16) ? 128 : 64);
+}
 
 typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 
@@ -153,9 +161,10 @@ __global__ __launch_bounds__(kProbeWgThreads) void lds_probe(int pattern, int rb
 constexpr int kMaxRowBytes = 480;
 static_assert(31 * kMaxRowBytes + 16 + 3 * 4096 + 25600 + 16 <= 4 * kProbeWords,
               "probe reads must stay inside the LDS array");
-// The block-layout tiles are 16 KB.
-static_assert(2 * KvTile::kSize + 3 * 4096 + 25600 <= 4 * kProbeWords,
-              "block-layout reads must stay inside the LDS array");
+// The block-layout tiles are 16 KB, the f32 forward tile 16 KB.
+static_assert(2 * KvTile::kSize + 3 * 4096 + 25600 <= 4 * kProbeWords &&
+                  4 * 64 * 64 + 3 * 4096 + 25600 <= 4 * kProbeWords,
+              "fixed-layout reads must stay inside the LDS array");
 
 }  // namespace
 }  // namespace mg
@@ -165,10 +174,10 @@ using namespace mg::host;
 
 extern "C" mg_status_t mg_lds_probe(int pattern, int row_bytes, int iters, double *clocks,
                                     hipStream_t stream) {
-    if (pattern < 0 || pattern > 16)
-        return fail(MG_ERR_INVALID_ARGUMENT, "pattern %d outside [0, 16]", pattern);
+    if (pattern < 0 || pattern > 18)
+        return fail(MG_ERR_INVALID_ARGUMENT, "pattern %d outside [0, 18]", pattern);
     if (pattern >= 7 && row_bytes != block_row_bytes(pattern))
-        return fail(MG_ERR_INVALID_ARGUMENT, "pattern %d reads %d-byte block rows, not %d",
+        return fail(MG_ERR_INVALID_ARGUMENT, "pattern %d reads %d-byte tile rows, not %d",
                     pattern, block_row_bytes(pattern), row_bytes);
     if (row_bytes < 16 || row_bytes > kMaxRowBytes || row_bytes % 16 != 0)
         return fail(MG_ERR_INVALID_ARGUMENT,

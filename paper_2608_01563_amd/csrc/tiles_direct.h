@@ -14,7 +14,7 @@ namespace mg {
 // Conflict-free for 16-byte reads of 16 consecutive rows at one chunk
 // position and for 4-byte reads of rows {4g + r : g < 4} x 16 columns.
 template <int D> struct RowXor {
-    __device__ static constexpr int f(int row) { return D == 32 ? ((row >> 1) & 7) : (row & 15); }
+    __host__ __device__ static constexpr int f(int row) { return D == 32 ? ((row >> 1) & 7) : (row & 15); }
 };
 
 // A [ROWS][D] f32 tile copied from global memory straight into LDS with
@@ -35,9 +35,9 @@ struct DirectTile {
     static constexpr bool kEven = kWaveLoads % NW == 0;
     static_assert(ROWS * kCpr % 64 == 0, "tile must be a whole number of 1 KB loads");
 
-    __device__ static constexpr int swz(int row) { return SW::f(row); }
+    __host__ __device__ static constexpr int swz(int row) { return SW::f(row); }
     // Float offset of logical element (row, col) inside the tile.
-    __device__ static constexpr int at(int row, int col) {
+    __host__ __device__ static constexpr int at(int row, int col) {
         return row * D + 4 * ((col >> 2) ^ swz(row)) + (col & 3);
     }
 

@@ -201,6 +201,7 @@ void runtime_checks() {
     EXPECT(mg_lds_probe(7, 256, 100, &out, nullptr) == MG_ERR_INVALID_ARGUMENT);
     EXPECT(mg_lds_probe(11, 64, 100, &out, nullptr) == MG_ERR_INVALID_ARGUMENT);
     EXPECT(mg_lds_probe(17, 64, 100, &out, nullptr) == MG_ERR_INVALID_ARGUMENT);
+    EXPECT(mg_lds_probe(19, 256, 100, &out, nullptr) == MG_ERR_INVALID_ARGUMENT);
     EXPECT(mg_lds_probe(0, 264, 100, &out, nullptr) == MG_ERR_INVALID_ARGUMENT);
     EXPECT(mg_lds_probe(0, 256, 0, &out, nullptr) == MG_ERR_INVALID_ARGUMENT);
     EXPECT(mg_lds_probe(0, 256, 100, nullptr, nullptr) == MG_ERR_INVALID_ARGUMENT);

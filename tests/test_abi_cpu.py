@@ -266,7 +266,7 @@ def test_mfma_probe_rejects_bad_arguments_before_any_device_call(lib):
 def test_lds_probe_rejects_bad_arguments_before_any_device_call(lib):
     out = ctypes.c_double(0.0)
     # block-layout patterns (7..16) take their block row only (64, or 128 for 11 and 16)
-    for args in ((7, 256, 100), (11, 64, 100), (16, 64, 100), (17, 64, 100), (-1, 256, 100),
+    for args in ((7, 256, 100), (11, 64, 100), (16, 64, 100), (17, 64, 100), (18, 128, 100), (19, 256, 100), (-1, 256, 100),
                  (0, 8, 100), (0, 488, 100), (0, 264, 100), (0, 256, 0),
                  (0, 256, (1 << 20) + 1)):
         assert lib.mg_lds_probe(*args, ctypes.byref(out), None) == 1, args

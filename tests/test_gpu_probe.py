@@ -69,3 +69,17 @@ def test_lds_probe_block_layouts_at_the_minimum(gpu_lib):
             assert t <= tr_best * 1.05, (pattern, t, tr_best)
     with pytest.raises(mg.MgError):
         mg.mg_lds_probe(7, 128)            # pattern 7 reads 64-byte block rows
+
+
+def test_lds_probe_f32_forward_tiles_at_the_best_padding(gpu_lib):
+    """The strict f32 forward's chunk-permuted K and V tiles (d = 64): each
+    read costs no more than the cheapest padded stride achieves for the same
+    read shape, and the 16x16x4 operand groups cost several times more on
+    unpermuted 256-byte rows."""
+    import paper_2608_01563_amd as mg
+    for pattern, shape in ((17, 1), (18, 6)):
+        t = mg.mg_lds_probe(pattern, 256, iters=2000)
+        best = min(mg.mg_lds_probe(shape, rb, iters=2000) for rb in (272, 288, 304, 336))
+        say("  f32 forward pattern %d: %.2f clocks, best padded stride %.2f" % (pattern, t, best))
+        assert t <= best * 1.05, (pattern, t, best)
+    assert mg.mg_lds_probe(1, 256, iters=2000) > 2 * mg.mg_lds_probe(17, 256, iters=2000)
