@@ -253,7 +253,7 @@ def main():
     if args.lds_probe:
         return lds_probe_main()
     if args.gpus != 1:
-        print("bench.py: this build runs on one GPU only; --gpus %d is not supported "
+        print("bench.py: the library runs on one GPU only; --gpus %d is not supported "
               "(B*H heads shard across GPUs with no exchange, see the design notes)"
               % args.gpus, file=sys.stderr)
         sys.exit(2)
