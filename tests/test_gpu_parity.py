@@ -13,7 +13,7 @@ import pytest
 
 from gpu_util import (TOL, TOL_ACCEL_ROUNDED, compare, key_len_device, normwise_error,
                       oracle_reference, run_gpu, say, to_device)
-from workloads import WORKLOADS, make_inputs, workload_inputs
+from workloads import WORKLOADS, AttnInputs, make_inputs, workload_inputs
 
 pytestmark = pytest.mark.gpu
 
@@ -264,6 +264,48 @@ def test_padded_keys_exact_zero_bf16(gpu_lib):
     assert torch.count_nonzero(O[1]) == 0 and torch.all(torch.isinf(LSE[1]))
     for t in (dQ, dK, dV):
         assert torch.count_nonzero(t[1]) == 0
+
+
+# One head below the element limit B*H*max(Lq, Lk)*d <= 2^31 - 1 that the
+# C ABI accepts: every tensor spans about 2^31 elements, so each byte offset
+# past 2^32 and each element index past 2^31 - 1 would show here.
+MAX_SIZE_CASES = [("strict_f32", 64, True, 524287, 1), ("fast_bf16", 128, False, 87381, 3)]
+
+
+@pytest.mark.parametrize("contract,d,causal,B,H", MAX_SIZE_CASES,
+                         ids=["strict_d64_causal", "bf16_d128_full"])
+def test_maximum_size_sampled_heads(gpu_lib, contract, d, causal, B, H):
+    """Inputs drawn on the device from a seeded generator; the first, a middle
+    and the last head (the one whose rows end just below 2^31 elements) are
+    copied back and compared with the oracle on exactly those values."""
+    import torch
+    import paper_2608_01563_amd as mg
+    L = 64
+    assert B * H * L * d <= 2 ** 31 - 1 < (B * H + 1) * L * d
+    say("maximum size %s B%d H%d L%d d%d (%.2f G elements per tensor)"
+        % (contract, B, H, L, d, B * H * L * d / 2 ** 30))
+    dt = torch.bfloat16 if contract == "fast_bf16" else torch.float32
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(97)
+    Q, K, V, dO = (torch.randn(B, H, L, d, device="cuda", generator=gen).to(dt) for _ in range(4))
+    scale = d ** -0.5
+    O, LSE = mg.attention_forward(Q, K, V, causal=causal, scale=scale, contract=contract)
+    dQ, dK, dV = mg.attention_backward(Q, K, V, O, LSE, dO, causal=causal, scale=scale,
+                                       contract=contract)
+    torch.cuda.synchronize()
+    heads = [(0, 0), (B // 2, H // 2), (B - 1, H - 1)]
+
+    def sub(t):   # the sampled heads as one batch of len(heads) heads, f32 on the host
+        return np.ascontiguousarray(np.stack([t[b, h].float().cpu().numpy() for b, h in heads])[None])
+
+    x = AttnInputs(Q=sub(Q), K=sub(K), V=sub(V), dO=sub(dO), key_len=None, contract=contract,
+                   causal=causal, scale=scale)
+    got = {n: sub(t) for n, t in zip(("O", "LSE", "dQ", "dK", "dV"), (O, LSE, dQ, dK, dV))}
+    del Q, K, V, dO, O, LSE, dQ, dK, dV
+    torch.cuda.empty_cache()
+    errs = compare(got, oracle_reference(x), contract)
+    say("  errors %s" % {k: "%.2e" % v for k, v in errs.items()})
+    assert max(errs.values()) <= TOL[contract], errs
 
 
 def test_strict_separate_dq_fallback_sampled_heads(gpu_lib):
