@@ -248,6 +248,188 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
     }
 }
 
+// The forward with its key tiles software-pipelined, for d <= 64: the score
+// product of key tile kt+1 is issued in the same iteration as the softmax
+// and P V of tile kt, so the matrix core has independent work while a wave
+// runs its softmax; K and V are both double-buffered (separate named arrays,
+// as in the backward kernels) and every load has a whole iteration to land.
+// At d = 128 the second score block pushes the kernel to two waves per SIMD
+// instead of three, and the plain form above is faster.
+template <int D, bool POS_SCALE>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
+void attn_fwd_bf16_pipe(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
+                        const uint16_t *__restrict__ V, uint16_t *__restrict__ O,
+                        float *__restrict__ LSE, const int32_t *__restrict__ key_len, int H, int Lq,
+                        int Lk, int causal, float scale_log2, int n_qtiles, int BH, int layer) {
+    constexpr int NS = D / 16;
+    constexpr int NCB = D / 32;
+    constexpr int NKB = kStream / 32;
+    using Tile = Bf16Tile<kStream, D, kWaves, 32, 2, 3, 1>;
+    constexpr int VW = (D >= 64) ? 64 : 32;
+    using TileV = std::conditional_t<VW == 64, Bf16Tile<kStream, D, kWaves, 64, 1, 1, 4>, Tile>;
+    constexpr int BLK = Tile::kBlock, BLKV = TileV::kBlock;
+    __shared__ __attribute__((aligned(16))) uint16_t K0[Tile::kSize], K1[Tile::kSize];
+    __shared__ __attribute__((aligned(16))) uint16_t V0[TileV::kSize], V1[TileV::kSize];
+
+    const int slot = blockIdx.x / BH;
+    const int head = blockIdx.x - slot * BH;
+    const int rank = serpentine_rank(slot, n_qtiles, layer);
+    const int qt = causal ? (n_qtiles - 1 - rank) : rank;
+    const int b = head / H;
+    const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
+    const int diag = Lk - Lq;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int c = lane & 31;
+    const int h = lane >> 5;
+    const int jr = (lane & 15) >> 2, jc = 4 * (lane & 3);
+    const int q0 = qt * kFwdRows;
+    const int qi = q0 + 32 * w + c;
+    const int klen = key_limit(key_len, b, Lk);
+    const int kend = causal ? min(klen, q0 + kFwdRows + diag) : klen;
+    const int ntiles = (kend + kStream - 1) / kStream;
+
+    Tile tile;
+    tile.init(lane);
+    TileV tilev;
+    tilev.init(lane);
+    const int kc[2] = {Tile::at(c, 8 * h), Tile::at(c, 16 + 8 * h)};
+    constexpr int NV = VW / 32;
+    int vlo[NV], vhi[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+        vlo[i] = TileV::at(4 * h + jr, 32 * i + 16 * (c >> 4) + jc);
+        vhi[i] = TileV::at(4 * h + jr + 8, 32 * i + 16 * (c >> 4) + jc);
+    }
+    bf16x8 qreg[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s)
+        qreg[s] = (qi < Lq) ? load_bf16x8(Q + qoff + (size_t)qi * D + 16 * s + 8 * h)
+                           : __builtin_bit_cast(bf16x8, u32x4{0u, 0u, 0u, 0u});
+    float m_run = -INFINITY, l_run = 0.f;
+    f32x16 oacc[NCB];
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) oacc[cb] = zero16();
+
+    auto scores = [&](const uint16_t *Kb, f32x16 (&sacc)[NKB]) {
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) {
+            sacc[kb] = zero16();
+#pragma unroll
+            for (int s = 0; s < NS; ++s)
+                sacc[kb] = mfma32x32x16bf16(
+                    load_bf16x8(Kb + kc[s & 1] + (s >> 1) * BLK + 32 * 32 * kb), qreg[s], sacc[kb]);
+        }
+    };
+    auto softmax_pv = [&](int kt, f32x16 (&sacc)[NKB], const uint16_t *Vb) {
+        if (!POS_SCALE) {
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) sacc[kb] *= scale_log2;
+        }
+        const bool full = (kt + 1) * kStream <= klen &&
+                          (!causal || (kt + 1) * kStream - 1 <= q0 + diag);
+        if (!full) {
+            const int j0 = kt * kStream + 4 * h;
+            const int thr = causal ? min(klen - j0, qi + diag - j0 + 1) : klen - j0;
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    if (32 * kb + 8 * (v >> 2) + (v & 3) >= thr) sacc[kb][v] = -INFINITY;
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+            for (int v = 0; v < 16; v += 2) mx = fmaxf(mx, fmaxf(sacc[kb][v], sacc[kb][v + 1]));
+        mx = max_xor32(mx);
+        const float grow2 = POS_SCALE ? (mx - m_run) * scale_log2 : mx - m_run;
+        if (__any(grow2 > kSlack)) {
+            const float m_new = fmaxf(m_run, mx);
+            const float m2_old = POS_SCALE ? m_run * scale_log2 : m_run;
+            const float m2_new =
+                (m_new == -INFINITY) ? 0.f : (POS_SCALE ? m_new * scale_log2 : m_new);
+            const float alpha = exp2_fast(m2_old - m2_new);
+            l_run *= alpha;
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) oacc[cb] *= alpha;
+            m_run = m_new;
+        }
+        const float m2 = (m_run == -INFINITY) ? 0.f : (POS_SCALE ? m_run * scale_log2 : m_run);
+        float psum = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const float p = POS_SCALE ? exp2_fast(fmaf(sacc[kb][v], scale_log2, -m2))
+                                          : exp2_fast(sacc[kb][v] - m2);
+                sacc[kb][v] = p;
+                psum += p;
+            }
+        l_run += psum;
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                const bf16x8 pb = pack_bf16_half(sacc[kb], t);
+                const int r0 = VW * (32 * kb + 16 * t);
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb) {
+                    const int o = (cb / NV) * BLKV + r0;
+                    oacc[cb] = mfma32x32x16bf16(
+                        load_tr_pair_at(Vb + vlo[cb % NV] + o, Vb + vhi[cb % NV] + o), pb,
+                        oacc[cb]);
+                }
+            }
+    };
+
+    // Prologue: K(0), V(0), K(1) in flight together; S(0).  Tile j lives in
+    // buffer j % 2 (K0/K1, V0/V1).
+    f32x16 sa[NKB], sb[NKB];
+    if (ntiles > 0) {
+        tile.issue(K0, K + hoff, 0, Lk, w);
+        tilev.issue(V0, V + hoff, 0, Lk, w);
+        if (ntiles > 1) tile.issue(K1, K + hoff, kStream, Lk, w);
+        wait_vmcnt<0>();
+        __syncthreads();
+        scores(K0, sa);
+    }
+    // Iteration kt: S(kt) is in `cur`; K(kt+1) arrives in Kn and V(kt) in Vc
+    // (both issued an iteration earlier); K(kt+2) goes to Kc, whose K(kt) the
+    // last iteration consumed, and V(kt+1) to Vn, whose V(kt-1) likewise.
+    auto iter = [&](int kt, f32x16 (&cur)[NKB], f32x16 (&nxt)[NKB], uint16_t *Kc, uint16_t *Kn,
+                    uint16_t *Vc, uint16_t *Vn) {
+        wait_vmcnt<0>();
+        __syncthreads();   // K(kt+1), V(kt) visible; K(kt) and V(kt-1) buffers free
+        if (kt + 2 < ntiles) tile.issue(Kc, K + hoff, (kt + 2) * kStream, Lk, w);
+        if (kt + 1 < ntiles) tilev.issue(Vn, V + hoff, (kt + 1) * kStream, Lk, w);
+        if (kt + 1 < ntiles) scores(Kn, nxt);
+        softmax_pv(kt, cur, Vc);
+    };
+    for (int kt = 0; kt < ntiles; kt += 2) {
+        iter(kt, sa, sb, K0, K1, V0, V1);
+        if (kt + 1 < ntiles) iter(kt + 1, sb, sa, K1, K0, V1, V0);
+    }
+
+    const float l = sum_xor32(l_run);
+    if (qi < Lq) {
+        const float inv = (l > 0.f) ? 1.f / l : 0.f;
+        uint16_t *orow = O + qoff + (size_t)qi * D;
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+            for (int a = 0; a < 4; ++a)
+                store_bf16x4(orow + 32 * cb + 8 * a + 4 * h,
+                             f32x4{oacc[cb][4 * a], oacc[cb][4 * a + 1], oacc[cb][4 * a + 2],
+                                   oacc[cb][4 * a + 3]} * inv);
+        if (h == 0) {
+            const float m2 = POS_SCALE ? m_run * scale_log2 : m_run;
+            LSE[(size_t)head * Lq + qi] = (l > 0.f) ? (m2 + log2f(l)) * kLn2 : -INFINITY;
+        }
+    }
+}
+
 // ------------------------------------------------- backward: D = rowsum(dO o O)
 template <int D>
 __global__ __launch_bounds__(256) void attn_rowdot_bf16(const uint16_t *__restrict__ O,
@@ -598,12 +780,12 @@ hipError_t launch_fwd_bf16(const AttnProblem &p, const uint16_t *Q, const uint16
         kern<<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal, sl2,
                                     nqt, BH, ly);
     };
-#define MG_FWD_BF16(DD) \
-    (p.scale > 0.f ? go(attn_fwd_bf16<DD, true>) : go(attn_fwd_bf16<DD, false>))
+#define MG_FWD_BF16(KERN, DD) \
+    (p.scale > 0.f ? go(KERN<DD, true>) : go(KERN<DD, false>))
     switch (p.d) {
-    case 32: MG_FWD_BF16(32); break;
-    case 64: MG_FWD_BF16(64); break;
-    case 128: MG_FWD_BF16(128); break;
+    case 32: MG_FWD_BF16(attn_fwd_bf16_pipe, 32); break;
+    case 64: MG_FWD_BF16(attn_fwd_bf16_pipe, 64); break;
+    case 128: MG_FWD_BF16(attn_fwd_bf16, 128); break;
     default: return hipErrorInvalidValue;
     }
 #undef MG_FWD_BF16
