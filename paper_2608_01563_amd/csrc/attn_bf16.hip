@@ -485,8 +485,8 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
     constexpr int BLK = Tile::kBlock;
     __shared__ __attribute__((aligned(16))) uint16_t Qr0[Tile::kSize], Qr1[Tile::kSize];
     __shared__ __attribute__((aligned(16))) uint16_t Or0[Tile::kSize], Or1[Tile::kSize];
-    __shared__ __attribute__((aligned(16))) float lse0[QR], lse1[QR];   // LSE (natural log)
-    __shared__ __attribute__((aligned(16))) float Ds0[QR], Ds1[QR];
+    __shared__ __attribute__((aligned(16))) float lse0[QR], lse1[QR];   // LSE * log2e
+    __shared__ __attribute__((aligned(16))) float Ds0[QR], Ds1[QR];     // -D
 
     const int slot = blockIdx.x / BH;
     const int head = blockIdx.x - slot * BH;
@@ -533,36 +533,41 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
     for (int i = 0; i < NA; ++i) qa[i] = Tile::at(il, 32 * i + 8 * g);
 #pragma unroll
     for (int i = 0; i < NB; ++i) qb[i] = Tile::at(4 * g + jr, 16 * i + jc);
-    // Direct-to-LDS loads of the Q and dO rows of tile qt and of their LSE
-    // (natural log; wave 0) and D (the last wave) values; rows past Lq arrive
-    // as zeros.
+    // Direct-to-LDS loads of the Q and dO rows of tile qt, and a register load
+    // of their LSE (natural log; wave 0) or D (the last wave), one row per
+    // lane; rows past Lq arrive as zeros.  Once the loads have landed,
+    // `publish` stores LSE * log2e and -D in LDS, so that each score needs
+    // one fma before its exp2 and dP accumulates straight onto -D.
     using Buf = uint16_t[Tile::kSize];
-    auto fetch = [&](int qt, Buf &Qn, Buf &On, float (&ln)[QR], float (&dn)[QR]) {
+    static_assert(QR == 64, "one statistic per lane");
+    float stat = 0.f;
+    auto fetch = [&](int qt, Buf &Qn, Buf &On) {
         tile.issue(Qn, Q + qoff, qt * QR, Lq, w);
         tile.issue(On, dO + qoff, qt * QR, Lq, w);
         if (w == 0 || w == kWaves - 1) {
             const int row0 = qt * QR;
             const int rows = min(max(Lq - row0, 0), QR);
             const float *src = (w == 0 ? LSE : Dws) + (size_t)head * Lq + row0;
-            if (lane < QR)
-                __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                buffer_rsrc(src, rows * 4),
-                (__attribute__((address_space(3))) void *)(w == 0 ? &ln[0] : &dn[0]), 4,
-                lane * 4, 0, 0, 0);
+            stat = buffer_load_f32(buffer_rsrc(src, rows * 4), lane * 4);
         }
+    };
+    auto publish = [&](float (&ln)[QR], float (&dn)[QR]) {
+        if (w == 0) ln[lane] = stat * kLog2e;
+        if (w == kWaves - 1) dn[lane] = -stat;
     };
 
     // One query tile from buffers (Qc, Oc, lc, dc) while tile qt + 1 loads
     // into (Qn, On, ln, dn).
     auto step = [&](int qt, Buf &Qc, Buf &Oc, float (&lc)[QR], float (&dc)[QR], Buf &Qn,
                     Buf &On, float (&ln)[QR], float (&dn)[QR]) {
-        if (qt + 1 < qstop) fetch(qt + 1, Qn, On, ln, dn);   // freed by the last barrier
+        if (qt + 1 < qstop) fetch(qt + 1, Qn, On);   // freed by the last barrier
 
+        // S = Q K^T; dP - D = dO V^T accumulated onto -D (rows 16ib + 4g + r)
         f32x4 sacc[QB], pacc[QB];
 #pragma unroll
         for (int ib = 0; ib < QB; ++ib) {
             sacc[ib] = zero4();
-            pacc[ib] = zero4();
+            pacc[ib] = *reinterpret_cast<const f32x4 *>(&dc[16 * ib + 4 * g]);
         }
 #pragma unroll
         for (int s = 0; s < NS; ++s)
@@ -573,20 +578,27 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
                 pacc[ib] = mfma16x16x32bf16(load_bf16x8(Oc + o), vreg[s], pacc[ib]);
             }
 
-        const int ibase = qt * QR + 4 * g;
-        const int thr = causal ? kj - diag - ibase : -(1 << 30);
+        // P = exp2(S * scale*log2e - LSE*log2e), dS = P (dP - D); the mask (row
+        // qt*QR + 16ib + 4g + r sees key kj iff 16ib + r >= thr) only in tiles
+        // that cross the wave's causal boundary.
+        auto softmax = [&](auto masked) {
+            const int thr = kj - diag - (qt * QR + 4 * g);
 #pragma unroll
-        for (int ib = 0; ib < QB; ++ib) {
-            const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lc[16 * ib + 4 * g]) * kLog2e;
-            const f32x4 dd = *reinterpret_cast<const f32x4 *>(&dc[16 * ib + 4 * g]);
+            for (int ib = 0; ib < QB; ++ib) {
+                const f32x4 l2 = *reinterpret_cast<const f32x4 *>(&lc[16 * ib + 4 * g]);
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                float p = exp2_fast(fmaf(sacc[ib][r], scale_log2, -l2[r]));
-                p = (16 * ib + r >= thr) ? p : 0.f;
-                sacc[ib][r] = p;
-                pacc[ib][r] = p * (pacc[ib][r] - dd[r]);
+                for (int r = 0; r < 4; ++r) {
+                    float p = exp2_fast(fmaf(sacc[ib][r], scale_log2, -l2[r]));
+                    if (masked && 16 * ib + r < thr) p = 0.f;
+                    sacc[ib][r] = p;
+                    pacc[ib][r] *= p;
+                }
             }
-        }
+        };
+        if (!causal || qt * QR + diag >= k0 + 16 * w + 15)
+            softmax(std::false_type{});
+        else
+            softmax(std::true_type{});
 
         // dV^T[16c + .][kj] += dO^T[16c + il'][i] P[i][kj]; dK^T likewise with Q, dS
 #pragma unroll
@@ -604,13 +616,17 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
             }
         }
 
-        if (qt + 1 < qstop) wait_vmcnt<0>();   // next tile and its LSE, D landed
+        if (qt + 1 < qstop) {
+            wait_vmcnt<0>();   // next tile and its LSE, D landed
+            publish(ln, dn);
+        }
         __syncthreads();   // next tile visible; buffers (Qc, Oc) free
     };
 
     if (qstart < qstop) {
-        fetch(qstart, Qr0, Or0, lse0, Ds0);
+        fetch(qstart, Qr0, Or0);
         wait_vmcnt<0>();
+        publish(lse0, Ds0);
     }
     __syncthreads();
     for (int qt = qstart; qt < qstop; qt += 2) {
@@ -716,20 +732,30 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
 
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb) {
-            f32x16 sacc = zero16(), pacc = zero16();
+            // S^T = K Q^T; dP^T - D = V dO^T accumulated onto -D
+            f32x16 sacc = zero16(), pacc;
+#pragma unroll
+            for (int v = 0; v < 16; ++v) pacc[v] = -Di;
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
                 const int o = kc[s & 1] + (s >> 1) * BLK + 32 * 32 * kb;
                 sacc = mfma32x32x16bf16(load_bf16x8(Kc + o), qreg[s], sacc);
                 pacc = mfma32x32x16bf16(load_bf16x8(Vc + o), oreg[s], pacc);
             }
-            // dS^T = P^T (dP^T - D), P^T = exp2(S^T * scale*log2e - LSE*log2e)
+            // dS^T = P^T (dP^T - D), P^T = exp2(S^T * scale*log2e - LSE*log2e);
+            // the mask only in tiles that cross the diagonal or the key length
+            auto softmax = [&](auto masked) {
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                float p = exp2_fast(fmaf(sacc[v], scale_log2, -lse2));
-                if (!full && 32 * kb + 8 * (v >> 2) + (v & 3) >= thr) p = 0.f;
-                pacc[v] = p * (pacc[v] - Di);
-            }
+                for (int v = 0; v < 16; ++v) {
+                    float p = exp2_fast(fmaf(sacc[v], scale_log2, -lse2));
+                    if (masked && 32 * kb + 8 * (v >> 2) + (v & 3) >= thr) p = 0.f;
+                    pacc[v] *= p;
+                }
+            };
+            if (full)
+                softmax(std::false_type{});
+            else
+                softmax(std::true_type{});
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
                 const bf16x8 sb = pack_bf16_half(pacc, t);
@@ -809,8 +835,8 @@ hipError_t launch_bwd_dkdv_bf16(const AttnProblem &p, const uint16_t *Q, const u
                                 const uint16_t *V, const uint16_t *dO, const float *LSE,
                                 const float *Dws, uint16_t *dK, uint16_t *dV, hipStream_t s) {
     const int BH = p.B * p.H;
-    const dim3 grid(cdiv(p.Lk, kStatRows) * BH), block(kThreads);
     const float sl2 = p.scale * kLog2e;
+    const dim3 grid(cdiv(p.Lk, kStatRows) * BH), block(kThreads);
     auto go = [&](auto kern) {
         const int ly = causal_rank_layer((const void *)kern, kThreads, grid.x, BH, p.causal);
         kern<<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, p.key_len, p.H, p.Lq, p.Lk,
