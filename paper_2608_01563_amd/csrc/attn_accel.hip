@@ -12,10 +12,12 @@
 // Structure as the bf16 forward (32 queries per wave on
 // v_mfma_f32_32x32x16_f16, K and V streamed 64 keys at a time through padded
 // row-major LDS tiles, V^T operands by 16-bit transpose reads), except that
-// the f32 tiles pass through registers to be rounded: the next K tile is
-// loaded while S of the current tile runs and written to LDS (as f16) after
-// the barrier that frees it; the next V tile likewise during P V.  K and V
-// staging never overlap in time, so one set of staging registers serves both.
+// the f32 tiles pass through registers to be rounded.  For d = 128 the plain
+// form: the next K tile is loaded while S of the current tile runs and
+// written to LDS (as f16) after the barrier that frees it, the next V tile
+// likewise during P V, and since the two never overlap in time one set of
+// staging registers serves both.  For d <= 64 the software-pipelined form
+// below (double-buffered K and V, one barrier per tile).
 #include "device_common.h"
 #include "launch.h"
 #include "tiles_bf16.h"
@@ -267,6 +269,201 @@ void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
     }
 }
 
+// The forward with its key tiles software-pipelined, for d <= 64 (as the bf16
+// forward of the same sizes): iteration kt issues the register loads of K(kt+2)
+// and V(kt+1), then the score product of tile kt+1, then the softmax and P V of
+// tile kt, and only then rounds the staged tiles to f16 and writes them into
+// the buffers that the iteration's barrier freed.  Every load has a whole
+// iteration to land, and one barrier per tile suffices.  K and V are
+// double-buffered in separate named arrays.  At d = 128 the second score
+// block and the second staging set do not fit two waves per SIMD, and the
+// plain form above is used.
+template <int D, bool POS_SCALE>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
+void attn_fwd_accel_pipe(const float *__restrict__ Q, const float *__restrict__ K,
+                         const float *__restrict__ V, float *__restrict__ O,
+                         float *__restrict__ LSE, const int32_t *__restrict__ key_len, int H,
+                         int Lq, int Lk, int causal, float scale_log2, int n_qtiles, int BH,
+                         int layer) {
+    constexpr int NS = D / 16;
+    constexpr int NCB = D / 32;
+    constexpr int NKB = kKeys / 32;
+    constexpr int LD = Bf16Ld<D>::value;     // K rows: 16-byte reads of 32 rows
+    constexpr int LDV = Bf16LdTr<D>::value;  // V rows: transpose reads only
+    using St = F16ConvStager<kKeys, D, kThreads>;
+    __shared__ __attribute__((aligned(16))) uint16_t K0[kKeys][LD], K1[kKeys][LD];
+    __shared__ __attribute__((aligned(16))) uint16_t V0[kKeys][LDV], V1[kKeys][LDV];
+    using KBuf = uint16_t[kKeys][LD];
+    using VBuf = uint16_t[kKeys][LDV];
+
+    const int slot = blockIdx.x / BH;
+    const int head = blockIdx.x - slot * BH;
+    const int rank = serpentine_rank(slot, n_qtiles, layer);
+    const int qt = causal ? (n_qtiles - 1 - rank) : rank;
+    const int b = head / H;
+    const size_t qoff = (size_t)head * Lq * D, hoff = (size_t)head * Lk * D;
+    const float *Kh = K + hoff;
+    const float *Vh = V + hoff;
+    const int diag = Lk - Lq;   // causal: row i sees keys j <= i + diag
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int c = lane & 31;
+    const int h = lane >> 5;
+    const int jr = (lane & 15) >> 2, jc = 4 * (lane & 3);   // transpose-read block offsets
+    const int q0 = qt * kRows;
+    const int qi = q0 + 32 * w + c;
+
+    const int klen = key_limit(key_len, b, Lk);
+    const int kend = causal ? min(klen, q0 + kRows + diag) : klen;
+    const int ntiles = (kend + kKeys - 1) / kKeys;
+
+    // B operand of S^T = K Q^T: lane holds f16(Q[qi][16s + 8h + e]).
+    f16x8 qreg[NS];
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        const float *qp = Q + qoff + (size_t)qi * D + 16 * s + 8 * h;
+        qreg[s] = (qi < Lq) ? to_f16x8(*reinterpret_cast<const f32x4 *>(qp),
+                                      *reinterpret_cast<const f32x4 *>(qp + 4))
+                           : f16x8{};
+    }
+
+    float m_run = -INFINITY, l_run = 0.f;
+    f32x16 oacc[NCB];   // O^T[32cb + 8a + 4h + r][qi] in register 4a + r
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) oacc[cb] = zero16();
+
+    // S^T[32kb + 8a + 4h + r][qi] in sacc[kb] register 4a + r
+    auto scores = [&](const KBuf &Kb, f32x16 (&sacc)[NKB]) {
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) {
+            sacc[kb] = zero16();
+#pragma unroll
+            for (int s = 0; s < NS; ++s)
+                sacc[kb] = mfma32x32x16f16(
+                    __builtin_bit_cast(f16x8, *reinterpret_cast<const u32x4 *>(
+                                                  &Kb[32 * kb + c][16 * s + 8 * h])),
+                    qreg[s], sacc[kb]);
+        }
+    };
+    auto softmax_pv = [&](int kt, f32x16 (&sacc)[NKB], const VBuf &Vb) {
+        if (!POS_SCALE) {
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb) sacc[kb] *= scale_log2;
+        }
+        // Masking only where the tile crosses the diagonal or the key length.
+        const bool full =
+            (kt + 1) * kKeys <= klen && (!causal || (kt + 1) * kKeys - 1 <= q0 + diag);
+        if (!full) {
+            const int j0 = kt * kKeys + 4 * h;
+            const int thr = causal ? min(klen - j0, qi + diag - j0 + 1) : klen - j0;
+#pragma unroll
+            for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    if (32 * kb + 8 * (v >> 2) + (v & 3) >= thr) sacc[kb][v] = -INFINITY;
+        }
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+            for (int v = 0; v < 16; v += 2) mx = fmaxf(mx, fmaxf(sacc[kb][v], sacc[kb][v + 1]));
+        mx = max_xor32(mx);
+        // Rescale O and l only when some row's maximum grew by more than
+        // kSlack (base 2), as in the plain form.
+        const float grow2 = POS_SCALE ? (mx - m_run) * scale_log2 : mx - m_run;
+        if (__any(grow2 > kSlack)) {
+            const float m_new = fmaxf(m_run, mx);
+            const float m2_old = POS_SCALE ? m_run * scale_log2 : m_run;
+            const float m2_new =
+                (m_new == -INFINITY) ? 0.f : (POS_SCALE ? m_new * scale_log2 : m_new);
+            const float alpha = exp2_fast(m2_old - m2_new);
+            l_run *= alpha;
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb) oacc[cb] *= alpha;
+            m_run = m_new;
+        }
+        const float m2 = (m_run == -INFINITY) ? 0.f : (POS_SCALE ? m_run * scale_log2 : m_run);
+        float psum = 0.f;
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const float p = POS_SCALE ? exp2_fast(fmaf(sacc[kb][v], scale_log2, -m2))
+                                          : exp2_fast(sacc[kb][v] - m2);
+                sacc[kb][v] = p;
+                psum += p;
+            }
+        l_run += psum;
+        // O^T[32cb + .][qi] += sum_j V^T[32cb + c'][j] P^T[j][qi], 16 keys per step
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                const f16x8 pb = pack_f16_half(sacc[kb], t);
+                const int r0 = 32 * kb + 16 * t + 4 * h;
+#pragma unroll
+                for (int cb = 0; cb < NCB; ++cb)
+                    oacc[cb] = mfma32x32x16f16(
+                        __builtin_bit_cast(f16x8, load_tr_pair<LDV>(Vb, r0, r0 + 8,
+                                                                   32 * cb + 16 * (c >> 4), jr, jc)),
+                        pb, oacc[cb]);
+            }
+    };
+
+    // Prologue: K(0) into K0, V(0) into V0, K(1) into K1; S(0).  Tile j lives
+    // in buffer j % 2.
+    St sk, sv;
+    f32x16 sa[NKB], sb[NKB];
+    if (ntiles > 0) {
+        sk.load(Kh, 0, Lk, tid);
+        sv.load(Vh, 0, Lk, tid);
+        sk.store(K0, tid);
+        sv.store(V0, tid);
+        if (ntiles > 1) {
+            sk.load(Kh, kKeys, Lk, tid);
+            sk.store(K1, tid);
+        }
+        __syncthreads();
+        scores(K0, sa);
+    }
+    // Iteration kt: S(kt) is in `cur`; K(kt+1) is in Kn and V(kt) in Vc,
+    // written an iteration earlier; K(kt+2) goes to Kc, whose K(kt) the last
+    // iteration consumed, and V(kt+1) to Vn, whose V(kt-1) likewise.
+    auto iter = [&](int kt, f32x16 (&cur)[NKB], f32x16 (&nxt)[NKB], KBuf &Kc, const KBuf &Kn,
+                    const VBuf &Vc, VBuf &Vn) {
+        __syncthreads();   // K(kt+1), V(kt) visible; K(kt) and V(kt-1) buffers free
+        if (kt + 2 < ntiles) sk.load(Kh, (kt + 2) * kKeys, Lk, tid);
+        if (kt + 1 < ntiles) sv.load(Vh, (kt + 1) * kKeys, Lk, tid);
+        if (kt + 1 < ntiles) scores(Kn, nxt);
+        softmax_pv(kt, cur, Vc);
+        if (kt + 2 < ntiles) sk.store(Kc, tid);
+        if (kt + 1 < ntiles) sv.store(Vn, tid);
+    };
+    for (int kt = 0; kt < ntiles; kt += 2) {
+        iter(kt, sa, sb, K0, K1, V0, V1);
+        if (kt + 1 < ntiles) iter(kt + 1, sb, sa, K1, K0, V1, V0);
+    }
+
+    const float l = sum_xor32(l_run);
+    if (qi < Lq) {
+        const float inv = (l > 0.f) ? 1.f / l : 0.f;
+        float *orow = O + qoff + (size_t)qi * D;
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+            for (int a = 0; a < 4; ++a)
+                *reinterpret_cast<f32x4 *>(orow + 32 * cb + 8 * a + 4 * h) =
+                    f32x4{oacc[cb][4 * a], oacc[cb][4 * a + 1], oacc[cb][4 * a + 2],
+                          oacc[cb][4 * a + 3]} * inv;
+        if (h == 0) {
+            const float m2 = POS_SCALE ? m_run * scale_log2 : m_run;
+            LSE[(size_t)head * Lq + qi] = (l > 0.f) ? (m2 + log2f(l)) * kLn2 : -INFINITY;
+        }
+    }
+}
+
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 }  // namespace
@@ -282,12 +479,12 @@ hipError_t launch_fwd_accel(const AttnProblem &p, const float *Q, const float *K
         kern<<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal, sl2,
                                     nqt, BH, ly);
     };
-#define MG_FWD_ACCEL(DD) \
-    (p.scale > 0.f ? go(attn_fwd_accel<DD, true>) : go(attn_fwd_accel<DD, false>))
+#define MG_FWD_ACCEL(KERN, DD) \
+    (p.scale > 0.f ? go(KERN<DD, true>) : go(KERN<DD, false>))
     switch (p.d) {
-    case 32: MG_FWD_ACCEL(32); break;
-    case 64: MG_FWD_ACCEL(64); break;
-    case 128: MG_FWD_ACCEL(128); break;
+    case 32: MG_FWD_ACCEL(attn_fwd_accel_pipe, 32); break;
+    case 64: MG_FWD_ACCEL(attn_fwd_accel_pipe, 64); break;
+    case 128: MG_FWD_ACCEL(attn_fwd_accel, 128); break;
     default: return hipErrorInvalidValue;
     }
 #undef MG_FWD_ACCEL
