@@ -533,14 +533,14 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
     for (int i = 0; i < NA; ++i) qa[i] = Tile::at(il, 32 * i + 8 * g);
 #pragma unroll
     for (int i = 0; i < NB; ++i) qb[i] = Tile::at(4 * g + jr, 16 * i + jc);
-    // Direct-to-LDS loads of the Q and dO rows of tile qt, and a register load
-    // of their LSE (natural log; wave 0) or D (the last wave), one row per
-    // lane; rows past Lq arrive as zeros.  Once the loads have landed,
-    // `publish` stores LSE * log2e and -D in LDS, so that each score needs
-    // one fma before its exp2 and dP accumulates straight onto -D.
+    // Direct-to-LDS loads of the Q and dO rows of tile qt and of their LSE
+    // (natural log; wave 0) and D (the last wave) into staging rows; rows
+    // past Lq arrive as zeros.  Once the loads have landed, `publish` (the
+    // same lanes) stores LSE * log2e and -D for the tile, so that each score
+    // needs one fma before its exp2 and dP accumulates straight onto -D.
     using Buf = uint16_t[Tile::kSize];
     static_assert(QR == 64, "one statistic per lane");
-    float stat = 0.f;
+    __shared__ __attribute__((aligned(16))) float raw[2][QR];   // LSE, D in flight
     auto fetch = [&](int qt, Buf &Qn, Buf &On) {
         tile.issue(Qn, Q + qoff, qt * QR, Lq, w);
         tile.issue(On, dO + qoff, qt * QR, Lq, w);
@@ -548,12 +548,15 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
             const int row0 = qt * QR;
             const int rows = min(max(Lq - row0, 0), QR);
             const float *src = (w == 0 ? LSE : Dws) + (size_t)head * Lq + row0;
-            stat = buffer_load_f32(buffer_rsrc(src, rows * 4), lane * 4);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                buffer_rsrc(src, rows * 4),
+                (__attribute__((address_space(3))) void *)&raw[w == 0 ? 0 : 1][0], 4, lane * 4, 0,
+                0, 0);
         }
     };
     auto publish = [&](float (&ln)[QR], float (&dn)[QR]) {
-        if (w == 0) ln[lane] = stat * kLog2e;
-        if (w == kWaves - 1) dn[lane] = -stat;
+        if (w == 0) ln[lane] = raw[0][lane] * kLog2e;
+        if (w == kWaves - 1) dn[lane] = -raw[1][lane];
     };
 
     // One query tile from buffers (Qc, Oc, lc, dc) while tile qt + 1 loads

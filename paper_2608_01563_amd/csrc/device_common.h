@@ -124,10 +124,6 @@ __device__ __forceinline__ f32x4 buffer_load_f32x4(__amdgpu_buffer_rsrc_t r, int
     return __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(r, byte_offset, 0, 0));
 }
 
-__device__ __forceinline__ float buffer_load_f32(__amdgpu_buffer_rsrc_t r, int byte_offset) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, byte_offset, 0, 0));
-}
-
 // s_waitcnt immediate that waits until at most `N` vector-memory operations
 // of this wave are outstanding (gfx9 encoding: vmcnt bits 3:0 in bits 3:0 and
 // bits 5:4 in bits 15:14; expcnt and lgkmcnt left at their maxima, i.e. not
