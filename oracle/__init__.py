@@ -17,6 +17,7 @@ from .oracle import (  # noqa: F401
     build_oracle,
     oracle_forward,
     oracle_backward,
+    oracle_backward_from,
     oracle_head_matrices,
     oracle_num_threads,
     round_to_f16,

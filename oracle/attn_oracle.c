@@ -112,17 +112,16 @@ static void head_forward(const double *Q, const double *K, const double *V,
     }
 }
 
-/* Backward pass of one head from its inputs.  O and LSE are recomputed here
- * by head_forward (not taken from the caller), so the gradients depend only
- * on Q, K, V, dO.  S is scratch of length Lk, O and LSE scratch of Lq*d and
- * Lq. */
-static void head_backward(const double *Q, const double *K, const double *V,
-                          const double *dO, int Lq, int Lk, int d, int causal, int klen,
-                          double scale, double *dQ, double *dK, double *dV,
-                          double *Dout, double *S, double *O, double *LSE)
+/* The backward equations of one head evaluated at a given O and LSE (the
+ * saved forward outputs a recompute-based backward consumes): P_ij =
+ * exp(S_ij - LSE_i) for allowed pairs, D_i = sum_k dO_ik O_ik, and dP, dS,
+ * dQ, dK, dV as above.  A row with LSE_i = -inf contributes nothing. */
+static void head_backward_from(const double *Q, const double *K, const double *V,
+                               const double *O, const double *LSE, const double *dO,
+                               int Lq, int Lk, int d, int causal, int klen, double scale,
+                               double *dQ, double *dK, double *dV, double *Dout)
 {
     const int off = Lk - Lq;
-    head_forward(Q, K, V, Lq, Lk, d, causal, klen, scale, O, LSE, S);
     for (size_t t = 0; t < (size_t)Lq * d; ++t) dQ[t] = 0.0;
     for (size_t t = 0; t < (size_t)Lk * d; ++t) { dK[t] = 0.0; dV[t] = 0.0; }
 
@@ -149,6 +148,19 @@ static void head_backward(const double *Q, const double *K, const double *V,
             }
         }
     }
+}
+
+/* Backward pass of one head from its inputs.  O and LSE are recomputed here
+ * by head_forward (not taken from the caller), so the gradients depend only
+ * on Q, K, V, dO.  S is scratch of length Lk, O and LSE scratch of Lq*d and
+ * Lq. */
+static void head_backward(const double *Q, const double *K, const double *V,
+                          const double *dO, int Lq, int Lk, int d, int causal, int klen,
+                          double scale, double *dQ, double *dK, double *dV,
+                          double *Dout, double *S, double *O, double *LSE)
+{
+    head_forward(Q, K, V, Lq, Lk, d, causal, klen, scale, O, LSE, S);
+    head_backward_from(Q, K, V, O, LSE, dO, Lq, Lk, d, causal, klen, scale, dQ, dK, dV, Dout);
 }
 
 static int head_selected(const unsigned char *head_mask, int bh)
@@ -205,6 +217,30 @@ int oracle_attn_bwd(const double *Q, const double *K, const double *V,
         free(S); free(O); free(LSE);
     }
     return failed ? -1 : 0;
+}
+
+/* Backward over all selected heads at a given O ([B][H][Lq][d]) and LSE
+ * ([B][H][Lq]) instead of the ones the forward equations give for Q, K, V:
+ * the gradients of a backward that consumes another forward's outputs (the
+ * accelerated contract's f32 backward after its rounded-input forward).
+ * D as in oracle_attn_bwd.  Returns 0, or -1 on a bad argument. */
+int oracle_attn_bwd_from(const double *Q, const double *K, const double *V,
+                         const double *O, const double *LSE, const double *dO,
+                         const int *key_len, int B, int H, int Lq, int Lk, int d, int causal,
+                         double scale, const unsigned char *head_mask,
+                         double *dQ, double *dK, double *dV, double *D)
+{
+    if (B < 1 || H < 1 || Lq < 1 || Lk < 1 || d < 1) return -1;
+    int nheads = B * H;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int bh = 0; bh < nheads; ++bh) {
+        if (!head_selected(head_mask, bh)) continue;
+        size_t qo = (size_t)bh * Lq * d, ko = (size_t)bh * Lk * d;
+        head_backward_from(Q + qo, K + ko, V + ko, O + qo, LSE + (size_t)bh * Lq, dO + qo,
+                           Lq, Lk, d, causal, key_limit(key_len, bh / H, Lk), scale,
+                           dQ + qo, dK + ko, dV + ko, D ? D + (size_t)bh * Lq : NULL);
+    }
+    return 0;
 }
 
 /* Full P and dS matrices of one head (b,h), [Lq][Lk] each, for the

@@ -39,6 +39,9 @@ def _bind(lib):
     lib.oracle_attn_bwd.argtypes = [dp, dp, dp, dp, ip, ci, ci, ci, ci, ci, ci, cd, up,
                                     dp, dp, dp, dp]
     lib.oracle_attn_bwd.restype = ci
+    lib.oracle_attn_bwd_from.argtypes = [dp, dp, dp, dp, dp, dp, ip, ci, ci, ci, ci, ci, ci,
+                                         cd, up, dp, dp, dp, dp]
+    lib.oracle_attn_bwd_from.restype = ci
     lib.oracle_head_matrices.argtypes = [dp, dp, dp, dp, ip, ci, ci, ci, ci, ci, ci, cd,
                                          ci, ci, dp, dp, dp]
     lib.oracle_head_matrices.restype = ci
@@ -130,6 +133,34 @@ def oracle_backward(Q, K, V, dO, causal, scale, key_len=None, heads=None, lib=No
                              _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(D))
     if rc != 0:
         raise RuntimeError("oracle_attn_bwd failed")
+    return dQ, dK, dV, D
+
+
+def oracle_backward_from(Q, K, V, O, LSE, dO, causal, scale, key_len=None, heads=None,
+                         lib=None):
+    """dQ, dK, dV and D of the backward equations evaluated at the given O
+    [B,H,Lq,d] and LSE [B,H,Lq] (natural log) instead of the ones the forward
+    equations give for Q, K, V: P = exp(S - LSE), D = rowsum(dO * O).  This is
+    what a recompute-based backward computes when it consumes the saved
+    outputs of a different forward, e.g. the accelerated contract's f32
+    backward after its forward on f16-rounded inputs (Sec. 4.2, table of
+    arithmetic permissions)."""
+    lib = lib or load_oracle()
+    Q, K, V, kl, mask, (B, H, Lq, Lk, d) = _prep(Q, K, V, key_len, heads)
+    O, LSE, dO = _f64(O), _f64(LSE), _f64(dO)
+    if O.shape != Q.shape or dO.shape != Q.shape or LSE.shape != Q.shape[:3]:
+        raise ValueError("O and dO must have the shape of Q, LSE [B,H,Lq]")
+    dQ = np.full((B, H, Lq, d), np.nan)
+    dK = np.full((B, H, Lk, d), np.nan)
+    dV = np.full((B, H, Lk, d), np.nan)
+    D = np.full((B, H, Lq), np.nan)
+    rc = lib.oracle_attn_bwd_from(_ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(LSE), _ptr(dO),
+                                  None if kl is None else _ptr(kl, ctypes.c_int),
+                                  B, H, Lq, Lk, d, int(bool(causal)), float(scale),
+                                  None if mask is None else _ptr(mask, ctypes.c_ubyte),
+                                  _ptr(dQ), _ptr(dK), _ptr(dV), _ptr(D))
+    if rc != 0:
+        raise RuntimeError("oracle_attn_bwd_from failed")
     return dQ, dK, dV, D
 
 

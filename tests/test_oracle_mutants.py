@@ -40,6 +40,9 @@ MUTANTS = {
                            "double Pij = exp(dot(q, kj, d) - LSE[i]);"),
     "key_len_batch_index": ("key_limit(key_len, bh / H, Lk)", "key_limit(key_len, bh % H, Lk)"),
     "key_len_clamped_to_Lq": ("key_limit(key_len, bh / H, Lk)", "key_limit(key_len, bh / H, Lq)"),
+    "bwd_from_first_head_lse": ("O + qo, LSE + (size_t)bh * Lq, dO + qo,", "O + qo, LSE, dO + qo,"),
+    "bwd_from_O_dO_swapped": ("O + qo, LSE + (size_t)bh * Lq, dO + qo,",
+                              "dO + qo, LSE + (size_t)bh * Lq, O + qo,"),
 }
 
 PINS = [
@@ -62,6 +65,9 @@ PINS = [
     pins.test_cross_single_key,
     lambda: pins.test_cross_matches_torch_autograd_f64(12, 30, False, True),
     lambda: pins.test_cross_central_finite_differences(3, 5, True, False),
+    lambda: pins.test_bwd_from_exact_forward_is_the_backward(False, True, 5, 7),
+    pins.test_bwd_from_single_key_closed_forms,
+    pins.test_bwd_from_linear_in_upstream_gradient,
 ]
 
 

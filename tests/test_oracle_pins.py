@@ -13,7 +13,8 @@ import numpy as np
 import pytest
 import scipy.special
 
-from oracle import oracle_forward, oracle_backward, oracle_head_matrices, round_to_f16
+from oracle import oracle_forward, oracle_backward, oracle_backward_from, \
+    oracle_head_matrices, round_to_f16
 
 RNG = np.random.default_rng(12345)
 
@@ -332,6 +333,60 @@ def test_bwd_linear_in_upstream_gradient_and_masked_batch():
         assert np.array_equal(2 * a, b)
     for g in g1[:3]:
         assert np.all(g[0] == 0.0)
+
+
+# ---- the backward equations at given saved outputs (a recompute-based
+# backward consuming another forward's O and LSE: the accelerated contract's
+# f32 backward after its rounded-input forward)
+
+@pytest.mark.parametrize("causal,padded,Lq,Lk", [(True, False, 6, 6), (False, True, 5, 7),
+                                                 (True, True, 7, 4)])
+def test_bwd_from_exact_forward_is_the_backward(causal, padded, Lq, Lk):
+    """At the forward's own O and LSE it is the pinned backward."""
+    Q, dO = rand(2, 2, Lq, 3), rand(2, 2, Lq, 3)
+    K, V = rand(2, 2, Lk, 3), rand(2, 2, Lk, 3)
+    kl = np.array([Lk - 1, 2], dtype=np.int32) if padded else None
+    O, LSE = oracle_forward(Q, K, V, causal, 0.6, key_len=kl)
+    for a, b in zip(oracle_backward(Q, K, V, dO, causal, 0.6, key_len=kl),
+                    oracle_backward_from(Q, K, V, O, LSE, dO, causal, 0.6, key_len=kl)):
+        assert np.array_equal(a, b)
+
+
+def test_bwd_from_single_key_closed_forms():
+    """Every row sees key 0 only (key length 1), so P_i = exp(S_i0 - LSE_i).
+    Given LSE_i = S_i0 + ln 2, P = 1/2: dV_0 = (1/2) sum_i dO_i.  Given O_i =
+    V_0, D_i = dP_i and every dS vanishes: dQ = dK = 0.  Given O_i = V_0 +
+    t u_i, dS_i = -(t/2) dO_i . u_i, dQ_i = scale dS_i K_0, dK_0 = scale sum_i
+    dS_i Q_i.  Keys past the key length get nothing."""
+    L, d, scale, t = 5, 3, 0.7, 0.3
+    Q, K, V, dO = (rand(1, 1, L, d) for _ in range(4))
+    kl = np.array([1], dtype=np.int32)
+    S0 = scale * np.einsum("id,d->i", Q[0, 0], K[0, 0, 0])
+    LSE = (S0 + math.log(2.0))[None, None]
+    O = np.broadcast_to(V[0, 0, 0], (1, 1, L, d)).copy()
+    dQ, dK, dV, D = oracle_backward_from(Q, K, V, O, LSE, dO, False, scale, key_len=kl)
+    assert np.all(dQ == 0.0) and np.all(dK == 0.0)
+    assert np.allclose(dV[0, 0, 0], 0.5 * dO[0, 0].sum(axis=0), rtol=1e-14, atol=1e-15)
+    assert np.all(dV[0, 0, 1:] == 0.0)
+    u = rand(1, 1, L, d)
+    dQ, dK, dV, D = oracle_backward_from(Q, K, V, O + t * u, LSE, dO, False, scale, key_len=kl)
+    dS = -(t / 2) * np.einsum("id,id->i", dO[0, 0], u[0, 0])
+    assert normwise(dQ[0, 0], scale * dS[:, None] * K[0, 0, 0][None]) < 1e-13
+    assert normwise(dK[0, 0, 0], scale * (dS[:, None] * Q[0, 0]).sum(axis=0)) < 1e-13
+    assert np.all(dK[0, 0, 1:] == 0.0)
+
+
+def test_bwd_from_linear_in_upstream_gradient():
+    """With O and LSE fixed (here unrelated to Q, K, V), D and all three
+    gradients are linear in dO."""
+    Q, dO1, dO2 = rand(2, 1, 6, 4), rand(2, 1, 6, 4), rand(2, 1, 6, 4)
+    K, V, O = rand(2, 1, 6, 4), rand(2, 1, 6, 4), rand(2, 1, 6, 4)
+    LSE = rand(2, 1, 6) + 2.0
+    g1 = oracle_backward_from(Q, K, V, O, LSE, dO1, True, 0.5)
+    g2 = oracle_backward_from(Q, K, V, O, LSE, dO2, True, 0.5)
+    g = oracle_backward_from(Q, K, V, O, LSE, 2.0 * dO1 - 3.0 * dO2, True, 0.5)
+    for a, b, c in zip(g1, g2, g):
+        assert normwise(c, 2.0 * a - 3.0 * b) < 1e-13
 
 
 # ---- f16 input rounding of the accelerated contract (Sec. 4.2 permissions)
