@@ -10,8 +10,8 @@ O = 0, LSE = -inf and zero gradients, and `compare` demands those exactly.
 import numpy as np
 import pytest
 
-from gpu_util import TOL, TOL_ACCEL_ROUNDED, compare, normwise_error, oracle_reference, \
-    run_gpu, say
+from gpu_util import TOL, TOL_ACCEL_BWD, TOL_ACCEL_ROUNDED, accel_backward_reference, \
+    compare, normwise_error, oracle_reference, run_gpu, say
 from workloads import WORKLOADS, make_inputs, workload_inputs
 
 pytestmark = pytest.mark.gpu
@@ -48,6 +48,9 @@ def check(x, contract):
                                 x.causal, x.scale, key_len=x.key_len)
         e_o, e_l = normwise_error(got["O"], Or), normwise_error(got["LSE"], Lr)
         assert e_o <= TOL_ACCEL_ROUNDED["O"] and e_l <= TOL_ACCEL_ROUNDED["LSE"], (e_o, e_l)
+        # the backward against the backward equations at the rounded-input forward
+        eb = compare(got, accel_backward_reference(x), "accelerated", names=("dQ", "dK", "dV"))
+        assert max(eb.values()) <= TOL_ACCEL_BWD, eb
     return got, ref, errs
 
 

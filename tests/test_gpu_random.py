@@ -14,8 +14,8 @@ import math
 import numpy as np
 import pytest
 
-from gpu_util import TOL, TOL_ACCEL_ROUNDED, compare, normwise_error, oracle_reference, \
-    run_gpu, say
+from gpu_util import TOL, TOL_ACCEL_BWD, TOL_ACCEL_ROUNDED, accel_backward_reference, \
+    compare, normwise_error, oracle_reference, run_gpu, say
 from workloads import make_inputs
 
 pytestmark = pytest.mark.gpu
@@ -67,3 +67,6 @@ def test_random_case(gpu_lib, i):
                                 x.causal, x.scale, key_len=x.key_len)
         e_o, e_l = normwise_error(got["O"], Or), normwise_error(got["LSE"], Lr)
         assert e_o <= TOL_ACCEL_ROUNDED["O"] and e_l <= TOL_ACCEL_ROUNDED["LSE"], (e_o, e_l)
+        # the backward against the backward equations at the rounded-input forward
+        eb = compare(got, accel_backward_reference(x), "accelerated", names=("dQ", "dK", "dV"))
+        assert max(eb.values()) <= TOL_ACCEL_BWD, eb
