@@ -1,11 +1,14 @@
-"""GPU parity at tile edges for the bf16 and accelerated kernels.
+"""GPU parity at tile edges, every contract.
 
 The bf16 dK/dV kernel streams 64 query rows against 64 stationary keys (16
 per wave), the bf16 dQ kernel 64-key tiles against 128 query rows, and the
 bf16 and accelerated forwards 64-key tiles against 128 query rows (software-
-pipelined for d <= 64, K and V double-buffered).  Each kernel masks only the
-tiles that cross the causal diagonal or the key length, and decides that per
-tile (per wave in the dK/dV kernel).  These cases put the query and key
+pipelined for d <= 64, K and V double-buffered).  The strict forward takes
+64 query rows (32 in its key-split form) against 64-key tiles, and the
+strict fused backward 64 or 128 stationary keys against 32-row query steps,
+split over several workgroups when the grid is small.  Each kernel masks
+only the tiles that cross the causal diagonal or the key length, and decides
+that per tile (per wave in the bf16 dK/dV kernel).  These cases put the query and key
 lengths, the causal diagonal (bottom-right aligned when Lq != Lk) and the
 key lengths on, just below and just above those tile edges, so that a tile
 taken for full one row or key too early, a pipelined tile one step off, or a
@@ -19,16 +22,16 @@ from workloads import make_inputs
 
 pytestmark = pytest.mark.gpu
 
-CONTRACTS = ("fast_bf16", "accelerated")
+CONTRACTS = ("strict_f32", "fast_bf16", "accelerated")
 
-SQUARE = [63, 64, 65, 127, 128, 129, 191, 192, 193, 257]
+SQUARE = [31, 33, 63, 64, 65, 127, 128, 129, 191, 192, 193, 257]
 CROSS = [(64, 127), (127, 64), (129, 192), (192, 129), (65, 256), (256, 65), (1, 129), (129, 1)]
 # (Lk, key lengths of the two batches): on, below and above 64-key edges
 PADDED = [(192, [64, 65]), (192, [63, 128]), (129, [1, 129]), (256, [191, 193])]
 
 
 def check(x, contract):
-    """fast_bf16: every output against the oracle.  accelerated: the forward
+    """strict_f32, fast_bf16: every output against the oracle.  accelerated: the forward
     against the oracle and against the oracle on f16-rounded inputs, the
     backward against the backward equations at that rounded-input forward
     (a batch whose rows each see one key has exact gradients of zero and
@@ -36,7 +39,7 @@ def check(x, contract):
     accel_backward_reference)."""
     got = run_gpu(x)
     ref = oracle_reference(x)
-    if contract == "fast_bf16":
+    if contract != "accelerated":
         errs = compare(got, ref, contract)
         assert max(errs.values()) <= TOL[contract], errs
         return
