@@ -193,7 +193,7 @@ void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-            for (int v = 0; v < 16; v += 2) mx = fmaxf(mx, fmaxf(sacc[kb][v], sacc[kb][v + 1]));
+            for (int v = 0; v < 16; v += 2) mx = max3_f32(mx, sacc[kb][v], sacc[kb][v + 1]);
         mx = max_xor32(mx);
         // The running maximum is only an offset: the probabilities are
         // exp2(s - m) for any m at or below the true row maximum, so O and l
@@ -368,7 +368,7 @@ void attn_fwd_accel_pipe(const float *__restrict__ Q, const float *__restrict__ 
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-            for (int v = 0; v < 16; v += 2) mx = fmaxf(mx, fmaxf(sacc[kb][v], sacc[kb][v + 1]));
+            for (int v = 0; v < 16; v += 2) mx = max3_f32(mx, sacc[kb][v], sacc[kb][v + 1]);
         mx = max_xor32(mx);
         // Rescale O and l only when some row's maximum grew by more than
         // kSlack (base 2), as in the plain form.

@@ -175,7 +175,7 @@ void attn_fwd_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ 
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-            for (int v = 0; v < 16; v += 2) mx = fmaxf(mx, fmaxf(sacc[kb][v], sacc[kb][v + 1]));
+            for (int v = 0; v < 16; v += 2) mx = max3_f32(mx, sacc[kb][v], sacc[kb][v + 1]);
         mx = max_xor32(mx);
         // The running maximum is only an offset: the probabilities are
         // exp2(s - m) for any m at or below the true row maximum, so O and l
@@ -342,7 +342,7 @@ void attn_fwd_bf16_pipe(const uint16_t *__restrict__ Q, const uint16_t *__restri
 #pragma unroll
         for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-            for (int v = 0; v < 16; v += 2) mx = fmaxf(mx, fmaxf(sacc[kb][v], sacc[kb][v + 1]));
+            for (int v = 0; v < 16; v += 2) mx = max3_f32(mx, sacc[kb][v], sacc[kb][v + 1]);
         mx = max_xor32(mx);
         const float grow2 = POS_SCALE ? (mx - m_run) * scale_log2 : mx - m_run;
         if (__any(grow2 > kSlack)) {

@@ -62,6 +62,17 @@ __device__ __forceinline__ f32x16 zero16() {
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 
 __device__ __forceinline__ float xor_lanes(float v, int mask) { return __shfl_xor(v, mask, 64); }
+// max(a, b, c) as one v_max3_f32.  Written out because in IEEE mode the
+// compiler must quiet a possible signalling NaN before each fmaxf, and for
+// values it cannot prove canonical (matrix-core results) it spends one
+// v_max per input on that; the row maxima here are taken over MFMA results
+// and -inf, which are never signalling NaNs.
+__device__ __forceinline__ float max3_f32(float a, float b, float c) {
+    float r;
+    asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+    return r;
+}
+
 
 // Cross-row exchanges on the VALU (no LDS crossbar round trip).  For
 // v_permlane16_swap(x, x) every lane receives {x of the even 16-lane row,
