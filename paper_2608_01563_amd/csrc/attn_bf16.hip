@@ -7,7 +7,10 @@
 // rounds matrix inputs locally and accumulates in f32; here Q, K, V, O, dO
 // and the gradients are stored bf16, and the softmax probabilities P and dS
 // are rounded to bf16 (nearest even) only as inputs of the second product of
-// each pass.  Softmax statistics, LSE and D stay f32.
+// each pass.  Softmax statistics, LSE and D stay f32.  D_i = rowsum(dO o O)
+// needs no launch of its own: the dQ kernel, which holds each row's dO in
+// registers, computes it on the way, writes it to the workspace, and runs
+// before the dK/dV kernel that reads it.
 //
 // Contraction order: for products over the head dimension a lane holds 8
 // consecutive d values (one 16-byte LDS read); for products over streamed
@@ -430,29 +433,6 @@ void attn_fwd_bf16_pipe(const uint16_t *__restrict__ Q, const uint16_t *__restri
     }
 }
 
-// ------------------------------------------------- backward: D = rowsum(dO o O)
-template <int D>
-__global__ __launch_bounds__(256) void attn_rowdot_bf16(const uint16_t *__restrict__ O,
-                                                        const uint16_t *__restrict__ dO,
-                                                        float *__restrict__ Dws, int rows) {
-    constexpr int TPR = D / 8;   // threads per row, 8 bf16 each
-    const int row = blockIdx.x * (256 / TPR) + threadIdx.x / TPR;
-    const int c8 = threadIdx.x % TPR;
-    float v = 0.f;
-    if (row < rows) {
-        const u32x4 o = *reinterpret_cast<const u32x4 *>(O + (size_t)row * D + 8 * c8);
-        const u32x4 go = *reinterpret_cast<const u32x4 *>(dO + (size_t)row * D + 8 * c8);
-#pragma unroll
-        for (int m = 0; m < 4; ++m) {
-            v += __uint_as_float(o[m] << 16) * __uint_as_float(go[m] << 16);
-            v += __uint_as_float(o[m] & 0xffff0000u) * __uint_as_float(go[m] & 0xffff0000u);
-        }
-    }
-#pragma unroll
-    for (int m = TPR / 2; m >= 1; m >>= 1) v += xor_lanes(v, m);
-    if (row < rows && c8 == 0) Dws[row] = v;
-}
-
 // ------------------------------------------------------- backward: dK, dV
 // Key tile of 64 keys stationary (16 per wave, one per lane column) on
 // 16x16x32 products; query tiles of 64 rows stream through LDS row-major.
@@ -662,9 +642,10 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
 template <int D, int KS>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
 void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K,
-                  const uint16_t *__restrict__ V, const uint16_t *__restrict__ dO,
-                  const float *__restrict__ LSE, const float *__restrict__ Dws,
-                  uint16_t *__restrict__ dQ, const int32_t *__restrict__ key_len, int H, int Lq, int Lk,
+                  const uint16_t *__restrict__ V, const uint16_t *__restrict__ O,
+                  const uint16_t *__restrict__ dO, const float *__restrict__ LSE,
+                  float *__restrict__ Dws, uint16_t *__restrict__ dQ,
+                  const int32_t *__restrict__ key_len, int H, int Lq, int Lk,
                   int causal, float scale, float scale_log2, int n_qtiles, int BH, int layer) {
     constexpr int NS = D / 16;
     constexpr int NCB = D / 32;
@@ -706,7 +687,21 @@ void attn_dq_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__ K
     }
     // Rows past Lq: Q = dO = 0 and LSE = D = 0, so their dS is exactly 0.
     const float lse2 = (qi < Lq) ? LSE[(size_t)head * Lq + qi] * kLog2e : 0.f;
-    const float Di = (qi < Lq) ? Dws[(size_t)head * Lq + qi] : 0.f;
+    // D_i = sum_d dO[i][d] O[i][d], in f32 from the bf16 values: this lane
+    // holds the d values of oreg, its partner (lane ^ 32) the other half of
+    // the row.  The row's D goes to the workspace for the dK/dV kernel,
+    // which runs after this one.
+    float Di = 0.f;
+    if (qi < Lq) {
+#pragma unroll
+        for (int s = 0; s < NS; ++s) {
+            const bf16x8 o8 = load_bf16x8(O + qoff + (size_t)qi * D + 16 * s + 8 * h);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) Di = fmaf((float)o8[e], (float)oreg[s][e], Di);
+        }
+    }
+    Di += xor_lanes(Di, 32);
+    if (qi < Lq && h == 0) Dws[(size_t)head * Lq + qi] = Di;
 
     f32x16 dqacc[NCB];   // dQ^T[32cb + 8a + 4h + r][qi]
 #pragma unroll
@@ -821,19 +816,6 @@ hipError_t launch_fwd_bf16(const AttnProblem &p, const uint16_t *Q, const uint16
     return hipGetLastError();
 }
 
-hipError_t launch_bwd_rowdot_bf16(const AttnProblem &p, const uint16_t *O, const uint16_t *dO,
-                                  float *Dws, hipStream_t s) {
-    const int rows = p.B * p.H * p.Lq;
-    const dim3 block(256);
-    switch (p.d) {
-    case 32: attn_rowdot_bf16<32><<<dim3(cdiv(rows, 256 / 4)), block, 0, s>>>(O, dO, Dws, rows); break;
-    case 64: attn_rowdot_bf16<64><<<dim3(cdiv(rows, 256 / 8)), block, 0, s>>>(O, dO, Dws, rows); break;
-    case 128: attn_rowdot_bf16<128><<<dim3(cdiv(rows, 256 / 16)), block, 0, s>>>(O, dO, Dws, rows); break;
-    default: return hipErrorInvalidValue;
-    }
-    return hipGetLastError();
-}
-
 hipError_t launch_bwd_dkdv_bf16(const AttnProblem &p, const uint16_t *Q, const uint16_t *K,
                                 const uint16_t *V, const uint16_t *dO, const float *LSE,
                                 const float *Dws, uint16_t *dK, uint16_t *dV, hipStream_t s) {
@@ -855,15 +837,15 @@ hipError_t launch_bwd_dkdv_bf16(const AttnProblem &p, const uint16_t *Q, const u
 }
 
 hipError_t launch_bwd_dq_bf16(const AttnProblem &p, const uint16_t *Q, const uint16_t *K,
-                              const uint16_t *V, const uint16_t *dO, const float *LSE,
-                              const float *Dws, uint16_t *dQ, hipStream_t s) {
+                              const uint16_t *V, const uint16_t *O, const uint16_t *dO,
+                              const float *LSE, float *Dws, uint16_t *dQ, hipStream_t s) {
     const int BH = p.B * p.H;
     const int nqt = cdiv(p.Lq, kFwdRows);
     const dim3 grid(nqt * BH), block(kThreads);
     const float sl2 = p.scale * kLog2e;
     auto go = [&](auto kern) {
         const int ly = causal_rank_layer((const void *)kern, kThreads, grid.x, BH, p.causal);
-        kern<<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk,
+        kern<<<grid, block, 0, s>>>(Q, K, V, O, dO, LSE, Dws, dQ, p.key_len, p.H, p.Lq, p.Lk,
                                     p.causal, p.scale, sl2, nqt, BH, ly);
     };
     switch (p.d) {

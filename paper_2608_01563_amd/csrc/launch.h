@@ -46,8 +46,6 @@ hipError_t launch_fwd_accel(const AttnProblem &p, const float *Q, const float *K
 // Backward step 1: D_i = sum_k dO_ik O_ik (f32 out, one per row).
 hipError_t launch_bwd_rowdot_f32(const AttnProblem &p, const float *O, const float *dO,
                                  float *Dws, hipStream_t s);
-hipError_t launch_bwd_rowdot_bf16(const AttnProblem &p, const uint16_t *O,
-                                  const uint16_t *dO, float *Dws, hipStream_t s);
 
 // Backward step 2: dK, dV with the key tile stationary.
 hipError_t launch_bwd_dkdv_f32(const AttnProblem &p, const float *Q, const float *K,
@@ -82,8 +80,11 @@ hipError_t launch_bwd_dq_reduce_f32(const AttnProblem &p, const float *dQp, floa
 hipError_t launch_bwd_dq_f32(const AttnProblem &p, const float *Q, const float *K,
                              const float *V, const float *dO, const float *LSE,
                              const float *Dws, float *dQ, hipStream_t s);
+// bf16: the dQ kernel also computes D_i = sum_k dO_ik O_ik for its rows
+// and writes it to Dws; it runs first, and the dK/dV kernel reads D from
+// Dws after it.
 hipError_t launch_bwd_dq_bf16(const AttnProblem &p, const uint16_t *Q, const uint16_t *K,
-                              const uint16_t *V, const uint16_t *dO, const float *LSE,
-                              const float *Dws, uint16_t *dQ, hipStream_t s);
+                              const uint16_t *V, const uint16_t *O, const uint16_t *dO,
+                              const float *LSE, float *Dws, uint16_t *dQ, hipStream_t s);
 
 }  // namespace mg

@@ -182,14 +182,14 @@ mg_status_t attn_bwd_enqueue(const void *Q, const void *K, const void *V, const 
         const uint16_t *q = (const uint16_t *)Q, *k = (const uint16_t *)K,
                        *v = (const uint16_t *)V;
         const uint16_t *o = (const uint16_t *)O, *go = (const uint16_t *)dO;
-        MG_TRY(run_kernel(kernel_name("attn_rowdot", contract, d), stream,
-                          [&] { return mg::launch_bwd_rowdot_bf16(p, o, go, Dws, stream); }));
+        // The dQ kernel computes D for its query rows on the way (it holds
+        // each row's dO already) and writes it for the dK/dV kernel.
+        MG_TRY(run_kernel(kernel_name("attn_dq", contract, d), stream, [&] {
+            return mg::launch_bwd_dq_bf16(p, q, k, v, o, go, LSE, Dws, (uint16_t *)dQ, stream);
+        }));
         MG_TRY(run_kernel(kernel_name("attn_dkdv", contract, d), stream, [&] {
             return mg::launch_bwd_dkdv_bf16(p, q, k, v, go, LSE, Dws, (uint16_t *)dK,
                                             (uint16_t *)dV, stream);
-        }));
-        MG_TRY(run_kernel(kernel_name("attn_dq", contract, d), stream, [&] {
-            return mg::launch_bwd_dq_bf16(p, q, k, v, go, LSE, Dws, (uint16_t *)dQ, stream);
         }));
     }
     return ok();
