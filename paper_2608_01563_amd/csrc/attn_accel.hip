@@ -275,26 +275,45 @@ void attn_fwd_accel(const float *__restrict__ Q, const float *__restrict__ K,
 // tile kt, and only then rounds the staged tiles to f16 and writes them into
 // the buffers that the iteration's barrier freed.  Every load has a whole
 // iteration to land, and one barrier per tile suffices.  K and V are
-// double-buffered in separate named arrays.  At d = 128 the second score
-// block and the second staging set do not fit two waves per SIMD, and the
-// plain form above is used.
-template <int D, bool POS_SCALE>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2, 8)))
+// double-buffered.  At d = 128 the second score block and the second staging
+// set do not fit two waves per SIMD, and the plain form above is used.
+//
+// KS = 2 is the key-split form for causal grids that the chip holds in one or
+// two rounds: the longest query tile's chain of key tiles, not the total
+// work, sets the kernel's time there.  A workgroup of eight waves holds two
+// key groups of four; both take the same 128 queries, group 0 the first
+// ceil(n/2) of the tile's n key tiles and group 1 the rest, each through its
+// own double-buffered K and V.  The groups run the same number of
+// iterations (group 1 idles through the last one when n is odd), so the
+// workgroup's barriers stay matched.  At the end group 1 leaves its (offset,
+// sum, O) state in LDS and group 0 merges it: with offsets m_a, m_b (base 2)
+// and m = max(m_a, m_b), l = l_a 2^(m_a - m) + l_b 2^(m_b - m), likewise O.
+template <int D, bool POS_SCALE, int KS>
+__global__ __launch_bounds__(kThreads * KS) __attribute__((amdgpu_waves_per_eu(2, 8)))
 void attn_fwd_accel_pipe(const float *__restrict__ Q, const float *__restrict__ K,
                          const float *__restrict__ V, float *__restrict__ O,
                          float *__restrict__ LSE, const int32_t *__restrict__ key_len, int H,
                          int Lq, int Lk, int causal, float scale_log2, int n_qtiles, int BH,
                          int layer) {
+    static_assert(KS == 1 || KS == 2, "one or two key groups");
     constexpr int NS = D / 16;
     constexpr int NCB = D / 32;
     constexpr int NKB = kKeys / 32;
     constexpr int LD = Bf16Ld<D>::value;     // K rows: 16-byte reads of 32 rows
     constexpr int LDV = Bf16LdTr<D>::value;  // V rows: transpose reads only
     using St = F16ConvStager<kKeys, D, kThreads>;
-    __shared__ __attribute__((aligned(16))) uint16_t K0[kKeys][LD], K1[kKeys][LD];
-    __shared__ __attribute__((aligned(16))) uint16_t V0[kKeys][LDV], V1[kKeys][LDV];
     using KBuf = uint16_t[kKeys][LD];
     using VBuf = uint16_t[kKeys][LDV];
+    struct Bufs {
+        KBuf K0, K1;
+        VBuf V0, V1;
+    };
+    // Group 1's state for the merge: per query wave and lane, the offset, the
+    // sum and the 16 * NCB registers of O^T, slot-major (lane-contiguous).
+    constexpr int NX = 2 + 16 * NCB;
+    static_assert(KS == 1 || (size_t)kWaves * NX * 64 * sizeof(float) <= KS * sizeof(Bufs),
+                  "merge state fits in the tile buffers");
+    __shared__ __attribute__((aligned(16))) unsigned char smem[KS * sizeof(Bufs)];
 
     const int slot = blockIdx.x / BH;
     const int head = blockIdx.x - slot * BH;
@@ -309,15 +328,23 @@ void attn_fwd_accel_pipe(const float *__restrict__ Q, const float *__restrict__ 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g = w / kWaves;          // key group
+    const int wq = w - g * kWaves;     // query wave within the group
+    const int tg = tid - g * kThreads; // thread index within the group
     const int c = lane & 31;
     const int h = lane >> 5;
     const int jr = (lane & 15) >> 2, jc = 4 * (lane & 3);   // transpose-read block offsets
     const int q0 = qt * kRows;
-    const int qi = q0 + 32 * w + c;
+    const int qi = q0 + 32 * wq + c;
+    Bufs &bf = *reinterpret_cast<Bufs *>(smem + g * sizeof(Bufs));
 
     const int klen = key_limit(key_len, b, Lk);
     const int kend = causal ? min(klen, q0 + kRows + diag) : klen;
-    const int ntiles = (kend + kKeys - 1) / kKeys;
+    const int ntiles = max((kend + kKeys - 1) / kKeys, 0);
+    // This group's key tiles [kbeg, kbeg + kcnt); both groups iterate nloop times.
+    const int nloop = (ntiles + KS - 1) / KS;
+    const int kbeg = g * nloop;
+    const int kcnt = min(nloop, ntiles - kbeg);
 
     // B operand of S^T = K Q^T: lane holds f16(Q[qi][16s + 8h + e]).
     f16x8 qreg[NS];
@@ -412,38 +439,67 @@ void attn_fwd_accel_pipe(const float *__restrict__ Q, const float *__restrict__ 
             }
     };
 
-    // Prologue: K(0) into K0, V(0) into V0, K(1) into K1; S(0).  Tile j lives
-    // in buffer j % 2.
+    // Prologue: K(0) into K0, V(0) into V0, K(1) into K1; S(0).  The
+    // group's j-th tile lives in buffer j % 2.
     St sk, sv;
     f32x16 sa[NKB], sb[NKB];
-    if (ntiles > 0) {
-        sk.load(Kh, 0, Lk, tid);
-        sv.load(Vh, 0, Lk, tid);
-        sk.store(K0, tid);
-        sv.store(V0, tid);
-        if (ntiles > 1) {
-            sk.load(Kh, kKeys, Lk, tid);
-            sk.store(K1, tid);
+    if (kcnt > 0) {
+        sk.load(Kh, kbeg * kKeys, Lk, tg);
+        sv.load(Vh, kbeg * kKeys, Lk, tg);
+        sk.store(bf.K0, tg);
+        sv.store(bf.V0, tg);
+        if (kcnt > 1) {
+            sk.load(Kh, (kbeg + 1) * kKeys, Lk, tg);
+            sk.store(bf.K1, tg);
+        }
+    }
+    __syncthreads();
+    if (kcnt > 0) scores(bf.K0, sa);
+    // Iteration j: S(j) is in `cur`; K(j+1) is in Kn and V(j) in Vc, written
+    // an iteration earlier; K(j+2) goes to Kc, whose K(j) the last iteration
+    // consumed, and V(j+1) to Vn, whose V(j-1) likewise.
+    auto iter = [&](int j, f32x16 (&cur)[NKB], f32x16 (&nxt)[NKB], KBuf &Kc, const KBuf &Kn,
+                    const VBuf &Vc, VBuf &Vn) {
+        __syncthreads();   // K(j+1), V(j) visible; K(j) and V(j-1) buffers free
+        if (j + 2 < kcnt) sk.load(Kh, (kbeg + j + 2) * kKeys, Lk, tg);
+        if (j + 1 < kcnt) sv.load(Vh, (kbeg + j + 1) * kKeys, Lk, tg);
+        if (j + 1 < kcnt) scores(Kn, nxt);
+        if (j < kcnt) softmax_pv(kbeg + j, cur, Vc);
+        if (j + 2 < kcnt) sk.store(Kc, tg);
+        if (j + 1 < kcnt) sv.store(Vn, tg);
+    };
+    for (int j = 0; j < nloop; j += 2) {
+        iter(j, sa, sb, bf.K0, bf.K1, bf.V0, bf.V1);
+        if (j + 1 < nloop) iter(j + 1, sb, sa, bf.K1, bf.K0, bf.V1, bf.V0);
+    }
+
+    // Offset of the probabilities in base-2 units; -inf for a row that saw
+    // no allowed key (its sum and O are zero).
+    float m2f = (m_run == -INFINITY) ? -INFINITY : (POS_SCALE ? m_run * scale_log2 : m_run);
+    if constexpr (KS == 2) {
+        float *xs = reinterpret_cast<float *>(smem) + wq * NX * 64 + lane;
+        __syncthreads();   // every wave is done with its tiles; smem is free
+        if (g == 1) {
+            xs[0] = m2f;
+            xs[64] = l_run;
+#pragma unroll
+            for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) xs[(2 + 16 * cb + v) * 64] = oacc[cb][v];
         }
         __syncthreads();
-        scores(K0, sa);
-    }
-    // Iteration kt: S(kt) is in `cur`; K(kt+1) is in Kn and V(kt) in Vc,
-    // written an iteration earlier; K(kt+2) goes to Kc, whose K(kt) the last
-    // iteration consumed, and V(kt+1) to Vn, whose V(kt-1) likewise.
-    auto iter = [&](int kt, f32x16 (&cur)[NKB], f32x16 (&nxt)[NKB], KBuf &Kc, const KBuf &Kn,
-                    const VBuf &Vc, VBuf &Vn) {
-        __syncthreads();   // K(kt+1), V(kt) visible; K(kt) and V(kt-1) buffers free
-        if (kt + 2 < ntiles) sk.load(Kh, (kt + 2) * kKeys, Lk, tid);
-        if (kt + 1 < ntiles) sv.load(Vh, (kt + 1) * kKeys, Lk, tid);
-        if (kt + 1 < ntiles) scores(Kn, nxt);
-        softmax_pv(kt, cur, Vc);
-        if (kt + 2 < ntiles) sk.store(Kc, tid);
-        if (kt + 1 < ntiles) sv.store(Vn, tid);
-    };
-    for (int kt = 0; kt < ntiles; kt += 2) {
-        iter(kt, sa, sb, K0, K1, V0, V1);
-        if (kt + 1 < ntiles) iter(kt + 1, sb, sa, K1, K0, V1, V0);
+        if (g == 1) return;   // no barrier follows
+        const float mb = xs[0];
+        const float mm = fmaxf(m2f, mb);
+        const float fa = (mm == -INFINITY) ? 0.f : exp2_fast(m2f - mm);
+        const float fb = (mm == -INFINITY) ? 0.f : exp2_fast(mb - mm);
+        l_run = l_run * fa + xs[64] * fb;
+#pragma unroll
+        for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                oacc[cb][v] = oacc[cb][v] * fa + xs[(2 + 16 * cb + v) * 64] * fb;
+        m2f = mm;
     }
 
     const float l = sum_xor32(l_run);
@@ -457,10 +513,7 @@ void attn_fwd_accel_pipe(const float *__restrict__ Q, const float *__restrict__ 
                 *reinterpret_cast<f32x4 *>(orow + 32 * cb + 8 * a + 4 * h) =
                     f32x4{oacc[cb][4 * a], oacc[cb][4 * a + 1], oacc[cb][4 * a + 2],
                           oacc[cb][4 * a + 3]} * inv;
-        if (h == 0) {
-            const float m2 = POS_SCALE ? m_run * scale_log2 : m_run;
-            LSE[(size_t)head * Lq + qi] = (l > 0.f) ? (m2 + log2f(l)) * kLn2 : -INFINITY;
-        }
+        if (h == 0) LSE[(size_t)head * Lq + qi] = (l > 0.f) ? (m2f + log2f(l)) * kLn2 : -INFINITY;
     }
 }
 
@@ -468,26 +521,44 @@ inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 
 }  // namespace
 
+// Causal grids of at most this many query-tile workgroups take the key-split
+// form (d <= 64).  The key-split kernel holds one workgroup per CU (eight
+// waves, 86 KB of LDS at d = 64), so up to the CU count of MI355X it runs in
+// one round, and there the longest query tile's chain of key tiles sets the
+// forward's time: B2 H8 L1024 d64 took 20.9 instead of 27.2 us, B4 H8 L1024
+// 22.5 instead of 27.9.  Grids that need a second round gained nothing or
+// lost (B8 H8 L1024: 31.0 against 30.4 us; B32 H8 L256: 24.2 against 16.7).
+#ifndef MG_ACCEL_SPLIT_UPTO
+#define MG_ACCEL_SPLIT_UPTO 256
+#endif
+
 hipError_t launch_fwd_accel(const AttnProblem &p, const float *Q, const float *K,
                             const float *V, float *O, float *LSE, hipStream_t s) {
     const int BH = p.B * p.H;
     const int nqt = cdiv(p.Lq, kRows);
-    const dim3 grid(nqt * BH), block(kThreads);
+    const dim3 grid(nqt * BH);
     const float sl2 = p.scale * kLog2e;
-    auto go = [&](auto kern) {
-        const int ly = causal_rank_layer((const void *)kern, kThreads, grid.x, BH, p.causal);
-        kern<<<grid, block, 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal, sl2,
-                                    nqt, BH, ly);
+    auto go = [&](auto kern, int ks) {
+        const int nt = kThreads * ks;
+        const int ly = causal_rank_layer((const void *)kern, nt, grid.x, BH, p.causal);
+        kern<<<grid, dim3(nt), 0, s>>>(Q, K, V, O, LSE, p.key_len, p.H, p.Lq, p.Lk, p.causal,
+                                       sl2, nqt, BH, ly);
     };
-#define MG_FWD_ACCEL(KERN, DD) \
-    (p.scale > 0.f ? go(KERN<DD, true>) : go(KERN<DD, false>))
+    const bool split = p.causal && (long)grid.x <= MG_ACCEL_SPLIT_UPTO;
+#define MG_FWD_ACCEL_PIPE(DD)                                                         \
+    (split ? (p.scale > 0.f ? go(attn_fwd_accel_pipe<DD, true, 2>, 2)                 \
+                            : go(attn_fwd_accel_pipe<DD, false, 2>, 2))               \
+           : (p.scale > 0.f ? go(attn_fwd_accel_pipe<DD, true, 1>, 1)                 \
+                            : go(attn_fwd_accel_pipe<DD, false, 1>, 1)))
     switch (p.d) {
-    case 32: MG_FWD_ACCEL(attn_fwd_accel_pipe, 32); break;
-    case 64: MG_FWD_ACCEL(attn_fwd_accel_pipe, 64); break;
-    case 128: MG_FWD_ACCEL(attn_fwd_accel, 128); break;
+    case 32: MG_FWD_ACCEL_PIPE(32); break;
+    case 64: MG_FWD_ACCEL_PIPE(64); break;
+    case 128:
+        p.scale > 0.f ? go(attn_fwd_accel<128, true>, 1) : go(attn_fwd_accel<128, false>, 1);
+        break;
     default: return hipErrorInvalidValue;
     }
-#undef MG_FWD_ACCEL
+#undef MG_FWD_ACCEL_PIPE
     return hipGetLastError();
 }
 

@@ -405,6 +405,20 @@ def test_workload6_accelerated(gpu_lib):
                                                         {k: "%.2e" % v for k, v in errs.items()}))
 
 
+@pytest.mark.parametrize("B,H,L,d,scale_sign", [(2, 8, 1024, 64, 1), (1, 4, 1000, 32, 1),
+                                                 (2, 3, 777, 64, -1)])
+def test_accelerated_key_split_forward(gpu_lib, B, H, L, d, scale_sign):
+    """Causal grids of at most 256 query tiles take the key-split forward
+    (two key groups per workgroup, merged through LDS): long key chains, an
+    odd key-tile count (777 keys: 13 tiles, the second group idles through
+    one iteration) and a negative scale, against the oracle."""
+    say("accelerated key-split forward B%d H%d L%d d%d scale sign %d" % (B, H, L, d, scale_sign))
+    x = make_inputs(B, H, L, d, causal=True, contract="accelerated", seed=31 + L,
+                    scale=scale_sign / math.sqrt(d))
+    assert B * H * -(-L // 128) <= 256
+    accel_check(x)
+
+
 def test_accelerated_backward_is_the_strict_backward(gpu_lib):
     """Given the same O and LSE, the accelerated backward is the strict one:
     bitwise equal outputs, and the oracle's O/LSE in gives strict parity."""
