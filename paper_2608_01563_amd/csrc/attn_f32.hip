@@ -671,15 +671,24 @@ void attn_dkdv_f32(const float *__restrict__ Q, const float *__restrict__ K,
 // during the whole current iteration; with one, during the dQ product.  A
 // tile's dQ partials are stored at the start of the next iteration, so the
 // wait for the next tile never waits on a just-issued store.
-template <int D, int NIB, class C>
+//
+// Small grids (LOCALD): the O rows of each query tile arrive with its Q and
+// dO rows, and the workgroup computes D_i = sum_k dO_ik O_ik in LDS before
+// the softmax needs it, so no separate D launch precedes the kernel.  With a
+// single key tile and no query split (direct_dq), the one partial of a row is
+// its dQ: it is scaled and written to dQ (dQp points there), rows outside the
+// tile's query range get zeros, and no reduction follows (LOCALD grids only,
+// so that the large-grid instances carry none of this).
+template <int D, int NIB, class C, bool LOCALD>
 __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::template occ<D>(), 8)))
 void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
-                    const float *__restrict__ V, const float *__restrict__ dO,
-                    const float *__restrict__ LSE, const float *__restrict__ Dws,
-                    float *__restrict__ dK, float *__restrict__ dV, float *__restrict__ dQp,
-                    float *__restrict__ dKVp, const int32_t *__restrict__ key_len, int H, int Lq,
-                    int Lk, int causal, float scale, float scale_log2, int BH, int nsplit,
-                    int nranks, int layer, int work_first) {
+                    const float *__restrict__ V, const float *__restrict__ O,
+                    const float *__restrict__ dO, const float *__restrict__ LSE,
+                    const float *__restrict__ Dws, float *__restrict__ dK,
+                    float *__restrict__ dV, float *__restrict__ dQp, float *__restrict__ dKVp,
+                    const int32_t *__restrict__ key_len, int H, int Lq, int Lk, int causal,
+                    float scale, float scale_log2, int BH, int nsplit, int nranks, int layer,
+                    int work_first, int direct_dq) {
     constexpr int DQ = D / 4;
     constexpr int NC = D / 16;
     constexpr int BR = 16 * NIB;
@@ -693,6 +702,7 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     __shared__ __attribute__((aligned(16))) float dOs[NB][BR][LD];
     __shared__ __attribute__((aligned(16))) float lse2s[NB][BR];    // LSE (natural log)
     __shared__ __attribute__((aligned(16))) float Ds[NB][BR];
+    __shared__ __attribute__((aligned(16))) float Os[LOCALD ? NB : 1][LOCALD ? BR : 1][LD];
     __shared__ __attribute__((aligned(16))) float Kt[D][KR + 4];    // key tile, transposed
     __shared__ __attribute__((aligned(16))) float dSs[BR][KR + 4];  // dS of the query tile
 
@@ -733,11 +743,13 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
     const Tile tile;
 
     // Direct-to-LDS loads of the Q and dO rows of query tile qt, and of their
-    // LSE (wave 0) and D (the last wave) values; rows past Lq arrive as zeros.
+    // LSE (wave 0) and D (the last wave) values, or with LOCALD of their O
+    // rows instead of D; rows past Lq arrive as zeros.
     auto fetch = [&](int qt, int buf) {
         tile.issue(Qs[buf], Qh, qt * BR, Lq, w, lane);
         tile.issue(dOs[buf], dOh, qt * BR, Lq, w, lane);
-        if (w == 0 || w == C::NW - 1) {
+        if constexpr (LOCALD) tile.issue(Os[buf], O + qoff, qt * BR, Lq, w, lane);
+        if (w == 0 || (!LOCALD && w == C::NW - 1)) {
             const int row0 = qt * BR;
             const int rows = min(max(Lq - row0, 0), BR);
             const float *src = (w == 0 ? LSE : Dws) + (size_t)head * Lq + row0;
@@ -806,13 +818,40 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
             const int ib = blk / NC;
             const int c = blk - ib * NC;
             __builtin_amdgcn_raw_buffer_store_b128(
-                __builtin_bit_cast(u32x4, dqacc[bb]), rsrc,
+                __builtin_bit_cast(u32x4, (LOCALD && direct_dq) ? dqacc[bb] * scale : dqacc[bb]),
+                rsrc,
                 ((16 * ib + il) * D + 16 * c + 4 * g) * 4, 0, 0);
+        }
+    };
+
+    // D of the tile in buffer buf from its landed dO and O rows: TPR threads
+    // per row, each summing every TPR-th 4-float chunk, then a butterfly.
+    auto local_d = [&](int buf) {
+        if constexpr (LOCALD) {
+            constexpr int TPR = C::NT / BR;
+            static_assert(C::NT % BR == 0 && (TPR & (TPR - 1)) == 0 && TPR <= 64,
+                          "threads per row");
+            const int row = tid / TPR, part = tid - (tid / TPR) * TPR;
+            float acc = 0.f;
+#pragma unroll
+            for (int c4 = part; c4 < D / 4; c4 += TPR) {
+                const f32x4 a = *reinterpret_cast<const f32x4 *>(&dOs[buf][row][4 * c4]);
+                const f32x4 o = *reinterpret_cast<const f32x4 *>(&Os[buf][row][4 * c4]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) acc = fmaf(a[e], o[e], acc);
+            }
+#pragma unroll
+            for (int m = TPR / 2; m >= 1; m >>= 1) acc += xor_lanes(acc, m);
+            if (part == 0) Ds[buf][row] = acc;
         }
     };
 
     if (qstart < qstop) wait_vmcnt<0>();
     __syncthreads();   // first tile, its LSE/D and Kt visible
+    if (LOCALD) {
+        if (qstart < qstop) local_d(0);
+        __syncthreads();   // its D visible
+    }
 
     for (int qt = qstart; qt < qstop; ++qt) {
         const int cb = (NB == 2) ? ((qt - qstart) & 1) : 0;
@@ -928,8 +967,23 @@ void attn_dkdvq_f32(const float *__restrict__ Q, const float *__restrict__ K,
 
         if (qt + 1 < qstop) wait_vmcnt<0>();   // next Q/dO tile and its LSE/D landed
         __syncthreads();   // next tile visible; dS and this tile's buffer free
+        if (LOCALD) {
+            if (qt + 1 < qstop) local_d(NB == 2 ? (cb ^ 1) : 0);
+            __syncthreads();   // its D visible
+        }
     }
     if (qstart < qstop) store_dq(qstop - 1);
+    if (LOCALD && direct_dq) {
+        // rows no query tile of this workgroup wrote (none see a key) get zeros
+        float *dqh = dQp + (size_t)head * Lq * D;
+        const int r0 = min(qstart * BR, Lq), r1 = min(qstop * BR, Lq);
+        const int nz = (r0 + (Lq - r1)) * (D / 4);
+        for (int f = tid; f < nz; f += C::NT) {
+            const int rr = f / (D / 4);
+            const int row = rr < r0 ? rr : r1 + (rr - r0);
+            *reinterpret_cast<f32x4 *>(dqh + (size_t)row * D + 4 * (f - rr * (D / 4))) = zero4();
+        }
+    }
 
     // One split writes dK and dV directly; several write partials laid out
     // [dK, dV][split][B*H][Lk][d] (every split writes its rows, zeros for an
@@ -1285,38 +1339,65 @@ int fused_dq_query_splits(const AttnProblem &p) {
     return (int)std::max(1L, std::min(by_grid, by_tiles));
 }
 
+// Small fused grids compute D in the kernel (LOCALD): at most this many key
+// tiles per head, so that each query tile's O rows are read a few times, and
+// a grid below MG_DKDV_SPLIT_BELOW workgroups.
+#ifndef MG_LOCAL_D_MAX_KEY_TILES
+#define MG_LOCAL_D_MAX_KEY_TILES 4
+#endif
+bool fused_local_d(const AttnProblem &p) {
+    const long nkt = cdiv(p.Lk, fused_dq_key_rows(p));
+    return nkt <= MG_LOCAL_D_MAX_KEY_TILES && nkt * p.B * p.H < MG_DKDV_SPLIT_BELOW;
+}
+bool fused_direct_dq(const AttnProblem &p) {
+    return fused_local_d(p) && cdiv(p.Lk, fused_dq_key_rows(p)) == 1 &&
+           fused_dq_query_splits(p) == 1;
+}
+
 template <class C, int NIB>
 static hipError_t launch_dkdvq(const AttnProblem &p, const float *Q, const float *K,
-                               const float *V, const float *dO, const float *LSE,
-                               const float *Dws, float *dK, float *dV, float *dQp,
-                               float *dKVp, hipStream_t s) {
+                               const float *V, const float *O, const float *dO,
+                               const float *LSE, const float *Dws, float *dK, float *dV,
+                               float *dQp, float *dKVp, hipStream_t s) {
     const int BH = p.B * p.H;
     const int ns = fused_dq_query_splits(p);
     const int nr = cdiv(p.Lk, C::ROWS) * ns;   // ranks: key tile x split
     const dim3 grid(nr * BH), block(C::NT);
     const float sl2 = p.scale * kLog2e;
+    const int direct = fused_direct_dq(p) ? 1 : 0;
     auto go = [&](auto kern) {
         const int ly = causal_rank_layer((const void *)kern, C::NT, grid.x, BH, p.causal);
-        kern<<<grid, block, 0, s>>>(Q, K, V, dO, LSE, Dws, dK, dV, dQp, dKVp, p.key_len, p.H,
-                                    p.Lq, p.Lk, p.causal, p.scale, sl2, BH, ns, nr, ly,
-                                    padded_work_order(p));
+        kern<<<grid, block, 0, s>>>(Q, K, V, O, dO, LSE, Dws, dK, dV, dQp, dKVp, p.key_len,
+                                    p.H, p.Lq, p.Lk, p.causal, p.scale, sl2, BH, ns, nr, ly,
+                                    padded_work_order(p), direct);
+    };
+    // Local D only in the 64-key form: grids small enough for it never take
+    // the 128-key tiles, which need at least 512 workgroups.
+    constexpr bool kLocalForm = !std::is_same<C, DkdvqCausalCfg>::value;
+    const bool local = kLocalForm && fused_local_d(p);
+    auto pick = [&](auto plain, auto with_local) {
+        if constexpr (kLocalForm) {
+            if (local) return go(with_local);
+        }
+        go(plain);
     };
     switch (p.d) {
-    case 32: go(attn_dkdvq_f32<32, NIB, C>); break;
-    case 64: go(attn_dkdvq_f32<64, NIB, C>); break;
+    case 32: pick(attn_dkdvq_f32<32, NIB, C, false>, attn_dkdvq_f32<32, NIB, C, kLocalForm>); break;
+    case 64: pick(attn_dkdvq_f32<64, NIB, C, false>, attn_dkdvq_f32<64, NIB, C, kLocalForm>); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
 hipError_t launch_bwd_dkdvq_f32(const AttnProblem &p, const float *Q, const float *K,
-                                const float *V, const float *dO, const float *LSE,
-                                const float *Dws, float *dK, float *dV, float *dQp,
-                                float *dKVp, hipStream_t s) {
+                                const float *V, const float *O, const float *dO,
+                                const float *LSE, const float *Dws, float *dK, float *dV,
+                                float *dQp, float *dKVp, hipStream_t s) {
     if (fused_dq_query_splits(p) > 1 && dKVp == nullptr) return hipErrorInvalidValue;
     return wide_key_tiles(p)
-        ? launch_dkdvq<DkdvqCausalCfg, MG_DKDVQ_CAUSAL_NIB>(p, Q, K, V, dO, LSE, Dws, dK, dV, dQp, dKVp, s)
-        : launch_dkdvq<DkdvCfg, MG_DKDV_NIB>(p, Q, K, V, dO, LSE, Dws, dK, dV, dQp, dKVp, s);
+        ? launch_dkdvq<DkdvqCausalCfg, MG_DKDVQ_CAUSAL_NIB>(p, Q, K, V, O, dO, LSE, Dws, dK, dV,
+                                                            dQp, dKVp, s)
+        : launch_dkdvq<DkdvCfg, MG_DKDV_NIB>(p, Q, K, V, O, dO, LSE, Dws, dK, dV, dQp, dKVp, s);
 }
 
 hipError_t launch_bwd_reduce_f32(const AttnProblem &p, const float *dKVp, float *dK,

@@ -65,12 +65,18 @@ hipError_t launch_bwd_dkdv_bf16(const AttnProblem &p, const uint16_t *Q,
 // ([dK, dV][split][B*H][Lk][d] f32; unused, may be null, with one split)
 // for launch_bwd_reduce_f32 to add, together with the dQ partials, in one
 // launch (launch_bwd_dq_reduce_f32 alone when there is one split).
+// Small grids (fused_local_d) compute D inside the kernel from O and dO, so
+// Dws is not read and needs no D launch before; with one key tile per head
+// and no split (fused_direct_dq) dQp must be dQ itself: the kernel writes
+// the scaled dQ there, zeros included, and no reduction follows.
 int fused_dq_key_rows(const AttnProblem &p);
 int fused_dq_query_splits(const AttnProblem &p);
+bool fused_local_d(const AttnProblem &p);
+bool fused_direct_dq(const AttnProblem &p);
 hipError_t launch_bwd_dkdvq_f32(const AttnProblem &p, const float *Q, const float *K,
-                                const float *V, const float *dO, const float *LSE,
-                                const float *Dws, float *dK, float *dV, float *dQp,
-                                float *dKVp, hipStream_t s);
+                                const float *V, const float *O, const float *dO,
+                                const float *LSE, const float *Dws, float *dK, float *dV,
+                                float *dQp, float *dKVp, hipStream_t s);
 hipError_t launch_bwd_reduce_f32(const AttnProblem &p, const float *dKVp, float *dK,
                                  float *dV, const float *dQp, float *dQ, hipStream_t s);
 hipError_t launch_bwd_dq_reduce_f32(const AttnProblem &p, const float *dQp, float *dQ,

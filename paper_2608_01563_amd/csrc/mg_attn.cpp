@@ -149,23 +149,29 @@ mg_status_t attn_bwd_enqueue(const void *Q, const void *K, const void *V, const 
     if (contract == MG_CONTRACT_STRICT_F32) {
         const float *q = (const float *)Q, *k = (const float *)K, *v = (const float *)V;
         const float *o = (const float *)O, *go = (const float *)dO;
-        MG_TRY(run_kernel(kernel_name("attn_rowdot", contract, d), stream,
-                          [&] { return mg::launch_bwd_rowdot_f32(p, o, go, Dws, stream); }));
-        if (use_fused_dq(B, H, Lq, Lk, d, causal, contract, partial_limit)) {
+        const bool fused = use_fused_dq(B, H, Lq, Lk, d, causal, contract, partial_limit);
+        // small fused grids compute D in the kernel itself
+        if (!fused || !mg::fused_local_d(p))
+            MG_TRY(run_kernel(kernel_name("attn_rowdot", contract, d), stream,
+                              [&] { return mg::launch_bwd_rowdot_f32(p, o, go, Dws, stream); }));
+        if (fused) {
             char *base = (char *)workspace;
             float *dQp = (float *)(base + round256((size_t)B * H * Lq * sizeof(float)));
             float *dKVp = dkdv_partial_bytes(B, H, Lq, Lk, d, causal) == 0 ? nullptr
                 : (float *)((char *)dQp + round256(dq_partial_bytes(B, H, Lq, Lk, d, causal)));
+            // one key tile and no split: the kernel writes dQ itself
+            const bool direct = mg::fused_direct_dq(p);
             MG_TRY(run_kernel(kernel_name("attn_dkdvq", contract, d), stream, [&] {
-                return mg::launch_bwd_dkdvq_f32(p, q, k, v, go, LSE, Dws, (float *)dK,
-                                                (float *)dV, dQp, dKVp, stream);
+                return mg::launch_bwd_dkdvq_f32(p, q, k, v, o, go, LSE, Dws, (float *)dK,
+                                                (float *)dV, direct ? (float *)dQ : dQp, dKVp,
+                                                stream);
             }));
             if (dKVp != nullptr)
                 MG_TRY(run_kernel(kernel_name("attn_bwdreduce", contract, d), stream, [&] {
                     return mg::launch_bwd_reduce_f32(p, dKVp, (float *)dK, (float *)dV, dQp,
                                                      (float *)dQ, stream);
                 }));
-            else
+            else if (!direct)
                 MG_TRY(run_kernel(kernel_name("attn_dqreduce", contract, d), stream, [&] {
                     return mg::launch_bwd_dq_reduce_f32(p, dQp, (float *)dQ, stream);
                 }));
