@@ -154,3 +154,44 @@ def test_split_query_tiles(gpu_lib, B, H, Lq, Lk, causal, kl, d):
     for n in ("dQ", "dK", "dV"):
         assert np.array_equal(got[n], again[n]), n
     torch.cuda.synchronize()
+
+
+# Small fused grids compute D inside the fused kernel; with a single key tile
+# and no query split the fused kernel writes dQ itself, including zero rows
+# for queries that see no key.  The outputs start as NaN, so a row that no
+# kernel writes fails the comparison.
+SMALL_GRID_CASES = [
+    # B, H, Lq, Lk, d, causal, key_len
+    (2, 3, 200, 40, 64, True, None),        # one key tile; rows below 160 see no key
+    (1, 1, 1, 1, 32, True, None),
+    (3, 2, 70, 64, 32, False, [0, 17, 64]),  # one key tile; batch 0 has no keys at all
+    (2, 2, 300, 250, 64, True, None),       # four key tiles, query split, local D
+    (2, 2, 64, 64, 64, True, [64, 5]),      # one key tile, padded
+]
+
+
+@pytest.mark.parametrize("B,H,Lq,Lk,d,causal,kl", SMALL_GRID_CASES)
+def test_small_grid_backward_writes_every_row(gpu_lib, B, H, Lq, Lk, d, causal, kl):
+    import torch
+    import paper_2608_01563_amd as mg
+    say("small-grid backward B%d H%d Lq%d Lk%d d%d causal=%s key_len=%s"
+        % (B, H, Lq, Lk, d, causal, kl))
+    x = make_inputs(B, H, Lq, d, causal=causal, seed=500 + Lq + Lk + d, key_len=kl, Lk=Lk)
+    Q, K, V, dO = (torch.from_numpy(getattr(x, n).copy()).cuda() for n in ("Q", "K", "V", "dO"))
+    key_len = None if kl is None else torch.tensor(kl, dtype=torch.int32).cuda()
+    O = torch.full((B, H, Lq, d), float("nan"), device="cuda")
+    LSE = torch.full((B, H, Lq), float("nan"), device="cuda")
+    dQ, dK, dV = (torch.full(t.shape, float("nan"), device="cuda") for t in (Q, K, V))
+    ws = torch.full((max(mg.mg_attn_bwd_cross_workspace_bytes(B, H, Lq, Lk, d, causal,
+                                                             "strict_f32"), 16),),
+                    0xFF, dtype=torch.uint8, device="cuda")   # NaN patterns throughout
+    mg.mg_attn_fwd_cross(Q, K, V, O, LSE, key_len, causal=causal, scale=x.scale,
+                         contract="strict_f32")
+    mg.mg_attn_bwd_cross(Q, K, V, O, LSE, dO, dQ, dK, dV, key_len, causal=causal,
+                         scale=x.scale, contract="strict_f32", workspace=ws)
+    torch.cuda.synchronize()
+    got = {n: t.cpu().numpy() for n, t in (("O", O), ("LSE", LSE), ("dQ", dQ), ("dK", dK),
+                                          ("dV", dV))}
+    errs = compare(got, oracle_reference(x), "strict_f32")
+    say("  errors %s" % {k: "%.2e" % v for k, v in errs.items()})
+    assert max(errs.values()) <= TOL["strict_f32"], errs
