@@ -328,9 +328,9 @@ void attn_fwd_accel_pipe(const float *__restrict__ Q, const float *__restrict__ 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int g = w / kWaves;          // key group
-    const int wq = w - g * kWaves;     // query wave within the group
-    const int tg = tid - g * kThreads; // thread index within the group
+    const int g = (KS == 1) ? 0 : w / kWaves;   // key group
+    const int wq = w - g * kWaves;              // query wave within the group
+    const int tg = tid - g * kThreads;          // thread index within the group
     const int c = lane & 31;
     const int h = lane >> 5;
     const int jr = (lane & 15) >> 2, jc = 4 * (lane & 3);   // transpose-read block offsets
@@ -342,9 +342,9 @@ void attn_fwd_accel_pipe(const float *__restrict__ Q, const float *__restrict__ 
     const int kend = causal ? min(klen, q0 + kRows + diag) : klen;
     const int ntiles = max((kend + kKeys - 1) / kKeys, 0);
     // This group's key tiles [kbeg, kbeg + kcnt); both groups iterate nloop times.
-    const int nloop = (ntiles + KS - 1) / KS;
-    const int kbeg = g * nloop;
-    const int kcnt = min(nloop, ntiles - kbeg);
+    const int nloop = (KS == 1) ? ntiles : (ntiles + 1) / 2;
+    const int kbeg = (KS == 1) ? 0 : g * nloop;
+    const int kcnt = (KS == 1) ? ntiles : min(nloop, ntiles - kbeg);
 
     // B operand of S^T = K Q^T: lane holds f16(Q[qi][16s + 8h + e]).
     f16x8 qreg[NS];
@@ -464,7 +464,7 @@ void attn_fwd_accel_pipe(const float *__restrict__ Q, const float *__restrict__ 
         if (j + 2 < kcnt) sk.load(Kh, (kbeg + j + 2) * kKeys, Lk, tg);
         if (j + 1 < kcnt) sv.load(Vh, (kbeg + j + 1) * kKeys, Lk, tg);
         if (j + 1 < kcnt) scores(Kn, nxt);
-        if (j < kcnt) softmax_pv(kbeg + j, cur, Vc);
+        if (KS == 1 || j < kcnt) softmax_pv(kbeg + j, cur, Vc);
         if (j + 2 < kcnt) sk.store(Kc, tg);
         if (j + 1 < kcnt) sv.store(Vn, tg);
     };
