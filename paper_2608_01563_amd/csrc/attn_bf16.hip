@@ -561,6 +561,11 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
                 pacc[ib] = mfma16x16x32bf16(load_bf16x8(Oc + o), vreg[s], pacc[ib]);
             }
 
+        // 2*NS*QB operand reads and as many products: eight reads ahead
+        // (d = 128: 279-282 -> 268-273 us at B2 H16 L4096; at d = 64 and 32,
+        // where a wave has half or a quarter of the reads, 1-3 % slower)
+        if constexpr (D == 128) sched_reads_ahead<2 * NS * QB, 2 * NS * QB, 8, 2, 2, 0>();
+
         // P = exp2(S * scale*log2e - LSE*log2e), dS = P (dP - D); the mask (row
         // qt*QR + 16ib + 4g + r sees key kj iff 16ib + r >= thr) only in tiles
         // that cross the wave's causal boundary.
@@ -598,6 +603,9 @@ void attn_dkdv_bf16(const uint16_t *__restrict__ Q, const uint16_t *__restrict__
                                             dkacc[c]);
             }
         }
+
+        // 2*QB*NC transpose reads for QB*NC products, eight ahead (d = 128)
+        if constexpr (D == 128) sched_reads_ahead<2 * QB * NC, QB * NC, 8, 2, 1, 1>();
 
         if (qt + 1 < qstop) {
             wait_vmcnt<0>();   // next tile and its LSE, D landed

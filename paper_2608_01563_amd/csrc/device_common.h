@@ -51,6 +51,29 @@ __device__ __forceinline__ f32x16 mfma32x32x16bf16(bf16x8 a, bf16x8 b, f32x16 c)
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+// Scheduling request for the region (basic block) in which it is placed:
+// PRE of its NREADS LDS reads first, then groups of MPG matrix products and
+// RPG reads in turn, then the remaining products.  A wave then keeps about
+// PRE operand reads in flight ahead of the products that consume them,
+// instead of the one or two the default schedule issues when registers are
+// tight.  (Mask 0x100: LDS reads; 0x008: matrix instructions.)
+// (PRE is capped at NREADS for small regions.)
+template <int NREADS, int NMFMA, int PRE_, int RPG, int MPG, int ID>
+__device__ __forceinline__ void sched_reads_ahead() {
+    constexpr int PRE = PRE_ < NREADS ? PRE_ : NREADS;
+    constexpr int NG = (NREADS - PRE) / RPG;
+    static_assert((NREADS - PRE) % RPG == 0 && MPG * NG <= NMFMA,
+                  "read and product counts of the region");
+    __builtin_amdgcn_sched_group_barrier(0x100, PRE, ID);
+#pragma unroll
+    for (int u = 0; u < NG; ++u) {
+        __builtin_amdgcn_sched_group_barrier(0x008, MPG, ID);
+        __builtin_amdgcn_sched_group_barrier(0x100, RPG, ID);
+    }
+    if constexpr (NMFMA > MPG * NG)
+        __builtin_amdgcn_sched_group_barrier(0x008, NMFMA - MPG * NG, ID);
+}
+
 __device__ __forceinline__ f32x16 zero16() {
     f32x16 z;
 #pragma unroll
