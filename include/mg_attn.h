@@ -124,7 +124,8 @@ size_t mg_attn_bwd_workspace_bytes(int B, int H, int L, int d, int causal,
  * the upstream gradient dO (the paper's attention derivative node, Sec. 3.1,
  * lowered to a fused dK+dV kernel and a separate dQ kernel, Sec. 3.3 and
  * Sec. 8; for strict_f32 with d <= 64 the dK+dV kernel also emits per-tile
- * dQ partials that a reduction kernel sums).  P is recomputed from Q, K and
+ * dQ partials that a reduction kernel sums, or, with a single key tile and
+ * no query split, writes dQ itself).  P is recomputed from Q, K and
  * the saved LSE; nothing of size L x L is stored.  `workspace` is
  * caller-owned device memory of at least mg_attn_bwd_workspace_bytes(...)
  * bytes; its contents on entry are ignored
