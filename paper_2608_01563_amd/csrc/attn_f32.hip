@@ -96,6 +96,12 @@ constexpr int kStream = 64;   // streamed rows per step
 #ifndef MG_FWD_KS
 #define MG_FWD_KS 64
 #endif
+#ifndef MG_FWD_SPLIT4_UPTO
+#define MG_FWD_SPLIT4_UPTO 256     // 32-row grids up to this size split their keys four ways...
+#endif
+#ifndef MG_FWD_SPLIT4_MIN_KEYS
+#define MG_FWD_SPLIT4_MIN_KEYS 256 // ...when each group still gets two or more 32-key tiles
+#endif
 constexpr int kFwdStream = MG_FWD_KS;   // keys per streamed forward tile
 
 template <int NW_, int OCC_, bool DB_>
@@ -211,11 +217,12 @@ __device__ __forceinline__ void fwd_f32_body(const float *__restrict__ Q, const 
     using Tile = DirectTile<KS, D, C::NW>;
     static_assert(Tile::kEven, "the vmcnt waits below count kPerWave loads per fetch");
     constexpr int NL = Tile::kPerWave;   // vector-memory operations per tile fetch
-    static_assert(KSPLIT == 1 || (KSPLIT == 2 && C::NW * NC * 256 <= KS * D),
-                  "half 1's O must fit in its K tile");
+    static_assert(KSPLIT == 1 || ((KSPLIT == 2 || KSPLIT == 4) && C::NW * NC * 256 <= KS * D),
+                  "a key group's O must fit in its K tile");
     __shared__ __attribute__((aligned(16))) float Ks[KSPLIT][KS * D];
     __shared__ __attribute__((aligned(16))) float Vs[KSPLIT][KS * D];
-    __shared__ float xml[KSPLIT > 1 ? 2 * C::NW * 64 : 1];   // key split: m, l of half 1
+    // key split: m, l of groups 1 .. KSPLIT-1
+    __shared__ float xml[KSPLIT > 1 ? (KSPLIT - 1) * 2 * C::NW * 64 : 1];
 
     int slot, head;
     if (work_first) {
@@ -235,7 +242,7 @@ __device__ __forceinline__ void fwd_f32_body(const float *__restrict__ Q, const 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wg = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int hh = (KSPLIT > 1) ? wg / C::NW : 0;   // key half of this wave
+    const int hh = (KSPLIT > 1) ? wg / C::NW : 0;   // key group of this wave
     const int w = (KSPLIT > 1) ? wg - hh * C::NW : wg;   // row wave within its half
     const int il = lane & 15;
     const int g = lane >> 4;
@@ -246,12 +253,12 @@ __device__ __forceinline__ void fwd_f32_body(const float *__restrict__ Q, const 
     const int klen = key_limit(key_len, b, Lk);
     const int kend = causal ? min(klen, q0 + C::ROWS + diag) : klen;
     const int ntiles = (kend + KS - 1) / KS;
-    // Key split: half 0 takes the first ceil(n/2) key tiles, half 1 the
-    // rest; both run ceil(n/2) iterations so that every barrier is reached
-    // by all waves (half 1's surplus iteration only waits).
-    const int iters = (KSPLIT > 1) ? (ntiles + 1) / 2 : ntiles;
+    // Key split: group h takes key tiles [h*m, min(n, (h+1)*m)) with
+    // m = ceil(n/KSPLIT); every group runs m iterations so that every barrier
+    // is reached by all waves (a group's surplus iterations only wait).
+    const int iters = (KSPLIT > 1) ? (ntiles + KSPLIT - 1) / KSPLIT : ntiles;
     const int tbeg = hh * iters;
-    const int tend = (KSPLIT > 1 && hh == 0) ? iters : ntiles;
+    const int tend = (KSPLIT > 1) ? min(ntiles, tbeg + iters) : ntiles;
     float *const Ksh = Ks[hh];
     float *const Vsh = Vs[hh];
 
@@ -398,11 +405,12 @@ __device__ __forceinline__ void fwd_f32_body(const float *__restrict__ Q, const 
 
     float l = sum_over_groups(l_run);
     if constexpr (KSPLIT > 1) {
-        // Half 1 hands its (m, l, O) to half 0 through its own K tile, which
-        // no wave reads any more; half 0 merges the two online-softmax states.
-        float *xo = Ks[1];
-        float *xm = xml, *xl = xml + C::NW * 64;
-        if (hh == 1) {
+        // Groups 1 .. KSPLIT-1 hand their (m, l, O) to group 0 through their
+        // own K tiles, which no wave reads any more; group 0 merges the
+        // online-softmax states in group order.
+        if (hh > 0) {
+            float *xo = Ks[hh];
+            float *xm = xml + (hh - 1) * 2 * C::NW * 64, *xl = xm + C::NW * 64;
 #pragma unroll
             for (int c = 0; c < NC; ++c)
                 *reinterpret_cast<f32x4 *>(&xo[((w * NC + c) * 64 + lane) * 4]) = oacc[c];
@@ -410,16 +418,25 @@ __device__ __forceinline__ void fwd_f32_body(const float *__restrict__ Q, const 
             xl[w * 64 + lane] = l;
         }
         __syncthreads();
-        if (hh == 1) return;
-        const float m1 = xm[w * 64 + lane];
-        const float mm = fmaxf(m_run, m1);
-        const float mu = (mm == -INFINITY) ? 0.f : mm;
-        const float a0 = exp2_fast(m_run - mu), a1 = exp2_fast(m1 - mu);
+        if (hh > 0) return;
+        float mm = m_run;
 #pragma unroll
-        for (int c = 0; c < NC; ++c)
-            oacc[c] = oacc[c] * a0 +
-                      *reinterpret_cast<const f32x4 *>(&xo[((w * NC + c) * 64 + lane) * 4]) * a1;
-        l = l * a0 + xl[w * 64 + lane] * a1;
+        for (int h = 1; h < KSPLIT; ++h) mm = fmaxf(mm, xml[(h - 1) * 2 * C::NW * 64 + w * 64 + lane]);
+        const float mu = (mm == -INFINITY) ? 0.f : mm;
+        const float a0 = exp2_fast(m_run - mu);
+        l *= a0;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) oacc[c] *= a0;
+#pragma unroll
+        for (int h = 1; h < KSPLIT; ++h) {
+            const float *xo = Ks[h];
+            const float *xm = xml + (h - 1) * 2 * C::NW * 64, *xl = xm + C::NW * 64;
+            const float ah = exp2_fast(xm[w * 64 + lane] - mu);
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+                oacc[c] += *reinterpret_cast<const f32x4 *>(&xo[((w * NC + c) * 64 + lane) * 4]) * ah;
+            l += xl[w * 64 + lane] * ah;
+        }
         m_run = mm;
     }
     if (qi < Lq) {
@@ -454,6 +471,12 @@ template <int D, class C>
 __global__ __launch_bounds__(2 * C::NT) __attribute__((amdgpu_waves_per_eu(C::template occ<D>(), 8)))
 void attn_fwd_f32_ks2(MG_FWD_F32_ARGS) {
     fwd_f32_body<D, C, 2>(Q, K, V, O, LSE, key_len, H, Lq, Lk, causal, scale_log2, n_qtiles, BH,
+                          layer, work_first);
+}
+template <int D, class C>
+__global__ __launch_bounds__(4 * C::NT) __attribute__((amdgpu_waves_per_eu(C::template occ<D>(), 8)))
+void attn_fwd_f32_ks4(MG_FWD_F32_ARGS) {
+    fwd_f32_body<D, C, 4>(Q, K, V, O, LSE, key_len, H, Lq, Lk, causal, scale_log2, n_qtiles, BH,
                           layer, work_first);
 }
 #undef MG_FWD_F32_ARGS
@@ -1247,18 +1270,28 @@ hipError_t launch_fwd_f32(const AttnProblem &p, const float *Q, const float *K,
     // then set the kernel's time).  There the query tiles shrink to 32 rows
     // and each workgroup splits its key tiles over two halves: four times
     // the workgroups, each a quarter of the work (d <= 64, two or more key tiles).
+    // When even the 32-row grid leaves most CUs without a workgroup and the
+    // key side is long, the key tiles go to four groups instead of two.
     const long grid = (long)cdiv(p.Lq, FwdCfg::ROWS) * p.B * p.H;
     const bool split = p.d <= 64 && grid < MG_FWD_SPLIT_BELOW && p.Lk > kFwdStream;
+    const bool split4 = split && (long)cdiv(p.Lq, FwdSplitCfg::ROWS) * p.B * p.H <=
+                                     MG_FWD_SPLIT4_UPTO && p.Lk >= MG_FWD_SPLIT4_MIN_KEYS;
     switch (p.d) {
     case 32:
-        if (split)
+        if (split4)
+            launch_fwd_f32_as<FwdSplitCfg>(attn_fwd_f32_ks4<32, FwdSplitCfg>, 4, p, Q, K, V, O,
+                                           LSE, s);
+        else if (split)
             launch_fwd_f32_as<FwdSplitCfg>(attn_fwd_f32_ks2<32, FwdSplitCfg>, 2, p, Q, K, V, O,
                                            LSE, s);
         else
             launch_fwd_f32_as<FwdCfg>(attn_fwd_f32<32, FwdCfg>, 1, p, Q, K, V, O, LSE, s);
         break;
     case 64:
-        if (split)
+        if (split4)
+            launch_fwd_f32_as<FwdSplitCfg>(attn_fwd_f32_ks4<64, FwdSplitCfg>, 4, p, Q, K, V, O,
+                                           LSE, s);
+        else if (split)
             launch_fwd_f32_as<FwdSplitCfg>(attn_fwd_f32_ks2<64, FwdSplitCfg>, 2, p, Q, K, V, O,
                                            LSE, s);
         else

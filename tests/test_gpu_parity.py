@@ -37,6 +37,22 @@ def test_small_shapes_strict(gpu_lib, L, d, mode):
     assert max(errs.values()) <= TOL["strict_f32"], errs
 
 
+@pytest.mark.parametrize("B,H,Lq,Lk,d,causal,kl", [
+    (4, 4, 256, 256, 64, True, None),      # workload 2's shape: four key groups
+    (1, 2, 300, 257, 32, True, None),      # nine 32-key tiles: the last group is empty
+    (2, 2, 513, 513, 64, False, [513, 40]),   # padded: one batch's groups mostly idle
+    (1, 3, 100, 300, 64, True, None),      # cross, bottom-right causal
+])
+def test_strict_four_group_forward(gpu_lib, B, H, Lq, Lk, d, causal, kl):
+    """Small grids with long key sides split their key tiles over four groups
+    of waves, merged in group order; against the oracle."""
+    say("strict four-group forward B%d H%d Lq%d Lk%d d%d causal=%s" % (B, H, Lq, Lk, d, causal))
+    assert B * H * -(-Lq // 32) <= 256 and Lk >= 256
+    x = make_inputs(B, H, Lq, d, causal=causal, seed=41 + Lq + Lk, key_len=kl, Lk=Lk)
+    errs = compare(run_gpu(x), oracle_reference(x), "strict_f32")
+    assert max(errs.values()) <= TOL["strict_f32"], errs
+
+
 @pytest.mark.parametrize("wid", [1, 2, 3, 5])
 def test_workload_full_compare_strict(gpu_lib, wid):
     w = WORKLOADS[wid]
